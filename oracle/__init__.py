@@ -1,0 +1,308 @@
+"""CPU oracle of the DualGCN aggregation path -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
+this package.  The GPU library never calls it and shares no code with it.
+
+Pieces and the passages they follow (DualGCN paper):
+
+* walks and density -- Sec. 3.2, Theorem 1 and "Neighbor Density": anonymous
+  random walks from every node; N_v = sum_i i P_i = S_v / k where S_v sums the
+  distinct-node counts of the node's k walks (C part, ``oracle.c``).
+* degree -- Sec. 3.2 "Node Degree": the row length read from the row pointers.
+* hybrid metric -- Sec. 3.2: H_v = alpha N_v + (1 - alpha) D_v.  With
+  alpha = p/q this is kept as the exact integer K_v = q k H_v = p S_v + (q-p) k D_v.
+* threshold and mode -- Sec. 3.3 Eq. (1): dense iff H_v >= tau with
+  tau = mu_H + 0.5 sigma_H (population statistics over all nodes).  Evaluated
+  exactly with Python integers: H >= mu + (b/c) sigma  <=>  c (n K - S1) >= b sqrt(V)
+  with S1 = sum K, V = n sum K^2 - S1^2.
+* sort -- Sec. 3.2 (proof of Theorem 2): nodes sorted by H ascending, ties by
+  node id, then split into the sparse prefix and the dense suffix.
+* SpMM -- Sec. 1 / Sec. 2.1 aggregation Y = A X, float64 (C part).
+* GCN layer -- Sec. 1 update phase: Y = act(A (X W)), float64 (C part + numpy).
+
+The whole-graph partition is exact and therefore unique; the SpMM and the GCN
+layer return float64 values with a per-element magnitude bound.
+"""
+import ctypes
+import math
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+FORCE_AUTO, FORCE_SPARSE, FORCE_DENSE = 0, 1, 2
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            from . import build as _build
+            _build.build()
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        L.philox4x64_10.argtypes = [P, P, P]
+        L.philox4x64_10.restype = None
+        L.oracle_walk.argtypes = [P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_uint32,
+                                  ctypes.c_uint64, ctypes.c_uint32, P]
+        L.oracle_walk.restype = ctypes.c_uint32
+        L.oracle_density.argtypes = [P, P, ctypes.c_int32, ctypes.c_uint64, ctypes.c_uint32,
+                                     ctypes.c_uint32, P, ctypes.c_int64, P]
+        L.oracle_density.restype = None
+        L.oracle_patterns.argtypes = [P, P, ctypes.c_int32, ctypes.c_uint64, ctypes.c_uint32,
+                                      ctypes.c_uint32, P]
+        L.oracle_patterns.restype = None
+        L.oracle_spmm_rows.argtypes = [P, P, P, P, ctypes.c_int32, P, ctypes.c_int64, P, P]
+        L.oracle_spmm_rows.restype = None
+        L.oracle_spmm_rows_f64.argtypes = [P, P, P, P, ctypes.c_int32, P, ctypes.c_int64, P, P]
+        L.oracle_spmm_rows_f64.restype = None
+        L.oracle_xw_rows.argtypes = [P, P, ctypes.c_int32, ctypes.c_int32, P, ctypes.c_int64,
+                                     P, P]
+        L.oracle_xw_rows.restype = None
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _csr(g):
+    rowptr = np.ascontiguousarray(g.rowptr, dtype=np.int32)
+    col = np.ascontiguousarray(g.col, dtype=np.int32)
+    val = np.ascontiguousarray(g.val, dtype=np.float32)
+    return rowptr, col, val
+
+
+# ------------------------------------------------------------------ random stream
+
+def philox(counter, key):
+    """One Philox-4x64-10 block: four 64-bit words for a 4-word counter and 2-word key."""
+    c = np.ascontiguousarray(counter, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, dtype=np.uint64)
+    lib().philox4x64_10(_p(c), _p(k), _p(out))
+    return out
+
+
+# ------------------------------------------------------------------ walks (Sec. 3.2)
+
+def walk(g, start, w, seed, steps):
+    """Labels (length steps+1) of walk ``w`` from node ``start``."""
+    rowptr, col, _ = _csr(g)
+    out = np.zeros(steps + 1, dtype=np.uint8)
+    u = lib().oracle_walk(_p(rowptr), _p(col), g.n, int(start), int(w), int(seed), int(steps),
+                          _p(out))
+    assert u == out.max()
+    return out
+
+
+def patterns(g, seed, k, steps):
+    """uint8 [n, k, steps+1] anonymous walks of every node."""
+    rowptr, col, _ = _csr(g)
+    out = np.zeros((g.n, k, steps + 1), dtype=np.uint8)
+    lib().oracle_patterns(_p(rowptr), _p(col), g.n, int(seed), int(k), int(steps), _p(out))
+    return out
+
+
+def density_sums(g, seed, k, steps, nodes=None):
+    """uint32 S_v (sum of distinct-node counts over the k walks) for ``nodes`` (default all)."""
+    rowptr, col, _ = _csr(g)
+    if nodes is None:
+        nodes = np.arange(g.n, dtype=np.int32)
+    nodes = np.ascontiguousarray(nodes, dtype=np.int32)
+    S = np.zeros(nodes.size, dtype=np.uint32)
+    lib().oracle_density(_p(rowptr), _p(col), g.n, int(seed), int(k), int(steps), _p(nodes),
+                         nodes.size, _p(S))
+    return S
+
+
+# ------------------------------------------------------------------ partition (Sec. 3.2, 3.3)
+
+def degrees(g):
+    """D_v: entries of row v, read from the row pointers."""
+    return np.diff(np.asarray(g.rowptr, dtype=np.int64))
+
+
+def hybrid_keys(S, D, k, alpha=(1, 2)):
+    """K_v = q k H_v = p S_v + (q - p) k D_v for alpha = p/q, as uint64."""
+    p, q = alpha
+    K = np.asarray(S, dtype=np.uint64) * np.uint64(p) + \
+        np.asarray(D, dtype=np.uint64) * np.uint64((q - p) * k)
+    return K
+
+
+def moments(K):
+    """(S1, S2) = (sum K, sum K^2) as exact Python integers."""
+    values, counts = np.unique(np.asarray(K, dtype=np.uint64), return_counts=True)
+    S1 = sum(int(v) * int(c) for v, c in zip(values, counts))
+    S2 = sum(int(v) * int(v) * int(c) for v, c in zip(values, counts))
+    return S1, S2
+
+
+def is_dense(Kv, n, S1, S2, beta=(1, 2)):
+    """Eq. (1): H_v >= mu_H + beta sigma_H, evaluated exactly in integers."""
+    b, c = beta
+    V = n * S2 - S1 * S1           # n^2 sigma^2 in K units
+    lhs = c * (n * int(Kv) - S1)   # c n (K - mu)
+    if lhs < 0:
+        return False
+    return lhs * lhs >= b * b * V
+
+
+def threshold_key(n, S1, S2, beta=(1, 2)):
+    """Least integer K with K >= mu + beta sigma (so dense iff K_v >= this)."""
+    b, c = beta
+    V = n * S2 - S1 * S1
+    guess = int(math.floor((S1 + (b / c) * math.sqrt(V)) / n)) if n else 0
+    K = max(guess, 0)
+    while K > 0 and is_dense(K - 1, n, S1, S2, beta):
+        K -= 1
+    while not is_dense(K, n, S1, S2, beta):
+        K += 1
+    return K
+
+
+def partition(g, seed, k, steps, alpha=(1, 2), beta=(1, 2), force=FORCE_AUTO, S=None):
+    """The whole plan: S, K, K*, dense flags, perm (sorted by (K, v)) and n_sparse."""
+    if S is None:
+        S = density_sums(g, seed, k, steps)
+    D = degrees(g)
+    K = hybrid_keys(S, D, k, alpha)
+    n = g.n
+    S1, S2 = moments(K)
+    kstar = threshold_key(n, S1, S2, beta)
+    values = np.unique(K)
+    dense_values = {int(v) for v in values if is_dense(int(v), n, S1, S2, beta)}
+    dense = np.isin(K, np.array(sorted(dense_values), dtype=np.uint64))
+    perm = np.lexsort((np.arange(n), K)).astype(np.int32)   # by K, then by node id
+    if force == FORCE_SPARSE:
+        n_sparse = n
+    elif force == FORCE_DENSE:
+        n_sparse = 0
+    else:
+        n_sparse = int(n - dense.sum())
+    return dict(S=S, D=D, K=K, S1=S1, S2=S2, kstar=kstar, dense=dense, perm=perm,
+                n_sparse=n_sparse)
+
+
+# ------------------------------------------------------------------ SpMM (Sec. 1, 2.1)
+
+def spmm(g, X, rows=None):
+    """float64 (Y, B) for the listed rows (default all): Y = A X, B = |A| |X|."""
+    rowptr, col, val = _csr(g)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    F = X.shape[1] if X.ndim == 2 else 1
+    if rows is None:
+        rows = np.arange(g.n, dtype=np.int32)
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    Y = np.zeros((rows.size, F), dtype=np.float64)
+    B = np.zeros((rows.size, F), dtype=np.float64)
+    lib().oracle_spmm_rows(_p(rowptr), _p(col), _p(val), _p(X), F, _p(rows), rows.size,
+                           _p(Y), _p(B))
+    return Y, B
+
+
+def xw(X, W, rows=None):
+    """float64 (T, BT) for the listed rows: T = X W, BT = |X| |W|."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    Fin, Fout = W.shape
+    if rows is None:
+        rows = np.arange(X.shape[0], dtype=np.int32)
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    T = np.zeros((rows.size, Fout), dtype=np.float64)
+    BT = np.zeros((rows.size, Fout), dtype=np.float64)
+    lib().oracle_xw_rows(_p(X), _p(W), Fin, Fout, _p(rows), rows.size, _p(T), _p(BT))
+    return T, BT
+
+
+def _spmm_f64(g, Xc, slot, rows):
+    rowptr, col, val = _csr(g)
+    Xc = np.ascontiguousarray(Xc, dtype=np.float64)
+    F = Xc.shape[1]
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    slot = np.ascontiguousarray(slot, dtype=np.int64)
+    Y = np.zeros((rows.size, F), dtype=np.float64)
+    lib().oracle_spmm_rows_f64(_p(rowptr), _p(col), _p(val), _p(Xc), F, _p(rows), rows.size,
+                               _p(slot), _p(Y))
+    return Y
+
+
+def neighbours(g, rows):
+    """Sorted distinct column ids referenced by the listed rows."""
+    rp = np.asarray(g.rowptr, dtype=np.int64)
+    rows = np.asarray(rows, dtype=np.int64)
+    if rows.size == 0:
+        return np.zeros(0, dtype=np.int32)
+    parts = [np.asarray(g.col[rp[r]:rp[r + 1]]) for r in rows]
+    return np.unique(np.concatenate(parts)).astype(np.int32)
+
+
+def _absolute(g):
+    from types import SimpleNamespace
+    return SimpleNamespace(n=g.n, rowptr=g.rowptr, col=g.col, val=np.abs(np.asarray(g.val)))
+
+
+def gcn_layer(g, X, W, relu=False, rows=None):
+    """One GCN layer Y = act(A (X W)) in float64 on the listed rows, with its bound.
+
+    Returns (Y, BY) where BY = |A| (|X| |W|) bounds the magnitude of every
+    product term; ReLU does not change it (ReLU is 1-Lipschitz).
+    """
+    if rows is None:
+        rows = np.arange(g.n, dtype=np.int32)
+    rows = np.asarray(rows, dtype=np.int32)
+    need = neighbours(g, rows)
+    T, BT = xw(X, W, need)
+    slot = np.full(g.n, -1, dtype=np.int64)
+    slot[need] = np.arange(need.size)
+    Y = _spmm_f64(g, T, slot, rows)
+    BY = _spmm_f64(_absolute(g), BT, slot, rows)
+    if relu:
+        Y = np.maximum(Y, 0.0)
+    return Y, BY
+
+
+def gcn_forward_rows(g, X, weights, rows):
+    """Two-layer (or deeper) forward  act(A (act(A (X W1)) W2))... on the listed output rows.
+
+    ReLU after every layer but the last.  Returns (Y, bound) where ``bound`` is
+    the end-to-end magnitude bound of the deviation budget used by the tests:
+    for the last layer |A| ((|H| + bound_prev) |W|).
+    """
+    rows = np.asarray(rows, dtype=np.int32)
+    # the set of nodes needed at every depth
+    levels = [rows]
+    for _ in range(len(weights) - 1):
+        levels.append(neighbours(g, levels[-1]))
+    H = None
+    Hbound = None
+    prev_nodes = None
+    for li, W in enumerate(weights):
+        out_nodes = levels[len(weights) - 1 - li]
+        relu = li < len(weights) - 1
+        if li == 0:
+            Y, BY = gcn_layer(g, X, W, relu=relu, rows=out_nodes)
+            H, Hbound = Y, BY
+        else:
+            slot_prev = np.full(g.n, -1, dtype=np.int64)
+            slot_prev[prev_nodes] = np.arange(prev_nodes.size)
+            need = neighbours(g, out_nodes)
+            Hn = H[slot_prev[need]]
+            Bn = Hbound[slot_prev[need]]
+            Wd = np.asarray(W, dtype=np.float64)
+            T = Hn @ Wd
+            BT = (np.abs(Hn) + Bn) @ np.abs(Wd)
+            slot = np.full(g.n, -1, dtype=np.int64)
+            slot[need] = np.arange(need.size)
+            Y = _spmm_f64(g, T, slot, out_nodes)
+            BY = _spmm_f64(_absolute(g), BT, slot, out_nodes)
+            if relu:
+                Y = np.maximum(Y, 0.0)
+            H, Hbound = Y, BY
+        prev_nodes = out_nodes
+    return H, Hbound
