@@ -1,0 +1,214 @@
+/*
+ * dualgcn.h -- C ABI of the MI355X (gfx950) DualGCN aggregation library.
+ *
+ * The library computes the aggregation phase of a GCN layer, the sparse-dense
+ * product Y = A X of the DualGCN paper (Sec. 1 and Sec. 2.1), scheduled by the
+ * paper's dual-metric partition (Sec. 3.2) and run by two kernels, one for the
+ * sparse region and one for the dense region of the partition (Sec. 3.3), and
+ * the update phase X W of a layer (Sec. 1).
+ *
+ * Conventions for every entry point
+ *   - Pointers named *_h are host memory; every other array pointer is device
+ *     memory on the current HIP device.  No entry point copies user arrays.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *     Work is enqueued on that stream.  Only dualgcn_partition,
+ *     dualgcn_plan_export and dualgcn_arw_patterns wait for it.
+ *   - Every function returns a dualgcn_status (0 = success).  Arguments are
+ *     checked before the device is touched.  Outputs are undefined after an
+ *     error.  No C++ exception crosses this interface.
+ *   - A plan may be used by one stream at a time.  Results do not depend on
+ *     the launch order of the kernels: every output element is written by
+ *     exactly one workgroup, in a fixed summation order (bit-reproducible).
+ */
+#ifndef DUALGCN_H
+#define DUALGCN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------------ status */
+
+typedef enum dualgcn_status {
+    DUALGCN_OK = 0,
+    DUALGCN_ERR_INVALID_ARG = -1,  /* NULL pointer, size out of range, bad rational */
+    DUALGCN_ERR_BAD_CSR = -2,      /* row pointers not monotone, rowptr[0] != 0,
+                                      rowptr[n] != nnz, or a column outside [0, n) */
+    DUALGCN_ERR_UNSUPPORTED = -3,  /* sizes the library does not handle (see each call) */
+    DUALGCN_ERR_OOM = -4,          /* a device allocation failed */
+    DUALGCN_ERR_HIP = -5,          /* a HIP runtime call failed; see dualgcn_last_hip_error */
+    DUALGCN_ERR_NO_DEVICE = -6     /* no usable HIP device */
+} dualgcn_status;
+
+/* Static text for a status code (never NULL). */
+const char *dualgcn_status_str(int status);
+
+/* hipError_t of the last failing HIP call made by the library in this thread (0 if none). */
+int dualgcn_last_hip_error(void);
+
+/* ------------------------------------------------------------------ inputs */
+
+/*
+ * A sparse matrix in CSR form (the adjacency A of Sec. 1; the degree metric of
+ * Sec. 3.2 is read from its row pointers).  The arrays are BORROWED: they must
+ * stay alive and unmodified for the lifetime of any plan built on them.
+ *   n       rows = columns, 1 <= n < 2^31
+ *   nnz     stored entries, 0 <= nnz < 2^31 (int32 row pointers)
+ *   rowptr  int32[n+1], rowptr[0] = 0, non-decreasing, rowptr[n] = nnz
+ *   col     int32[nnz], each in [0, n); order inside a row is free and
+ *           duplicates are allowed (they add in the product and weight walks)
+ *   val     float[nnz] entry values (any finite floats)
+ */
+typedef struct dualgcn_csr {
+    int32_t n;
+    int64_t nnz;
+    const int32_t *rowptr;
+    const int32_t *col;
+    const float *val;
+} dualgcn_csr;
+
+enum { DUALGCN_FORCE_AUTO = 0, DUALGCN_FORCE_SPARSE = 1, DUALGCN_FORCE_DENSE = 2 };
+
+/*
+ * Partition parameters, as exact rationals.
+ *   alpha = alpha_num / alpha_den, the weight of density against degree in the
+ *           hybrid metric H_v = alpha N_v + (1 - alpha) D_v (Sec. 3.2); the
+ *           paper's default is 1/2.  Requires alpha_num <= alpha_den, den > 0.
+ *   beta  = beta_num / beta_den, the threshold tau = mu_H + beta sigma_H of
+ *           Eq. (1) (Sec. 3.3); the paper uses 1/2.  Requires den > 0.
+ *   force_mode  DUALGCN_FORCE_AUTO applies Eq. (1); FORCE_SPARSE / FORCE_DENSE
+ *           send every row to one kernel (the plan's order and K* are unchanged).
+ * Numerators and denominators must be below 2^16.  A NULL pointer means
+ * {1, 2, 1, 2, DUALGCN_FORCE_AUTO}.
+ */
+typedef struct dualgcn_thresholds {
+    uint32_t alpha_num, alpha_den;
+    uint32_t beta_num, beta_den;
+    int32_t force_mode;
+} dualgcn_thresholds;
+
+/* ------------------------------------------------------------------ plan */
+
+typedef struct dualgcn_plan dualgcn_plan;
+
+/*
+ * dualgcn_partition -- the dual-metric partition of Sec. 3.2 and Eq. (1).
+ *
+ * For every node v, `walks_per_node` (k) anonymous random walks of `walk_len`
+ * (d) steps give S_v = sum over the walks of the number of distinct nodes seen
+ * (start included), so the neighbour density of Theorem 1 is N_v = S_v / k.
+ * A step moves to entry floor(r * deg / 2^64) of the current CSR row, r being
+ * 64-bit word (s mod 4) of Philox-4x64-10 (Salmon et al., SC'11) with counter
+ * (v, w, floor(s / 4), 0) and key (seed, 0); an empty row keeps the walk in place.
+ * D_v is the row length.  With alpha = p/q the hybrid metric is kept as the
+ * exact integer K_v = q k H_v = p S_v + (q - p) k D_v.  The threshold key K* is
+ * the least integer with K* >= mu_K + beta sigma_K (population statistics over
+ * all n nodes, evaluated exactly in 128-bit integers), so row v is dense iff
+ * K_v >= K* (Eq. (1), ties dense).  `perm` lists the nodes sorted by (K_v, v)
+ * ascending; its first n_sparse entries form the sparse region.
+ *
+ * Requirements: 1 <= k, 1 <= d <= 255, q k max(d + 1, nnz) < 2^63 and the
+ * moment sums must fit 128 bits (else DUALGCN_ERR_UNSUPPORTED).  The CSR is
+ * validated on the device first (DUALGCN_ERR_BAD_CSR).
+ *
+ * The plan owns device memory (S, K, perm, the dense-region schedule and the
+ * partial sums of split rows), released by dualgcn_plan_destroy.  The call waits
+ * for `stream` twice (to read the moment sums and the schedule sizes).
+ * *out is set to NULL on error.
+ */
+int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,
+                      uint32_t walk_len, const dualgcn_thresholds *th, void *stream,
+                      dualgcn_plan **out);
+
+/* Releases a plan and its device memory (waits for the device).  NULL is a no-op. */
+void dualgcn_plan_destroy(dualgcn_plan *plan);
+
+/*
+ * dualgcn_spmm -- Y = A X, the aggregation SpMM (Sec. 1, Sec. 2.1).
+ *
+ * X and Y are float32 row-major n x F, contiguous (leading dimension F), and
+ * must not overlap.  Rows of the sparse region are computed by the sparse
+ * kernel (one row per lane group of a wavefront); rows of the dense region by
+ * the dense kernel (one workgroup per row; rows longer than the dense chunk are
+ * split over several workgroups and combined in a fixed order).  Every row of
+ * Y is written, rows without entries with zeros.  Products are float32; sums
+ * are formed in float32 over at most 64 terms and then in float64, and each
+ * output is rounded once to float32.  1 <= F < 2^20.  Asynchronous.
+ */
+int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, void *stream);
+
+/* ------------------------------------------------------------------ GCN layer */
+
+#define DUALGCN_RELU 1u
+
+/* Bytes of device workspace dualgcn_gcn_layer needs (host-only, no device use). */
+int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,
+                                size_t *bytes);
+
+/*
+ * dualgcn_gcn_layer -- one GCN layer Y = act(A (X W)): the update phase X W
+ * (Sec. 1) followed by the aggregation of dualgcn_spmm.
+ *
+ * X is float32 n x F_in row-major, W float32 F_in x F_out row-major, Y float32
+ * n x F_out row-major.  X W is computed on the matrix cores with X and W
+ * rounded to bfloat16 (nearest-even) and float32 accumulation; the result T is
+ * kept in float32 in `workspace` and aggregated by the SpMM kernels.  act is
+ * ReLU if `flags & DUALGCN_RELU`, else the identity (no bias).  `workspace` is
+ * caller-owned device memory of at least dualgcn_gcn_layer_workspace() bytes,
+ * 256-byte aligned (else DUALGCN_ERR_INVALID_ARG).  F_in and F_out must be
+ * multiples of 32 with F_in <= 1024 and F_out <= 256 (else UNSUPPORTED).
+ * Asynchronous.
+ */
+int dualgcn_gcn_layer(const dualgcn_plan *plan, const float *X, const float *W, float *Y,
+                      int32_t F_in, int32_t F_out, uint32_t flags, void *workspace,
+                      size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------ introspection */
+
+typedef struct dualgcn_plan_info {
+    int32_t n;
+    int64_t nnz;
+    int32_t n_sparse;        /* rows in the sparse region: perm[0 .. n_sparse) */
+    int32_t n_dense;         /* n - n_sparse */
+    uint64_t kstar;          /* threshold key K* */
+    uint64_t s1_hi, s1_lo;   /* sum of K_v, 128-bit */
+    uint64_t s2_hi, s2_lo;   /* sum of K_v^2, 128-bit */
+    uint64_t kmax;           /* largest K_v */
+    uint32_t alpha_num, alpha_den, beta_num, beta_den;
+    int32_t force_mode;
+    uint64_t seed;
+    uint32_t walks_per_node, walk_len;
+    int32_t max_degree;
+    int32_t dense_chunk;     /* entries per dense workgroup */
+    int32_t n_split_rows;    /* dense rows longer than dense_chunk */
+    int32_t n_split_parts;   /* workgroups those rows are split over */
+} dualgcn_plan_info;
+
+/* Fills *out from host-side copies kept in the plan (no device use). */
+int dualgcn_plan_query(const dualgcn_plan *plan, dualgcn_plan_info *out);
+
+/*
+ * Copies the plan's perm (int32[n]), S (uint32[n]) and K (uint64[n]) to host
+ * buffers; any of them may be NULL.  Waits for the device.
+ */
+int dualgcn_plan_export(const dualgcn_plan *plan, int32_t *perm_h, uint32_t *S_h,
+                        uint64_t *K_h);
+
+/*
+ * dualgcn_arw_patterns -- the anonymous walks themselves (Sec. 3.2), for tests:
+ * out (device, uint8[n][k][d+1]) receives, for walk w of node v, the label of
+ * each visited position (1 + order of first occurrence), with the random
+ * stream of dualgcn_partition.  Requires n k (d + 1) < 2^40 and d <= 255
+ * (else DUALGCN_ERR_UNSUPPORTED).  Waits for `stream`.
+ */
+int dualgcn_arw_patterns(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,
+                         uint32_t walk_len, uint8_t *out, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DUALGCN_H */

@@ -1,0 +1,232 @@
+"""MI355X-native DualGCN aggregation: Python binding of ``libdualgcn.so``.
+
+Argument marshalling only -- every step of the path runs in the library's HIP
+kernels.  torch provides device memory and the current stream.  The library is
+built by ``paper_2609_01983_amd.build`` (or ``__graft_entry__.build()``); if it
+is missing, importing this package raises ImportError: there is no fallback.
+
+    plan = Plan(rowptr, col, val, seed=0, walks_per_node=16, walk_len=5)
+    Y = spmm(plan, X)                           # Y = A X
+    H = gcn_layer(plan, X, W, relu=True)        # H = relu(A (X W)), X W in bf16 MFMA
+"""
+import ctypes
+import os
+
+import torch  # must load before the library: it provides the process's HIP runtime
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdualgcn.so")
+
+OK, ERR_INVALID_ARG, ERR_BAD_CSR, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP, ERR_NO_DEVICE = \
+    0, -1, -2, -3, -4, -5, -6
+FORCE_AUTO, FORCE_SPARSE, FORCE_DENSE = 0, 1, 2
+RELU = 1
+
+_FORCE = {"auto": FORCE_AUTO, "sparse": FORCE_SPARSE, "dense": FORCE_DENSE,
+          FORCE_AUTO: FORCE_AUTO, FORCE_SPARSE: FORCE_SPARSE, FORCE_DENSE: FORCE_DENSE}
+
+
+class DualGCNError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {status_str(status)} ({status})"
+                         + (f", hip error {_lib.dualgcn_last_hip_error()}" if status == ERR_HIP else ""))
+
+
+class Csr(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("nnz", ctypes.c_int64), ("rowptr", ctypes.c_void_p),
+                ("col", ctypes.c_void_p), ("val", ctypes.c_void_p)]
+
+
+class Thresholds(ctypes.Structure):
+    _fields_ = [("alpha_num", ctypes.c_uint32), ("alpha_den", ctypes.c_uint32),
+                ("beta_num", ctypes.c_uint32), ("beta_den", ctypes.c_uint32),
+                ("force_mode", ctypes.c_int32)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("nnz", ctypes.c_int64), ("n_sparse", ctypes.c_int32),
+                ("n_dense", ctypes.c_int32), ("kstar", ctypes.c_uint64),
+                ("s1_hi", ctypes.c_uint64), ("s1_lo", ctypes.c_uint64),
+                ("s2_hi", ctypes.c_uint64), ("s2_lo", ctypes.c_uint64), ("kmax", ctypes.c_uint64),
+                ("alpha_num", ctypes.c_uint32), ("alpha_den", ctypes.c_uint32),
+                ("beta_num", ctypes.c_uint32), ("beta_den", ctypes.c_uint32),
+                ("force_mode", ctypes.c_int32), ("seed", ctypes.c_uint64),
+                ("walks_per_node", ctypes.c_uint32), ("walk_len", ctypes.c_uint32),
+                ("max_degree", ctypes.c_int32), ("dense_chunk", ctypes.c_int32),
+                ("n_split_rows", ctypes.c_int32), ("n_split_parts", ctypes.c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_01983_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, U32, U64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64, \
+        ctypes.c_size_t
+    sig = {
+        "dualgcn_status_str": ([ctypes.c_int], ctypes.c_char_p),
+        "dualgcn_last_hip_error": ([], ctypes.c_int),
+        "dualgcn_partition": ([ctypes.POINTER(Csr), U64, U32, U32, ctypes.POINTER(Thresholds), P,
+                               ctypes.POINTER(P)], ctypes.c_int),
+        "dualgcn_plan_destroy": ([P], None),
+        "dualgcn_spmm": ([P, P, P, I32, P], ctypes.c_int),
+        "dualgcn_gcn_layer_workspace": ([P, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
+        "dualgcn_gcn_layer": ([P, P, P, P, I32, I32, U32, P, SZ, P], ctypes.c_int),
+        "dualgcn_plan_query": ([P, ctypes.POINTER(PlanInfo)], ctypes.c_int),
+        "dualgcn_plan_export": ([P, P, P, P], ctypes.c_int),
+        "dualgcn_arw_patterns": ([ctypes.POINTER(Csr), U64, U32, U32, P, P], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    return L
+
+
+_lib = _load()
+
+
+def lib():
+    return _lib
+
+
+def status_str(status):
+    return _lib.dualgcn_status_str(status).decode()
+
+
+def _check(status, what):
+    if status != OK:
+        raise DualGCNError(status, what)
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, dtype, name):
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def make_csr(rowptr, col, val):
+    _dev(rowptr, torch.int32, "rowptr")
+    _dev(col, torch.int32, "col")
+    _dev(val, torch.float32, "val")
+    n = rowptr.numel() - 1
+    return Csr(n, col.numel(), rowptr.data_ptr(), col.data_ptr() if col.numel() else None,
+               val.data_ptr() if val.numel() else None)
+
+
+class Plan:
+    """The dual-metric partition of one CSR matrix (device arrays, borrowed)."""
+
+    def __init__(self, rowptr, col, val, seed=0, walks_per_node=16, walk_len=5,
+                 alpha=(1, 2), beta=(1, 2), force_mode="auto", stream=None):
+        self._keep = (rowptr, col, val)        # the plan borrows these arrays
+        self.csr = make_csr(rowptr, col, val)
+        self.n = self.csr.n
+        th = Thresholds(alpha[0], alpha[1], beta[0], beta[1], _FORCE[force_mode])
+        out = ctypes.c_void_p()
+        _check(_lib.dualgcn_partition(ctypes.byref(self.csr), seed, walks_per_node, walk_len,
+                                      ctypes.byref(th), _stream(stream), ctypes.byref(out)),
+               "dualgcn_partition")
+        self._h = out
+
+    @property
+    def handle(self):
+        if not self._h:
+            raise ValueError("plan destroyed")
+        return self._h
+
+    def info(self):
+        pi = PlanInfo()
+        _check(_lib.dualgcn_plan_query(self.handle, ctypes.byref(pi)), "dualgcn_plan_query")
+        d = {name: getattr(pi, name) for name, _ in PlanInfo._fields_}
+        d["s1"] = (d.pop("s1_hi") << 64) | d.pop("s1_lo")
+        d["s2"] = (d.pop("s2_hi") << 64) | d.pop("s2_lo")
+        return d
+
+    def export(self):
+        """(perm int32[n], S uint32[n], K uint64[n]) as numpy arrays."""
+        import numpy as np
+        perm = np.empty(self.n, dtype=np.int32)
+        S = np.empty(self.n, dtype=np.uint32)
+        K = np.empty(self.n, dtype=np.uint64)
+        _check(_lib.dualgcn_plan_export(self.handle, perm.ctypes.data, S.ctypes.data,
+                                        K.ctypes.data), "dualgcn_plan_export")
+        return perm, S, K
+
+    def destroy(self):
+        if getattr(self, "_h", None):
+            _lib.dualgcn_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def spmm(plan, X, Y=None, stream=None):
+    """Y = A X on the plan's matrix.  X: float32 [n, F] on the device."""
+    _dev(X, torch.float32, "X")
+    if X.dim() != 2 or X.shape[0] != plan.n:
+        raise ValueError("X must be [n, F]")
+    if Y is None:
+        Y = torch.empty_like(X)
+    _dev(Y, torch.float32, "Y")
+    if Y.shape != X.shape:
+        raise ValueError("Y must have X's shape")
+    _check(_lib.dualgcn_spmm(plan.handle, X.data_ptr(), Y.data_ptr(), X.shape[1], _stream(stream)),
+           "dualgcn_spmm")
+    return Y
+
+
+def gcn_layer_workspace_bytes(plan, F_in, F_out):
+    nbytes = ctypes.c_size_t()
+    _check(_lib.dualgcn_gcn_layer_workspace(plan.handle, F_in, F_out, ctypes.byref(nbytes)),
+           "dualgcn_gcn_layer_workspace")
+    return nbytes.value
+
+
+def gcn_layer(plan, X, W, relu=False, Y=None, workspace=None, stream=None):
+    """Y = act(A (X W)) with X W on the bf16 matrix cores (float32 accumulation)."""
+    _dev(X, torch.float32, "X")
+    _dev(W, torch.float32, "W")
+    F_in, F_out = W.shape
+    if X.shape != (plan.n, F_in):
+        raise ValueError("X must be [n, F_in]")
+    if Y is None:
+        Y = torch.empty((plan.n, F_out), dtype=torch.float32, device=X.device)
+    _dev(Y, torch.float32, "Y")
+    need = gcn_layer_workspace_bytes(plan, F_in, F_out)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    _dev(workspace, torch.uint8, "workspace")
+    _check(_lib.dualgcn_gcn_layer(plan.handle, X.data_ptr(), W.data_ptr(), Y.data_ptr(), F_in,
+                                  F_out, RELU if relu else 0, workspace.data_ptr(),
+                                  workspace.numel(), _stream(stream)), "dualgcn_gcn_layer")
+    return Y
+
+
+def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
+    """uint8 [n, k, d+1] anonymous walks (labels) of every node, on the device."""
+    csr = make_csr(rowptr, col, val)
+    out = torch.empty((csr.n, walks_per_node, walk_len + 1), dtype=torch.uint8,
+                      device=rowptr.device)
+    _check(_lib.dualgcn_arw_patterns(ctypes.byref(csr), seed, walks_per_node, walk_len,
+                                     out.data_ptr(), _stream(stream)), "dualgcn_arw_patterns")
+    return out
+
+
+__all__ = ["Plan", "spmm", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
+           "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
+           "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU"]

@@ -1,0 +1,242 @@
+// C ABI of libdualgcn: argument checks, status codes and dispatch to the kernels.
+// Every check that needs no device runs before the device is touched.
+#include <new>
+
+#include "internal.h"
+
+namespace dgc {
+
+namespace {
+thread_local int g_last_hip_error = 0;
+}
+
+int hip_status(hipError_t e) {
+    if (e == hipSuccess) return DUALGCN_OK;
+    g_last_hip_error = static_cast<int>(e);
+    if (e == hipErrorOutOfMemory) return DUALGCN_ERR_OOM;
+    if (e == hipErrorNoDevice || e == hipErrorInvalidDevice) return DUALGCN_ERR_NO_DEVICE;
+    return DUALGCN_ERR_HIP;
+}
+
+int device_status() {
+    int count = 0;
+    const hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess || count <= 0) {
+        if (e != hipSuccess) g_last_hip_error = static_cast<int>(e);
+        return DUALGCN_ERR_NO_DEVICE;
+    }
+    return DUALGCN_OK;
+}
+
+int alloc_bytes(void **p, size_t bytes) {
+    *p = nullptr;
+    const hipError_t e = hipMalloc(p, bytes ? bytes : 1);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        g_last_hip_error = static_cast<int>(e);
+        return e == hipErrorOutOfMemory ? DUALGCN_ERR_OOM : DUALGCN_ERR_HIP;
+    }
+    return DUALGCN_OK;
+}
+
+}  // namespace dgc
+
+using dgc::Plan;
+
+namespace {
+
+constexpr uint32_t kMaxRational = 1u << 16;
+
+int check_csr(const dualgcn_csr *c) {
+    if (!c || !c->rowptr) return DUALGCN_ERR_INVALID_ARG;
+    if (c->n < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (c->nnz < 0) return DUALGCN_ERR_INVALID_ARG;
+    if (c->nnz >= (static_cast<int64_t>(1) << 31)) return DUALGCN_ERR_UNSUPPORTED;
+    if (c->nnz > 0 && (!c->col || !c->val)) return DUALGCN_ERR_INVALID_ARG;
+    return DUALGCN_OK;
+}
+
+int check_walks(uint32_t k, uint32_t d) {
+    if (k < 1 || d < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (d > 255) return DUALGCN_ERR_UNSUPPORTED;
+    return DUALGCN_OK;
+}
+
+// q k max(d + 1, nnz) < 2^63 keeps every key K_v = p S_v + (q - p) k D_v in 63 bits.
+bool keys_fit(uint32_t q, uint32_t k, uint32_t d, int64_t nnz) {
+    const dgc::u128 m = static_cast<dgc::u128>(q) * k *
+                        static_cast<dgc::u128>(nnz > static_cast<int64_t>(d) + 1 ? nnz : d + 1);
+    return m < (static_cast<dgc::u128>(1) << 63);
+}
+
+int check_plan(const dualgcn_plan *plan) {
+    return plan ? DUALGCN_OK : DUALGCN_ERR_INVALID_ARG;
+}
+
+const Plan *as_plan(const dualgcn_plan *p) { return reinterpret_cast<const Plan *>(p); }
+
+}  // namespace
+
+extern "C" {
+
+const char *dualgcn_status_str(int status) {
+    switch (status) {
+        case DUALGCN_OK: return "ok";
+        case DUALGCN_ERR_INVALID_ARG: return "invalid argument";
+        case DUALGCN_ERR_BAD_CSR: return "malformed CSR matrix";
+        case DUALGCN_ERR_UNSUPPORTED: return "unsupported size or parameter";
+        case DUALGCN_ERR_OOM: return "device out of memory";
+        case DUALGCN_ERR_HIP: return "HIP runtime error";
+        case DUALGCN_ERR_NO_DEVICE: return "no HIP device";
+        default: return "unknown status";
+    }
+}
+
+int dualgcn_last_hip_error(void) { return dgc::g_last_hip_error; }
+
+int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,
+                      uint32_t walk_len, const dualgcn_thresholds *th, void *stream,
+                      dualgcn_plan **out) {
+    if (!out) return DUALGCN_ERR_INVALID_ARG;
+    *out = nullptr;
+    int st = check_csr(csr);
+    if (st) return st;
+    if ((st = check_walks(walks_per_node, walk_len))) return st;
+    dualgcn_thresholds t{1, 2, 1, 2, DUALGCN_FORCE_AUTO};
+    if (th) t = *th;
+    if (t.alpha_den == 0 || t.beta_den == 0 || t.alpha_num > t.alpha_den) return DUALGCN_ERR_INVALID_ARG;
+    if (t.alpha_den >= kMaxRational || t.beta_den >= kMaxRational || t.beta_num >= kMaxRational)
+        return DUALGCN_ERR_INVALID_ARG;
+    if (t.force_mode < DUALGCN_FORCE_AUTO || t.force_mode > DUALGCN_FORCE_DENSE)
+        return DUALGCN_ERR_INVALID_ARG;
+    if (!keys_fit(t.alpha_den, walks_per_node, walk_len, csr->nnz)) return DUALGCN_ERR_UNSUPPORTED;
+    if ((st = dgc::device_status())) return st;
+    Plan *p = nullptr;
+    st = dgc::build_plan(csr, seed, walks_per_node, walk_len, t,
+                         static_cast<hipStream_t>(stream), &p);
+    if (st) return st;
+    *out = reinterpret_cast<dualgcn_plan *>(p);
+    return DUALGCN_OK;
+}
+
+void dualgcn_plan_destroy(dualgcn_plan *plan) {
+    if (!plan) return;
+    (void)hipDeviceSynchronize();
+    dgc::free_plan(reinterpret_cast<Plan *>(plan));
+}
+
+int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, void *stream) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if (!X || !Y || F < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (F >= (1 << 20)) return DUALGCN_ERR_UNSUPPORTED;
+    const Plan *p = as_plan(plan);
+    const size_t bytes = static_cast<size_t>(p->n) * F * sizeof(float);
+    const char *x = reinterpret_cast<const char *>(X);
+    const char *y = reinterpret_cast<const char *>(Y);
+    if (x < y + bytes && y < x + bytes) return DUALGCN_ERR_INVALID_ARG;   // overlap
+    if ((st = dgc::device_status())) return st;
+    return dgc::launch_spmm(*p, X, Y, F, false, static_cast<hipStream_t>(stream));
+}
+
+int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,
+                                size_t *bytes) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if (!bytes || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
+    *bytes = dgc::xw_workspace_bytes(as_plan(plan)->n, F_in, F_out);
+    return DUALGCN_OK;
+}
+
+int dualgcn_gcn_layer(const dualgcn_plan *plan, const float *X, const float *W, float *Y,
+                      int32_t F_in, int32_t F_out, uint32_t flags, void *workspace,
+                      size_t workspace_bytes, void *stream) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if (!X || !W || !Y || !workspace || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (flags & ~DUALGCN_RELU) return DUALGCN_ERR_INVALID_ARG;
+    if (F_in % 32 || F_out % 32 || F_in > 1024 || F_out > 256) return DUALGCN_ERR_UNSUPPORTED;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 || reinterpret_cast<uintptr_t>(X) % 16)
+        return DUALGCN_ERR_INVALID_ARG;
+    const Plan *p = as_plan(plan);
+    if (workspace_bytes < dgc::xw_workspace_bytes(p->n, F_in, F_out)) return DUALGCN_ERR_INVALID_ARG;
+    if ((st = dgc::device_status())) return st;
+    return dgc::launch_gcn_layer(*p, X, W, Y, F_in, F_out, (flags & DUALGCN_RELU) != 0, workspace,
+                                 static_cast<hipStream_t>(stream));
+}
+
+int dualgcn_plan_query(const dualgcn_plan *plan, dualgcn_plan_info *out) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if (!out) return DUALGCN_ERR_INVALID_ARG;
+    const Plan *p = as_plan(plan);
+    dualgcn_plan_info i{};
+    i.n = p->n;
+    i.nnz = p->nnz;
+    i.n_sparse = p->n_sparse;
+    i.n_dense = p->n - p->n_sparse;
+    i.kstar = p->kstar;
+    i.s1_hi = static_cast<uint64_t>(p->s1 >> 64);
+    i.s1_lo = static_cast<uint64_t>(p->s1);
+    i.s2_hi = static_cast<uint64_t>(p->s2 >> 64);
+    i.s2_lo = static_cast<uint64_t>(p->s2);
+    i.kmax = p->kmax;
+    i.alpha_num = p->th.alpha_num;
+    i.alpha_den = p->th.alpha_den;
+    i.beta_num = p->th.beta_num;
+    i.beta_den = p->th.beta_den;
+    i.force_mode = p->th.force_mode;
+    i.seed = p->seed;
+    i.walks_per_node = p->k;
+    i.walk_len = p->d;
+    i.max_degree = p->max_degree;
+    i.dense_chunk = dgc::kDenseChunk;
+    i.n_split_rows = p->n_split_rows;
+    i.n_split_parts = p->n_split_parts;
+    *out = i;
+    return DUALGCN_OK;
+}
+
+int dualgcn_plan_export(const dualgcn_plan *plan, int32_t *perm_h, uint32_t *S_h, uint64_t *K_h) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if ((st = dgc::device_status())) return st;
+    const Plan *p = as_plan(plan);
+    const size_t n = static_cast<size_t>(p->n);
+    if ((st = dgc::hip_status(hipDeviceSynchronize()))) return st;
+    if (perm_h && (st = dgc::hip_status(hipMemcpy(perm_h, p->perm, n * 4, hipMemcpyDeviceToHost))))
+        return st;
+    if (S_h && (st = dgc::hip_status(hipMemcpy(S_h, p->S, n * 4, hipMemcpyDeviceToHost)))) return st;
+    if (K_h && (st = dgc::hip_status(hipMemcpy(K_h, p->K, n * 8, hipMemcpyDeviceToHost)))) return st;
+    return DUALGCN_OK;
+}
+
+int dualgcn_arw_patterns(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,
+                         uint32_t walk_len, uint8_t *out, void *stream) {
+    int st = check_csr(csr);
+    if (st) return st;
+    if ((st = check_walks(walks_per_node, walk_len))) return st;
+    if (!out) return DUALGCN_ERR_INVALID_ARG;
+    const dgc::u128 total = static_cast<dgc::u128>(csr->n) * walks_per_node * (walk_len + 1);
+    if (total >= (static_cast<dgc::u128>(1) << 40)) return DUALGCN_ERR_UNSUPPORTED;
+    if ((st = dgc::device_status())) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *scratch = nullptr;   // [n] sums + 2 validation words
+    if ((st = dgc::alloc_bytes(&scratch, sizeof(uint32_t) * (static_cast<size_t>(csr->n) + 2))))
+        return st;
+    uint32_t *S = static_cast<uint32_t *>(scratch);
+    int32_t *flags = reinterpret_cast<int32_t *>(S + csr->n);
+    st = dgc::hip_status(hipMemsetAsync(flags, 0, 2 * sizeof(int32_t), s));
+    if (!st) st = dgc::validate_csr(csr, flags, s);
+    if (!st)
+        st = dgc::launch_arw(csr->rowptr, csr->col, csr->n, seed, walks_per_node, walk_len, S, out,
+                             flags, s);
+    int32_t bad = 0;
+    if (!st) st = dgc::hip_status(hipMemcpyAsync(&bad, flags, sizeof(bad), hipMemcpyDeviceToHost, s));
+    if (!st) st = dgc::hip_status(hipStreamSynchronize(s));
+    (void)hipFree(scratch);
+    if (!st && bad) st = DUALGCN_ERR_BAD_CSR;
+    return st;
+}
+
+}  // extern "C"

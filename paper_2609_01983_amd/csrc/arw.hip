@@ -1,0 +1,156 @@
+// Anonymous random walks and neighbour-density sums on gfx950.
+//
+// DualGCN Sec. 3.2 ("Theoretical Foundation", Theorem 1, "Neighbor Density"):
+// a walk repeatedly moves to a random neighbour and labels every visited node
+// by the order of its first occurrence; the density of node v is the mean
+// number of distinct nodes over its k walks, N_v = S_v / k.
+//
+// One lane runs one (node, walk) pair.  Lanes of a node are adjacent, so when
+// k is a power of two no larger than 64 the k counts are summed with
+// cross-lane shuffles and written with one plain store; otherwise each lane
+// adds its count with an integer atomic (order-independent, hence exact).
+//
+// Random stream: step s of walk w from v uses 64-bit word (s mod 4) of the
+// Philox-4x64-10 block (Salmon, Moraes, Dror & Shaw, SC'11) with counter
+// (v, w, floor(s/4), 0) and key (seed, 0).  The neighbour is entry
+// floor(r * deg / 2^64) of the current row (uniform over stored entries); an
+// empty row keeps the walk in place.
+#include "internal.h"
+
+namespace dgc {
+namespace {
+
+// Philox-4x64 multipliers and Weyl key increments, as published.
+constexpr uint64_t kPhiloxM0 = 0xD2E7470EE14C6C93ull;
+constexpr uint64_t kPhiloxM1 = 0xCA5A826395121157ull;
+constexpr uint64_t kPhiloxW0 = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kPhiloxW1 = 0xBB67AE8584CAA73Bull;
+
+struct Block4 {
+    uint64_t w[4];
+};
+
+__device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2,
+                                                uint64_t c3, uint64_t k0, uint64_t k1) {
+#pragma unroll
+    for (int round = 0; round < 10; ++round) {
+        const uint64_t lo0 = kPhiloxM0 * c0;
+        const uint64_t hi0 = __umul64hi(kPhiloxM0, c0);
+        const uint64_t lo1 = kPhiloxM1 * c2;
+        const uint64_t hi1 = __umul64hi(kPhiloxM1, c2);
+        const uint64_t n0 = hi1 ^ c1 ^ k0;
+        const uint64_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+        k0 += kPhiloxW0;
+        k1 += kPhiloxW1;
+    }
+    return Block4{{c0, c1, c2, c3}};
+}
+
+// One walk of `d` steps (d <= MAXD).  Returns the number of distinct nodes.
+// path[i] is the i-th visited node and lab[i] its label; a revisited node takes
+// the label of any earlier position holding it.  With UNROLL the arrays are
+// indexed only by compile-time positions and stay in registers.
+template <int MAXD, bool UNROLL>
+__device__ __forceinline__ uint32_t walk_one(const int32_t *__restrict__ rowptr,
+                                             const int32_t *__restrict__ col, uint32_t v,
+                                             uint32_t w, uint32_t d, uint64_t seed,
+                                             uint8_t *__restrict__ pat) {
+    int32_t path[MAXD + 1];
+    uint8_t lab[MAXD + 1];
+    path[0] = static_cast<int32_t>(v);
+    lab[0] = 1;
+    if (pat) pat[0] = 1;
+    uint32_t distinct = 1;
+    int32_t cur = static_cast<int32_t>(v);
+    Block4 blk{};
+    constexpr int kUnrollSteps = UNROLL ? MAXD : 1;
+#pragma unroll kUnrollSteps
+    for (int s = 0; s < MAXD; ++s) {
+        if (static_cast<uint32_t>(s) >= d) break;
+        if ((s & 3) == 0) blk = philox4x64_10(v, w, static_cast<uint64_t>(s >> 2), 0, seed, 0);
+        const uint64_t r = blk.w[s & 3];
+        const int32_t b = rowptr[cur];
+        const int32_t e = rowptr[cur + 1];
+        int32_t nxt = cur;
+        if (e > b) nxt = col[b + static_cast<int32_t>(__umul64hi(r, static_cast<uint64_t>(e - b)))];
+        uint8_t label = 0;
+#pragma unroll kUnrollSteps
+        for (int i = 0; i <= s; ++i)
+            if (path[i] == nxt) label = lab[i];
+        if (label == 0) label = static_cast<uint8_t>(++distinct);
+        path[s + 1] = nxt;
+        lab[s + 1] = label;
+        if (pat) pat[s + 1] = label;
+        cur = nxt;
+    }
+    return distinct;
+}
+
+template <int MAXD, bool UNROLL>
+__global__ __launch_bounds__(256) void arw_kernel(const int32_t *__restrict__ rowptr,
+                                                  const int32_t *__restrict__ col, int32_t n,
+                                                  uint64_t seed, uint32_t k, uint32_t d,
+                                                  int k_log2, uint32_t *__restrict__ S,
+                                                  uint8_t *__restrict__ patterns,
+                                                  const int32_t *__restrict__ bad_flag) {
+    if (*bad_flag) return;  // the CSR failed validation: touch nothing
+    const int64_t gid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t total = static_cast<int64_t>(n) * k;
+    const bool valid = gid < total;
+    uint32_t v = 0, w = 0, u = 0;
+    if (valid) {
+        if (k_log2 >= 0) {
+            v = static_cast<uint32_t>(gid >> k_log2);
+            w = static_cast<uint32_t>(gid & ((1 << k_log2) - 1));
+        } else {
+            v = static_cast<uint32_t>(gid / k);
+            w = static_cast<uint32_t>(gid - static_cast<int64_t>(v) * k);
+        }
+        uint8_t *pat = patterns ? patterns + gid * (d + 1) : nullptr;
+        u = walk_one<MAXD, UNROLL>(rowptr, col, v, w, d, seed, pat);
+    }
+    if (k_log2 >= 0 && k_log2 <= 6) {
+        // the k lanes of a node are adjacent and aligned inside the wavefront
+        for (int off = 1; off < (1 << k_log2); off <<= 1) u += __shfl_xor(u, off, 64);
+        if (valid && w == 0) S[v] = u;
+    } else if (valid) {
+        atomicAdd(&S[v], u);
+    }
+}
+
+}  // namespace
+
+int launch_arw(const int32_t *rowptr, const int32_t *col, int32_t n, uint64_t seed, uint32_t k,
+               uint32_t d, uint32_t *S, uint8_t *patterns, const int32_t *bad_flag,
+               hipStream_t stream) {
+    int k_log2 = -1;
+    if ((k & (k - 1)) == 0) {
+        k_log2 = 0;
+        while ((1u << k_log2) < k) ++k_log2;
+    }
+    const bool shuffle_sum = k_log2 >= 0 && k_log2 <= 6;
+    if (!shuffle_sum) {
+        int st = hip_status(hipMemsetAsync(S, 0, sizeof(uint32_t) * static_cast<size_t>(n), stream));
+        if (st) return st;
+    }
+    const int64_t total = static_cast<int64_t>(n) * k;
+    const int64_t blocks = (total + 255) / 256;
+    if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
+    const dim3 grid(static_cast<unsigned>(blocks)), block(256);
+    if (d <= 8)
+        hipLaunchKernelGGL((arw_kernel<8, true>), grid, block, 0, stream, rowptr, col, n, seed, k,
+                           d, k_log2, S, patterns, bad_flag);
+    else if (d <= 32)
+        hipLaunchKernelGGL((arw_kernel<32, true>), grid, block, 0, stream, rowptr, col, n, seed,
+                           k, d, k_log2, S, patterns, bad_flag);
+    else
+        hipLaunchKernelGGL((arw_kernel<255, false>), grid, block, 0, stream, rowptr, col, n,
+                           seed, k, d, k_log2, S, patterns, bad_flag);
+    return hip_status(hipGetLastError());
+}
+
+}  // namespace dgc

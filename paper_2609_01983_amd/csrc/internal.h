@@ -1,0 +1,85 @@
+// Internal declarations shared by the translation units of libdualgcn.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "dualgcn.h"
+
+namespace dgc {
+
+using u128 = unsigned __int128;
+
+// Entries of one CSR row handled by one dense-region workgroup; longer rows are
+// split into parts of this many entries and combined in a fixed order.
+constexpr int kDenseChunk = 4096;
+// Widest feature slice one SpMM launch covers; wider F is processed in slices.
+constexpr int kMaxSlice = 256;
+
+// One part of a split dense row: row id, part index, number of parts, index of
+// the row's first part (which owns the arrival counter).
+struct SplitPart {
+    int32_t row;
+    int32_t part;
+    int32_t nparts;
+    int32_t first;
+};
+
+struct Plan {
+    int device = 0;
+    int32_t n = 0;
+    int64_t nnz = 0;
+    const int32_t *rowptr = nullptr;   // borrowed
+    const int32_t *col = nullptr;      // borrowed
+    const float *val = nullptr;        // borrowed
+
+    uint32_t *S = nullptr;             // [n] density sums
+    uint64_t *K = nullptr;             // [n] hybrid keys
+    int32_t *perm = nullptr;           // [n] nodes sorted by (K, v)
+
+    int32_t n_sparse = 0;
+    int32_t n_split_rows = 0;
+    int32_t n_split_parts = 0;
+    SplitPart *parts = nullptr;        // [n_split_parts]
+    int32_t *counters = nullptr;       // [n_split_parts] arrival counters (zero between calls)
+    double *partials = nullptr;        // [n_split_parts][kMaxSlice]
+
+    uint64_t kstar = 0, kmax = 0;
+    u128 s1 = 0, s2 = 0;
+    dualgcn_thresholds th{};
+    uint64_t seed = 0;
+    uint32_t k = 0, d = 0;
+    int32_t max_degree = 0;
+};
+
+// ---- status helpers (api.hip)
+int hip_status(hipError_t e);          // records e; returns DUALGCN_OK or DUALGCN_ERR_HIP
+int device_status();                   // DUALGCN_OK or DUALGCN_ERR_NO_DEVICE / _HIP
+int alloc_bytes(void **p, size_t bytes);  // DUALGCN_OK or DUALGCN_ERR_OOM / _HIP
+
+// ---- anonymous walks (arw.hip)
+// S[v] = sum over k walks of distinct-node counts; patterns (may be null) receives labels.
+int launch_arw(const int32_t *rowptr, const int32_t *col, int32_t n, uint64_t seed, uint32_t k,
+               uint32_t d, uint32_t *S, uint8_t *patterns, const int32_t *bad_flag,
+               hipStream_t stream);
+
+// ---- partition (partition.hip)
+// Checks the CSR on the device: flags[0] |= 1 (row pointers) | 2 (columns);
+// flags[1] = max(flags[1], largest row length).  flags must start at zero.
+int validate_csr(const dualgcn_csr *csr, int32_t *flags, hipStream_t stream);
+int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
+               const dualgcn_thresholds &th, hipStream_t stream, Plan **out);
+void free_plan(Plan *p);
+
+// ---- SpMM (spmm.hip): Y = A X on one plan, optional ReLU on the result.
+int launch_spmm(const Plan &p, const float *X, float *Y, int32_t F, bool relu,
+                hipStream_t stream);
+
+// ---- update phase (xw.hip)
+size_t xw_workspace_bytes(int32_t n, int32_t F_in, int32_t F_out);
+int launch_gcn_layer(const Plan &p, const float *X, const float *W, float *Y, int32_t F_in,
+                     int32_t F_out, bool relu, void *workspace, hipStream_t stream);
+
+}  // namespace dgc

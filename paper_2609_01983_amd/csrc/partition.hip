@@ -1,0 +1,620 @@
+// Dual-metric partition on gfx950 (DualGCN Sec. 3.2 and Sec. 3.3 Eq. (1)).
+//
+// Pipeline (one stream, two host waits):
+//   validate        rowptr / col checks and the largest degree        -> flag
+//   walks           S_v (arw.hip)
+//   keys            K_v = p S_v + (q - p) k D_v, D_v from the row pointers, and the
+//                   exact 128-bit sums of K and K^2 per workgroup, then one
+//                   workgroup folds them                              -> host wait 1
+//   host            K* = least integer >= mu_K + beta sigma_K (exact integers)
+//   radix sort      stable LSD sort of (K_v, v) on 8-bit digits      -> perm
+//   split           n_sparse = lower_bound(sorted K, K*); dense rows longer than
+//                   one dense chunk are listed as parts               -> host wait 2
+//
+// Everything is integer arithmetic, so the plan does not depend on launch order
+// or reduction order: it is the unique sort of (K_v, v) cut at K*.
+#include "internal.h"
+
+#include <algorithm>
+#include <cstring>
+
+namespace dgc {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kItems = 16;                    // items per thread in tiled kernels
+constexpr int kTile = kThreads * kItems;      // 4096
+constexpr int kRadixBits = 8;
+constexpr int kRadix = 1 << kRadixBits;
+
+// ------------------------------------------------------------------ validation
+
+__global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__restrict__ rowptr,
+                                                            const int32_t *__restrict__ col,
+                                                            int32_t n, int64_t nnz,
+                                                            int32_t *__restrict__ flag,
+                                                            int32_t *__restrict__ maxdeg) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    int32_t bad = 0, dmax = 0;
+    for (int64_t i = t0; i < n; i += stride) {
+        const int32_t a = rowptr[i], b = rowptr[i + 1];
+        if (b < a) bad |= 1;
+        dmax = max(dmax, b - a);
+    }
+    if (t0 == 0) {
+        if (rowptr[0] != 0) bad |= 1;
+        if (static_cast<int64_t>(rowptr[n]) != nnz) bad |= 1;
+    }
+    for (int64_t p = t0; p < nnz; p += stride) {
+        const int32_t c = col[p];
+        if (c < 0 || c >= n) bad |= 2;
+    }
+    if (bad) atomicOr(flag, bad);
+    if (dmax) atomicMax(maxdeg, dmax);
+}
+
+// ------------------------------------------------------------------ keys and moments
+
+struct Moments {
+    uint64_t s1_lo, s1_hi, s2_lo, s2_hi, kmax;
+};
+
+__host__ __device__ __forceinline__ u128 join(uint64_t lo, uint64_t hi) {
+    return (static_cast<u128>(hi) << 64) | lo;
+}
+
+__global__ __launch_bounds__(kThreads) void keys_kernel(
+    const int32_t *__restrict__ rowptr, const uint32_t *__restrict__ S, int32_t n, uint64_t p,
+    uint64_t qmp_k, uint64_t *__restrict__ K, Moments *__restrict__ partial,
+    const int32_t *__restrict__ bad_flag) {
+    __shared__ u128 sh1[kThreads], sh2[kThreads];
+    __shared__ uint64_t shm[kThreads];
+    u128 s1 = 0, s2 = 0;
+    uint64_t kmax = 0;
+    if (*bad_flag == 0) {
+        const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+        for (int64_t v = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; v < n;
+             v += stride) {
+            const uint64_t deg = static_cast<uint64_t>(rowptr[v + 1] - rowptr[v]);
+            const uint64_t key = p * S[v] + qmp_k * deg;
+            K[v] = key;
+            s1 += key;
+            s2 += static_cast<u128>(key) * key;
+            kmax = key > kmax ? key : kmax;
+        }
+    }
+    const int t = threadIdx.x;
+    sh1[t] = s1;
+    sh2[t] = s2;
+    shm[t] = kmax;
+    __syncthreads();
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        if (t < h) {
+            sh1[t] += sh1[t + h];
+            sh2[t] += sh2[t + h];
+            shm[t] = shm[t] > shm[t + h] ? shm[t] : shm[t + h];
+        }
+        __syncthreads();
+    }
+    if (t == 0) {
+        partial[blockIdx.x] = Moments{static_cast<uint64_t>(sh1[0]),
+                                      static_cast<uint64_t>(sh1[0] >> 64),
+                                      static_cast<uint64_t>(sh2[0]),
+                                      static_cast<uint64_t>(sh2[0] >> 64), shm[0]};
+    }
+}
+
+struct Summary {
+    Moments m;
+    int32_t flag;
+    int32_t maxdeg;
+};
+
+__global__ __launch_bounds__(kThreads) void fold_kernel(const Moments *__restrict__ partial,
+                                                        int32_t count,
+                                                        const int32_t *__restrict__ flag,
+                                                        const int32_t *__restrict__ maxdeg,
+                                                        Summary *__restrict__ out) {
+    __shared__ u128 sh1[kThreads], sh2[kThreads];
+    __shared__ uint64_t shm[kThreads];
+    const int t = threadIdx.x;
+    u128 s1 = 0, s2 = 0;
+    uint64_t kmax = 0;
+    for (int i = t; i < count; i += kThreads) {
+        s1 += join(partial[i].s1_lo, partial[i].s1_hi);
+        s2 += join(partial[i].s2_lo, partial[i].s2_hi);
+        kmax = partial[i].kmax > kmax ? partial[i].kmax : kmax;
+    }
+    sh1[t] = s1;
+    sh2[t] = s2;
+    shm[t] = kmax;
+    __syncthreads();
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        if (t < h) {
+            sh1[t] += sh1[t + h];
+            sh2[t] += sh2[t + h];
+            shm[t] = shm[t] > shm[t + h] ? shm[t] : shm[t + h];
+        }
+        __syncthreads();
+    }
+    if (t == 0) {
+        out->m = Moments{static_cast<uint64_t>(sh1[0]), static_cast<uint64_t>(sh1[0] >> 64),
+                         static_cast<uint64_t>(sh2[0]), static_cast<uint64_t>(sh2[0] >> 64),
+                         shm[0]};
+        out->flag = *flag;
+        out->maxdeg = *maxdeg;
+    }
+}
+
+// ------------------------------------------------------------------ block scan helpers
+
+// Exclusive scan of one value per thread across a 256-thread workgroup.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t *total,
+                                                         uint32_t *sh_waves) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t inc = x;
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(inc, off, 64);
+        if (lane >= off) inc += y;
+    }
+    if (lane == 63) sh_waves[wave] = inc;
+    __syncthreads();
+    uint32_t wave_base = 0, sum = 0;
+    for (int i = 0; i < kThreads / 64; ++i) {
+        if (i < wave) wave_base += sh_waves[i];
+        sum += sh_waves[i];
+    }
+    __syncthreads();
+    *total = sum;
+    return wave_base + inc - x;
+}
+
+// Tile sums of a u32 array (tiles of kTile elements).
+__global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const uint32_t *__restrict__ in,
+                                                               int64_t count,
+                                                               uint32_t *__restrict__ sums) {
+    __shared__ uint32_t shw[kThreads / 64];
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile;
+    uint32_t s = 0;
+    for (int i = 0; i < kItems; ++i) {
+        const int64_t idx = base + static_cast<int64_t>(threadIdx.x) * kItems + i;
+        if (idx < count) s += in[idx];
+    }
+    uint32_t total;
+    block_exclusive_scan(s, &total, shw);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+// Exclusive scan of the tile sums by one workgroup (in place); writes the grand total.
+__global__ __launch_bounds__(kThreads) void scan_top_kernel(uint32_t *__restrict__ sums,
+                                                            int32_t count,
+                                                            uint32_t *__restrict__ grand) {
+    __shared__ uint32_t shw[kThreads / 64];
+    uint32_t carry = 0;
+    for (int32_t base = 0; base < count; base += kThreads) {
+        const int32_t i = base + threadIdx.x;
+        const uint32_t x = i < count ? sums[i] : 0;
+        uint32_t total;
+        const uint32_t ex = block_exclusive_scan(x, &total, shw);
+        if (i < count) sums[i] = carry + ex;
+        carry += total;
+    }
+    if (threadIdx.x == 0 && grand) *grand = carry;
+}
+
+// Exclusive scan inside each tile plus the tile's offset; out may alias in.
+__global__ __launch_bounds__(kThreads) void scan_apply_kernel(const uint32_t *in, int64_t count,
+                                                              const uint32_t *__restrict__ sums,
+                                                              uint32_t *out) {
+    __shared__ uint32_t shw[kThreads / 64];
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile +
+                         static_cast<int64_t>(threadIdx.x) * kItems;
+    uint32_t v[kItems];
+    uint32_t s = 0;
+    for (int i = 0; i < kItems; ++i) {
+        v[i] = base + i < count ? in[base + i] : 0;
+        s += v[i];
+    }
+    uint32_t total;
+    uint32_t run = block_exclusive_scan(s, &total, shw) + sums[blockIdx.x];
+    for (int i = 0; i < kItems; ++i) {
+        if (base + i < count) out[base + i] = run;
+        run += v[i];
+    }
+}
+
+// ------------------------------------------------------------------ radix sort of (K, v)
+
+__global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint64_t *__restrict__ keys,
+                                                              int32_t n, int shift,
+                                                              uint32_t *__restrict__ hist,
+                                                              int32_t nblocks) {
+    __shared__ uint32_t h[kRadix];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile;
+    for (int i = 0; i < kItems; ++i) {
+        const int64_t idx = base + static_cast<int64_t>(i) * kThreads + threadIdx.x;
+        if (idx < n) atomicAdd(&h[(keys[idx] >> shift) & (kRadix - 1)], 1u);
+    }
+    __syncthreads();
+    hist[static_cast<int64_t>(threadIdx.x) * nblocks + blockIdx.x] = h[threadIdx.x];
+}
+
+// Stable scatter of one 8-bit digit.  Wave w owns items [base + 1024 w, base + 1024 (w+1)),
+// taken in rounds of 64 consecutive items; lanes with equal digits find each other with
+// eight ballots, so an item's rank is (earlier items of its digit in this wave) +
+// (earlier lanes of its digit in this round).  Tile order = index order, hence stable.
+__global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
+    const uint64_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in, int32_t n,
+    int shift, const uint32_t *__restrict__ offsets, int32_t nblocks,
+    uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out) {
+    __shared__ uint32_t cnt[kThreads / 64][kRadix];
+    __shared__ uint32_t goff[kRadix];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int w = 0; w < kThreads / 64; ++w) cnt[w][threadIdx.x] = 0;
+    goff[threadIdx.x] = offsets[static_cast<int64_t>(threadIdx.x) * nblocks + blockIdx.x];
+    __syncthreads();
+
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile +
+                         static_cast<int64_t>(wave) * (kItems * 64);
+    uint32_t rank[kItems];
+    for (int j = 0; j < kItems; ++j) {
+        const int64_t idx = base + static_cast<int64_t>(j) * 64 + lane;
+        const bool valid = idx < n;
+        const uint32_t dg = valid ? static_cast<uint32_t>((keys_in[idx] >> shift) & (kRadix - 1)) : 0;
+        uint64_t m = __ballot(valid);
+        for (int b = 0; b < kRadixBits; ++b) {
+            const bool bit = (dg >> b) & 1u;
+            const uint64_t bal = __ballot(valid && bit);
+            m &= bit ? bal : ~bal;
+        }
+        const uint32_t below = static_cast<uint32_t>(__popcll(m & lt_mask));
+        const uint32_t before = valid ? cnt[wave][dg] : 0;
+        __builtin_amdgcn_wave_barrier();
+        if (valid && below == 0) cnt[wave][dg] = before + static_cast<uint32_t>(__popcll(m));
+        __builtin_amdgcn_wave_barrier();
+        rank[j] = before + below;
+    }
+    __syncthreads();
+    {   // exclusive prefix of the per-wave counts, digit by digit
+        uint32_t run = 0;
+        for (int w = 0; w < kThreads / 64; ++w) {
+            const uint32_t c = cnt[w][threadIdx.x];
+            cnt[w][threadIdx.x] = run;
+            run += c;
+        }
+    }
+    __syncthreads();
+    for (int j = 0; j < kItems; ++j) {
+        const int64_t idx = base + static_cast<int64_t>(j) * 64 + lane;
+        if (idx < n) {
+            const uint64_t key = keys_in[idx];
+            const uint32_t dg = static_cast<uint32_t>((key >> shift) & (kRadix - 1));
+            const uint32_t dest = goff[dg] + cnt[wave][dg] + rank[j];
+            if (dest < static_cast<uint32_t>(n)) {   // always true for a consistent histogram
+                keys_out[dest] = key;
+                vals_out[dest] = vals_in ? vals_in[idx] : static_cast<int32_t>(idx);
+            }
+        }
+    }
+}
+
+__global__ void iota_kernel(int32_t *__restrict__ out, int32_t n) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n) out[i] = static_cast<int32_t>(i);
+}
+
+// ------------------------------------------------------------------ split and schedule
+
+struct SplitSummary {
+    int32_t n_sparse;
+    int32_t split_rows;
+    uint32_t parts;
+    int32_t pad;
+};
+
+// n_sparse = first position whose key is >= K* (one thread; keys are sorted).
+__global__ void lower_bound_kernel(const uint64_t *__restrict__ sorted, int32_t n, uint64_t kstar,
+                                   int32_t force_sparse_count, SplitSummary *__restrict__ out) {
+    int32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (sorted[mid] < kstar) lo = mid + 1;
+        else hi = mid;
+    }
+    out->n_sparse = force_sparse_count >= 0 ? force_sparse_count : lo;
+    out->split_rows = 0;
+    out->parts = 0;
+}
+
+__global__ __launch_bounds__(kThreads) void split_count_kernel(
+    const int32_t *__restrict__ perm, const int32_t *__restrict__ rowptr, int32_t n,
+    SplitSummary *__restrict__ sum, uint32_t *__restrict__ counts) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    uint32_t c = 0;
+    if (i >= sum->n_sparse) {
+        const int32_t r = perm[i];
+        const int32_t deg = rowptr[r + 1] - rowptr[r];
+        if (deg > kDenseChunk) {
+            c = static_cast<uint32_t>((deg + kDenseChunk - 1) / kDenseChunk);
+            atomicAdd(&sum->split_rows, 1);
+        }
+    }
+    counts[i] = c;
+}
+
+__global__ __launch_bounds__(kThreads) void split_fill_kernel(
+    const int32_t *__restrict__ perm, int32_t n, const uint32_t *__restrict__ counts,
+    const uint32_t *__restrict__ offsets, SplitPart *__restrict__ parts, uint32_t n_parts) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const uint32_t c = counts[i];
+    if (c == 0) return;
+    const uint32_t off = offsets[i];
+    for (uint32_t j = 0; j < c && off + j < n_parts; ++j)
+        parts[off + j] = SplitPart{perm[i], static_cast<int32_t>(j), static_cast<int32_t>(c),
+                                   static_cast<int32_t>(off)};
+}
+
+// ------------------------------------------------------------------ host helpers
+
+struct DevBuf {
+    void *p = nullptr;
+    ~DevBuf() {
+        if (p) (void)hipFree(p);
+    }
+    template <typename T>
+    T *as() const { return static_cast<T *>(p); }
+};
+
+// Exclusive scan of `count` u32 values in place; `sums` holds one word per tile.
+// Writes the grand total to *grand (device) when grand is not null.
+int exclusive_scan(uint32_t *data, int64_t count, uint32_t *sums, uint32_t *grand,
+                   hipStream_t s) {
+    const int64_t tiles = (count + kTile - 1) / kTile;
+    if (tiles > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
+    if (tiles > 0) {
+        hipLaunchKernelGGL(scan_reduce_kernel, dim3(static_cast<unsigned>(tiles)), dim3(kThreads),
+                           0, s, data, count, sums);
+    }
+    hipLaunchKernelGGL(scan_top_kernel, dim3(1), dim3(kThreads), 0, s, sums,
+                       static_cast<int32_t>(tiles), grand);
+    if (tiles > 0) {
+        hipLaunchKernelGGL(scan_apply_kernel, dim3(static_cast<unsigned>(tiles)), dim3(kThreads),
+                           0, s, data, count, sums, data);
+    }
+    return hip_status(hipGetLastError());
+}
+
+int bit_length(uint64_t x) {
+    int b = 0;
+    while (x) {
+        ++b;
+        x >>= 1;
+    }
+    return b;
+}
+
+// Integer square root rounded up: least r with r*r >= x (digit-by-digit method).
+u128 isqrt_ceil(u128 x) {
+    u128 rem = x, root = 0, bit = static_cast<u128>(1) << 126;
+    while (bit > rem) bit >>= 2;
+    while (bit != 0) {
+        if (rem >= root + bit) {
+            rem -= root + bit;
+            root = (root >> 1) + bit;
+        } else {
+            root >>= 1;
+        }
+        bit >>= 2;
+    }
+    return root * root == x ? root : root + 1;
+}
+
+bool mul_overflows(u128 a, u128 b, u128 *out) {
+    if (a != 0 && b > (~static_cast<u128>(0)) / a) return true;
+    *out = a * b;
+    return false;
+}
+
+// K* = least integer K >= mu + (b/c) sigma over the n keys with sums s1, s2:
+//   c (n K - s1) >= b sqrt(V),  V = n s2 - s1^2  (= n^2 sigma^2)
+//   <=>  n K - s1 >= t := ceil(ceil(sqrt(b^2 V)) / c)  <=>  K >= ceil((s1 + t) / n).
+int threshold_key(int32_t n, u128 s1, u128 s2, uint32_t b, uint32_t c, uint64_t *kstar) {
+    u128 ns2, s1sq, bb, bbv;
+    if (mul_overflows(static_cast<u128>(n), s2, &ns2)) return DUALGCN_ERR_UNSUPPORTED;
+    if (mul_overflows(s1, s1, &s1sq)) return DUALGCN_ERR_UNSUPPORTED;
+    if (ns2 < s1sq) return DUALGCN_ERR_HIP;  // impossible for exact sums
+    const u128 V = ns2 - s1sq;
+    bb = static_cast<u128>(b) * b;
+    if (mul_overflows(bb, V, &bbv)) return DUALGCN_ERR_UNSUPPORTED;
+    const u128 root = isqrt_ceil(bbv);
+    const u128 t = (root + c - 1) / c;
+    const u128 num = s1 + t;
+    const u128 k = (num + static_cast<u128>(n) - 1) / static_cast<u128>(n);
+    *kstar = k > static_cast<u128>(~0ull) ? ~0ull : static_cast<uint64_t>(k);
+    return DUALGCN_OK;
+}
+
+}  // namespace
+
+int validate_csr(const dualgcn_csr *csr, int32_t *flags, hipStream_t s) {
+    const int64_t work = std::max<int64_t>(csr->nnz, csr->n);
+    const int64_t blocks = std::min<int64_t>((work + kThreads - 1) / kThreads, 4096);
+    hipLaunchKernelGGL(validate_kernel, dim3(static_cast<unsigned>(std::max<int64_t>(blocks, 1))),
+                       dim3(kThreads), 0, s, csr->rowptr, csr->col, csr->n, csr->nnz, flags,
+                       flags + 1);
+    return hip_status(hipGetLastError());
+}
+
+void free_plan(Plan *p) {
+    if (!p) return;
+    void *bufs[] = {p->S, p->K, p->perm, p->parts, p->counters, p->partials};
+    for (void *b : bufs)
+        if (b) (void)hipFree(b);
+    delete p;
+}
+
+int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
+               const dualgcn_thresholds &th, hipStream_t s, Plan **out) {
+    const int32_t n = csr->n;
+    const int64_t nnz = csr->nnz;
+    Plan *p = new (std::nothrow) Plan();
+    if (!p) return DUALGCN_ERR_OOM;
+    struct Guard {
+        Plan *p;
+        ~Guard() { free_plan(p); }
+    } guard{p};
+    int st;
+    if ((st = hip_status(hipGetDevice(&p->device)))) return st;
+    p->n = n;
+    p->nnz = nnz;
+    p->rowptr = csr->rowptr;
+    p->col = csr->col;
+    p->val = csr->val;
+    p->th = th;
+    p->seed = seed;
+    p->k = k;
+    p->d = d;
+
+    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->S), sizeof(uint32_t) * n))) return st;
+    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->K), sizeof(uint64_t) * n))) return st;
+    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->perm), sizeof(int32_t) * n))) return st;
+
+    const int32_t nb_keys = static_cast<int32_t>(std::min<int64_t>((n + kThreads - 1) / kThreads, 1024));
+    DevBuf flags, partial, summary;
+    if ((st = alloc_bytes(&flags.p, 2 * sizeof(int32_t)))) return st;
+    if ((st = alloc_bytes(&partial.p, sizeof(Moments) * nb_keys))) return st;
+    if ((st = alloc_bytes(&summary.p, sizeof(Summary)))) return st;
+    int32_t *bad = flags.as<int32_t>();
+    int32_t *maxdeg = bad + 1;
+    if ((st = hip_status(hipMemsetAsync(bad, 0, 2 * sizeof(int32_t), s)))) return st;
+
+    if ((st = validate_csr(csr, bad, s))) return st;
+    // walks
+    if ((st = launch_arw(csr->rowptr, csr->col, n, seed, k, d, p->S, nullptr, bad, s))) return st;
+    // keys and moments
+    const uint64_t pa = th.alpha_num, qa = th.alpha_den;
+    hipLaunchKernelGGL(keys_kernel, dim3(nb_keys), dim3(kThreads), 0, s, csr->rowptr, p->S, n,
+                       pa, (qa - pa) * k, p->K, partial.as<Moments>(), bad);
+    hipLaunchKernelGGL(fold_kernel, dim3(1), dim3(kThreads), 0, s, partial.as<Moments>(), nb_keys,
+                       bad, maxdeg, summary.as<Summary>());
+    if ((st = hip_status(hipGetLastError()))) return st;
+    Summary sum{};
+    if ((st = hip_status(hipMemcpyAsync(&sum, summary.p, sizeof(sum), hipMemcpyDeviceToHost, s))))
+        return st;
+    if ((st = hip_status(hipStreamSynchronize(s)))) return st;           // host wait 1
+    if (sum.flag) return DUALGCN_ERR_BAD_CSR;
+
+    p->max_degree = sum.maxdeg;
+    p->s1 = join(sum.m.s1_lo, sum.m.s1_hi);
+    p->s2 = join(sum.m.s2_lo, sum.m.s2_hi);
+    p->kmax = sum.m.kmax;
+    if ((st = threshold_key(n, p->s1, p->s2, th.beta_num, th.beta_den, &p->kstar))) return st;
+
+    // stable radix sort of (K, v) on the bits the keys use
+    DevBuf kb0, kb1, vb0;
+    if ((st = alloc_bytes(&kb0.p, sizeof(uint64_t) * n))) return st;
+    if ((st = alloc_bytes(&kb1.p, sizeof(uint64_t) * n))) return st;
+    if ((st = alloc_bytes(&vb0.p, sizeof(int32_t) * n))) return st;
+    const int passes = (bit_length(p->kmax) + kRadixBits - 1) / kRadixBits;
+    const int32_t nblocks = static_cast<int32_t>((static_cast<int64_t>(n) + kTile - 1) / kTile);
+    DevBuf scan_sums;   // tile sums of every scan below
+    {
+        const int64_t t1 = (static_cast<int64_t>(kRadix) * nblocks + kTile - 1) / kTile;
+        const int64_t t2 = (static_cast<int64_t>(n) + kTile - 1) / kTile;
+        if ((st = alloc_bytes(&scan_sums.p, sizeof(uint32_t) * (std::max(t1, t2) + 1)))) return st;
+    }
+    uint64_t *sorted = nullptr;
+    // every entry of perm is a valid node id even before the sort writes it
+    if ((st = hip_status(hipMemsetAsync(p->perm, 0, sizeof(int32_t) * n, s)))) return st;
+    if ((st = hip_status(hipMemsetAsync(vb0.p, 0, sizeof(int32_t) * n, s)))) return st;
+    if (passes == 0) {
+        hipLaunchKernelGGL(iota_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads), 0, s,
+                           p->perm, n);
+        if ((st = hip_status(hipMemcpyAsync(kb0.p, p->K, sizeof(uint64_t) * n,
+                                            hipMemcpyDeviceToDevice, s))))
+            return st;
+        sorted = kb0.as<uint64_t>();
+    } else {
+        DevBuf hist;
+        if ((st = alloc_bytes(&hist.p, sizeof(uint32_t) * kRadix * nblocks))) return st;
+        // ping-pong so that the last pass lands its values in p->perm
+        int32_t *vbuf[2];
+        uint64_t *kbuf[2] = {kb0.as<uint64_t>(), kb1.as<uint64_t>()};
+        if (passes % 2 == 1) {
+            vbuf[0] = p->perm;
+            vbuf[1] = vb0.as<int32_t>();
+        } else {
+            vbuf[0] = vb0.as<int32_t>();
+            vbuf[1] = p->perm;
+        }
+        const uint64_t *kin = p->K;
+        const int32_t *vin = nullptr;   // identity on the first pass
+        for (int pass = 0; pass < passes; ++pass) {
+            const int shift = pass * kRadixBits;
+            uint64_t *kout = kbuf[pass % 2];
+            int32_t *vout = vbuf[pass % 2];
+            hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, n,
+                               shift, hist.as<uint32_t>(), nblocks);
+            if ((st = hip_status(hipGetLastError()))) return st;
+            if ((st = exclusive_scan(hist.as<uint32_t>(), static_cast<int64_t>(kRadix) * nblocks,
+                                     scan_sums.as<uint32_t>(), nullptr, s)))
+                return st;
+            hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, vin,
+                               n, shift, hist.as<uint32_t>(), nblocks, kout, vout);
+            if ((st = hip_status(hipGetLastError()))) return st;
+            kin = kout;
+            vin = vout;
+        }
+        sorted = const_cast<uint64_t *>(kin);
+        if ((st = hip_status(hipStreamSynchronize(s)))) return st;   // hist is released here
+    }
+
+    // region split and dense-row parts
+    DevBuf ssum, counts;
+    if ((st = alloc_bytes(&ssum.p, sizeof(SplitSummary)))) return st;
+    if ((st = alloc_bytes(&counts.p, sizeof(uint32_t) * (static_cast<size_t>(n) * 2)))) return st;
+    int32_t forced = -1;
+    if (th.force_mode == DUALGCN_FORCE_SPARSE) forced = n;
+    if (th.force_mode == DUALGCN_FORCE_DENSE) forced = 0;
+    hipLaunchKernelGGL(lower_bound_kernel, dim3(1), dim3(1), 0, s, sorted, n, p->kstar, forced,
+                       ssum.as<SplitSummary>());
+    uint32_t *cnt = counts.as<uint32_t>();
+    uint32_t *off = cnt + n;
+    hipLaunchKernelGGL(split_count_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads), 0,
+                       s, p->perm, csr->rowptr, n, ssum.as<SplitSummary>(), cnt);
+    if ((st = hip_status(hipMemcpyAsync(off, cnt, sizeof(uint32_t) * n, hipMemcpyDeviceToDevice, s))))
+        return st;
+    if ((st = exclusive_scan(off, n, scan_sums.as<uint32_t>(), &ssum.as<SplitSummary>()->parts, s)))
+        return st;
+    SplitSummary ss{};
+    if ((st = hip_status(hipMemcpyAsync(&ss, ssum.p, sizeof(ss), hipMemcpyDeviceToHost, s))))
+        return st;
+    if ((st = hip_status(hipStreamSynchronize(s)))) return st;           // host wait 2
+    p->n_sparse = ss.n_sparse;
+    p->n_split_rows = ss.split_rows;
+    p->n_split_parts = static_cast<int32_t>(ss.parts);
+    if (p->n_split_parts > 0) {
+        const size_t np = static_cast<size_t>(p->n_split_parts);
+        if ((st = alloc_bytes(reinterpret_cast<void **>(&p->parts), sizeof(SplitPart) * np))) return st;
+        if ((st = alloc_bytes(reinterpret_cast<void **>(&p->counters), sizeof(int32_t) * np))) return st;
+        if ((st = alloc_bytes(reinterpret_cast<void **>(&p->partials), sizeof(double) * np * kMaxSlice)))
+            return st;
+        if ((st = hip_status(hipMemsetAsync(p->counters, 0, sizeof(int32_t) * np, s)))) return st;
+        hipLaunchKernelGGL(split_fill_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads),
+                           0, s, p->perm, n, cnt, off, p->parts, static_cast<uint32_t>(np));
+        if ((st = hip_status(hipGetLastError()))) return st;
+    }
+    // the scratch buffers above are released on return: wait for their users
+    if ((st = hip_status(hipStreamSynchronize(s)))) return st;
+    guard.p = nullptr;
+    *out = p;
+    return DUALGCN_OK;
+}
+
+}  // namespace dgc

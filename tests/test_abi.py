@@ -1,0 +1,97 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+declared entry point, and rejects bad arguments before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT, gpu_available
+
+HEADER = os.path.join(ROOT, "include", "dualgcn.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dualgcn_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def dg():
+    import paper_2609_01983_amd as dg
+    return dg
+
+
+def test_every_declared_symbol_is_exported(dg):
+    names = _declared()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(dg.lib(), name), name
+
+
+def test_status_strings(dg):
+    for code in range(-6, 1):
+        assert dg.status_str(code) and dg.status_str(code) != "unknown status"
+    assert dg.status_str(42) == "unknown status"
+
+
+def _csr(dg, n=4, nnz=4, rowptr=1, col=1, val=1):
+    return dg.Csr(n, nnz, rowptr, col, val)
+
+
+def test_partition_argument_checks(dg):
+    L = dg.lib()
+    out = ctypes.c_void_p(123)
+    assert L.dualgcn_partition(None, 0, 4, 4, None, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
+    assert out.value is None                         # *out cleared on error
+    c = _csr(dg)
+    assert L.dualgcn_partition(ctypes.byref(c), 0, 4, 4, None, None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_partition(ctypes.byref(c), 0, 0, 4, None, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_partition(ctypes.byref(c), 0, 4, 0, None, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_partition(ctypes.byref(c), 0, 4, 256, None, None, ctypes.byref(out)) == dg.ERR_UNSUPPORTED
+    big = _csr(dg, nnz=1 << 31)
+    assert L.dualgcn_partition(ctypes.byref(big), 0, 4, 4, None, None, ctypes.byref(out)) == dg.ERR_UNSUPPORTED
+    for bad in [_csr(dg, n=0), _csr(dg, nnz=-1), _csr(dg, rowptr=0), _csr(dg, col=0)]:
+        assert L.dualgcn_partition(ctypes.byref(bad), 0, 4, 4, None, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
+    for th in [dg.Thresholds(1, 0, 1, 2, 0), dg.Thresholds(3, 2, 1, 2, 0), dg.Thresholds(1, 2, 1, 0, 0),
+               dg.Thresholds(1, 2, 1, 2, 7), dg.Thresholds(1, 1 << 16, 1, 2, 0)]:
+        assert L.dualgcn_partition(ctypes.byref(c), 0, 4, 4, ctypes.byref(th), None,
+                                   ctypes.byref(out)) == dg.ERR_INVALID_ARG
+    # keys would not fit 63 bits
+    th = dg.Thresholds(1, 60000, 1, 2, 0)
+    huge = _csr(dg, nnz=(1 << 31) - 1)
+    assert L.dualgcn_partition(ctypes.byref(huge), 0, 0xFFFFFFFF, 4, ctypes.byref(th), None,
+                               ctypes.byref(out)) == dg.ERR_UNSUPPORTED
+
+
+def test_other_entry_points_reject_null(dg):
+    L = dg.lib()
+    assert L.dualgcn_spmm(None, 1, 2, 4, None) == dg.ERR_INVALID_ARG
+    nbytes = ctypes.c_size_t()
+    assert L.dualgcn_gcn_layer_workspace(None, 32, 32, ctypes.byref(nbytes)) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_gcn_layer(None, 1, 2, 3, 32, 32, 0, 256, 1 << 20, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_plan_query(None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_plan_export(None, None, None, None) == dg.ERR_INVALID_ARG
+    c = _csr(dg)
+    assert L.dualgcn_arw_patterns(ctypes.byref(c), 0, 4, 4, None, None) == dg.ERR_INVALID_ARG
+    huge = _csr(dg, n=1 << 30)
+    assert L.dualgcn_arw_patterns(ctypes.byref(huge), 0, 1 << 10, 255, 1, None) == dg.ERR_UNSUPPORTED
+    L.dualgcn_plan_destroy(None)                     # no-op
+
+
+@pytest.mark.skipif(gpu_available(), reason="checks the no-device path")
+def test_valid_arguments_without_device_report_no_device(dg):
+    L = dg.lib()
+    c = _csr(dg)
+    out = ctypes.c_void_p()
+    assert L.dualgcn_partition(ctypes.byref(c), 0, 4, 4, None, None, ctypes.byref(out)) == dg.ERR_NO_DEVICE
+    assert out.value is None
+    assert L.dualgcn_arw_patterns(ctypes.byref(c), 0, 4, 4, 1, None) == dg.ERR_NO_DEVICE
+
+
+def test_binding_rejects_host_tensors(dg):
+    import torch
+    r = torch.zeros(5, dtype=torch.int32)
+    with pytest.raises(TypeError):
+        dg.Plan(r, torch.zeros(0, dtype=torch.int32), torch.zeros(0))

@@ -1,0 +1,259 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+* partition (walk patterns, S, K, K*, sums, perm, n_sparse): bit-exact;
+* SpMM: |y - y_oracle| <= 1e-5 * sum |a||x| element by element;
+* GCN layer (bf16 matrix cores): |y - y_oracle| <= 1e-2 * |A| (|X| |W|).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from graphgen import configs, small, dense
+
+pytestmark = pytest.mark.gpu
+
+SPMM_TOL = 1e-5
+GCN_TOL = 1e-2
+
+
+@pytest.fixture(scope="module")
+def dg(device):
+    import paper_2609_01983_amd as dg
+    return dg
+
+
+def to_dev(g, device):
+    return (torch.from_numpy(np.ascontiguousarray(g.rowptr)).to(device),
+            torch.from_numpy(np.ascontiguousarray(g.col)).to(device),
+            torch.from_numpy(np.ascontiguousarray(g.val)).to(device))
+
+
+def assert_plan_matches(dg, plan, g, seed, k, d, alpha=(1, 2), beta=(1, 2), force=0):
+    perm, S, K = plan.export()
+    info = plan.info()
+    ref = oracle.partition(g, seed, k, d, alpha, beta, force)
+    assert np.array_equal(S, ref["S"]), f"S differs at {np.flatnonzero(S != ref['S'])[:10]}"
+    assert np.array_equal(K, ref["K"])
+    assert info["s1"] == ref["S1"] and info["s2"] == ref["S2"]
+    assert info["kstar"] == ref["kstar"]
+    assert info["n_sparse"] == ref["n_sparse"]
+    assert np.array_equal(perm, ref["perm"])
+    return ref
+
+
+def assert_spmm_close(Y, Yr, B, tol=SPMM_TOL, what=""):
+    Y = np.asarray(Y, dtype=np.float64)
+    err = np.abs(Y - Yr)
+    bad = ~(err <= tol * B)
+    if bad.any():
+        i = np.argwhere(bad)[0]
+        raise AssertionError(f"{what}: {bad.sum()} elements outside {tol} sum|a||x|; first at "
+                             f"{tuple(i)}: got {Y[tuple(i)]!r} want {Yr[tuple(i)]!r} bound {B[tuple(i)]!r}")
+
+
+TINY = {
+    "gnp30": lambda: small.random_graph(30, 0.2, seed=1),
+    "gnp257": lambda: small.random_graph(257, 0.03, seed=2),
+    "star50": lambda: small.star(50, self_loops=True, normalise=True),
+    "clique20": lambda: small.clique(20, self_loops=True, normalise=True),
+    "path31": lambda: small.path(31, self_loops=True, normalise=True),
+    "cycle40": lambda: small.cycle(40, self_loops=True, normalise=True),
+    "edgeless7": lambda: small.edgeless(7),
+    "single": lambda: small.edgeless(1),
+    "rows_dup_empty": lambda: small.from_rows([[1, 1, 2], [], [0, 3, 3, 3], [2], [], [0, 1, 2, 3, 4]]),
+    "hub_star": lambda: small.star(10000, self_loops=True, normalise=True),   # one row of 10001 entries
+}
+
+
+# ---------------------------------------------------------------- walks and partition
+
+@pytest.mark.parametrize("name", ["gnp30", "star50", "clique20", "path31", "rows_dup_empty", "single"])
+@pytest.mark.parametrize("k,d", [(8, 4), (3, 7), (1, 1), (100, 2), (4, 40)])
+def test_walk_patterns_bitexact(dg, device, name, k, d):
+    g = TINY[name]()
+    rp, c, v = to_dev(g, device)
+    P = dg.arw_patterns(rp, c, v, seed=11, walks_per_node=k, walk_len=d).cpu().numpy()
+    assert np.array_equal(P, oracle.patterns(g, 11, k, d))
+
+
+def test_walk_patterns_c1(dg, device):
+    g = configs.load_graph("c1")
+    rp, c, v = to_dev(g, device)
+    P = dg.arw_patterns(rp, c, v, seed=0, walks_per_node=8, walk_len=4).cpu().numpy()
+    assert np.array_equal(P, oracle.patterns(g, 0, 8, 4))
+
+
+@pytest.mark.parametrize("name", sorted(TINY))
+@pytest.mark.parametrize("k,d", [(8, 4), (16, 5), (3, 2), (100, 3)])
+def test_partition_bitexact_tiny(dg, device, name, k, d):
+    g = TINY[name]()
+    plan = dg.Plan(*to_dev(g, device), seed=5, walks_per_node=k, walk_len=d)
+    assert_plan_matches(dg, plan, g, 5, k, d)
+
+
+@pytest.mark.parametrize("alpha,beta", [((0, 1), (1, 2)), ((1, 1), (1, 2)), ((1, 3), (3, 2)),
+                                        ((1, 2), (0, 1)), ((2, 5), (7, 3))])
+@pytest.mark.parametrize("force", [0, 1, 2])
+def test_partition_parameters(dg, device, alpha, beta, force):
+    g = small.random_graph(300, 0.02, seed=9)
+    plan = dg.Plan(*to_dev(g, device), seed=1, walks_per_node=8, walk_len=4, alpha=alpha,
+                   beta=beta, force_mode=force)
+    assert_plan_matches(dg, plan, g, 1, 8, 4, alpha, beta, force)
+
+
+@pytest.mark.parametrize("cfg", ["c1", "c2"])
+def test_partition_bitexact_configs(dg, device, cfg):
+    w = configs.WORKLOADS[cfg]
+    g = configs.load_graph(cfg)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    ref = assert_plan_matches(dg, plan, g, 0, w.walks, w.steps)
+    assert 0 < ref["n_sparse"] < g.n
+
+
+def test_bad_csr_rejected(dg, device):
+    g = small.random_graph(20, 0.2, seed=3)
+    rp, c, v = to_dev(g, device)
+    c_bad = c.clone()
+    c_bad[3] = 20                                    # column out of range
+    with pytest.raises(dg.DualGCNError) as e:
+        dg.Plan(rp, c_bad, v, walks_per_node=4, walk_len=3)
+    assert e.value.status == dg.ERR_BAD_CSR
+    rp_bad = rp.clone()
+    rp_bad[5] = rp_bad[6] + 1                        # not monotone
+    with pytest.raises(dg.DualGCNError) as e:
+        dg.Plan(rp_bad, c, v, walks_per_node=4, walk_len=3)
+    assert e.value.status == dg.ERR_BAD_CSR
+
+
+# ---------------------------------------------------------------- SpMM
+
+@pytest.mark.parametrize("name", sorted(TINY))
+@pytest.mark.parametrize("force", ["auto", "sparse", "dense"])
+@pytest.mark.parametrize("F", [1, 3, 16, 17, 64, 128, 256])
+def test_spmm_tiny(dg, device, name, force, F):
+    g = TINY[name]()
+    X = dense.features_normal(g.n, F, seed=F, stream_id=21)
+    plan = dg.Plan(*to_dev(g, device), seed=2, walks_per_node=8, walk_len=4, force_mode=force)
+    Y = dg.spmm(plan, torch.from_numpy(X).to(device)).cpu().numpy()
+    Yr, B = oracle.spmm(g, X)
+    assert_spmm_close(Y, Yr, B, what=f"{name} F={F} {force}")
+
+
+@pytest.mark.parametrize("F", [512, 320, 1000])
+def test_spmm_wide_features(dg, device, F):
+    g = small.random_graph(150, 0.05, seed=4)
+    X = dense.features_normal(g.n, F, seed=1, stream_id=22)
+    plan = dg.Plan(*to_dev(g, device), seed=2, walks_per_node=4, walk_len=3)
+    Y = dg.spmm(plan, torch.from_numpy(X).to(device)).cpu().numpy()
+    Yr, B = oracle.spmm(g, X)
+    assert_spmm_close(Y, Yr, B, what=f"F={F}")
+
+
+def test_spmm_poison_and_determinism(dg, device):
+    g = configs.load_graph("c1")
+    X = torch.from_numpy(configs.load_features("c1")).to(device)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=8, walk_len=4)
+    for force in ["auto", "sparse", "dense"]:
+        p = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=8, walk_len=4, force_mode=force)
+        Y1 = torch.full_like(X, float("nan"))
+        dg.spmm(p, X, Y1)
+        Y2 = torch.full_like(X, float("nan"))
+        dg.spmm(p, X, Y2)
+        torch.cuda.synchronize()
+        assert torch.isfinite(Y1).all()
+        assert torch.equal(Y1, Y2)
+    del plan
+
+
+def test_spmm_split_rows_repeat_calls(dg, device):
+    """A hub row split over several workgroups: counters are reset between calls."""
+    g = small.star(20000, self_loops=True, normalise=True)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=4, walk_len=3)
+    info = plan.info()
+    assert info["n_split_rows"] == 1 and info["n_split_parts"] == 5
+    Yr = None
+    for F in (128, 64, 128, 17):
+        X = dense.features_normal(g.n, F, seed=F, stream_id=23)
+        Y = dg.spmm(plan, torch.from_numpy(X).to(device)).cpu().numpy()
+        Yr, B = oracle.spmm(g, X)
+        assert_spmm_close(Y, Yr, B, what=f"star F={F}")
+
+
+@pytest.mark.parametrize("cfg", ["c1", "c2"])
+def test_spmm_configs_full(dg, device, cfg):
+    w = configs.WORKLOADS[cfg]
+    g = configs.load_graph(cfg)
+    X = configs.load_features(cfg)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    Y = dg.spmm(plan, torch.from_numpy(X).to(device)).cpu().numpy()
+    Yr, B = oracle.spmm(g, X)
+    assert_spmm_close(Y, Yr, B, what=cfg)
+
+
+def _sample_rows(g, plan_info_perm, n_sparse, count, seed):
+    """Random rows plus the heaviest dense rows and the rows around the region boundary."""
+    gen = np.random.default_rng(seed)
+    rnd = gen.choice(g.n, size=min(count, g.n), replace=False)
+    heavy = plan_info_perm[-min(64, g.n):]
+    edge = plan_info_perm[max(0, n_sparse - 32):min(g.n, n_sparse + 32)]
+    return np.unique(np.concatenate([rnd, heavy, edge])).astype(np.int32)
+
+
+@pytest.mark.parametrize("cfg", ["c3"])
+def test_config_partition_and_sampled_spmm(dg, device, cfg):
+    w = configs.WORKLOADS[cfg]
+    g = configs.load_graph(cfg)
+    X = configs.load_features(cfg)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    ref = assert_plan_matches(dg, plan, g, 0, w.walks, w.steps)
+    Y = dg.spmm(plan, torch.from_numpy(X).to(device)).cpu().numpy()
+    rows = _sample_rows(g, ref["perm"], ref["n_sparse"], 20000, seed=1)
+    Yr, B = oracle.spmm(g, X, rows)
+    assert_spmm_close(Y[rows], Yr, B, what=cfg)
+
+
+# ---------------------------------------------------------------- GCN layer (bf16 MFMA)
+
+@pytest.mark.parametrize("fin,fout", [(32, 32), (64, 32), (256, 128), (128, 64), (96, 160)])
+@pytest.mark.parametrize("relu", [False, True])
+def test_gcn_layer_small(dg, device, fin, fout, relu):
+    g = small.random_graph(333, 0.02, seed=7)
+    X = dense.features_normal(g.n, fin, seed=fin, stream_id=24)
+    W = dense.glorot(fin, fout, seed=fout, stream_id=25)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=8, walk_len=4)
+    Y = dg.gcn_layer(plan, torch.from_numpy(X).to(device), torch.from_numpy(W).to(device),
+                     relu=relu).cpu().numpy()
+    Yr, BY = oracle.gcn_layer(g, X, W, relu=relu)
+    assert_spmm_close(Y, Yr, BY, tol=GCN_TOL, what=f"gcn {fin}->{fout}")
+
+
+def test_gcn_layer_identity_graph_is_xw(dg, device):
+    """Edgeless graph: A = I, so the layer is the bf16 product itself (ragged n)."""
+    g = small.edgeless(1000)
+    X = dense.features_normal(g.n, 256, seed=3, stream_id=26)
+    W = dense.glorot(256, 128, seed=3)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=2, walk_len=2)
+    Y = dg.gcn_layer(plan, torch.from_numpy(X).to(device), torch.from_numpy(W).to(device)).cpu().numpy()
+    T, BT = oracle.xw(X, W)
+    assert_spmm_close(Y, T, BT, tol=GCN_TOL, what="xw")
+    # the bf16 rounding of both operands, done here in numpy, reproduces it much closer
+    def bf16(a):
+        u = a.astype(np.float32).view(np.uint32).astype(np.uint64)
+        u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
+        return u.astype(np.uint32).view(np.float32).astype(np.float64)
+    Tb = bf16(X) @ bf16(W)
+    assert np.max(np.abs(Y - Tb) / (BT + 1e-30)) < 1e-5
+
+
+def test_gcn_two_layer_c2_graph(dg, device):
+    g = configs.load_graph("c2")
+    X = dense.features_normal(g.n, 256, seed=0, stream_id=27)
+    W1 = dense.glorot(256, 128, seed=0, stream_id=4)
+    W2 = dense.glorot(128, 64, seed=0, stream_id=5)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=16, walk_len=5)
+    H = dg.gcn_layer(plan, torch.from_numpy(X).to(device), torch.from_numpy(W1).to(device), relu=True)
+    Y = dg.gcn_layer(plan, H, torch.from_numpy(W2).to(device)).cpu().numpy()
+    rows = np.random.default_rng(3).choice(g.n, 300, replace=False).astype(np.int32)
+    Yr, bound = oracle.gcn_forward_rows(g, X, [W1, W2], rows)
+    assert_spmm_close(Y[rows], Yr, bound, tol=GCN_TOL, what="2-layer")
