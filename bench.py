@@ -100,6 +100,10 @@ def main():
     ap.add_argument("--config", default=os.environ.get("DUALGCN_BENCH_CONFIG", "c5"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--spmm-reps", type=int, default=20)
+    ap.add_argument("--mode", choices=["full", "spmm"], default="full",
+                    help="spmm: one partition, then only the SpMM launches (for counter runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first copy 1 GiB device to device (a dispatch of known traffic)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -127,6 +131,34 @@ def main():
     Wd = [torch.from_numpy(W).to(dev) for W in weights]
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)                     # reads 1 GiB, writes 1 GiB
+        torch.cuda.synchronize()
+        del src, dst
+        print("[bench] copy calibration: 1073741824 bytes read + written", file=sys.stderr,
+              flush=True)
+    if args.mode == "spmm":
+        F_spmm = w.layers[0][1] if w.is_gcn else w.F
+        plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
+        Xs = Xd[:, :F_spmm].contiguous() if w.is_gcn else Xd
+        Ys = torch.empty_like(Xs)
+        times = []
+        for _ in range(args.spmm_reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            dg.spmm(plan, Xs, Ys)
+            b.record(stream)
+            times.append((a, b))
+        torch.cuda.synchronize()
+        ms = [a.elapsed_time(b) for a, b in times]
+        print(json.dumps({"mode": "spmm", "config": w.name, "F": F_spmm,
+                          "ms": [round(x, 4) for x in ms],
+                          "bytes_min": spmm_bytes(g.n, g.nnz, F_spmm)}), flush=True)
+        plan.destroy()
+        return
 
     if w.is_gcn:
         fouts = [fo for _, fo in w.layers]
