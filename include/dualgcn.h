@@ -56,7 +56,8 @@ int dualgcn_last_hip_error(void);
  * Sec. 3.2 is read from its row pointers).  The arrays are BORROWED: they must
  * stay alive and unmodified for the lifetime of any plan built on them.
  *   n       rows = columns, 1 <= n < 2^31
- *   nnz     stored entries, 0 <= nnz < 2^31 (int32 row pointers)
+ *   nnz     stored entries, 0 <= nnz <= 2^31 - 2^16 (int32 row pointers; larger
+ *           matrices return DUALGCN_ERR_UNSUPPORTED)
  *   rowptr  int32[n+1], rowptr[0] = 0, non-decreasing, rowptr[n] = nnz
  *   col     int32[nnz], each in [0, n); order inside a row is free and
  *           duplicates are allowed (they add in the product and weight walks)
@@ -114,8 +115,9 @@ typedef struct dualgcn_plan dualgcn_plan;
  * moment sums must fit 128 bits (else DUALGCN_ERR_UNSUPPORTED).  The CSR is
  * validated on the device first (DUALGCN_ERR_BAD_CSR).
  *
- * The plan owns device memory (S, K, perm, the dense-region schedule and the
- * partial sums of split rows), released by dualgcn_plan_destroy.  The call waits
+ * The plan owns device memory (S, K, perm, a copy of the matrix with its rows
+ * in perm order -- about 8 nnz + 8 n bytes --, the sparse tasks, the dense-region
+ * schedule and the partial sums of split rows), released by dualgcn_plan_destroy.  The call waits
  * for `stream` twice (to read the moment sums and the schedule sizes).
  * *out is set to NULL on error.
  */
@@ -131,12 +133,14 @@ void dualgcn_plan_destroy(dualgcn_plan *plan);
  *
  * X and Y are float32 row-major n x F, contiguous (leading dimension F), and
  * must not overlap.  Rows of the sparse region are computed by the sparse
- * kernel (one row per lane group of a wavefront); rows of the dense region by
- * the dense kernel (one workgroup per row; rows longer than the dense chunk are
- * split over several workgroups and combined in a fixed order).  Every row of
- * Y is written, rows without entries with zeros.  Products are float32; sums
- * are formed in float32 over at most 64 terms and then in float64, and each
- * output is rounded once to float32.  1 <= F < 2^20.  Asynchronous.
+ * path (runs of up to 8 short rows per lane group of a wavefront); rows of the
+ * dense region by the dense path (one wavefront per row; rows longer than the
+ * dense chunk are split over several wavefronts and combined in a fixed order).
+ * Every row of Y is written, rows without entries with zeros.  Products are
+ * float32; sums are formed in float32 over at most 16 terms and then in
+ * float64, and each output is rounded once to float32, so results do not
+ * depend on timing (bit-reproducible for a given plan and F).
+ * 1 <= F < 2^20.  Asynchronous.
  */
 int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, void *stream);
 
@@ -182,9 +186,10 @@ typedef struct dualgcn_plan_info {
     uint64_t seed;
     uint32_t walks_per_node, walk_len;
     int32_t max_degree;
-    int32_t dense_chunk;     /* entries per dense workgroup */
+    int32_t dense_chunk;     /* entries per dense-region wavefront */
     int32_t n_split_rows;    /* dense rows longer than dense_chunk */
-    int32_t n_split_parts;   /* workgroups those rows are split over */
+    int32_t n_split_parts;   /* wavefronts those rows are split over */
+    int32_t n_tasks;         /* sparse-region tasks (runs of at most 8 short rows) */
 } dualgcn_plan_info;
 
 /* Fills *out from host-side copies kept in the plan (no device use). */

@@ -2,7 +2,7 @@
 
 Argument marshalling only -- every step of the path runs in the library's HIP
 kernels.  torch provides device memory and the current stream.  The library is
-built by ``paper_2609_01983_amd.build`` (or ``__graft_entry__.build()``); if it
+built by ``python paper_2609_01983_amd/build.py`` (or ``__graft_entry__.build()``); if it
 is missing, importing this package raises ImportError: there is no fallback.
 
     plan = Plan(rowptr, col, val, seed=0, walks_per_node=16, walk_len=5)
@@ -54,12 +54,13 @@ class PlanInfo(ctypes.Structure):
                 ("force_mode", ctypes.c_int32), ("seed", ctypes.c_uint64),
                 ("walks_per_node", ctypes.c_uint32), ("walk_len", ctypes.c_uint32),
                 ("max_degree", ctypes.c_int32), ("dense_chunk", ctypes.c_int32),
-                ("n_split_rows", ctypes.c_int32), ("n_split_parts", ctypes.c_int32)]
+                ("n_split_rows", ctypes.c_int32), ("n_split_parts", ctypes.c_int32),
+                ("n_tasks", ctypes.c_int32)]
 
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_01983_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2609_01983_amd/build.py`")
     L = ctypes.CDLL(LIB_PATH)
     P, I32, U32, U64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64, \
         ctypes.c_size_t

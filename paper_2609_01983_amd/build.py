@@ -1,6 +1,6 @@
 """Build ``libdualgcn.so`` (all HIP sources, gfx950) next to this file.
 
-Run directly (``python -m paper_2609_01983_amd.build``) or through the repository's
+Run as a script (``python paper_2609_01983_amd/build.py``) or through the repository's
 ``__graft_entry__.build()``.  Always recompiles.
 """
 import os

@@ -46,12 +46,15 @@ using dgc::Plan;
 namespace {
 
 constexpr uint32_t kMaxRational = 1u << 16;
+// Largest number of entries: 32-bit entry offsets keep some headroom for the
+// kernels' round arithmetic.
+constexpr int64_t kMaxNnz = (static_cast<int64_t>(1) << 31) - (1 << 16);
 
 int check_csr(const dualgcn_csr *c) {
     if (!c || !c->rowptr) return DUALGCN_ERR_INVALID_ARG;
     if (c->n < 1) return DUALGCN_ERR_INVALID_ARG;
     if (c->nnz < 0) return DUALGCN_ERR_INVALID_ARG;
-    if (c->nnz >= (static_cast<int64_t>(1) << 31)) return DUALGCN_ERR_UNSUPPORTED;
+    if (c->nnz > kMaxNnz) return DUALGCN_ERR_UNSUPPORTED;
     if (c->nnz > 0 && (!c->col || !c->val)) return DUALGCN_ERR_INVALID_ARG;
     return DUALGCN_OK;
 }
@@ -193,6 +196,7 @@ int dualgcn_plan_query(const dualgcn_plan *plan, dualgcn_plan_info *out) {
     i.dense_chunk = dgc::kDenseChunk;
     i.n_split_rows = p->n_split_rows;
     i.n_split_parts = p->n_split_parts;
+    i.n_tasks = p->n_tasks;
     *out = i;
     return DUALGCN_OK;
 }

@@ -12,14 +12,20 @@ namespace dgc {
 
 using u128 = unsigned __int128;
 
-// Entries of one CSR row handled by one dense-region workgroup; longer rows are
-// split into parts of this many entries and combined in a fixed order.
+// Entries of one dense row handled by one wavefront; longer rows are split into
+// parts of this many entries and combined in a fixed order.
 constexpr int kDenseChunk = 4096;
-// Widest feature slice one SpMM launch covers; wider F is processed in slices.
+// Widest feature window one SpMM launch covers; wider F is processed in windows.
 constexpr int kMaxSlice = 256;
+// Feature slices of one window are at most this many (arrival counters per part).
+constexpr int kMaxSlices = 8;
+// A sparse-region task is a run of at most kTaskRows consecutive rows of the sorted
+// order whose first entries fall in one window of kTaskEntries entries.
+constexpr int kTaskRows = 8;
+constexpr int kTaskEntries = 32;
 
-// One part of a split dense row: row id, part index, number of parts, index of
-// the row's first part (which owns the arrival counter).
+// One part of a split dense row: position of the row in the sorted order, part index,
+// number of parts, index of the row's first part (which owns the arrival counters).
 struct SplitPart {
     int32_t row;
     int32_t part;
@@ -39,11 +45,19 @@ struct Plan {
     uint64_t *K = nullptr;             // [n] hybrid keys
     int32_t *perm = nullptr;           // [n] nodes sorted by (K, v)
 
+    // The matrix with its rows in sorted order (row i of this copy is row perm[i]):
+    // the contiguous sparse and dense regions the SpMM kernels stream through.
+    int32_t *pptr = nullptr;           // [n + 1]
+    int32_t *pcol = nullptr;           // [nnz]
+    float *pval = nullptr;             // [nnz]
+    int32_t *tasks = nullptr;          // [n_tasks + 1] first sorted row of each sparse task
+
     int32_t n_sparse = 0;
+    int32_t n_tasks = 0;
     int32_t n_split_rows = 0;
     int32_t n_split_parts = 0;
     SplitPart *parts = nullptr;        // [n_split_parts]
-    int32_t *counters = nullptr;       // [n_split_parts] arrival counters (zero between calls)
+    int32_t *counters = nullptr;       // [n_split_parts][kMaxSlices] arrival counters (zero between calls)
     double *partials = nullptr;        // [n_split_parts][kMaxSlice]
 
     uint64_t kstar = 0, kmax = 0;

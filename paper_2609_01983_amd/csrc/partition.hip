@@ -8,8 +8,12 @@
 //                   workgroup folds them                              -> host wait 1
 //   host            K* = least integer >= mu_K + beta sigma_K (exact integers)
 //   radix sort      stable LSD sort of (K_v, v) on 8-bit digits      -> perm
-//   split           n_sparse = lower_bound(sorted K, K*); dense rows longer than
-//                   one dense chunk are listed as parts               -> host wait 2
+//   split           n_sparse = lower_bound(sorted K, K*)
+//   sorted copy     the rows of the matrix in perm order (row pointers by a scan),
+//                   so that both regions are contiguous streams (Sec. 3.2: the
+//                   sorted nodes are cut into contiguous blocks)
+//   schedule        sparse tasks (runs of at most kTaskRows short rows) and the
+//                   parts of dense rows longer than one dense chunk   -> host wait 2
 //
 // Everything is integer arithmetic, so the plan does not depend on launch order
 // or reduction order: it is the unique sort of (K_v, v) cut at K*.
@@ -313,7 +317,7 @@ struct SplitSummary {
     int32_t n_sparse;
     int32_t split_rows;
     uint32_t parts;
-    int32_t pad;
+    uint32_t tasks;
 };
 
 // n_sparse = first position whose key is >= K* (one thread; keys are sorted).
@@ -328,17 +332,105 @@ __global__ void lower_bound_kernel(const uint64_t *__restrict__ sorted, int32_t 
     out->n_sparse = force_sparse_count >= 0 ? force_sparse_count : lo;
     out->split_rows = 0;
     out->parts = 0;
+    out->tasks = 0;
 }
 
-__global__ __launch_bounds__(kThreads) void split_count_kernel(
-    const int32_t *__restrict__ perm, const int32_t *__restrict__ rowptr, int32_t n,
-    SplitSummary *__restrict__ sum, uint32_t *__restrict__ counts) {
+// pptr[i] = length of row perm[i] for i < n and pptr[n] = 0; an exclusive scan then turns
+// pptr into the row pointers of the sorted copy.
+__global__ __launch_bounds__(kThreads) void sorted_degree_kernel(const int32_t *__restrict__ perm,
+                                                                 const int32_t *__restrict__ rowptr,
+                                                                 int32_t n, uint32_t *__restrict__ pptr) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n) {
+        const int32_t r = perm[i];
+        pptr[i] = static_cast<uint32_t>(rowptr[r + 1] - rowptr[r]);
+    } else if (i == n) {
+        pptr[n] = 0;
+    }
+}
+
+// Copies row perm[i] of the CSR into row i of the sorted copy.  A lane copies its own row
+// when it has at most 32 entries; longer rows are copied by the whole wavefront in turn.
+__global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
+    const int32_t *__restrict__ perm, const int32_t *__restrict__ rowptr,
+    const int32_t *__restrict__ col, const float *__restrict__ val,
+    const int32_t *__restrict__ pptr, int32_t n, int32_t *__restrict__ pcol,
+    float *__restrict__ pval) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    int32_t src = 0, dst = 0, len = 0;
+    if (i < n) {
+        const int32_t r = perm[i];
+        src = rowptr[r];
+        len = rowptr[r + 1] - src;
+        dst = pptr[i];
+    }
+    const bool wide = len > 32;
+    if (!wide) {
+        for (int32_t k = 0; k < len; ++k) {
+            pcol[dst + k] = col[src + k];
+            pval[dst + k] = val[src + k];
+        }
+    }
+    uint64_t mask = __ballot(wide);
+    while (mask) {
+        const int l = __ffsll(static_cast<unsigned long long>(mask)) - 1;
+        mask &= mask - 1;
+        const int32_t s2 = __shfl(src, l), d2 = __shfl(dst, l), n2 = __shfl(len, l);
+        for (int32_t k = lane; k < n2; k += 64) {
+            pcol[d2 + k] = col[s2 + k];
+            pval[d2 + k] = val[s2 + k];
+        }
+    }
+}
+
+// Does row i of the sorted order start a sparse-region task?  A task is a run of at most
+// kTaskRows consecutive rows whose first entries lie in one window of kTaskEntries entries;
+// an empty row forms a task of its own.
+__device__ __forceinline__ bool starts_task(const int32_t *__restrict__ pptr, int32_t i) {
+    const int32_t b = pptr[i];
+    if (i == 0 || pptr[i + 1] == b || pptr[i - 1] == b) return true;
+    const int32_t w0 = (b / kTaskEntries) * kTaskEntries;
+    int32_t lo = 0, hi = i;        // first row whose first entry is >= w0
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (pptr[mid] < w0) lo = mid + 1;
+        else hi = mid;
+    }
+    return (i - lo) % kTaskRows == 0;
+}
+
+__global__ __launch_bounds__(kThreads) void task_flag_kernel(const int32_t *__restrict__ pptr,
+                                                             int32_t n,
+                                                             const SplitSummary *__restrict__ sum,
+                                                             uint32_t *__restrict__ flags) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    flags[i] = (i < sum->n_sparse && starts_task(pptr, static_cast<int32_t>(i))) ? 1u : 0u;
+}
+
+// tasks[offsets[i]] = i for every task start i; tasks[n_tasks] = n_sparse.
+__global__ __launch_bounds__(kThreads) void task_fill_kernel(const int32_t *__restrict__ pptr,
+                                                             int32_t n,
+                                                             const SplitSummary *__restrict__ sum,
+                                                             const uint32_t *__restrict__ offsets,
+                                                             int32_t *__restrict__ tasks) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int32_t ns = sum->n_sparse;
+    if (i == 0) tasks[sum->tasks] = ns;
+    if (i < ns && starts_task(pptr, static_cast<int32_t>(i))) tasks[offsets[i]] = static_cast<int32_t>(i);
+}
+
+// Dense rows of the sorted order longer than one chunk: counts[i] = number of parts.
+__global__ __launch_bounds__(kThreads) void split_count_kernel(const int32_t *__restrict__ pptr,
+                                                               int32_t n,
+                                                               SplitSummary *__restrict__ sum,
+                                                               uint32_t *__restrict__ counts) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i >= n) return;
     uint32_t c = 0;
     if (i >= sum->n_sparse) {
-        const int32_t r = perm[i];
-        const int32_t deg = rowptr[r + 1] - rowptr[r];
+        const int32_t deg = pptr[i + 1] - pptr[i];
         if (deg > kDenseChunk) {
             c = static_cast<uint32_t>((deg + kDenseChunk - 1) / kDenseChunk);
             atomicAdd(&sum->split_rows, 1);
@@ -347,17 +439,19 @@ __global__ __launch_bounds__(kThreads) void split_count_kernel(
     counts[i] = c;
 }
 
-__global__ __launch_bounds__(kThreads) void split_fill_kernel(
-    const int32_t *__restrict__ perm, int32_t n, const uint32_t *__restrict__ counts,
-    const uint32_t *__restrict__ offsets, SplitPart *__restrict__ parts, uint32_t n_parts) {
+__global__ __launch_bounds__(kThreads) void split_fill_kernel(const uint32_t *__restrict__ counts,
+                                                              const uint32_t *__restrict__ offsets,
+                                                              int32_t n,
+                                                              SplitPart *__restrict__ parts,
+                                                              uint32_t n_parts) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i >= n) return;
     const uint32_t c = counts[i];
     if (c == 0) return;
     const uint32_t off = offsets[i];
     for (uint32_t j = 0; j < c && off + j < n_parts; ++j)
-        parts[off + j] = SplitPart{perm[i], static_cast<int32_t>(j), static_cast<int32_t>(c),
-                                   static_cast<int32_t>(off)};
+        parts[off + j] = SplitPart{static_cast<int32_t>(i), static_cast<int32_t>(j),
+                                   static_cast<int32_t>(c), static_cast<int32_t>(off)};
 }
 
 // ------------------------------------------------------------------ host helpers
@@ -453,7 +547,8 @@ int validate_csr(const dualgcn_csr *csr, int32_t *flags, hipStream_t s) {
 
 void free_plan(Plan *p) {
     if (!p) return;
-    void *bufs[] = {p->S, p->K, p->perm, p->parts, p->counters, p->partials};
+    void *bufs[] = {p->S,     p->K,     p->perm,  p->pptr,    p->pcol,
+                    p->pval,  p->tasks, p->parts, p->counters, p->partials};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
     delete p;
@@ -526,7 +621,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     DevBuf scan_sums;   // tile sums of every scan below
     {
         const int64_t t1 = (static_cast<int64_t>(kRadix) * nblocks + kTile - 1) / kTile;
-        const int64_t t2 = (static_cast<int64_t>(n) + kTile - 1) / kTile;
+        const int64_t t2 = (static_cast<int64_t>(n) + 1 + kTile - 1) / kTile;
         if ((st = alloc_bytes(&scan_sums.p, sizeof(uint32_t) * (std::max(t1, t2) + 1)))) return st;
     }
     uint64_t *sorted = nullptr;
@@ -575,7 +670,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
         if ((st = hip_status(hipStreamSynchronize(s)))) return st;   // hist is released here
     }
 
-    // region split and dense-row parts
+    // region split, the sorted copy of the matrix, sparse tasks and dense-row parts
     DevBuf ssum, counts;
     if ((st = alloc_bytes(&ssum.p, sizeof(SplitSummary)))) return st;
     if ((st = alloc_bytes(&counts.p, sizeof(uint32_t) * (static_cast<size_t>(n) * 2)))) return st;
@@ -584,30 +679,56 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if (th.force_mode == DUALGCN_FORCE_DENSE) forced = 0;
     hipLaunchKernelGGL(lower_bound_kernel, dim3(1), dim3(1), 0, s, sorted, n, p->kstar, forced,
                        ssum.as<SplitSummary>());
+    SplitSummary *dsum = ssum.as<SplitSummary>();
+    const unsigned grid_n1 = static_cast<unsigned>((static_cast<int64_t>(n) + 1 + kThreads - 1) / kThreads);
+    const unsigned grid_n = static_cast<unsigned>((static_cast<int64_t>(n) + kThreads - 1) / kThreads);
+
+    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->pptr), sizeof(int32_t) * (static_cast<size_t>(n) + 1))))
+        return st;
+    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->pcol), sizeof(int32_t) * static_cast<size_t>(nnz))))
+        return st;
+    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->pval), sizeof(float) * static_cast<size_t>(nnz))))
+        return st;
+    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->tasks), sizeof(int32_t) * (static_cast<size_t>(n) + 1))))
+        return st;
+    uint32_t *pptr_u = reinterpret_cast<uint32_t *>(p->pptr);
+    hipLaunchKernelGGL(sorted_degree_kernel, dim3(grid_n1), dim3(kThreads), 0, s, p->perm, csr->rowptr,
+                       n, pptr_u);
+    if ((st = exclusive_scan(pptr_u, static_cast<int64_t>(n) + 1, scan_sums.as<uint32_t>(), nullptr, s)))
+        return st;
+    hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->perm, csr->rowptr,
+                       csr->col, csr->val, p->pptr, n, p->pcol, p->pval);
+
     uint32_t *cnt = counts.as<uint32_t>();
     uint32_t *off = cnt + n;
-    hipLaunchKernelGGL(split_count_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads), 0,
-                       s, p->perm, csr->rowptr, n, ssum.as<SplitSummary>(), cnt);
+    hipLaunchKernelGGL(task_flag_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, off);
+    if ((st = exclusive_scan(off, n, scan_sums.as<uint32_t>(), &dsum->tasks, s))) return st;
+    hipLaunchKernelGGL(task_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, off,
+                       p->tasks);
+
+    hipLaunchKernelGGL(split_count_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt);
     if ((st = hip_status(hipMemcpyAsync(off, cnt, sizeof(uint32_t) * n, hipMemcpyDeviceToDevice, s))))
         return st;
-    if ((st = exclusive_scan(off, n, scan_sums.as<uint32_t>(), &ssum.as<SplitSummary>()->parts, s)))
-        return st;
+    if ((st = exclusive_scan(off, n, scan_sums.as<uint32_t>(), &dsum->parts, s))) return st;
     SplitSummary ss{};
     if ((st = hip_status(hipMemcpyAsync(&ss, ssum.p, sizeof(ss), hipMemcpyDeviceToHost, s))))
         return st;
     if ((st = hip_status(hipStreamSynchronize(s)))) return st;           // host wait 2
     p->n_sparse = ss.n_sparse;
+    p->n_tasks = static_cast<int32_t>(ss.tasks);
     p->n_split_rows = ss.split_rows;
     p->n_split_parts = static_cast<int32_t>(ss.parts);
     if (p->n_split_parts > 0) {
         const size_t np = static_cast<size_t>(p->n_split_parts);
         if ((st = alloc_bytes(reinterpret_cast<void **>(&p->parts), sizeof(SplitPart) * np))) return st;
-        if ((st = alloc_bytes(reinterpret_cast<void **>(&p->counters), sizeof(int32_t) * np))) return st;
+        if ((st = alloc_bytes(reinterpret_cast<void **>(&p->counters), sizeof(int32_t) * np * kMaxSlices)))
+            return st;
         if ((st = alloc_bytes(reinterpret_cast<void **>(&p->partials), sizeof(double) * np * kMaxSlice)))
             return st;
-        if ((st = hip_status(hipMemsetAsync(p->counters, 0, sizeof(int32_t) * np, s)))) return st;
-        hipLaunchKernelGGL(split_fill_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads),
-                           0, s, p->perm, n, cnt, off, p->parts, static_cast<uint32_t>(np));
+        if ((st = hip_status(hipMemsetAsync(p->counters, 0, sizeof(int32_t) * np * kMaxSlices, s))))
+            return st;
+        hipLaunchKernelGGL(split_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, cnt, off, n,
+                           p->parts, static_cast<uint32_t>(np));
         if ((st = hip_status(hipGetLastError()))) return st;
     }
     // the scratch buffers above are released on return: wait for their users

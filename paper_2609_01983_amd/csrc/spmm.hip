@@ -1,34 +1,47 @@
 // Dual-path aggregation SpMM Y = A X on gfx950 (DualGCN Sec. 3.3).
 //
-// One launch; every workgroup picks its path from its index (Eq. (1) was
-// applied when the plan was built, so the paths are contiguous index ranges):
+// The kernels stream the plan's sorted copy of the matrix: row i of the copy is
+// row perm[i] of A, the sparse region is rows [0, n_sparse) and the dense region
+// rows [n_sparse, n) (Eq. (1) was applied when the plan was built).  One launch
+// covers both paths; every workgroup picks its path from its index:
 //
-//   [0, n_parts)                    parts of dense rows longer than one chunk,
-//                                   heaviest row first
-//   [n_parts, n_parts + n_dense)    whole dense rows, heaviest first
-//   [.., + sparse blocks)           sparse rows, several per workgroup
+//   parts      rows of the dense region longer than one chunk, split into parts
+//              of kDenseChunk entries (heaviest row first), one wavefront per part
+//   dense      the other dense rows, one wavefront per row, heaviest first
+//   sparse     tasks of up to kTaskRows short consecutive rows, one lane group per
+//              task (the paper's "several rows per block")
 //
-// Feature layout (both paths): a row of X is read by a lane group of LPR lanes,
-// each lane holding VEC consecutive features (float4 loads when VEC = 4), so one
-// neighbour costs one coalesced load of LPR*VEC*4 bytes per group.  The group
-// loads LPR (column, value) pairs of its batch with one coalesced load and
-// passes them lane to lane with shuffles; up to 8 neighbour rows are in flight
-// per lane (the ILP of the paper's dense path, re-derived for 64-lane waves).
+// Feature layout.  A lane group of LPR lanes covers SW = LPR * VEC consecutive
+// features of a row: with VEC = 4 every lane makes one 16-byte load, so one
+// neighbour costs one coalesced load of the whole row (512 bytes = four 128-byte
+// lines at F = 128, 32 lanes).  Features beyond 256 are processed in windows of
+// 256; a window may be cut into S slices, workgroup b working on slice b % S
+// (used by the one-feature-per-lane path for arbitrary F).  Measured on c4/c5
+// (F = 128): cutting rows into 128-byte slices so that each XCD reads only its
+// own slice raises the L2 hit rate of a plain gather, but costs more in the SpMM
+// than it saves (every slice re-reads the indices and repeats the shuffles), so
+// rows are read whole.
 //
-// Sparse path (paper: several rows per block, warp-feature association): one
-// row per lane group, 64/LPR rows per wavefront; each row is written once.
+// Gathers.  A group takes the entries of its row (or task) in rounds of kRound:
+// each lane loads kRound / LPR (column, value) pairs with coalesced loads, the
+// pairs are broadcast inside the group with shuffles, and all kRound neighbour
+// slices are requested before the first product, so every group keeps kRound
+// loads in flight (the ILP of the paper's dense path, Alg. 1, deepened).
 //
-// Dense path (paper: one row per block, 4-way ILP, shared-memory reduction):
-// the workgroup's 256/LPR lane groups take the row's batches round robin and
-// the group partials are summed in LDS in group order.  Rows longer than one
-// chunk are split over several workgroups: each writes a float64 partial, and
-// the last one to arrive (integer counter) sums the parts in part order, writes
-// the row and clears the counter.  No floating-point atomics: Y is
-// bit-reproducible.
+// Dense path (one row per wavefront, paper: one row per block, 4-way ILP and a
+// shared reduction): the wavefront's groups take rounds of the row in turn and
+// are summed with a butterfly over the lanes.  A split row's parts each write a
+// float64 partial; the last part to arrive (integer counter per row and slice)
+// sums them in part order, writes the row and clears its counter.  No
+// floating-point atomics: Y is bit-reproducible.
 //
-// Summation: products and the sum of one batch (<= LPR <= 64 terms) are float32;
-// batch sums, group sums and part sums are float64; the output is rounded once.
-// The error of every element is then below ~(LPR + 2) * 2^-24 * sum |a||x|.
+// Sparse path (tasks): the group walks the task's entries as one stream, so even
+// rows with one or two entries share a round of kRound gathers; a row is written
+// as soon as its last entry has been added.
+//
+// Summation: products and the sum of one round (<= kRound terms) are float32,
+// rounds are added in float64, and each output is rounded once to float32.  The
+// error of every element is below ~(kRound + 2) * 2^-24 * sum |a||x|.
 #include "internal.h"
 
 namespace dgc {
@@ -36,11 +49,12 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kRound = 16;            // entries a lane group gathers per round
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <int VEC>
-__device__ __forceinline__ void load_row(const float *__restrict__ p, float (&x)[VEC]) {
+__device__ __forceinline__ void load_x(const float *__restrict__ p, float (&x)[VEC]) {
     if constexpr (VEC == 4) {
         const f32x4 v = *reinterpret_cast<const f32x4 *>(p);
         x[0] = v[0];
@@ -54,7 +68,7 @@ __device__ __forceinline__ void load_row(const float *__restrict__ p, float (&x)
 }
 
 template <int VEC>
-__device__ __forceinline__ void store_row(float *__restrict__ p, const double (&s)[VEC], bool relu) {
+__device__ __forceinline__ void store_y(float *__restrict__ p, const double (&s)[VEC], bool relu) {
     float o[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
@@ -70,169 +84,248 @@ __device__ __forceinline__ void store_row(float *__restrict__ p, const double (&
     }
 }
 
-// Accumulates entries [first, last) of one CSR row, in batches of LPR entries
-// starting at `first` and then every `step` entries, into tot (float64).
-template <int LPR, int VEC>
-__device__ __forceinline__ void gather_rows(const int32_t *__restrict__ col,
-                                            const float *__restrict__ val,
-                                            const float *__restrict__ X, int64_t ldx, int f,
-                                            bool fin, int li, int32_t first, int32_t last,
-                                            int32_t step, double (&tot)[VEC]) {
-    constexpr int U = LPR < 8 ? LPR : 8;
-    for (int32_t base = first; base < last; base += step) {
-        const int cnt = min(LPR, last - base);
-        int32_t c = 0;
-        float a = 0.f;
-        if (li < cnt) {
-            c = col[base + li];
-            a = val[base + li];
-        }
-        float acc[VEC];
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
-        for (int t = 0; t < cnt; t += U) {
-            float xs[U][VEC];
-            float as[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int src = t + u;
-                const int32_t cc = __shfl(c, src, LPR);
-                as[u] = __shfl(a, src, LPR);
-                if (src < cnt && fin) {
-                    load_row<VEC>(X + static_cast<int64_t>(cc) * ldx + f, xs[u]);
-                } else {
-                    as[u] = 0.f;
-#pragma unroll
-                    for (int j = 0; j < VEC; ++j) xs[u][j] = 0.f;
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int j = 0; j < VEC; ++j) acc[j] = fmaf(as[u], xs[u][j], acc[j]);
-        }
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) tot[j] += static_cast<double>(acc[j]);
-    }
-}
-
 struct Args {
-    const int32_t *perm;
-    int32_t n, n_sparse;
+    const int32_t *pptr;        // sorted copy of the matrix
+    const int32_t *pcol;
+    const float *pval;
+    const int32_t *perm;        // output row of each sorted row
+    const int32_t *tasks;
     const SplitPart *parts;
-    int32_t n_parts;
-    int32_t n_dense_blocks;     // n_parts + (n - n_sparse)
     int32_t *counters;
     double *partials;
-    const int32_t *rowptr;
-    const int32_t *col;
-    const float *val;
     const float *X;
     float *Y;
-    int32_t F;                  // leading dimension of X and Y
-    int32_t f0;                 // first feature of this slice
+    int32_t n, n_sparse, n_tasks, n_parts;
+    int32_t ld;                 // leading dimension of X and Y (= F)
+    int32_t f0;                 // first feature of this launch window
+    int32_t fend;               // end of the valid features of the window
+    int32_t S;                  // feature slices in the window
+    int32_t nb_parts;           // logical workgroups of hub-row parts
+    int32_t nb_dense;           // logical workgroups of whole dense rows
     int32_t relu;
 };
 
-template <int LPR, int VEC>
-__global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
-    constexpr int G = kThreads / LPR;       // lane groups per workgroup
-    constexpr int SW = LPR * VEC;           // features per slice
-    __shared__ double red[G][SW];
-    __shared__ int last_flag;
+// Entries [e, min(e + kRound, e_end)) of the sorted copy, as seen by lane li of a
+// group whose first lane is gbase: lane li loads entries e + li + k LPR; entry u is
+// then held by lane u % LPR in register u / LPR.
+template <int LPR>
+struct Round {
+    static constexpr int EPL = (kRound + LPR - 1) / LPR;   // entries per lane
+    int32_t c[EPL];
+    float v[EPL];
 
-    const int b = static_cast<int>(blockIdx.x);
-    const int li = static_cast<int>(threadIdx.x) % LPR;
-    const int f = a.f0 + li * VEC;
-    const bool fin = (VEC == 1) ? (f < a.F) : true;
-
-    if (b >= a.n_dense_blocks) {
-        // ---------------- sparse path: one row per lane group
-        constexpr int GPW = 64 / LPR;
-        const int lane = static_cast<int>(threadIdx.x) & 63;
-        const int64_t gid = (static_cast<int64_t>(b - a.n_dense_blocks) * kWaves +
-                             (threadIdx.x >> 6)) * GPW + lane / LPR;
-        if (gid >= a.n_sparse) return;
-        const int32_t r = a.perm[gid];
-        double tot[VEC];
+    __device__ __forceinline__ void load(const Args &a, int32_t e, int32_t e_end, int li) {
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) tot[j] = 0.0;
-        gather_rows<LPR, VEC>(a.col, a.val, a.X, a.F, f, fin, li, a.rowptr[r], a.rowptr[r + 1],
-                              LPR, tot);
-        if (fin) store_row<VEC>(a.Y + static_cast<int64_t>(r) * a.F + f, tot, a.relu);
-        return;
+        for (int k = 0; k < EPL; ++k) {
+            const int slot = li + k * LPR;
+            const int32_t idx = e + slot;
+            const bool ok = slot < kRound && idx < e_end;
+            c[k] = ok ? a.pcol[idx] : -1;
+            v[k] = ok ? a.pval[idx] : 0.f;
+        }
     }
+};
 
-    // ---------------- dense path: one workgroup per row (or per part of a long row)
-    int32_t r, p0, p1;
-    int part = -1, nparts = 1, first = 0;
-    if (b < a.n_parts) {
-        const SplitPart sp = a.parts[a.n_parts - 1 - b];
-        r = sp.row;
-        part = sp.part;
-        nparts = sp.nparts;
-        first = sp.first;
-        const int32_t row_end = a.rowptr[r + 1];
-        p0 = a.rowptr[r] + part * kDenseChunk;
-        p1 = min(p0 + kDenseChunk, row_end);
-    } else {
-        const int32_t i = a.n - 1 - (b - a.n_parts);
-        r = a.perm[i];
-        p0 = a.rowptr[r];
-        p1 = a.rowptr[r + 1];
-        if (p1 - p0 > kDenseChunk) return;   // this row is covered by its parts
+// Requests the kRound neighbour slices of a round (invalid entries read nothing and
+// get weight zero).
+template <int LPR, int VEC>
+__device__ __forceinline__ void gather(const Args &a, const Round<LPR> &r, int gbase, int f,
+                                       bool fin, float (&as)[kRound], float (&xs)[kRound][VEC]) {
+#pragma unroll
+    for (int u = 0; u < kRound; ++u) {
+        const int32_t cc = __shfl(r.c[u / LPR], gbase + u % LPR, 64);
+        as[u] = __shfl(r.v[u / LPR], gbase + u % LPR, 64);
+        if (cc >= 0 && fin) {
+            load_x<VEC>(a.X + static_cast<int64_t>(cc) * a.ld + f, xs[u]);
+        } else {
+            as[u] = 0.f;
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) xs[u][j] = 0.f;
+        }
     }
-    const int g = static_cast<int>(threadIdx.x) / LPR;
-    double tot[VEC];
+}
+
+// Dense path: one wavefront accumulates entries [e0, e1) of one row; on return every
+// lane holds the row's sums for its features (groups reduced by a butterfly).
+template <int LPR, int VEC>
+__device__ __forceinline__ void dense_row(const Args &a, int32_t e0, int32_t e1, int li, int gw,
+                                          int gbase, int f, bool fin, double (&tot)[VEC]) {
+    constexpr int GPW = 64 / LPR;
 #pragma unroll
     for (int j = 0; j < VEC; ++j) tot[j] = 0.0;
-    gather_rows<LPR, VEC>(a.col, a.val, a.X, a.F, f, fin, li, p0 + g * LPR, p1, G * LPR, tot);
+    for (int32_t e = e0 + gw * kRound; e < e1; e += GPW * kRound) {
+        Round<LPR> r;
+        r.load(a, e, e1, li);
+        float as[kRound], xs[kRound][VEC];
+        gather<LPR, VEC>(a, r, gbase, f, fin, as, xs);
+        float acc[VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) red[g][li * VEC + j] = tot[j];
-    __syncthreads();
-    const int t = static_cast<int>(threadIdx.x);
-    const int ft = a.f0 + t;
-    if (part < 0) {
-        if (t < SW && ft < a.F) {
-            double s = 0.0;
-#pragma unroll 4
-            for (int q = 0; q < G; ++q) s += red[q][t];
-            float o = static_cast<float>(s);
-            if (a.relu) o = o > 0.f ? o : 0.f;
-            __builtin_nontemporal_store(o, a.Y + static_cast<int64_t>(r) * a.F + ft);
-        }
-        return;
+        for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
+#pragma unroll
+        for (int u = 0; u < kRound; ++u)
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) acc[j] = fmaf(as[u], xs[u][j], acc[j]);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) tot[j] += static_cast<double>(acc[j]);
     }
-    if (t < SW) {
-        double s = 0.0;
-#pragma unroll 4
-        for (int q = 0; q < G; ++q) s += red[q][t];
-        __hip_atomic_store(a.partials + static_cast<int64_t>(first + part) * kMaxSlice + t, s,
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    __threadfence();      // publish this part before counting it
-    __syncthreads();
-    if (t == 0) last_flag = atomicAdd(&a.counters[first], 1) == nparts - 1;
-    __syncthreads();
-    if (!last_flag) return;
-    __threadfence();      // see every other part
-    if (t < SW && ft < a.F) {
-        double s = 0.0;
-        for (int q = 0; q < nparts; ++q)
-            s += __hip_atomic_load(a.partials + static_cast<int64_t>(first + q) * kMaxSlice + t,
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        float o = static_cast<float>(s);
-        if (a.relu) o = o > 0.f ? o : 0.f;
-        __builtin_nontemporal_store(o, a.Y + static_cast<int64_t>(r) * a.F + ft);
-    }
-    if (t == 0) a.counters[first] = 0;   // ready for the next call on this plan
+#pragma unroll
+    for (int m = LPR; m < 64; m <<= 1)
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) tot[j] += __shfl_xor(tot[j], m, 64);
+}
+
+// Selects register j / LPR of a per-lane array and reads it from lane j % LPR.
+template <int LPR, int N>
+__device__ __forceinline__ int32_t task_meta(const int32_t (&m)[N], int j, int gbase) {
+    int32_t x = m[0];
+#pragma unroll
+    for (int k = 1; k < N; ++k)
+        if (j / LPR == k) x = m[k];
+    return __shfl(x, gbase + j % LPR, 64);
 }
 
 template <int LPR, int VEC>
-int launch_slice(Args a, hipStream_t s) {
-    constexpr int rows_per_block = kWaves * (64 / LPR);
-    const int64_t sparse_blocks = (static_cast<int64_t>(a.n_sparse) + rows_per_block - 1) / rows_per_block;
-    const int64_t blocks = static_cast<int64_t>(a.n_dense_blocks) + sparse_blocks;
+__global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
+    constexpr int GPW = 64 / LPR;                 // lane groups per wavefront
+    constexpr int SW = LPR * VEC;                 // features per slice
+    constexpr int RPL = (kTaskRows + LPR - 1) / LPR;
+
+    const int slice = static_cast<int>(blockIdx.x) % a.S;
+    const int lb = static_cast<int>(blockIdx.x) / a.S;
+    const int lane = static_cast<int>(threadIdx.x) & 63;
+    const int wave = static_cast<int>(threadIdx.x) >> 6;
+    const int li = lane % LPR;
+    const int gw = lane / LPR;
+    const int gbase = lane - li;
+    const int f = a.f0 + slice * SW + li * VEC;
+    const bool fin = f < a.fend;
+
+    if (lb < a.nb_parts + a.nb_dense) {
+        // ---------------- dense path: one wavefront per row or per part of a split row
+        const int w = lb * kWaves + wave;
+        int32_t i, e0, e1;
+        int part = -1, nparts = 1, first = 0;
+        if (lb < a.nb_parts) {
+            if (w >= a.n_parts) return;
+            const SplitPart sp = a.parts[a.n_parts - 1 - w];
+            i = sp.row;
+            part = sp.part;
+            nparts = sp.nparts;
+            first = sp.first;
+            e0 = a.pptr[i] + part * kDenseChunk;
+            e1 = min(e0 + kDenseChunk, a.pptr[i + 1]);
+        } else {
+            i = a.n - 1 - (w - a.nb_parts * kWaves);
+            if (i < a.n_sparse) return;
+            e0 = a.pptr[i];
+            e1 = a.pptr[i + 1];
+            if (e1 - e0 > kDenseChunk) return;     // covered by its parts
+        }
+        double tot[VEC];
+        dense_row<LPR, VEC>(a, e0, e1, li, gw, gbase, f, fin, tot);
+        if (part < 0) {
+            if (gw == 0 && fin) store_y<VEC>(a.Y + static_cast<int64_t>(a.perm[i]) * a.ld + f, tot, a.relu);
+            return;
+        }
+        double *pp = a.partials + static_cast<int64_t>(first) * kMaxSlice + (f - a.f0);
+        if (gw == 0 && fin) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j)
+                __hip_atomic_store(pp + static_cast<int64_t>(part) * kMaxSlice + j, tot[j],
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __threadfence();      // publish this part before counting it
+        int32_t *counter = a.counters + static_cast<int64_t>(first) * kMaxSlices + slice;
+        int last = 0;
+        if (lane == 0) last = atomicAdd(counter, 1) == nparts - 1;
+        last = __shfl(last, 0, 64);
+        if (!last) return;
+        __threadfence();      // see every other part
+        if (gw == 0 && fin) {
+            double s[VEC];
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) s[j] = 0.0;
+            for (int q = 0; q < nparts; ++q)
+#pragma unroll
+                for (int j = 0; j < VEC; ++j)
+                    s[j] += __hip_atomic_load(pp + static_cast<int64_t>(q) * kMaxSlice + j,
+                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            store_y<VEC>(a.Y + static_cast<int64_t>(a.perm[i]) * a.ld + f, s, a.relu);
+        }
+        if (lane == 0) *counter = 0;          // ready for the next call on this plan
+        return;
+    }
+
+    // ---------------- sparse path: one task (up to kTaskRows short rows) per lane group
+    const int64_t t = (static_cast<int64_t>(lb - a.nb_parts - a.nb_dense) * kWaves + wave) * GPW + gw;
+    if (t >= a.n_tasks) return;               // the whole group leaves together
+    const int32_t r0 = a.tasks[t];
+    const int m = a.tasks[t + 1] - r0;        // 1 .. kTaskRows rows
+    int32_t rend[RPL], rout[RPL];             // row j: lane j % LPR, register j / LPR
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) {
+        const int j = li + k * LPR;
+        rend[k] = j < m ? a.pptr[r0 + j + 1] : 0;
+        rout[k] = j < m ? a.perm[r0 + j] : 0;
+    }
+    const int32_t e_begin = a.pptr[r0];
+    const int32_t e_end = task_meta<LPR>(rend, m - 1, gbase);
+    if (e_begin == e_end) {                   // an empty row is a task of its own
+        double z[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) z[j] = 0.0;
+        if (fin) store_y<VEC>(a.Y + static_cast<int64_t>(task_meta<LPR>(rout, 0, gbase)) * a.ld + f, z, a.relu);
+        return;
+    }
+    int cur = 0;                              // every row of a task with entries is non-empty
+    int32_t cur_end = task_meta<LPR>(rend, 0, gbase);
+    int32_t cur_out = task_meta<LPR>(rout, 0, gbase);
+    double tot[VEC];
+    float part[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        tot[j] = 0.0;
+        part[j] = 0.f;
+    }
+    for (int32_t e = e_begin; e < e_end; e += kRound) {
+        Round<LPR> r;
+        r.load(a, e, e_end, li);
+        float as[kRound], xs[kRound][VEC];
+        gather<LPR, VEC>(a, r, gbase, f, fin, as, xs);
+#pragma unroll
+        for (int u = 0; u < kRound; ++u) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) part[j] = fmaf(as[u], xs[u][j], part[j]);
+            if (e + u + 1 == cur_end) {       // the current row ends with this entry
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) {
+                    tot[j] += static_cast<double>(part[j]);
+                    part[j] = 0.f;
+                }
+                if (fin) store_y<VEC>(a.Y + static_cast<int64_t>(cur_out) * a.ld + f, tot, a.relu);
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) tot[j] = 0.0;
+                if (++cur < m) {
+                    cur_end = task_meta<LPR>(rend, cur, gbase);
+                    cur_out = task_meta<LPR>(rout, cur, gbase);
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            tot[j] += static_cast<double>(part[j]);
+            part[j] = 0.f;
+        }
+    }
+}
+
+template <int LPR, int VEC>
+int launch_window(Args a, hipStream_t s) {
+    constexpr int GPB = kThreads / LPR;       // sparse tasks per workgroup
+    a.nb_parts = (a.n_parts + kWaves - 1) / kWaves;
+    a.nb_dense = (a.n - a.n_sparse + kWaves - 1) / kWaves;
+    const int64_t nb_sparse = (static_cast<int64_t>(a.n_tasks) + GPB - 1) / GPB;
+    const int64_t blocks = (static_cast<int64_t>(a.nb_parts) + a.nb_dense + nb_sparse) * a.S;
     if (blocks == 0) return DUALGCN_OK;
     if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
     hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC>), dim3(static_cast<unsigned>(blocks)),
@@ -244,47 +337,45 @@ int launch_slice(Args a, hipStream_t s) {
 
 int launch_spmm(const Plan &p, const float *X, float *Y, int32_t F, bool relu, hipStream_t s) {
     Args a{};
+    a.pptr = p.pptr;
+    a.pcol = p.pcol;
+    a.pval = p.pval;
     a.perm = p.perm;
-    a.n = p.n;
-    a.n_sparse = p.n_sparse;
+    a.tasks = p.tasks;
     a.parts = p.parts;
-    a.n_parts = p.n_split_parts;
-    a.n_dense_blocks = p.n_split_parts + (p.n - p.n_sparse);
     a.counters = p.counters;
     a.partials = p.partials;
-    a.rowptr = p.rowptr;
-    a.col = p.col;
-    a.val = p.val;
     a.X = X;
     a.Y = Y;
-    a.F = F;
+    a.n = p.n;
+    a.n_sparse = p.n_sparse;
+    a.n_tasks = p.n_tasks;
+    a.n_parts = p.n_split_parts;
+    a.ld = F;
     a.relu = relu ? 1 : 0;
 
-    const bool aligned = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
-                         (reinterpret_cast<uintptr_t>(Y) % 16 == 0) && (F % 4 == 0);
+    const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
+                     (reinterpret_cast<uintptr_t>(Y) % 16 == 0) && (F % 4 == 0);
     int st = DUALGCN_OK;
-    if (aligned && (F == 4 || F == 8 || F == 16 || F == 32 || F == 64 || F == 128 || F == 256)) {
-        a.f0 = 0;
-        switch (F) {
-            case 4: return launch_slice<1, 4>(a, s);
-            case 8: return launch_slice<2, 4>(a, s);
-            case 16: return launch_slice<4, 4>(a, s);
-            case 32: return launch_slice<8, 4>(a, s);
-            case 64: return launch_slice<16, 4>(a, s);
-            case 128: return launch_slice<32, 4>(a, s);
-            default: return launch_slice<64, 4>(a, s);
-        }
-    }
-    if (aligned && F % 256 == 0) {
-        for (int32_t f0 = 0; f0 < F && !st; f0 += 256) {
-            a.f0 = f0;
-            st = launch_slice<64, 4>(a, s);
-        }
-        return st;
-    }
-    for (int32_t f0 = 0; f0 < F && !st; f0 += 64) {
+    for (int32_t f0 = 0; f0 < F && !st; f0 += kMaxSlice) {
+        const int32_t w = F - f0 < kMaxSlice ? F - f0 : kMaxSlice;
         a.f0 = f0;
-        st = launch_slice<64, 1>(a, s);
+        a.fend = f0 + w;
+        if (vec) {
+            // whole rows: the smallest power-of-two lane group with 4 features per lane
+            a.S = 1;
+            if (w <= 4) st = launch_window<1, 4>(a, s);
+            else if (w <= 8) st = launch_window<2, 4>(a, s);
+            else if (w <= 16) st = launch_window<4, 4>(a, s);
+            else if (w <= 32) st = launch_window<8, 4>(a, s);
+            else if (w <= 64) st = launch_window<16, 4>(a, s);
+            else if (w <= 128) st = launch_window<32, 4>(a, s);
+            else st = launch_window<64, 4>(a, s);
+        } else {
+            // any other width or alignment: one feature per lane, 64-feature slices
+            a.S = (w + 63) / 64;
+            st = launch_window<64, 1>(a, s);
+        }
     }
     return st;
 }
