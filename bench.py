@@ -5,20 +5,27 @@ A step is one pass of the whole path over one synthetic workload, inputs
 already resident in HBM:
   c1        SpMM                                  (F = 16)
   c2,c3,c4  dual-metric partition + SpMM          (F = 64 / 128 / 128)
-  c5        partition + 2 GCN layers, each X W on the bf16 matrix cores then SpMM,
-            ReLU between (256 -> 128 -> 64)
+  c5        partition + 2 GCN layers (256 -> 128 -> 64); each layer is the update
+            X W on the bf16 matrix cores then the SpMM, ReLU after layer 1
 Metric: edge-features per second, GE/s = sum over the step's SpMMs of nnz F / step time.
 
 The JSON line also carries
-  roofline      the SpMM kernel (dominant HBM kernel) against 8 TB/s: algorithmic bytes
-                B_min = 4(n+1) + 8 nnz + 4 n F (X once) + 4 n F (Y) + 4 n (perm) per
-                launch over its mean duration, timed with HIP events on its stream;
+  roofline      the dominant kernel, the F=128 SpMM (the F=64 one for c2, F=16 for c1),
+                against 8 TB/s: algorithmic bytes
+                B_min = 4(n+1) + 8 nnz + 4 n F (X once) + 4 n F (Y) + 4 n (perm)
+                per launch over its mean duration, timed with HIP events on its
+                stream around every launch of it inside the timed steps;
+                `traffic` is the HBM bytes per launch from the rocprofv3 FETCH_SIZE /
+                WRITE_SIZE summary under profiles/ (null when the kernel source has
+                changed since those counters were taken);
   cpu_baseline  the CPU oracle timed on a bounded sample of the same workload;
-  phases        mean milliseconds of partition / X W / SpMM inside the timed steps.
+  phases_ms     mean milliseconds of each phase inside the timed steps.
 """
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -27,35 +34,65 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 METRIC = "SpMM GE/s (nnz·F/s) and achieved HBM GB/s vs peak, 1×MI355X"
+COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "spmm_c5_hbm_counters.md")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_01983_amd", "csrc", f)
+                  for f in ("spmm.hip", "internal.h")]
 
 
 def spmm_bytes(n, nnz, F):
     return 4 * (n + 1) + 8 * nnz + 4 * n * F + 4 * n * F + 4 * n
 
 
-def xw_bytes(n, fin, fout):
-    return 4 * n * fin + 4 * n * fout
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
-def cpu_baseline(cfg, g, X, weights, budget_s=12.0):
-    """Time the oracle on a bounded random sample and scale to one whole step."""
+def counter_traffic(workload):
+    """HBM bytes per SpMM launch from the committed counter summary, if still valid."""
+    if not os.path.exists(COUNTER_SUMMARY):
+        return None, "no counter summary"
+    text = open(COUNTER_SUMMARY).read()
+    m_w = re.search(r"^workload: (\S+)", text, re.M)
+    m_t = re.search(r"^traffic_bytes_per_launch: (\d+)", text, re.M)
+    m_h = re.search(r"^kernel_source_sha256: ([0-9a-f]{64})", text, re.M)
+    if not (m_w and m_t and m_h) or m_w.group(1) != workload:
+        return None, "no counters for this workload"
+    if m_h.group(1) != kernel_source_hash():
+        return None, "kernel changed since the counters were taken"
+    return int(m_t.group(1)), "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
+
+
+def _grow(fn, total, first, budget_s):
+    """Runs fn(size) on samples of growing size until one takes >= budget_s (or covers
+    `total`); returns (seconds, size) of the last run."""
+    size = min(first, total)
+    while True:
+        t0 = time.perf_counter()
+        fn(size)
+        dt = time.perf_counter() - t0
+        if dt >= budget_s or size >= total:
+            return dt, size
+        size = min(total, max(size * 2, int(size * budget_s / max(dt, 1e-3) * 1.2)))
+
+
+def cpu_baseline(w, g, X, weights, part_budget_s=2.5):
+    """Times the oracle on bounded random samples of each part of one step and scales
+    every part to the whole workload."""
     import numpy as np
     import oracle
-    w = cfg
     gen = np.random.default_rng(7)
-    rp = g.rowptr.astype(np.int64)
     t_total = 0.0
     parts = []
-    # walks: sample nodes, scale by n / sample
     if w.name != "c1":
-        ns = min(g.n, 20000)
-        nodes = gen.choice(g.n, ns, replace=False).astype(np.int32)
-        t0 = time.perf_counter()
-        oracle.density_sums(g, 0, w.walks, w.steps, nodes)
-        dt = time.perf_counter() - t0
+        order = gen.permutation(g.n).astype(np.int32)
+        dt, ns = _grow(lambda s: oracle.density_sums(g, 0, w.walks, w.steps, order[:s]),
+                       g.n, 2000, part_budget_s)
         t_total += dt * g.n / ns
         parts.append(f"walks of {ns} nodes")
-        # keys, exact threshold and sort: on the full node count with sampled-size keys
         S = gen.integers(w.walks, w.walks * (w.steps + 1) + 1, g.n).astype(np.uint32)
         t0 = time.perf_counter()
         K = oracle.hybrid_keys(S, oracle.degrees(g), w.walks)
@@ -63,32 +100,39 @@ def cpu_baseline(cfg, g, X, weights, budget_s=12.0):
         oracle.threshold_key(g.n, S1, S2)
         np.lexsort((np.arange(g.n), K))
         t_total += time.perf_counter() - t0
-        parts.append("keys/threshold/sort of all nodes")
-    # per layer: X W on sampled rows (scaled by n / rows) and the SpMM of sampled rows
-    # (scaled by nnz / sampled nnz); the SpMM input of a GCN layer is a stand-in of
-    # the same shape (the first F_out columns of X)
+        parts.append("keys, threshold and sort of all nodes")
+    rp = np.asarray(g.rowptr, dtype=np.int64)
     layers = w.layers if w.is_gcn else ((None, w.F),)
     for li, (fin, fout) in enumerate(layers):
-        rows = gen.choice(g.n, min(g.n, 4000), replace=False).astype(np.int32)
-        nnz_s = int((rp[rows + 1] - rp[rows]).sum())
+        rows_all = gen.permutation(g.n).astype(np.int32)
         if fin is not None:
-            xin = np.ascontiguousarray(X[rows, :fin])
-            t0 = time.perf_counter()
-            oracle.xw(xin, weights[li])
-            t_total += (time.perf_counter() - t0) * g.n / rows.size
-            T = np.ascontiguousarray(X[:, :fout])
+            Wl = weights[li]
+            # the layer's input has the shape of X's first fin columns (a stand-in)
+            Xin = X if fin == X.shape[1] else np.ascontiguousarray(X[:, :fin])
+            dt, nr = _grow(lambda s: oracle.xw(Xin, Wl, rows_all[:s]), g.n, 500,
+                           part_budget_s / 2)
+            del Xin
+            t_total += dt * g.n / nr
+            parts.append(f"layer {li + 1}: X W of {nr} rows")
+            T = np.ascontiguousarray(X[:, :fout])   # a stand-in of the layer's SpMM input shape
         else:
             T = X
-        t0 = time.perf_counter()
-        oracle.spmm(g, T, rows)
-        t_total += (time.perf_counter() - t0) * g.nnz / max(nnz_s, 1)
+        nnz_of = {}
+
+        def run_spmm(s):
+            rows = rows_all[:s]
+            nnz_of[s] = int((rp[rows + 1] - rp[rows]).sum())
+            oracle.spmm(g, T, rows)
+
+        dt, nr = _grow(run_spmm, g.n, 500, part_budget_s / 2)
+        t_total += dt * g.nnz / max(nnz_of[nr], 1)
+        parts.append(f"layer {li + 1}: SpMM of {nr} rows ({nnz_of[nr]} entries)"
+                     if w.is_gcn else f"SpMM of {nr} rows ({nnz_of[nr]} entries)")
         del T
-        parts.append(f"layer {li}: SpMM of {rows.size} rows ({nnz_s} nnz)"
-                     + (f", X W of {rows.size} rows" if fin is not None else ""))
     ge = g.nnz * sum(fo for _, fo in layers)
     return {"value": ge / t_total / 1e9, "unit": "GE/s", "cores": 1, "kind": "oracle",
-            "sample": "single-threaded C oracle; " + "; ".join(parts) +
-                      "; each part scaled to the whole workload",
+            "sample": "single-threaded C oracle on random samples of the same workload: "
+                      + "; ".join(parts) + "; each part scaled to the whole workload",
             "est_step_s": round(t_total, 3)}
 
 
@@ -101,7 +145,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--spmm-reps", type=int, default=20)
     ap.add_argument("--mode", choices=["full", "spmm"], default="full",
-                    help="spmm: one partition, then only the SpMM launches (for counter runs)")
+                    help="spmm: one partition, then only the dominant SpMM launches (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device to device (a dispatch of known traffic)")
     args = ap.parse_args()
@@ -131,6 +175,7 @@ def main():
     Wd = [torch.from_numpy(W).to(dev) for W in weights]
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
+    F_dom = w.layers[0][1] if w.is_gcn else w.F      # width of the dominant SpMM
     if args.copy_calibration:
         src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
@@ -141,121 +186,102 @@ def main():
         print("[bench] copy calibration: 1073741824 bytes read + written", file=sys.stderr,
               flush=True)
     if args.mode == "spmm":
-        F_spmm = w.layers[0][1] if w.is_gcn else w.F
         plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
-        Xs = Xd[:, :F_spmm].contiguous() if w.is_gcn else Xd
+        Xs = torch.randn((g.n, F_dom), dtype=torch.float32, device=dev) if w.is_gcn else Xd
         Ys = torch.empty_like(Xs)
         times = []
         for _ in range(args.spmm_reps):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            dg.spmm(plan, Xs, Ys)
+            dg.spmm(plan, Xs, Ys, relu=w.is_gcn)
             b.record(stream)
             times.append((a, b))
         torch.cuda.synchronize()
         ms = [a.elapsed_time(b) for a, b in times]
-        print(json.dumps({"mode": "spmm", "config": w.name, "F": F_spmm,
+        print(json.dumps({"mode": "spmm", "config": w.name, "F": F_dom,
                           "ms": [round(x, 4) for x in ms],
-                          "bytes_min": spmm_bytes(g.n, g.nnz, F_spmm)}), flush=True)
+                          "bytes_min": spmm_bytes(g.n, g.nnz, F_dom)}), flush=True)
         plan.destroy()
         return
 
+    ev = lambda: torch.cuda.Event(enable_timing=True)
     if w.is_gcn:
-        fouts = [fo for _, fo in w.layers]
-        Hs = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for fo in fouts]
-        ws_bytes = max(4 * g.n * fo + 2 * fi * fo + 256 for fi, fo in w.layers)
+        Ts = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for _, fo in w.layers]
+        Hs = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for _, fo in w.layers]
     else:
         Y = torch.empty_like(Xd)
+    holder = {"plan": None}
+    if w.name == "c1":      # c1 is one SpMM per step on a fixed plan
+        holder["plan"] = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks,
+                                 walk_len=w.steps)
 
-    ev = lambda: torch.cuda.Event(enable_timing=True)
-    phase_ms = {"partition": [], "xw_spmm": [], "spmm": []}
-    kernel_ms = []
-
-    plan_holder = {}
-
-    def step(timed):
-        e0, e1 = ev(), ev()
-        e0.record(stream)
-        plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
-        e1.record(stream)
-        if plan_holder.get("plan") is not None:
-            plan_holder["plan"].destroy()
-        plan_holder["plan"] = plan
-        if w.name == "c1":
-            e0.record(stream)   # c1 is one SpMM per step; the partition is not part of it
+    def step():
+        """Enqueues one step; returns {phase: [(start, end) events]}."""
+        marks = {}
+        if w.name != "c1":
+            a, b = ev(), ev()
+            a.record(stream)
+            plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
+            b.record(stream)
+            marks["partition"] = [(a, b)]
+            if holder["plan"] is not None:
+                holder["plan"].destroy()
+            holder["plan"] = plan
+        plan = holder["plan"]
         if w.is_gcn:
             x = Xd
-            layer_ev = []
             for li, (fin, fout) in enumerate(w.layers):
-                a, b = ev(), ev()
+                a, b, c = ev(), ev(), ev()
                 a.record(stream)
-                dg.gcn_layer(plan, x, Wd[li], relu=li < len(w.layers) - 1, Y=Hs[li],
-                             workspace=ws)
+                dg.update(plan, x, Wd[li], Ts[li])
                 b.record(stream)
-                layer_ev.append((a, b))
+                dg.spmm(plan, Ts[li], Hs[li], relu=li < len(w.layers) - 1)
+                c.record(stream)
+                marks[f"update_{li + 1}"] = [(a, b)]
+                marks[f"spmm_{li + 1}_F{fout}"] = [(b, c)]
                 x = Hs[li]
-            if timed:
-                torch.cuda.synchronize()
-                phase_ms["partition"].append(e0.elapsed_time(e1))
-                phase_ms["xw_spmm"].append(sum(a.elapsed_time(b) for a, b in layer_ev))
         else:
             a, b = ev(), ev()
             a.record(stream)
             dg.spmm(plan, Xd, Y)
             b.record(stream)
-            if timed:
-                torch.cuda.synchronize()
-                if w.name != "c1":
-                    phase_ms["partition"].append(e0.elapsed_time(e1))
-                phase_ms["spmm"].append(a.elapsed_time(b))
-
-    if w.is_gcn:
-        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-
-    if w.name == "c1":
-        plan_holder["plan"] = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks,
-                                      walk_len=w.steps)
-
-        def step(timed):  # noqa: F811 -- c1: one SpMM per step on a fixed plan
-            a, b = ev(), ev()
-            a.record(stream)
-            dg.spmm(plan_holder["plan"], Xd, Y)
-            b.record(stream)
-            if timed:
-                torch.cuda.synchronize()
-                phase_ms["spmm"].append(a.elapsed_time(b))
+            marks[f"spmm_1_F{w.F}"] = [(a, b)]
+        return marks
 
     for _ in range(args.warmup):
-        step(False)
+        step()
     torch.cuda.synchronize()
+    all_marks = []
     t_start = time.perf_counter()
     for _ in range(args.steps):
-        step(True)
+        all_marks.append(step())
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = elapsed * 1e3 / args.steps
 
-    # SpMM kernel alone on the last plan, HIP events on its stream (the roofline figure)
-    plan = plan_holder["plan"]
-    F_spmm = w.layers[0][1] if w.is_gcn else w.F
-    Xs = torch.randn((g.n, F_spmm), dtype=torch.float32, device=dev) if w.is_gcn else Xd
-    Ys = torch.empty_like(Xs)
-    for _ in range(3):
-        dg.spmm(plan, Xs, Ys)
-    for _ in range(args.spmm_reps):
-        a, b = ev(), ev()
-        a.record(stream)
-        dg.spmm(plan, Xs, Ys)
-        b.record(stream)
-        kernel_ms.append((a, b))
-    torch.cuda.synchronize()
-    spmm_ms = float(np.mean([a.elapsed_time(b) for a, b in kernel_ms]))
-    info = plan.info()
+    phases = {}
+    for marks in all_marks:
+        for k, lst in marks.items():
+            phases.setdefault(k, []).extend(a.elapsed_time(b) for a, b in lst)
+    dom_key = f"spmm_1_F{F_dom}"
+    spmm_ms = float(np.mean(phases[dom_key]))
+    info = holder["plan"].info()
 
     ge_per_step = g.nnz * (sum(fo for _, fo in w.layers) if w.is_gcn else w.F)
     value = ge_per_step / (ms_per_step * 1e-3) / 1e9
-    bmin = spmm_bytes(g.n, g.nnz, F_spmm)
+    bmin = spmm_bytes(g.n, g.nnz, F_dom)
     achieved = bmin / (spmm_ms * 1e-3) / 1e9
+    traffic, traffic_src = counter_traffic(w.name)
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+            "kernel": f"spmm_dual_kernel<{min(64, max(1, F_dom // 4))}, 4> "
+                      f"(F={F_dom}{', ReLU' if w.is_gcn else ''})",
+            "bytes_per_launch": bmin, "ms_per_launch": round(spmm_ms, 4),
+            "launches_timed": len(phases[dom_key]),
+            "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
+            "gather_bytes_per_launch": 4 * (g.n + 1) + 8 * g.nnz + 4 * g.nnz * F_dom
+                                       + 4 * g.n * F_dom + 4 * g.n,
+            "spmm_ge_s": round(g.nnz * F_dom / (spmm_ms * 1e-3) / 1e9, 2)}
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -273,21 +299,17 @@ def main():
                    "max_degree": g.max_degree(), "F": w.F, "walks_per_node": w.walks,
                    "walk_len": w.steps, "layers": [list(l) for l in w.layers],
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": f"spmm_dual_kernel (F={F_spmm})",
-                     "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
-                     "bytes_per_launch": bmin, "ms_per_launch": round(spmm_ms, 4),
-                     "spmm_ge_s": round(g.nnz * F_spmm / (spmm_ms * 1e-3) / 1e9, 2)},
-        "phases_ms": {k: round(float(np.mean(v)), 4) for k, v in phase_ms.items() if v},
+        "roofline": roof,
+        "phases_ms": {k: round(float(np.mean(v)), 4) for k, v in phases.items()},
         "plan": {"n_sparse": info["n_sparse"], "n_dense": info["n_dense"],
-                 "kstar": info["kstar"], "n_split_rows": info["n_split_rows"],
-                 "n_split_parts": info["n_split_parts"]},
+                 "kstar": info["kstar"], "n_tasks": info["n_tasks"],
+                 "n_split_rows": info["n_split_rows"], "n_split_parts": info["n_split_parts"]},
     }
+    holder["plan"].destroy()
     if not args.no_cpu_baseline:
         t0 = time.time()
         out["cpu_baseline"] = cpu_baseline(w, g, X, weights)
         print(f"[bench] cpu baseline {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
-    plan.destroy()
     print(json.dumps(out), flush=True)
 
 

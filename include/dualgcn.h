@@ -148,23 +148,44 @@ int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, 
 
 #define DUALGCN_RELU 1u
 
-/* Bytes of device workspace dualgcn_gcn_layer needs (host-only, no device use). */
+/*
+ * dualgcn_spmm_act -- Y = act(A X): dualgcn_spmm with the activation of a GCN
+ * layer applied to every output before it is stored (Sec. 1: a layer ends with
+ * a non-linearity).  act is ReLU if `flags & DUALGCN_RELU`, else the identity;
+ * other flag bits are DUALGCN_ERR_INVALID_ARG.  Same layout, summation and
+ * errors as dualgcn_spmm.  Asynchronous.
+ */
+int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, float *Y, int32_t F,
+                     uint32_t flags, void *stream);
+
+/*
+ * dualgcn_update -- the update phase of a GCN layer alone, T = X W (Sec. 1: the
+ * aggregated features are multiplied by a small dense weight matrix).
+ *
+ * X is float32 n x F_in row-major (16-byte aligned), W float32 F_in x F_out
+ * row-major, T float32 n x F_out row-major; n is the plan's.  Computed on the
+ * matrix cores with X and W rounded to bfloat16 (nearest-even) and float32
+ * accumulation.  F_in and F_out must be multiples of 32 with F_in <= 1024 and
+ * F_out <= 256 (else DUALGCN_ERR_UNSUPPORTED).  X and T must not overlap.  No
+ * workspace.  Asynchronous.
+ */
+int dualgcn_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
+                   int32_t F_in, int32_t F_out, void *stream);
+
+/* Bytes of device workspace dualgcn_gcn_layer needs (host-only, no device use):
+ * room for the float32 n x F_out product T. */
 int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,
                                 size_t *bytes);
 
 /*
- * dualgcn_gcn_layer -- one GCN layer Y = act(A (X W)): the update phase X W
- * (Sec. 1) followed by the aggregation of dualgcn_spmm.
+ * dualgcn_gcn_layer -- one GCN layer Y = act(A (X W)): dualgcn_update into the
+ * workspace followed by dualgcn_spmm_act (Sec. 1: update, aggregation, no bias).
  *
  * X is float32 n x F_in row-major, W float32 F_in x F_out row-major, Y float32
- * n x F_out row-major.  X W is computed on the matrix cores with X and W
- * rounded to bfloat16 (nearest-even) and float32 accumulation; the result T is
- * kept in float32 in `workspace` and aggregated by the SpMM kernels.  act is
- * ReLU if `flags & DUALGCN_RELU`, else the identity (no bias).  `workspace` is
+ * n x F_out row-major; X and Y may be the same buffer.  `workspace` is
  * caller-owned device memory of at least dualgcn_gcn_layer_workspace() bytes,
- * 256-byte aligned (else DUALGCN_ERR_INVALID_ARG).  F_in and F_out must be
- * multiples of 32 with F_in <= 1024 and F_out <= 256 (else UNSUPPORTED).
- * Asynchronous.
+ * 256-byte aligned, overlapping neither X nor Y (else DUALGCN_ERR_INVALID_ARG).
+ * Shape limits as for dualgcn_update.  Asynchronous.
  */
 int dualgcn_gcn_layer(const dualgcn_plan *plan, const float *X, const float *W, float *Y,
                       int32_t F_in, int32_t F_out, uint32_t flags, void *workspace,

@@ -7,6 +7,7 @@ is missing, importing this package raises ImportError: there is no fallback.
 
     plan = Plan(rowptr, col, val, seed=0, walks_per_node=16, walk_len=5)
     Y = spmm(plan, X)                           # Y = A X
+    T = update(plan, X, W)                      # T = X W, bf16 matrix cores
     H = gcn_layer(plan, X, W, relu=True)        # H = relu(A (X W)), X W in bf16 MFMA
 """
 import ctypes
@@ -71,6 +72,8 @@ def _load():
                                ctypes.POINTER(P)], ctypes.c_int),
         "dualgcn_plan_destroy": ([P], None),
         "dualgcn_spmm": ([P, P, P, I32, P], ctypes.c_int),
+        "dualgcn_spmm_act": ([P, P, P, I32, U32, P], ctypes.c_int),
+        "dualgcn_update": ([P, P, P, P, I32, I32, P], ctypes.c_int),
         "dualgcn_gcn_layer_workspace": ([P, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "dualgcn_gcn_layer": ([P, P, P, P, I32, I32, U32, P, SZ, P], ctypes.c_int),
         "dualgcn_plan_query": ([P, ctypes.POINTER(PlanInfo)], ctypes.c_int),
@@ -176,8 +179,8 @@ class Plan:
             pass
 
 
-def spmm(plan, X, Y=None, stream=None):
-    """Y = A X on the plan's matrix.  X: float32 [n, F] on the device."""
+def spmm(plan, X, Y=None, relu=False, stream=None):
+    """Y = A X (or relu(A X)) on the plan's matrix.  X: float32 [n, F] on the device."""
     _dev(X, torch.float32, "X")
     if X.dim() != 2 or X.shape[0] != plan.n:
         raise ValueError("X must be [n, F]")
@@ -186,9 +189,30 @@ def spmm(plan, X, Y=None, stream=None):
     _dev(Y, torch.float32, "Y")
     if Y.shape != X.shape:
         raise ValueError("Y must have X's shape")
-    _check(_lib.dualgcn_spmm(plan.handle, X.data_ptr(), Y.data_ptr(), X.shape[1], _stream(stream)),
-           "dualgcn_spmm")
+    if relu:
+        _check(_lib.dualgcn_spmm_act(plan.handle, X.data_ptr(), Y.data_ptr(), X.shape[1], RELU,
+                                     _stream(stream)), "dualgcn_spmm_act")
+    else:
+        _check(_lib.dualgcn_spmm(plan.handle, X.data_ptr(), Y.data_ptr(), X.shape[1],
+                                 _stream(stream)), "dualgcn_spmm")
     return Y
+
+
+def update(plan, X, W, T=None, stream=None):
+    """T = X W on the bf16 matrix cores (float32 accumulation).  X: [n, F_in], W: [F_in, F_out]."""
+    _dev(X, torch.float32, "X")
+    _dev(W, torch.float32, "W")
+    F_in, F_out = W.shape
+    if X.shape != (plan.n, F_in):
+        raise ValueError("X must be [n, F_in]")
+    if T is None:
+        T = torch.empty((plan.n, F_out), dtype=torch.float32, device=X.device)
+    _dev(T, torch.float32, "T")
+    if T.shape != (plan.n, F_out):
+        raise ValueError("T must be [n, F_out]")
+    _check(_lib.dualgcn_update(plan.handle, X.data_ptr(), W.data_ptr(), T.data_ptr(), F_in, F_out,
+                               _stream(stream)), "dualgcn_update")
+    return T
 
 
 def gcn_layer_workspace_bytes(plan, F_in, F_out):
@@ -228,6 +252,6 @@ def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
     return out
 
 
-__all__ = ["Plan", "spmm", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
+__all__ = ["Plan", "spmm", "update", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
            "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
            "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU"]

@@ -78,6 +78,21 @@ int check_plan(const dualgcn_plan *plan) {
 
 const Plan *as_plan(const dualgcn_plan *p) { return reinterpret_cast<const Plan *>(p); }
 
+// Do [a, a + abytes) and [b, b + bbytes) share a byte?
+bool overlaps(const void *a, size_t abytes, const void *b, size_t bbytes) {
+    const char *x = static_cast<const char *>(a);
+    const char *y = static_cast<const char *>(b);
+    return x < y + bbytes && y < x + abytes;
+}
+
+// Shapes of the update phase T = X W handled by the matrix-core kernel.
+int check_update(const float *X, const float *W, const float *T, int32_t F_in, int32_t F_out) {
+    if (!X || !W || !T || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (F_in % 32 || F_out % 32 || F_in > 1024 || F_out > 256) return DUALGCN_ERR_UNSUPPORTED;
+    if (reinterpret_cast<uintptr_t>(X) % 16) return DUALGCN_ERR_INVALID_ARG;
+    return DUALGCN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -135,11 +150,37 @@ int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, 
     if (F >= (1 << 20)) return DUALGCN_ERR_UNSUPPORTED;
     const Plan *p = as_plan(plan);
     const size_t bytes = static_cast<size_t>(p->n) * F * sizeof(float);
-    const char *x = reinterpret_cast<const char *>(X);
-    const char *y = reinterpret_cast<const char *>(Y);
-    if (x < y + bytes && y < x + bytes) return DUALGCN_ERR_INVALID_ARG;   // overlap
+    if (overlaps(X, bytes, Y, bytes)) return DUALGCN_ERR_INVALID_ARG;
     if ((st = dgc::device_status())) return st;
     return dgc::launch_spmm(*p, X, Y, F, false, static_cast<hipStream_t>(stream));
+}
+
+int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, float *Y, int32_t F,
+                     uint32_t flags, void *stream) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if (!X || !Y || F < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (flags & ~DUALGCN_RELU) return DUALGCN_ERR_INVALID_ARG;
+    if (F >= (1 << 20)) return DUALGCN_ERR_UNSUPPORTED;
+    const Plan *p = as_plan(plan);
+    const size_t bytes = static_cast<size_t>(p->n) * F * sizeof(float);
+    if (overlaps(X, bytes, Y, bytes)) return DUALGCN_ERR_INVALID_ARG;
+    if ((st = dgc::device_status())) return st;
+    return dgc::launch_spmm(*p, X, Y, F, (flags & DUALGCN_RELU) != 0,
+                            static_cast<hipStream_t>(stream));
+}
+
+int dualgcn_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
+                   int32_t F_in, int32_t F_out, void *stream) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if ((st = check_update(X, W, T, F_in, F_out))) return st;
+    const Plan *p = as_plan(plan);
+    const size_t n = static_cast<size_t>(p->n);
+    if (overlaps(X, n * F_in * sizeof(float), T, n * F_out * sizeof(float)))
+        return DUALGCN_ERR_INVALID_ARG;
+    if ((st = dgc::device_status())) return st;
+    return dgc::launch_xw(*p, X, W, T, F_in, F_out, static_cast<hipStream_t>(stream));
 }
 
 int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,
@@ -147,7 +188,7 @@ int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t 
     int st = check_plan(plan);
     if (st) return st;
     if (!bytes || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
-    *bytes = dgc::xw_workspace_bytes(as_plan(plan)->n, F_in, F_out);
+    *bytes = dgc::xw_workspace_bytes(as_plan(plan)->n, F_out);
     return DUALGCN_OK;
 }
 
@@ -156,13 +197,17 @@ int dualgcn_gcn_layer(const dualgcn_plan *plan, const float *X, const float *W, 
                       size_t workspace_bytes, void *stream) {
     int st = check_plan(plan);
     if (st) return st;
-    if (!X || !W || !Y || !workspace || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (!Y || !workspace) return DUALGCN_ERR_INVALID_ARG;
+    if ((st = check_update(X, W, Y, F_in, F_out))) return st;
     if (flags & ~DUALGCN_RELU) return DUALGCN_ERR_INVALID_ARG;
-    if (F_in % 32 || F_out % 32 || F_in > 1024 || F_out > 256) return DUALGCN_ERR_UNSUPPORTED;
-    if (reinterpret_cast<uintptr_t>(workspace) % 256 || reinterpret_cast<uintptr_t>(X) % 16)
-        return DUALGCN_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256) return DUALGCN_ERR_INVALID_ARG;
     const Plan *p = as_plan(plan);
-    if (workspace_bytes < dgc::xw_workspace_bytes(p->n, F_in, F_out)) return DUALGCN_ERR_INVALID_ARG;
+    const size_t ws = dgc::xw_workspace_bytes(p->n, F_out);
+    if (workspace_bytes < ws) return DUALGCN_ERR_INVALID_ARG;
+    const size_t n = static_cast<size_t>(p->n);
+    if (overlaps(X, n * F_in * sizeof(float), workspace, ws) ||
+        overlaps(Y, n * F_out * sizeof(float), workspace, ws))
+        return DUALGCN_ERR_INVALID_ARG;
     if ((st = dgc::device_status())) return st;
     return dgc::launch_gcn_layer(*p, X, W, Y, F_in, F_out, (flags & DUALGCN_RELU) != 0, workspace,
                                  static_cast<hipStream_t>(stream));

@@ -349,37 +349,60 @@ __global__ __launch_bounds__(kThreads) void sorted_degree_kernel(const int32_t *
     }
 }
 
-// Copies row perm[i] of the CSR into row i of the sorted copy.  A lane copies its own row
-// when it has at most 32 entries; longer rows are copied by the whole wavefront in turn.
+// Last row r in [lo, hi] with ptr[r] <= e (the row whose entries contain e when ptr
+// holds row pointers and lo's range starts at or before e).
+template <typename P>
+__device__ __forceinline__ int32_t row_of(const P &ptr, int32_t lo, int32_t hi, int64_t e) {
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo + 1) / 2;
+        if (static_cast<int64_t>(ptr[mid]) <= e) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+constexpr int kCopyTile = 4096;     // entries of the sorted copy one workgroup fills
+
+// Fills entries [b kCopyTile, (b + 1) kCopyTile) of the sorted copy: entry e of sorted
+// row i is entry e - pptr[i] of row perm[i].  The tile's rows are located once, their
+// pointers staged in LDS, and every thread copies the entries e = tile start + t +
+// 256 k (writes are coalesced; reads are coalesced inside a row).
 __global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
     const int32_t *__restrict__ perm, const int32_t *__restrict__ rowptr,
     const int32_t *__restrict__ col, const float *__restrict__ val,
-    const int32_t *__restrict__ pptr, int32_t n, int32_t *__restrict__ pcol,
+    const int32_t *__restrict__ pptr, int32_t n, int64_t nnz, int32_t *__restrict__ pcol,
     float *__restrict__ pval) {
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    const int lane = threadIdx.x & 63;
-    int32_t src = 0, dst = 0, len = 0;
-    if (i < n) {
-        const int32_t r = perm[i];
-        src = rowptr[r];
-        len = rowptr[r + 1] - src;
-        dst = pptr[i];
+    __shared__ int32_t sh_ptr[kCopyTile + 1];
+    __shared__ int32_t sh_src[kCopyTile];
+    __shared__ int32_t sh_rows[2];
+    const int64_t e0 = static_cast<int64_t>(blockIdx.x) * kCopyTile;
+    const int64_t e1 = e0 + kCopyTile < nnz ? e0 + kCopyTile : nnz;
+    if (threadIdx.x == 0) {
+        sh_rows[0] = row_of(pptr, 0, n - 1, e0);
+        sh_rows[1] = row_of(pptr, sh_rows[0], n - 1, e1 - 1);
     }
-    const bool wide = len > 32;
-    if (!wide) {
-        for (int32_t k = 0; k < len; ++k) {
-            pcol[dst + k] = col[src + k];
-            pval[dst + k] = val[src + k];
+    __syncthreads();
+    const int32_t r_lo = sh_rows[0], r_hi = sh_rows[1];
+    const int32_t rows = r_hi - r_lo + 1;
+    if (rows <= kCopyTile) {
+        for (int32_t k = threadIdx.x; k < rows; k += kThreads) {
+            sh_ptr[k] = pptr[r_lo + k];
+            sh_src[k] = rowptr[perm[r_lo + k]];
         }
-    }
-    uint64_t mask = __ballot(wide);
-    while (mask) {
-        const int l = __ffsll(static_cast<unsigned long long>(mask)) - 1;
-        mask &= mask - 1;
-        const int32_t s2 = __shfl(src, l), d2 = __shfl(dst, l), n2 = __shfl(len, l);
-        for (int32_t k = lane; k < n2; k += 64) {
-            pcol[d2 + k] = col[s2 + k];
-            pval[d2 + k] = val[s2 + k];
+        __syncthreads();
+        for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) {
+            const int32_t k = row_of(sh_ptr, 0, rows - 1, e);
+            const int64_t src = sh_src[k] + (e - sh_ptr[k]);
+            pcol[e] = col[src];
+            pval[e] = val[src];
+        }
+    } else {
+        // more rows than entries (empty rows): search the row pointers in memory
+        for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) {
+            const int32_t r = row_of(pptr, r_lo, r_hi, e);
+            const int64_t src = rowptr[perm[r]] + (e - pptr[r]);
+            pcol[e] = col[src];
+            pval[e] = val[src];
         }
     }
 }
@@ -696,8 +719,11 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                        n, pptr_u);
     if ((st = exclusive_scan(pptr_u, static_cast<int64_t>(n) + 1, scan_sums.as<uint32_t>(), nullptr, s)))
         return st;
-    hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->perm, csr->rowptr,
-                       csr->col, csr->val, p->pptr, n, p->pcol, p->pval);
+    if (nnz > 0) {
+        const unsigned grid_e = static_cast<unsigned>((nnz + kCopyTile - 1) / kCopyTile);
+        hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_e), dim3(kThreads), 0, s, p->perm,
+                           csr->rowptr, csr->col, csr->val, p->pptr, n, nnz, p->pcol, p->pval);
+    }
 
     uint32_t *cnt = counts.as<uint32_t>();
     uint32_t *off = cnt + n;

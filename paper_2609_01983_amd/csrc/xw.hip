@@ -1,14 +1,15 @@
 // Update phase T = X W of a GCN layer on the gfx950 matrix cores (DualGCN Sec. 1:
-// after aggregation a layer multiplies by a small dense weight matrix), followed
-// by the aggregation Y = act(A T) of spmm.hip.
+// after aggregation a layer multiplies by a small dense weight matrix).
 //
 // X (n x F_in, float32) is rounded to bfloat16 (nearest-even) in registers, W is
-// rounded once into a transposed bfloat16 copy, and v_mfma_f32_16x16x32_bf16
-// accumulates in float32.  The product is memory-bound (it reads 4 F_in and
-// writes 4 F_out bytes per row for 2 F_in F_out flops), so the kernel streams X
-// once: every wavefront owns 16-row tiles, loads all of a tile's K fragments
-// before its first MFMA, and reads W^T from LDS, where each workgroup stages it
-// once for all the tiles it processes.
+// rounded to bfloat16 while each workgroup stages its transpose in LDS, and
+// v_mfma_f32_16x16x32_bf16 accumulates in float32.  The product is memory-bound
+// (it reads 4 F_in and writes 4 F_out bytes per row for 2 F_in F_out flops, far
+// below the ridge of the bf16 matrix cores), so the kernel is built to stream X:
+// 512-thread workgroups (eight wavefronts share one staged W, so a CU holds 16
+// wavefronts even when W^T takes 64 KiB of LDS), every wavefront owns 16-row
+// tiles and requests the next 32-wide k-step of its tile while the MFMAs of the
+// current one run, and the grid is persistent (one pass over the row tiles).
 //
 // MFMA 16x16x32 operand layout (64 lanes, l = lane):
 //   A (16 x 32):  lane l supplies row l % 16, eight consecutive k of group l / 16
@@ -27,7 +28,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
 constexpr int kRowsPerWave = 16;
 constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
@@ -42,31 +43,19 @@ __device__ __forceinline__ unsigned short to_bf16(float f) {
     return static_cast<unsigned short>(u >> 16);
 }
 
-// Wt[j][c] = bf16(W[c][j]): the transposed weight matrix, row stride F_in.
-__global__ __launch_bounds__(kThreads) void weight_bf16_kernel(const float *__restrict__ W,
-                                                               int32_t F_in, int32_t F_out,
-                                                               unsigned short *__restrict__ Wt) {
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= static_cast<int64_t>(F_in) * F_out) return;
-    const int32_t j = static_cast<int32_t>(i / F_in), c = static_cast<int32_t>(i % F_in);
-    Wt[i] = to_bf16(W[static_cast<int64_t>(c) * F_out + j]);
-}
-
-// T[:, c0 : c0 + 16 ntiles] = bf16(X) * Wt[c0 : ..]^T for every row tile; F_in % 32 == 0.
+// T[:, c0 : c0 + 16 ntiles] = bf16(X) bf16(W[:, c0 : ..]) for every row tile; F_in % 32 == 0.
 template <int NTMAX>
 __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const float *__restrict__ X,
-                                                           const unsigned short *__restrict__ Wt,
+                                                           const float *__restrict__ W,
                                                            float *__restrict__ T, int32_t n,
                                                            int32_t F_in, int32_t F_out,
                                                            int32_t c0, int32_t ntiles) {
-    extern __shared__ unsigned short w_lds[];   // [16 ntiles][F_in + kPad]
+    extern __shared__ unsigned short w_lds[];   // [16 ntiles][F_in + kPad]: W^T in bf16
     const int ldw = F_in + kPad;
     const int ncols = 16 * ntiles;
-    // stage W^T rows c0 .. c0 + ncols in LDS, 16 bytes per lane
-    for (int idx = threadIdx.x; idx < ncols * (F_in / 8); idx += kThreads) {
-        const int j = idx / (F_in / 8), c8 = idx % (F_in / 8);
-        const uint4 v = *reinterpret_cast<const uint4 *>(Wt + static_cast<int64_t>(c0 + j) * F_in + c8 * 8);
-        *reinterpret_cast<uint4 *>(w_lds + j * ldw + c8 * 8) = v;
+    for (int idx = threadIdx.x; idx < F_in * ncols; idx += kThreads) {
+        const int c = idx / ncols, j = idx % ncols;
+        w_lds[j * ldw + c] = to_bf16(W[static_cast<int64_t>(c) * F_out + c0 + j]);
     }
     __syncthreads();
 
@@ -84,25 +73,35 @@ __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const float *__restri
 #pragma unroll
         for (int t = 0; t < NTMAX; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
         const float *xr = X + arow * F_in + kgrp * 8;
+        // k-step ks + 1 is requested while the MFMAs of k-step ks run
+        f32x4 lo = f32x4{0.f, 0.f, 0.f, 0.f}, hi = lo;
+        if (arow_ok) {
+            lo = *reinterpret_cast<const f32x4 *>(xr);
+            hi = *reinterpret_cast<const f32x4 *>(xr + 4);
+        }
         for (int ks = 0; ks < ksteps; ++ks) {
-            float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
-            if (arow_ok) {
-                lo = *reinterpret_cast<const float4 *>(xr + ks * 32);
-                hi = *reinterpret_cast<const float4 *>(xr + ks * 32 + 4);
+            f32x4 nlo = f32x4{0.f, 0.f, 0.f, 0.f}, nhi = nlo;
+            if (arow_ok && ks + 1 < ksteps) {
+                nlo = *reinterpret_cast<const f32x4 *>(xr + (ks + 1) * 32);
+                nhi = *reinterpret_cast<const f32x4 *>(xr + (ks + 1) * 32 + 4);
             }
             u16x8 a16;
-            a16[0] = to_bf16(lo.x); a16[1] = to_bf16(lo.y); a16[2] = to_bf16(lo.z); a16[3] = to_bf16(lo.w);
-            a16[4] = to_bf16(hi.x); a16[5] = to_bf16(hi.y); a16[6] = to_bf16(hi.z); a16[7] = to_bf16(hi.w);
-            const bf16x8 a = __builtin_bit_cast(bf16x8, a16);
+            a16[0] = to_bf16(lo[0]); a16[1] = to_bf16(lo[1]);
+            a16[2] = to_bf16(lo[2]); a16[3] = to_bf16(lo[3]);
+            a16[4] = to_bf16(hi[0]); a16[5] = to_bf16(hi[1]);
+            a16[6] = to_bf16(hi[2]); a16[7] = to_bf16(hi[3]);
+            const bf16x8 av = __builtin_bit_cast(bf16x8, a16);
+            const int kk = ks * 32 + kgrp * 8;
 #pragma unroll
             for (int t = 0; t < NTMAX; ++t) {
                 if (t < ntiles) {
-                    const u16x8 b16 = *reinterpret_cast<const u16x8 *>(
-                        w_lds + (t * 16 + lrow) * ldw + ks * 32 + kgrp * 8);
+                    const u16x8 b16 = *reinterpret_cast<const u16x8 *>(w_lds + (t * 16 + lrow) * ldw + kk);
                     acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        a, __builtin_bit_cast(bf16x8, b16), acc[t], 0, 0, 0);
+                        av, __builtin_bit_cast(bf16x8, b16), acc[t], 0, 0, 0);
                 }
             }
+            lo = nlo;
+            hi = nhi;
         }
 #pragma unroll
         for (int t = 0; t < NTMAX; ++t) {
@@ -136,50 +135,49 @@ int allow_lds(const void *kernel, size_t bytes) {
                                           static_cast<int>(bytes)));
 }
 
-}  // namespace
-
-size_t xw_workspace_bytes(int32_t n, int32_t F_in, int32_t F_out) {
-    const size_t t_bytes = (static_cast<size_t>(n) * F_out * sizeof(float) + 255) / 256 * 256;
-    return t_bytes + static_cast<size_t>(F_in) * F_out * sizeof(unsigned short);
+template <int NT>
+int launch_xw(const float *X, const float *W, float *T, int32_t n, int32_t F_in, int32_t F_out,
+              int c0, int ntiles, size_t lds, hipStream_t s) {
+    int st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<NT>), lds);
+    if (st) return st;
+    // workgroups per CU allowed by the LDS of one CU (160 KiB) and by 2048 threads per CU
+    const int per_cu = std::max<int>(1, std::min<int>(2048 / kThreads, static_cast<int>((160 * 1024) / lds)));
+    const int64_t tiles = (static_cast<int64_t>(n) + kRowsPerBlock - 1) / kRowsPerBlock;
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(tiles, static_cast<int64_t>(num_cus()) * per_cu));
+    hipLaunchKernelGGL((xw_mfma_kernel<NT>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
+                       lds, s, X, W, T, n, F_in, F_out, c0, ntiles);
+    return hip_status(hipGetLastError());
 }
 
-int launch_gcn_layer(const Plan &p, const float *X, const float *W, float *Y, int32_t F_in,
-                     int32_t F_out, bool relu, void *workspace, hipStream_t s) {
-    const size_t t_bytes = (static_cast<size_t>(p.n) * F_out * sizeof(float) + 255) / 256 * 256;
-    float *T = static_cast<float *>(workspace);
-    unsigned short *Wt = reinterpret_cast<unsigned short *>(static_cast<char *>(workspace) + t_bytes);
-    {
-        const int64_t count = static_cast<int64_t>(F_in) * F_out;
-        hipLaunchKernelGGL(weight_bf16_kernel, dim3(static_cast<unsigned>((count + kThreads - 1) / kThreads)),
-                           dim3(kThreads), 0, s, W, F_in, F_out, Wt);
-    }
+}  // namespace
+
+size_t xw_workspace_bytes(int32_t n, int32_t F_out) {
+    return (static_cast<size_t>(n) * F_out * sizeof(float) + 255) / 256 * 256;
+}
+
+int launch_xw(const Plan &p, const float *X, const float *W, float *T, int32_t F_in,
+              int32_t F_out, hipStream_t s) {
     // column blocks whose W^T slice fits the LDS budget
-    int cb = std::min<int>(F_out, (kLdsElems / F_in) / 16 * 16);
+    const int cb = std::min<int>(F_out, (kLdsElems / F_in) / 16 * 16);
     if (cb < 16) return DUALGCN_ERR_UNSUPPORTED;
-    const int64_t tiles = (static_cast<int64_t>(p.n) + kRowsPerBlock - 1) / kRowsPerBlock;
     for (int c0 = 0; c0 < F_out; c0 += cb) {
         const int width = std::min(cb, F_out - c0);
         const int ntiles = width / 16;
         const size_t lds = static_cast<size_t>(width) * (F_in + kPad) * sizeof(unsigned short);
-        const int per_cu = lds <= 80 * 1024 ? 2 : 1;
-        int st = DUALGCN_OK;
-        if (ntiles <= 4) st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<4>), lds);
-        else if (ntiles <= 8) st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<8>), lds);
-        else st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<16>), lds);
-        if (st) return st;
-        const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(tiles, static_cast<int64_t>(num_cus()) * per_cu));
-        if (ntiles <= 4)
-            hipLaunchKernelGGL((xw_mfma_kernel<4>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                               lds, s, X, Wt, T, p.n, F_in, F_out, c0, ntiles);
-        else if (ntiles <= 8)
-            hipLaunchKernelGGL((xw_mfma_kernel<8>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                               lds, s, X, Wt, T, p.n, F_in, F_out, c0, ntiles);
-        else
-            hipLaunchKernelGGL((xw_mfma_kernel<16>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                               lds, s, X, Wt, T, p.n, F_in, F_out, c0, ntiles);
-        st = hip_status(hipGetLastError());
+        int st;
+        if (ntiles <= 4) st = launch_xw<4>(X, W, T, p.n, F_in, F_out, c0, ntiles, lds, s);
+        else if (ntiles <= 8) st = launch_xw<8>(X, W, T, p.n, F_in, F_out, c0, ntiles, lds, s);
+        else st = launch_xw<16>(X, W, T, p.n, F_in, F_out, c0, ntiles, lds, s);
         if (st) return st;
     }
+    return DUALGCN_OK;
+}
+
+int launch_gcn_layer(const Plan &p, const float *X, const float *W, float *Y, int32_t F_in,
+                     int32_t F_out, bool relu, void *workspace, hipStream_t s) {
+    float *T = static_cast<float *>(workspace);
+    const int st = launch_xw(p, X, W, T, F_in, F_out, s);
+    if (st) return st;
     return launch_spmm(p, T, Y, F_out, relu, s);
 }
 

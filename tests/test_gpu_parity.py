@@ -213,6 +213,38 @@ def test_config_partition_and_sampled_spmm(dg, device, cfg):
     assert_spmm_close(Y[rows], Yr, B, what=cfg)
 
 
+@pytest.mark.parametrize("F", [16, 64, 128, 17])
+def test_spmm_act_relu(dg, device, F):
+    g = small.random_graph(400, 0.02, seed=12)
+    X = dense.features_normal(g.n, F, seed=F, stream_id=28)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=8, walk_len=4)
+    Y = dg.spmm(plan, torch.from_numpy(X).to(device), relu=True).cpu().numpy()
+    Yr, B = oracle.spmm(g, X)
+    assert (Y >= 0).all()
+    assert_spmm_close(Y, np.maximum(Yr, 0.0), B, what=f"relu F={F}")
+
+
+def _bf16(a):
+    """float32 -> bfloat16 (nearest-even) -> float64, done in numpy."""
+    u = np.asarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("fin,fout", [(32, 32), (256, 128), (128, 64), (96, 160), (1024, 32),
+                                      (256, 256), (64, 256)])
+def test_update_alone(dg, device, fin, fout):
+    g = small.edgeless(777)                       # only n matters; ragged against 128-row tiles
+    X = dense.features_normal(g.n, fin, seed=fin, stream_id=29)
+    W = dense.glorot(fin, fout, seed=fout, stream_id=30)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=2, walk_len=2)
+    T = dg.update(plan, torch.from_numpy(X).to(device), torch.from_numpy(W).to(device)).cpu().numpy()
+    Tr, BT = oracle.xw(X, W)
+    assert_spmm_close(T, Tr, BT, tol=GCN_TOL, what=f"update {fin}->{fout}")
+    # with both operands rounded to bf16 in numpy the product is reproduced to float32 rounding
+    assert np.max(np.abs(T - _bf16(X) @ _bf16(W)) / (BT + 1e-30)) < 1e-5
+
+
 # ---------------------------------------------------------------- GCN layer (bf16 MFMA)
 
 @pytest.mark.parametrize("fin,fout", [(32, 32), (64, 32), (256, 128), (128, 64), (96, 160)])
@@ -238,12 +270,7 @@ def test_gcn_layer_identity_graph_is_xw(dg, device):
     T, BT = oracle.xw(X, W)
     assert_spmm_close(Y, T, BT, tol=GCN_TOL, what="xw")
     # the bf16 rounding of both operands, done here in numpy, reproduces it much closer
-    def bf16(a):
-        u = a.astype(np.float32).view(np.uint32).astype(np.uint64)
-        u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
-        return u.astype(np.uint32).view(np.float32).astype(np.float64)
-    Tb = bf16(X) @ bf16(W)
-    assert np.max(np.abs(Y - Tb) / (BT + 1e-30)) < 1e-5
+    assert np.max(np.abs(Y - _bf16(X) @ _bf16(W)) / (BT + 1e-30)) < 1e-5
 
 
 def test_gcn_two_layer_c2_graph(dg, device):
