@@ -115,9 +115,10 @@ typedef struct dualgcn_plan dualgcn_plan;
  * moment sums must fit 128 bits (else DUALGCN_ERR_UNSUPPORTED).  The CSR is
  * validated on the device first (DUALGCN_ERR_BAD_CSR).
  *
- * The plan owns device memory (S, K, perm, a copy of the matrix with its rows
- * in perm order -- about 8 nnz + 8 n bytes --, the sparse tasks, the dense-region
- * schedule and the partial sums of split rows), released by dualgcn_plan_destroy.  The call waits
+ * The plan owns one block of device memory of about 9 nnz + 24 n bytes (S, K,
+ * perm, a copy of the matrix with its rows in perm order, the sparse tasks, the
+ * dense-region schedule and the partial sums of split rows), released by
+ * dualgcn_plan_destroy; a scratch block is allocated and released inside the call.  The call waits
  * for `stream` twice (to read the moment sums and the schedule sizes).
  * *out is set to NULL on error.
  */

@@ -1,6 +1,8 @@
 // C ABI of libdualgcn: argument checks, status codes and dispatch to the kernels.
 // Every check that needs no device runs before the device is touched.
+#include <mutex>
 #include <new>
+#include <vector>
 
 #include "internal.h"
 
@@ -37,6 +39,86 @@ int alloc_bytes(void **p, size_t bytes) {
         return e == hipErrorOutOfMemory ? DUALGCN_ERR_OOM : DUALGCN_ERR_HIP;
     }
     return DUALGCN_OK;
+}
+
+// ---- cached device blocks
+//
+// A plan takes one large block and its build one scratch block.  Released blocks are
+// kept (per device, at most kCachedBlocks) and handed out again to a request of at
+// most their size and at least half of it, so that rebuilding a plan of the same
+// matrix does not pay hipMalloc and hipFree of gigabytes every time.  The cache holds
+// its blocks until the process ends; a failed hipMalloc first returns the device's
+// cached blocks to HIP and tries again.
+namespace {
+struct CachedBlock {
+    int device;
+    size_t bytes;
+    void *ptr;
+};
+std::mutex g_cache_mu;
+std::vector<CachedBlock> g_cache;
+constexpr size_t kCachedBlocks = 4;
+}  // namespace
+
+int alloc_block(void **p, size_t *capacity, size_t bytes) {
+    *p = nullptr;
+    *capacity = 0;
+    if (bytes == 0) bytes = 1;
+    int dev = 0;
+    int st = hip_status(hipGetDevice(&dev));
+    if (st) return st;
+    {
+        std::lock_guard<std::mutex> lock(g_cache_mu);
+        size_t best = g_cache.size();
+        for (size_t i = 0; i < g_cache.size(); ++i) {
+            const CachedBlock &b = g_cache[i];
+            if (b.device == dev && b.bytes >= bytes && b.bytes / 2 <= bytes &&
+                (best == g_cache.size() || b.bytes < g_cache[best].bytes))
+                best = i;
+        }
+        if (best < g_cache.size()) {
+            *p = g_cache[best].ptr;
+            *capacity = g_cache[best].bytes;
+            g_cache.erase(g_cache.begin() + static_cast<std::ptrdiff_t>(best));
+            return DUALGCN_OK;
+        }
+    }
+    hipError_t e = hipMalloc(p, bytes);
+    if (e == hipErrorOutOfMemory) {
+        (void)hipGetLastError();
+        std::vector<void *> drop;
+        {
+            std::lock_guard<std::mutex> lock(g_cache_mu);
+            for (size_t i = g_cache.size(); i-- > 0;) {
+                if (g_cache[i].device == dev) {
+                    drop.push_back(g_cache[i].ptr);
+                    g_cache.erase(g_cache.begin() + static_cast<std::ptrdiff_t>(i));
+                }
+            }
+        }
+        for (void *q : drop) (void)hipFree(q);
+        e = hipMalloc(p, bytes);
+    }
+    if (e != hipSuccess) {
+        *p = nullptr;
+        g_last_hip_error = static_cast<int>(e);
+        return e == hipErrorOutOfMemory ? DUALGCN_ERR_OOM : DUALGCN_ERR_HIP;
+    }
+    *capacity = bytes;
+    return DUALGCN_OK;
+}
+
+void release_block(void *p, size_t capacity) {
+    if (!p) return;
+    int dev = 0;
+    if (hipGetDevice(&dev) == hipSuccess) {
+        std::lock_guard<std::mutex> lock(g_cache_mu);
+        if (g_cache.size() < kCachedBlocks) {
+            g_cache.push_back(CachedBlock{dev, capacity, p});
+            return;
+        }
+    }
+    (void)hipFree(p);
 }
 
 }  // namespace dgc
@@ -276,7 +358,7 @@ int dualgcn_arw_patterns(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_p
     uint32_t *S = static_cast<uint32_t *>(scratch);
     int32_t *flags = reinterpret_cast<int32_t *>(S + csr->n);
     st = dgc::hip_status(hipMemsetAsync(flags, 0, 2 * sizeof(int32_t), s));
-    if (!st) st = dgc::validate_csr(csr, flags, s);
+    if (!st) st = dgc::validate_csr(csr, flags, nullptr, nullptr, s);
     if (!st)
         st = dgc::launch_arw(csr->rowptr, csr->col, csr->n, seed, walks_per_node, walk_len, S, out,
                              flags, s);

@@ -5,10 +5,12 @@
 // by the order of its first occurrence; the density of node v is the mean
 // number of distinct nodes over its k walks, N_v = S_v / k.
 //
-// One lane runs one (node, walk) pair.  Lanes of a node are adjacent, so when
-// k is a power of two no larger than 64 the k counts are summed with
-// cross-lane shuffles and written with one plain store; otherwise each lane
-// adds its count with an integer atomic (order-independent, hence exact).
+// One lane runs one (node, walk) pair, or two walks of a node in lockstep (so
+// that both walks' reads are in flight together) when only the sums are needed,
+// d <= 8 and k is a power of two between 2 and 128.  Lanes of a node are
+// adjacent, so for such k the counts are summed with cross-lane shuffles and
+// written with one plain store; otherwise each lane adds its count with an
+// integer atomic (order-independent, hence exact).
 //
 // Random stream: step s of walk w from v uses 64-bit word (s mod 4) of the
 // Philox-4x64-10 block (Salmon, Moraes, Dror & Shaw, SC'11) with counter
@@ -90,6 +92,65 @@ __device__ __forceinline__ uint32_t walk_one(const int32_t *__restrict__ rowptr,
     return distinct;
 }
 
+// WPL walks of d steps (d <= MAXD) from node v advanced in lockstep, so that their
+// memory reads are in flight together; u[j] receives the distinct-node count of walk
+// w0 + j.  Same stream and counts as walk_one (no pattern output).  A walk that
+// steps onto a node whose only entry is a self-loop (or that has no entry) can never
+// leave it nor meet a new node, so it stops reading memory there: its lane is masked
+// off for the remaining steps, which saves L2 requests without changing any count.
+template <int MAXD, int WPL>
+__device__ __forceinline__ void walk_lockstep(const int2 *__restrict__ nodeinfo,
+                                              const int32_t *__restrict__ col, uint32_t v,
+                                              uint32_t w0, uint32_t d, uint64_t seed,
+                                              uint32_t (&u)[WPL]) {
+    int32_t path[WPL][MAXD + 1];
+    int32_t cur[WPL];
+    bool live[WPL];
+    Block4 blk[WPL];
+#pragma unroll
+    for (int j = 0; j < WPL; ++j) {
+        path[j][0] = static_cast<int32_t>(v);
+        cur[j] = static_cast<int32_t>(v);
+        live[j] = true;
+        u[j] = 1;
+    }
+#pragma unroll
+    for (int s = 0; s < MAXD; ++s) {
+        if (static_cast<uint32_t>(s) >= d) break;
+        int2 ni[WPL];             // (first entry, degree) of the current nodes
+#pragma unroll
+        for (int j = 0; j < WPL; ++j) {
+            ni[j] = make_int2(0, 0);
+            if (live[j]) {
+                if ((s & 3) == 0) blk[j] = philox4x64_10(v, w0 + j, static_cast<uint64_t>(s >> 2), 0, seed, 0);
+                ni[j] = nodeinfo[cur[j]];
+            }
+        }
+        int32_t nxt[WPL];
+#pragma unroll
+        for (int j = 0; j < WPL; ++j) {
+            nxt[j] = cur[j];
+            if (live[j] && ni[j].y > 0) {
+                const uint64_t r = blk[j].w[s & 3];
+                nxt[j] = col[ni[j].x + static_cast<int32_t>(__umul64hi(r, static_cast<uint64_t>(ni[j].y)))];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < WPL; ++j) {
+            if (live[j]) {
+                bool seen = false;
+#pragma unroll
+                for (int i = 0; i <= s; ++i) seen |= path[j][i] == nxt[j];
+                if (!seen) ++u[j];
+                live[j] = !(ni[j].y <= 1 && nxt[j] == cur[j]);   // absorbed: stays put for good
+            }
+            path[j][s + 1] = nxt[j];
+            cur[j] = nxt[j];
+        }
+    }
+}
+
+// One lane per (node, walk); with `patterns` the labels are written out.
 template <int MAXD, bool UNROLL>
 __global__ __launch_bounds__(256) void arw_kernel(const int32_t *__restrict__ rowptr,
                                                   const int32_t *__restrict__ col, int32_t n,
@@ -122,7 +183,48 @@ __global__ __launch_bounds__(256) void arw_kernel(const int32_t *__restrict__ ro
     }
 }
 
+// Density sums only, WPL walks per lane: k = 2^k_log2 with WPL <= k <= 64 WPL, so the
+// k / WPL lanes of a node are adjacent and aligned inside the wavefront.
+template <int MAXD, int WPL>
+__global__ __launch_bounds__(256) void arw_sum_kernel(const int2 *__restrict__ nodeinfo,
+                                                      const int32_t *__restrict__ col,
+                                                      int32_t n, uint64_t seed, uint32_t d,
+                                                      int k_log2, uint32_t *__restrict__ S,
+                                                      const int32_t *__restrict__ bad_flag) {
+    if (*bad_flag) return;
+    const int64_t gid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int lanes_log2 = k_log2 - (WPL == 2 ? 1 : (WPL == 4 ? 2 : 0));
+    const bool valid = gid < (static_cast<int64_t>(n) << lanes_log2);
+    const uint32_t v = static_cast<uint32_t>(gid >> lanes_log2);
+    const uint32_t w0 = static_cast<uint32_t>(gid & ((1 << lanes_log2) - 1)) * WPL;
+    uint32_t u = 0;
+    if (valid) {
+        uint32_t uj[WPL];
+        walk_lockstep<MAXD, WPL>(nodeinfo, col, v, w0, d, seed, uj);
+#pragma unroll
+        for (int j = 0; j < WPL; ++j) u += uj[j];
+    }
+    for (int off = 1; off < (1 << lanes_log2); off <<= 1) u += __shfl_xor(u, off, 64);
+    if (valid && w0 == 0) S[v] = u;
+}
+
 }  // namespace
+
+int launch_density(const int2 *nodeinfo, const int32_t *col, int32_t n, uint64_t seed,
+                   uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
+                   hipStream_t stream) {
+    int k_log2 = -1;
+    if ((k & (k - 1)) == 0) {
+        k_log2 = 0;
+        while ((1u << k_log2) < k) ++k_log2;
+    }
+    if (d > 8 || k_log2 < 1 || k_log2 > 7) return DUALGCN_ERR_UNSUPPORTED;
+    const int64_t blocks = (static_cast<int64_t>(n) * k / 2 + 255) / 256;   // two walks per lane
+    if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL((arw_sum_kernel<8, 2>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                       stream, nodeinfo, col, n, seed, d, k_log2, S, bad_flag);
+    return hip_status(hipGetLastError());
+}
 
 int launch_arw(const int32_t *rowptr, const int32_t *col, int32_t n, uint64_t seed, uint32_t k,
                uint32_t d, uint32_t *S, uint8_t *patterns, const int32_t *bad_flag,

@@ -35,6 +35,8 @@ struct SplitPart {
 
 struct Plan {
     int device = 0;
+    void *mem = nullptr;               // one device block holding every array below
+    size_t mem_bytes = 0;
     int32_t n = 0;
     int64_t nnz = 0;
     const int32_t *rowptr = nullptr;   // borrowed
@@ -72,17 +74,32 @@ struct Plan {
 int hip_status(hipError_t e);          // records e; returns DUALGCN_OK or DUALGCN_ERR_HIP
 int device_status();                   // DUALGCN_OK or DUALGCN_ERR_NO_DEVICE / _HIP
 int alloc_bytes(void **p, size_t bytes);  // DUALGCN_OK or DUALGCN_ERR_OOM / _HIP
+// A device block of at least `bytes` on the current device, possibly a cached one;
+// *capacity receives its real size, to be passed back to release_block.
+int alloc_block(void **p, size_t *capacity, size_t bytes);
+// Returns a block to the cache (or to HIP); the device must no longer use it.
+void release_block(void *p, size_t capacity);
 
 // ---- anonymous walks (arw.hip)
 // S[v] = sum over k walks of distinct-node counts; patterns (may be null) receives labels.
 int launch_arw(const int32_t *rowptr, const int32_t *col, int32_t n, uint64_t seed, uint32_t k,
                uint32_t d, uint32_t *S, uint8_t *patterns, const int32_t *bad_flag,
                hipStream_t stream);
+// The same sums from nodeinfo (every node's (first entry, degree), as validate_csr writes
+// it), two walks per lane advanced in lockstep.  DUALGCN_ERR_UNSUPPORTED (nothing
+// launched) unless d <= 8 and k is a power of two in [2, 128].
+int launch_density(const int2 *nodeinfo, const int32_t *col, int32_t n, uint64_t seed,
+                   uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
+                   hipStream_t stream);
 
 // ---- partition (partition.hip)
-// Checks the CSR on the device: flags[0] |= 1 (row pointers) | 2 (columns);
-// flags[1] = max(flags[1], largest row length).  flags must start at zero.
-int validate_csr(const dualgcn_csr *csr, int32_t *flags, hipStream_t stream);
+// Checks the CSR on the device: flags[0] |= 1 (row pointers) | 2 (columns); flags must
+// start at zero.  nodeinfo (may be null, n entries) receives (rowptr[v], rowptr[v+1] -
+// rowptr[v]); blockmax (may be null, kValidateBlocks entries) each workgroup's largest
+// row length.
+constexpr int kValidateBlocks = 2048;
+int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t *blockmax,
+                 hipStream_t stream);
 int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                const dualgcn_thresholds &th, hipStream_t stream, Plan **out);
 void free_plan(Plan *p);

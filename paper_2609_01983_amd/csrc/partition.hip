@@ -33,11 +33,15 @@ constexpr int kRadix = 1 << kRadixBits;
 
 // ------------------------------------------------------------------ validation
 
+// Checks the row pointers and columns, records the largest degree, and writes every
+// node's (first entry, degree) record for the walks (one 8-byte read per step).
 __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__restrict__ rowptr,
                                                             const int32_t *__restrict__ col,
                                                             int32_t n, int64_t nnz,
                                                             int32_t *__restrict__ flag,
-                                                            int32_t *__restrict__ maxdeg) {
+                                                            int2 *__restrict__ nodeinfo,
+                                                            int32_t *__restrict__ blockmax) {
+    __shared__ int32_t sh_bad[kThreads / 64], sh_max[kThreads / 64];
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
     const int64_t t0 = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     int32_t bad = 0, dmax = 0;
@@ -45,17 +49,49 @@ __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__res
         const int32_t a = rowptr[i], b = rowptr[i + 1];
         if (b < a) bad |= 1;
         dmax = max(dmax, b - a);
+        if (nodeinfo) nodeinfo[i] = make_int2(a, b - a);
     }
     if (t0 == 0) {
         if (rowptr[0] != 0) bad |= 1;
         if (static_cast<int64_t>(rowptr[n]) != nnz) bad |= 1;
     }
-    for (int64_t p = t0; p < nnz; p += stride) {
+    // columns: scalar head up to a 16-byte boundary, 16-byte loads, scalar tail
+    const int64_t head = std::min<int64_t>(nnz, ((16 - (reinterpret_cast<uintptr_t>(col) & 15)) & 15) / 4);
+    const int64_t body = (nnz - head) / 4;
+    const int4 *__restrict__ c4 = reinterpret_cast<const int4 *>(col + head);
+#pragma unroll 4
+    for (int64_t q = t0; q < body; q += stride) {
+        const int4 c = c4[q];
+        if (c.x < 0 || c.x >= n || c.y < 0 || c.y >= n || c.z < 0 || c.z >= n || c.w < 0 || c.w >= n)
+            bad |= 2;
+    }
+    if (t0 < head) {
+        const int32_t c = col[t0];
+        if (c < 0 || c >= n) bad |= 2;
+    }
+    for (int64_t p = head + 4 * body + t0; p < nnz; p += stride) {
         const int32_t c = col[p];
         if (c < 0 || c >= n) bad |= 2;
     }
-    if (bad) atomicOr(flag, bad);
-    if (dmax) atomicMax(maxdeg, dmax);
+    // one result per workgroup: the flag by an atomic only when something is wrong, the
+    // largest degree into blockmax (folded later), so no address is contended
+    for (int off = 32; off > 0; off >>= 1) {
+        bad |= __shfl_xor(bad, off, 64);
+        dmax = max(dmax, __shfl_xor(dmax, off, 64));
+    }
+    if ((threadIdx.x & 63) == 0) {
+        sh_bad[threadIdx.x >> 6] = bad;
+        sh_max[threadIdx.x >> 6] = dmax;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kThreads / 64; ++w) {
+            bad |= sh_bad[w];
+            dmax = max(dmax, sh_max[w]);
+        }
+        if (bad) atomicOr(flag, bad);
+        if (blockmax) blockmax[blockIdx.x] = dmax;
+    }
 }
 
 // ------------------------------------------------------------------ keys and moments
@@ -118,27 +154,32 @@ struct Summary {
 __global__ __launch_bounds__(kThreads) void fold_kernel(const Moments *__restrict__ partial,
                                                         int32_t count,
                                                         const int32_t *__restrict__ flag,
-                                                        const int32_t *__restrict__ maxdeg,
+                                                        const int32_t *__restrict__ blockmax,
                                                         Summary *__restrict__ out) {
     __shared__ u128 sh1[kThreads], sh2[kThreads];
     __shared__ uint64_t shm[kThreads];
+    __shared__ int32_t shd[kThreads];
     const int t = threadIdx.x;
     u128 s1 = 0, s2 = 0;
     uint64_t kmax = 0;
+    int32_t dmax = 0;
     for (int i = t; i < count; i += kThreads) {
         s1 += join(partial[i].s1_lo, partial[i].s1_hi);
         s2 += join(partial[i].s2_lo, partial[i].s2_hi);
         kmax = partial[i].kmax > kmax ? partial[i].kmax : kmax;
     }
+    for (int i = t; i < kValidateBlocks; i += kThreads) dmax = max(dmax, blockmax[i]);
     sh1[t] = s1;
     sh2[t] = s2;
     shm[t] = kmax;
+    shd[t] = dmax;
     __syncthreads();
     for (int h = kThreads / 2; h > 0; h >>= 1) {
         if (t < h) {
             sh1[t] += sh1[t + h];
             sh2[t] += sh2[t + h];
             shm[t] = shm[t] > shm[t + h] ? shm[t] : shm[t + h];
+            shd[t] = max(shd[t], shd[t + h]);
         }
         __syncthreads();
     }
@@ -147,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const Moments *__restric
                          static_cast<uint64_t>(sh2[0]), static_cast<uint64_t>(sh2[0] >> 64),
                          shm[0]};
         out->flag = *flag;
-        out->maxdeg = *maxdeg;
+        out->maxdeg = shd[0];
     }
 }
 
@@ -423,25 +464,28 @@ __device__ __forceinline__ bool starts_task(const int32_t *__restrict__ pptr, in
     return (i - lo) % kTaskRows == 0;
 }
 
+// flags[i] = offsets[i] = 1 if row i starts a task (offsets is scanned afterwards).
 __global__ __launch_bounds__(kThreads) void task_flag_kernel(const int32_t *__restrict__ pptr,
                                                              int32_t n,
                                                              const SplitSummary *__restrict__ sum,
-                                                             uint32_t *__restrict__ flags) {
+                                                             uint32_t *__restrict__ flags,
+                                                             uint32_t *__restrict__ offsets) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i >= n) return;
-    flags[i] = (i < sum->n_sparse && starts_task(pptr, static_cast<int32_t>(i))) ? 1u : 0u;
+    const uint32_t f = (i < sum->n_sparse && starts_task(pptr, static_cast<int32_t>(i))) ? 1u : 0u;
+    flags[i] = f;
+    offsets[i] = f;
 }
 
 // tasks[offsets[i]] = i for every task start i; tasks[n_tasks] = n_sparse.
-__global__ __launch_bounds__(kThreads) void task_fill_kernel(const int32_t *__restrict__ pptr,
-                                                             int32_t n,
+__global__ __launch_bounds__(kThreads) void task_fill_kernel(int32_t n,
                                                              const SplitSummary *__restrict__ sum,
+                                                             const uint32_t *__restrict__ flags,
                                                              const uint32_t *__restrict__ offsets,
                                                              int32_t *__restrict__ tasks) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    const int32_t ns = sum->n_sparse;
-    if (i == 0) tasks[sum->tasks] = ns;
-    if (i < ns && starts_task(pptr, static_cast<int32_t>(i))) tasks[offsets[i]] = static_cast<int32_t>(i);
+    if (i == 0) tasks[sum->tasks] = sum->n_sparse;
+    if (i < n && flags[i]) tasks[offsets[i]] = static_cast<int32_t>(i);
 }
 
 // Dense rows of the sorted order longer than one chunk: counts[i] = number of parts.
@@ -479,13 +523,26 @@ __global__ __launch_bounds__(kThreads) void split_fill_kernel(const uint32_t *__
 
 // ------------------------------------------------------------------ host helpers
 
-struct DevBuf {
-    void *p = nullptr;
-    ~DevBuf() {
-        if (p) (void)hipFree(p);
+// Offsets of sub-arrays of one device block, each 256-byte aligned.
+struct Layout {
+    size_t bytes = 0;
+    size_t take(size_t count_bytes) {
+        const size_t o = bytes;
+        bytes += (count_bytes + 255) / 256 * 256;
+        return o;
     }
-    template <typename T>
-    T *as() const { return static_cast<T *>(p); }
+};
+
+// A scratch block returned to the block cache once `stream` has finished with it.
+struct ScratchBlock {
+    void *p = nullptr;
+    size_t bytes = 0;
+    hipStream_t stream = nullptr;
+    ~ScratchBlock() {
+        if (!p) return;
+        (void)hipStreamSynchronize(stream);
+        release_block(p, bytes);
+    }
 };
 
 // Exclusive scan of `count` u32 values in place; `sums` holds one word per tile.
@@ -559,21 +616,16 @@ int threshold_key(int32_t n, u128 s1, u128 s2, uint32_t b, uint32_t c, uint64_t 
 
 }  // namespace
 
-int validate_csr(const dualgcn_csr *csr, int32_t *flags, hipStream_t s) {
-    const int64_t work = std::max<int64_t>(csr->nnz, csr->n);
-    const int64_t blocks = std::min<int64_t>((work + kThreads - 1) / kThreads, 4096);
-    hipLaunchKernelGGL(validate_kernel, dim3(static_cast<unsigned>(std::max<int64_t>(blocks, 1))),
-                       dim3(kThreads), 0, s, csr->rowptr, csr->col, csr->n, csr->nnz, flags,
-                       flags + 1);
+int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t *blockmax,
+                 hipStream_t s) {
+    hipLaunchKernelGGL(validate_kernel, dim3(kValidateBlocks), dim3(kThreads), 0, s, csr->rowptr,
+                       csr->col, csr->n, csr->nnz, flags, nodeinfo, blockmax);
     return hip_status(hipGetLastError());
 }
 
 void free_plan(Plan *p) {
     if (!p) return;
-    void *bufs[] = {p->S,     p->K,     p->perm,  p->pptr,    p->pcol,
-                    p->pval,  p->tasks, p->parts, p->counters, p->partials};
-    for (void *b : bufs)
-        if (b) (void)hipFree(b);
+    release_block(p->mem, p->mem_bytes);
     delete p;
 }
 
@@ -581,12 +633,18 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                const dualgcn_thresholds &th, hipStream_t s, Plan **out) {
     const int32_t n = csr->n;
     const int64_t nnz = csr->nnz;
+    const size_t un = static_cast<size_t>(n), unnz = static_cast<size_t>(nnz);
     Plan *p = new (std::nothrow) Plan();
     if (!p) return DUALGCN_ERR_OOM;
-    struct Guard {
+    struct Guard {   // on an error return: wait for the queued work, then release
         Plan *p;
-        ~Guard() { free_plan(p); }
-    } guard{p};
+        hipStream_t s;
+        ~Guard() {
+            if (!p) return;
+            (void)hipStreamSynchronize(s);
+            free_plan(p);
+        }
+    } guard{p, s};
     int st;
     if ((st = hip_status(hipGetDevice(&p->device)))) return st;
     p->n = n;
@@ -599,31 +657,78 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     p->k = k;
     p->d = d;
 
-    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->S), sizeof(uint32_t) * n))) return st;
-    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->K), sizeof(uint64_t) * n))) return st;
-    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->perm), sizeof(int32_t) * n))) return st;
-
+    // Every array of the plan lives in one device block, every scratch array of the
+    // build in another: two allocations per plan.  Split parts are bounded by
+    // sum over rows longer than C of ceil(deg / C) < 2 nnz / C + 1.
+    const size_t max_parts = unnz / kDenseChunk * 2 + 1;
     const int32_t nb_keys = static_cast<int32_t>(std::min<int64_t>((n + kThreads - 1) / kThreads, 1024));
-    DevBuf flags, partial, summary;
-    if ((st = alloc_bytes(&flags.p, 2 * sizeof(int32_t)))) return st;
-    if ((st = alloc_bytes(&partial.p, sizeof(Moments) * nb_keys))) return st;
-    if ((st = alloc_bytes(&summary.p, sizeof(Summary)))) return st;
-    int32_t *bad = flags.as<int32_t>();
-    int32_t *maxdeg = bad + 1;
-    if ((st = hip_status(hipMemsetAsync(bad, 0, 2 * sizeof(int32_t), s)))) return st;
+    const int32_t nblocks = static_cast<int32_t>((static_cast<int64_t>(n) + kTile - 1) / kTile);
+    const int64_t scan_tiles = std::max((static_cast<int64_t>(kRadix) * nblocks + kTile - 1) / kTile,
+                                        (static_cast<int64_t>(n) + 1 + kTile - 1) / kTile) + 1;
+    Layout lp, ls;
+    const size_t o_S = lp.take(sizeof(uint32_t) * un), o_K = lp.take(sizeof(uint64_t) * un),
+                 o_perm = lp.take(sizeof(int32_t) * un), o_pptr = lp.take(sizeof(int32_t) * (un + 1)),
+                 o_pcol = lp.take(sizeof(int32_t) * unnz), o_pval = lp.take(sizeof(float) * unnz),
+                 o_tasks = lp.take(sizeof(int32_t) * (un + 1)),
+                 o_parts = lp.take(sizeof(SplitPart) * max_parts),
+                 o_cnt = lp.take(sizeof(int32_t) * max_parts * kMaxSlices),
+                 o_partials = lp.take(sizeof(double) * max_parts * kMaxSlice);
+    const size_t o_flags = ls.take(2 * sizeof(int32_t)), o_mom = ls.take(sizeof(Moments) * nb_keys),
+                 o_sum = ls.take(sizeof(Summary)), o_kb0 = ls.take(sizeof(uint64_t) * un),
+                 o_kb1 = ls.take(sizeof(uint64_t) * un), o_vb0 = ls.take(sizeof(int32_t) * un),
+                 o_scan = ls.take(sizeof(uint32_t) * static_cast<size_t>(scan_tiles)),
+                 o_hist = ls.take(sizeof(uint32_t) * kRadix * static_cast<size_t>(nblocks)),
+                 o_ssum = ls.take(sizeof(SplitSummary)), o_counts = ls.take(sizeof(uint32_t) * 2 * un),
+                 o_info = ls.take(sizeof(int2) * un),
+                 o_bmax = ls.take(sizeof(int32_t) * kValidateBlocks);
+    if ((st = alloc_block(&p->mem, &p->mem_bytes, lp.bytes))) return st;
+    ScratchBlock scratch;
+    scratch.stream = s;
+    if ((st = alloc_block(&scratch.p, &scratch.bytes, ls.bytes))) return st;
+    char *pm = static_cast<char *>(p->mem);
+    char *sm = static_cast<char *>(scratch.p);
+    p->S = reinterpret_cast<uint32_t *>(pm + o_S);
+    p->K = reinterpret_cast<uint64_t *>(pm + o_K);
+    p->perm = reinterpret_cast<int32_t *>(pm + o_perm);
+    p->pptr = reinterpret_cast<int32_t *>(pm + o_pptr);
+    p->pcol = reinterpret_cast<int32_t *>(pm + o_pcol);
+    p->pval = reinterpret_cast<float *>(pm + o_pval);
+    p->tasks = reinterpret_cast<int32_t *>(pm + o_tasks);
+    p->parts = reinterpret_cast<SplitPart *>(pm + o_parts);
+    p->counters = reinterpret_cast<int32_t *>(pm + o_cnt);
+    p->partials = reinterpret_cast<double *>(pm + o_partials);
+    int32_t *bad = reinterpret_cast<int32_t *>(sm + o_flags);
+    Moments *moments = reinterpret_cast<Moments *>(sm + o_mom);
+    Summary *summary = reinterpret_cast<Summary *>(sm + o_sum);
+    uint64_t *kb0 = reinterpret_cast<uint64_t *>(sm + o_kb0);
+    uint64_t *kb1 = reinterpret_cast<uint64_t *>(sm + o_kb1);
+    int32_t *vb0 = reinterpret_cast<int32_t *>(sm + o_vb0);
+    uint32_t *scan_sums = reinterpret_cast<uint32_t *>(sm + o_scan);
+    uint32_t *hist = reinterpret_cast<uint32_t *>(sm + o_hist);
+    SplitSummary *dsum = reinterpret_cast<SplitSummary *>(sm + o_ssum);
+    uint32_t *cnt = reinterpret_cast<uint32_t *>(sm + o_counts);
+    uint32_t *off = cnt + n;
+    int2 *nodeinfo = reinterpret_cast<int2 *>(sm + o_info);
+    int32_t *blockmax = reinterpret_cast<int32_t *>(sm + o_bmax);
 
-    if ((st = validate_csr(csr, bad, s))) return st;
-    // walks
-    if ((st = launch_arw(csr->rowptr, csr->col, n, seed, k, d, p->S, nullptr, bad, s))) return st;
+    if ((st = hip_status(hipMemsetAsync(bad, 0, 2 * sizeof(int32_t), s)))) return st;
+    if ((st = hip_status(hipMemsetAsync(p->counters, 0, sizeof(int32_t) * max_parts * kMaxSlices, s))))
+        return st;
+    if ((st = validate_csr(csr, bad, nodeinfo, blockmax, s))) return st;
+    // walks: the lockstep walker where it applies, else one walk per lane
+    st = launch_density(nodeinfo, csr->col, n, seed, k, d, p->S, bad, s);
+    if (st == DUALGCN_ERR_UNSUPPORTED)
+        st = launch_arw(csr->rowptr, csr->col, n, seed, k, d, p->S, nullptr, bad, s);
+    if (st) return st;
     // keys and moments
     const uint64_t pa = th.alpha_num, qa = th.alpha_den;
     hipLaunchKernelGGL(keys_kernel, dim3(nb_keys), dim3(kThreads), 0, s, csr->rowptr, p->S, n,
-                       pa, (qa - pa) * k, p->K, partial.as<Moments>(), bad);
-    hipLaunchKernelGGL(fold_kernel, dim3(1), dim3(kThreads), 0, s, partial.as<Moments>(), nb_keys,
-                       bad, maxdeg, summary.as<Summary>());
+                       pa, (qa - pa) * k, p->K, moments, bad);
+    hipLaunchKernelGGL(fold_kernel, dim3(1), dim3(kThreads), 0, s, moments, nb_keys, bad, blockmax,
+                       summary);
     if ((st = hip_status(hipGetLastError()))) return st;
     Summary sum{};
-    if ((st = hip_status(hipMemcpyAsync(&sum, summary.p, sizeof(sum), hipMemcpyDeviceToHost, s))))
+    if ((st = hip_status(hipMemcpyAsync(&sum, summary, sizeof(sum), hipMemcpyDeviceToHost, s))))
         return st;
     if ((st = hip_status(hipStreamSynchronize(s)))) return st;           // host wait 1
     if (sum.flag) return DUALGCN_ERR_BAD_CSR;
@@ -634,41 +739,27 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     p->kmax = sum.m.kmax;
     if ((st = threshold_key(n, p->s1, p->s2, th.beta_num, th.beta_den, &p->kstar))) return st;
 
-    // stable radix sort of (K, v) on the bits the keys use
-    DevBuf kb0, kb1, vb0;
-    if ((st = alloc_bytes(&kb0.p, sizeof(uint64_t) * n))) return st;
-    if ((st = alloc_bytes(&kb1.p, sizeof(uint64_t) * n))) return st;
-    if ((st = alloc_bytes(&vb0.p, sizeof(int32_t) * n))) return st;
+    // stable radix sort of (K, v) on the bits the keys use; every entry of perm is a
+    // valid node id even before the sort writes it
+    if ((st = hip_status(hipMemsetAsync(p->perm, 0, sizeof(int32_t) * un, s)))) return st;
     const int passes = (bit_length(p->kmax) + kRadixBits - 1) / kRadixBits;
-    const int32_t nblocks = static_cast<int32_t>((static_cast<int64_t>(n) + kTile - 1) / kTile);
-    DevBuf scan_sums;   // tile sums of every scan below
-    {
-        const int64_t t1 = (static_cast<int64_t>(kRadix) * nblocks + kTile - 1) / kTile;
-        const int64_t t2 = (static_cast<int64_t>(n) + 1 + kTile - 1) / kTile;
-        if ((st = alloc_bytes(&scan_sums.p, sizeof(uint32_t) * (std::max(t1, t2) + 1)))) return st;
-    }
     uint64_t *sorted = nullptr;
-    // every entry of perm is a valid node id even before the sort writes it
-    if ((st = hip_status(hipMemsetAsync(p->perm, 0, sizeof(int32_t) * n, s)))) return st;
-    if ((st = hip_status(hipMemsetAsync(vb0.p, 0, sizeof(int32_t) * n, s)))) return st;
     if (passes == 0) {
         hipLaunchKernelGGL(iota_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads), 0, s,
                            p->perm, n);
-        if ((st = hip_status(hipMemcpyAsync(kb0.p, p->K, sizeof(uint64_t) * n,
+        if ((st = hip_status(hipMemcpyAsync(kb0, p->K, sizeof(uint64_t) * un,
                                             hipMemcpyDeviceToDevice, s))))
             return st;
-        sorted = kb0.as<uint64_t>();
+        sorted = kb0;
     } else {
-        DevBuf hist;
-        if ((st = alloc_bytes(&hist.p, sizeof(uint32_t) * kRadix * nblocks))) return st;
         // ping-pong so that the last pass lands its values in p->perm
         int32_t *vbuf[2];
-        uint64_t *kbuf[2] = {kb0.as<uint64_t>(), kb1.as<uint64_t>()};
+        uint64_t *kbuf[2] = {kb0, kb1};
         if (passes % 2 == 1) {
             vbuf[0] = p->perm;
-            vbuf[1] = vb0.as<int32_t>();
+            vbuf[1] = vb0;
         } else {
-            vbuf[0] = vb0.as<int32_t>();
+            vbuf[0] = vb0;
             vbuf[1] = p->perm;
         }
         const uint64_t *kin = p->K;
@@ -678,87 +769,57 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
             uint64_t *kout = kbuf[pass % 2];
             int32_t *vout = vbuf[pass % 2];
             hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, n,
-                               shift, hist.as<uint32_t>(), nblocks);
+                               shift, hist, nblocks);
             if ((st = hip_status(hipGetLastError()))) return st;
-            if ((st = exclusive_scan(hist.as<uint32_t>(), static_cast<int64_t>(kRadix) * nblocks,
-                                     scan_sums.as<uint32_t>(), nullptr, s)))
+            if ((st = exclusive_scan(hist, static_cast<int64_t>(kRadix) * nblocks, scan_sums,
+                                     nullptr, s)))
                 return st;
             hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, vin,
-                               n, shift, hist.as<uint32_t>(), nblocks, kout, vout);
+                               n, shift, hist, nblocks, kout, vout);
             if ((st = hip_status(hipGetLastError()))) return st;
             kin = kout;
             vin = vout;
         }
         sorted = const_cast<uint64_t *>(kin);
-        if ((st = hip_status(hipStreamSynchronize(s)))) return st;   // hist is released here
     }
 
     // region split, the sorted copy of the matrix, sparse tasks and dense-row parts
-    DevBuf ssum, counts;
-    if ((st = alloc_bytes(&ssum.p, sizeof(SplitSummary)))) return st;
-    if ((st = alloc_bytes(&counts.p, sizeof(uint32_t) * (static_cast<size_t>(n) * 2)))) return st;
     int32_t forced = -1;
     if (th.force_mode == DUALGCN_FORCE_SPARSE) forced = n;
     if (th.force_mode == DUALGCN_FORCE_DENSE) forced = 0;
-    hipLaunchKernelGGL(lower_bound_kernel, dim3(1), dim3(1), 0, s, sorted, n, p->kstar, forced,
-                       ssum.as<SplitSummary>());
-    SplitSummary *dsum = ssum.as<SplitSummary>();
+    hipLaunchKernelGGL(lower_bound_kernel, dim3(1), dim3(1), 0, s, sorted, n, p->kstar, forced, dsum);
     const unsigned grid_n1 = static_cast<unsigned>((static_cast<int64_t>(n) + 1 + kThreads - 1) / kThreads);
     const unsigned grid_n = static_cast<unsigned>((static_cast<int64_t>(n) + kThreads - 1) / kThreads);
-
-    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->pptr), sizeof(int32_t) * (static_cast<size_t>(n) + 1))))
-        return st;
-    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->pcol), sizeof(int32_t) * static_cast<size_t>(nnz))))
-        return st;
-    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->pval), sizeof(float) * static_cast<size_t>(nnz))))
-        return st;
-    if ((st = alloc_bytes(reinterpret_cast<void **>(&p->tasks), sizeof(int32_t) * (static_cast<size_t>(n) + 1))))
-        return st;
     uint32_t *pptr_u = reinterpret_cast<uint32_t *>(p->pptr);
     hipLaunchKernelGGL(sorted_degree_kernel, dim3(grid_n1), dim3(kThreads), 0, s, p->perm, csr->rowptr,
                        n, pptr_u);
-    if ((st = exclusive_scan(pptr_u, static_cast<int64_t>(n) + 1, scan_sums.as<uint32_t>(), nullptr, s)))
-        return st;
+    if ((st = exclusive_scan(pptr_u, static_cast<int64_t>(n) + 1, scan_sums, nullptr, s))) return st;
     if (nnz > 0) {
         const unsigned grid_e = static_cast<unsigned>((nnz + kCopyTile - 1) / kCopyTile);
         hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_e), dim3(kThreads), 0, s, p->perm,
                            csr->rowptr, csr->col, csr->val, p->pptr, n, nnz, p->pcol, p->pval);
     }
-
-    uint32_t *cnt = counts.as<uint32_t>();
-    uint32_t *off = cnt + n;
-    hipLaunchKernelGGL(task_flag_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, off);
-    if ((st = exclusive_scan(off, n, scan_sums.as<uint32_t>(), &dsum->tasks, s))) return st;
-    hipLaunchKernelGGL(task_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, off,
+    hipLaunchKernelGGL(task_flag_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt,
+                       off);
+    if ((st = exclusive_scan(off, n, scan_sums, &dsum->tasks, s))) return st;
+    hipLaunchKernelGGL(task_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, n, dsum, cnt, off,
                        p->tasks);
-
     hipLaunchKernelGGL(split_count_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt);
-    if ((st = hip_status(hipMemcpyAsync(off, cnt, sizeof(uint32_t) * n, hipMemcpyDeviceToDevice, s))))
+    if ((st = hip_status(hipMemcpyAsync(off, cnt, sizeof(uint32_t) * un, hipMemcpyDeviceToDevice, s))))
         return st;
-    if ((st = exclusive_scan(off, n, scan_sums.as<uint32_t>(), &dsum->parts, s))) return st;
+    if ((st = exclusive_scan(off, n, scan_sums, &dsum->parts, s))) return st;
+    hipLaunchKernelGGL(split_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, cnt, off, n, p->parts,
+                       static_cast<uint32_t>(max_parts));
+    if ((st = hip_status(hipGetLastError()))) return st;
     SplitSummary ss{};
-    if ((st = hip_status(hipMemcpyAsync(&ss, ssum.p, sizeof(ss), hipMemcpyDeviceToHost, s))))
-        return st;
-    if ((st = hip_status(hipStreamSynchronize(s)))) return st;           // host wait 2
+    if ((st = hip_status(hipMemcpyAsync(&ss, dsum, sizeof(ss), hipMemcpyDeviceToHost, s)))) return st;
+    // host wait 2: the region and schedule sizes; the scratch block is released after it
+    if ((st = hip_status(hipStreamSynchronize(s)))) return st;
+    if (ss.parts > max_parts) return DUALGCN_ERR_HIP;    // impossible: bounded above
     p->n_sparse = ss.n_sparse;
     p->n_tasks = static_cast<int32_t>(ss.tasks);
     p->n_split_rows = ss.split_rows;
     p->n_split_parts = static_cast<int32_t>(ss.parts);
-    if (p->n_split_parts > 0) {
-        const size_t np = static_cast<size_t>(p->n_split_parts);
-        if ((st = alloc_bytes(reinterpret_cast<void **>(&p->parts), sizeof(SplitPart) * np))) return st;
-        if ((st = alloc_bytes(reinterpret_cast<void **>(&p->counters), sizeof(int32_t) * np * kMaxSlices)))
-            return st;
-        if ((st = alloc_bytes(reinterpret_cast<void **>(&p->partials), sizeof(double) * np * kMaxSlice)))
-            return st;
-        if ((st = hip_status(hipMemsetAsync(p->counters, 0, sizeof(int32_t) * np * kMaxSlices, s))))
-            return st;
-        hipLaunchKernelGGL(split_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, cnt, off, n,
-                           p->parts, static_cast<uint32_t>(np));
-        if ((st = hip_status(hipGetLastError()))) return st;
-    }
-    // the scratch buffers above are released on return: wait for their users
-    if ((st = hip_status(hipStreamSynchronize(s)))) return st;
     guard.p = nullptr;
     *out = p;
     return DUALGCN_OK;
