@@ -164,14 +164,15 @@ int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, float *Y, int32_t
  * aggregated features are multiplied by a small dense weight matrix).
  *
  * X is float32 n x F_in row-major (16-byte aligned), W float32 F_in x F_out
- * row-major, T float32 n x F_out row-major; n is the plan's.  Computed on the
- * matrix cores with X and W rounded to bfloat16 (nearest-even) and float32
+ * row-major, T float32 n x F_out row-major, n >= 1.  Computed on the matrix
+ * cores with X and W rounded to bfloat16 (nearest-even) and float32
  * accumulation.  F_in and F_out must be multiples of 32 with F_in <= 1024 and
  * F_out <= 256 (else DUALGCN_ERR_UNSUPPORTED).  X and T must not overlap.  No
- * workspace.  Asynchronous.
+ * plan and no workspace: the update does not depend on the partition, so it may
+ * run on another stream while dualgcn_partition works.  Asynchronous.
  */
-int dualgcn_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
-                   int32_t F_in, int32_t F_out, void *stream);
+int dualgcn_update(const float *X, const float *W, float *T, int32_t n, int32_t F_in,
+                   int32_t F_out, void *stream);
 
 /* Bytes of device workspace dualgcn_gcn_layer needs (host-only, no device use):
  * room for the float32 n x F_out product T. */

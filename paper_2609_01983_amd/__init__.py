@@ -7,7 +7,7 @@ is missing, importing this package raises ImportError: there is no fallback.
 
     plan = Plan(rowptr, col, val, seed=0, walks_per_node=16, walk_len=5)
     Y = spmm(plan, X)                           # Y = A X
-    T = update(plan, X, W)                      # T = X W, bf16 matrix cores
+    T = update(X, W)                            # T = X W, bf16 matrix cores
     H = gcn_layer(plan, X, W, relu=True)        # H = relu(A (X W)), X W in bf16 MFMA
 """
 import ctypes
@@ -73,7 +73,7 @@ def _load():
         "dualgcn_plan_destroy": ([P], None),
         "dualgcn_spmm": ([P, P, P, I32, P], ctypes.c_int),
         "dualgcn_spmm_act": ([P, P, P, I32, U32, P], ctypes.c_int),
-        "dualgcn_update": ([P, P, P, P, I32, I32, P], ctypes.c_int),
+        "dualgcn_update": ([P, P, P, I32, I32, I32, P], ctypes.c_int),
         "dualgcn_gcn_layer_workspace": ([P, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "dualgcn_gcn_layer": ([P, P, P, P, I32, I32, U32, P, SZ, P], ctypes.c_int),
         "dualgcn_plan_query": ([P, ctypes.POINTER(PlanInfo)], ctypes.c_int),
@@ -198,19 +198,22 @@ def spmm(plan, X, Y=None, relu=False, stream=None):
     return Y
 
 
-def update(plan, X, W, T=None, stream=None):
-    """T = X W on the bf16 matrix cores (float32 accumulation).  X: [n, F_in], W: [F_in, F_out]."""
+def update(X, W, T=None, stream=None):
+    """T = X W on the bf16 matrix cores (float32 accumulation).  X: [n, F_in], W: [F_in, F_out].
+
+    Needs no plan: it may run on another stream while a partition is built."""
     _dev(X, torch.float32, "X")
     _dev(W, torch.float32, "W")
     F_in, F_out = W.shape
-    if X.shape != (plan.n, F_in):
+    if X.dim() != 2 or X.shape[1] != F_in:
         raise ValueError("X must be [n, F_in]")
+    n = X.shape[0]
     if T is None:
-        T = torch.empty((plan.n, F_out), dtype=torch.float32, device=X.device)
+        T = torch.empty((n, F_out), dtype=torch.float32, device=X.device)
     _dev(T, torch.float32, "T")
-    if T.shape != (plan.n, F_out):
+    if T.shape != (n, F_out):
         raise ValueError("T must be [n, F_out]")
-    _check(_lib.dualgcn_update(plan.handle, X.data_ptr(), W.data_ptr(), T.data_ptr(), F_in, F_out,
+    _check(_lib.dualgcn_update(X.data_ptr(), W.data_ptr(), T.data_ptr(), n, F_in, F_out,
                                _stream(stream)), "dualgcn_update")
     return T
 

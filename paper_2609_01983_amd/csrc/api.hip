@@ -252,17 +252,16 @@ int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, float *Y, int32_t
                             static_cast<hipStream_t>(stream));
 }
 
-int dualgcn_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
-                   int32_t F_in, int32_t F_out, void *stream) {
-    int st = check_plan(plan);
+int dualgcn_update(const float *X, const float *W, float *T, int32_t n, int32_t F_in,
+                   int32_t F_out, void *stream) {
+    if (n < 1) return DUALGCN_ERR_INVALID_ARG;
+    int st = check_update(X, W, T, F_in, F_out);
     if (st) return st;
-    if ((st = check_update(X, W, T, F_in, F_out))) return st;
-    const Plan *p = as_plan(plan);
-    const size_t n = static_cast<size_t>(p->n);
-    if (overlaps(X, n * F_in * sizeof(float), T, n * F_out * sizeof(float)))
+    const size_t un = static_cast<size_t>(n);
+    if (overlaps(X, un * F_in * sizeof(float), T, un * F_out * sizeof(float)))
         return DUALGCN_ERR_INVALID_ARG;
     if ((st = dgc::device_status())) return st;
-    return dgc::launch_xw(*p, X, W, T, F_in, F_out, static_cast<hipStream_t>(stream));
+    return dgc::launch_xw(X, W, T, n, F_in, F_out, static_cast<hipStream_t>(stream));
 }
 
 int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,

@@ -112,8 +112,8 @@ int launch_spmm(const Plan &p, const float *X, float *Y, int32_t F, bool relu,
 // Bytes of the float32 T = X W buffer a layer keeps in its workspace (256-byte multiple).
 size_t xw_workspace_bytes(int32_t n, int32_t F_out);
 // T = bf16(X) bf16(W) with float32 accumulation.
-int launch_xw(const Plan &p, const float *X, const float *W, float *T, int32_t F_in,
-              int32_t F_out, hipStream_t stream);
+int launch_xw(const float *X, const float *W, float *T, int32_t n, int32_t F_in, int32_t F_out,
+              hipStream_t stream);
 // Y = act(A (X W)): launch_xw into the workspace, then launch_spmm.
 int launch_gcn_layer(const Plan &p, const float *X, const float *W, float *Y, int32_t F_in,
                      int32_t F_out, bool relu, void *workspace, hipStream_t stream);

@@ -155,8 +155,8 @@ size_t xw_workspace_bytes(int32_t n, int32_t F_out) {
     return (static_cast<size_t>(n) * F_out * sizeof(float) + 255) / 256 * 256;
 }
 
-int launch_xw(const Plan &p, const float *X, const float *W, float *T, int32_t F_in,
-              int32_t F_out, hipStream_t s) {
+int launch_xw(const float *X, const float *W, float *T, int32_t n, int32_t F_in, int32_t F_out,
+              hipStream_t s) {
     // column blocks whose W^T slice fits the LDS budget
     const int cb = std::min<int>(F_out, (kLdsElems / F_in) / 16 * 16);
     if (cb < 16) return DUALGCN_ERR_UNSUPPORTED;
@@ -165,9 +165,9 @@ int launch_xw(const Plan &p, const float *X, const float *W, float *T, int32_t F
         const int ntiles = width / 16;
         const size_t lds = static_cast<size_t>(width) * (F_in + kPad) * sizeof(unsigned short);
         int st;
-        if (ntiles <= 4) st = launch_xw<4>(X, W, T, p.n, F_in, F_out, c0, ntiles, lds, s);
-        else if (ntiles <= 8) st = launch_xw<8>(X, W, T, p.n, F_in, F_out, c0, ntiles, lds, s);
-        else st = launch_xw<16>(X, W, T, p.n, F_in, F_out, c0, ntiles, lds, s);
+        if (ntiles <= 4) st = launch_xw<4>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+        else if (ntiles <= 8) st = launch_xw<8>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+        else st = launch_xw<16>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
         if (st) return st;
     }
     return DUALGCN_OK;
@@ -176,7 +176,7 @@ int launch_xw(const Plan &p, const float *X, const float *W, float *T, int32_t F
 int launch_gcn_layer(const Plan &p, const float *X, const float *W, float *Y, int32_t F_in,
                      int32_t F_out, bool relu, void *workspace, hipStream_t s) {
     float *T = static_cast<float *>(workspace);
-    const int st = launch_xw(p, X, W, T, F_in, F_out, s);
+    const int st = launch_xw(X, W, T, p.n, F_in, F_out, s);
     if (st) return st;
     return launch_spmm(p, T, Y, F_out, relu, s);
 }
