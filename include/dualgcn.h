@@ -115,11 +115,14 @@ typedef struct dualgcn_plan dualgcn_plan;
  * moment sums must fit 128 bits (else DUALGCN_ERR_UNSUPPORTED).  The CSR is
  * validated on the device first (DUALGCN_ERR_BAD_CSR).
  *
- * The plan owns one block of device memory of about 9 nnz + 24 n bytes (S, K,
- * perm, a copy of the matrix with its rows in perm order, the sparse tasks, the
- * dense-region schedule and the partial sums of split rows), released by
- * dualgcn_plan_destroy; a scratch block is allocated and released inside the call.  The call waits
- * for `stream` twice (to read the moment sums and the schedule sizes).
+ * The plan owns one block of device memory of about 9 nnz + 28 n bytes (S, K,
+ * perm, the processing order, a copy of the matrix with its rows in that order,
+ * the sparse tasks, the dense-region schedule and the partial sums of split
+ * rows), released by dualgcn_plan_destroy; a scratch block is allocated and
+ * released inside the call.  The processing order keeps perm's split into the
+ * sparse and the dense region; inside a region rows go by row-length octave,
+ * then node id (balanced work, and the locality of the node numbering).  The
+ * call waits for `stream` twice (to read the moment sums and the schedule sizes).
  * *out is set to NULL on error.
  */
 int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,

@@ -46,8 +46,11 @@ struct Plan {
     uint32_t *S = nullptr;             // [n] density sums
     uint64_t *K = nullptr;             // [n] hybrid keys
     int32_t *perm = nullptr;           // [n] nodes sorted by (K, v)
+    // [n] processing order: sparse rows then dense rows (the same split as perm),
+    // each region by row-length octave, then node id
+    int32_t *order = nullptr;
 
-    // The matrix with its rows in sorted order (row i of this copy is row perm[i]):
+    // The matrix with its rows in processing order (row i of this copy is row order[i]):
     // the contiguous sparse and dense regions the SpMM kernels stream through.
     int32_t *pptr = nullptr;           // [n + 1]
     int32_t *pcol = nullptr;           // [nnz]

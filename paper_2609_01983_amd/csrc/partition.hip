@@ -9,9 +9,10 @@
 //   host            K* = least integer >= mu_K + beta sigma_K (exact integers)
 //   radix sort      stable LSD sort of (K_v, v) on 8-bit digits      -> perm
 //   split           n_sparse = lower_bound(sorted K, K*)
-//   sorted copy     the rows of the matrix in perm order (row pointers by a scan),
-//                   so that both regions are contiguous streams (Sec. 3.2: the
-//                   sorted nodes are cut into contiguous blocks)
+//   sorted copy     the rows of the matrix in processing order (region, row-length
+//                   octave, node id; row pointers by a scan), so that both regions
+//                   are contiguous streams (Sec. 3.2: the sorted nodes are cut into
+//                   contiguous blocks)
 //   schedule        sparse tasks (runs of at most kTaskRows short rows) and the
 //                   parts of dense rows longer than one dense chunk   -> host wait 2
 //
@@ -376,14 +377,32 @@ __global__ void lower_bound_kernel(const uint64_t *__restrict__ sorted, int32_t 
     out->tasks = 0;
 }
 
-// pptr[i] = length of row perm[i] for i < n and pptr[n] = 0; an exclusive scan then turns
+// Processing order of the SpMM (the row order of the sorted copy): region first (sparse
+// rows, then dense rows, Eq. (1)), then the octave of the row length, then node id.  Rows
+// that share an octave cost about the same (the balance the paper sorts for); keeping node
+// ids in order inside an octave keeps whatever locality the numbering has (e.g. the
+// contiguous communities of a block-structured graph).  forced = 0 / 1 puts every row in
+// one region, -1 applies K >= K*.
+__global__ __launch_bounds__(kThreads) void order_key_kernel(const uint64_t *__restrict__ K,
+                                                             uint64_t kstar, int32_t forced,
+                                                             const int32_t *__restrict__ rowptr,
+                                                             int32_t n, uint64_t *__restrict__ key) {
+    const int64_t v = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (v >= n) return;
+    const uint32_t deg = static_cast<uint32_t>(rowptr[v + 1] - rowptr[v]);
+    const uint64_t octave = deg ? 31u - static_cast<uint32_t>(__clz(deg)) : 0u;
+    const uint64_t dense = forced >= 0 ? static_cast<uint64_t>(forced) : (K[v] >= kstar ? 1u : 0u);
+    key[v] = dense * 32u + octave;
+}
+
+// pptr[i] = length of row order[i] for i < n and pptr[n] = 0; an exclusive scan then turns
 // pptr into the row pointers of the sorted copy.
-__global__ __launch_bounds__(kThreads) void sorted_degree_kernel(const int32_t *__restrict__ perm,
+__global__ __launch_bounds__(kThreads) void sorted_degree_kernel(const int32_t *__restrict__ order,
                                                                  const int32_t *__restrict__ rowptr,
                                                                  int32_t n, uint32_t *__restrict__ pptr) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i < n) {
-        const int32_t r = perm[i];
+        const int32_t r = order[i];
         pptr[i] = static_cast<uint32_t>(rowptr[r + 1] - rowptr[r]);
     } else if (i == n) {
         pptr[n] = 0;
@@ -405,11 +424,11 @@ __device__ __forceinline__ int32_t row_of(const P &ptr, int32_t lo, int32_t hi, 
 constexpr int kCopyTile = 4096;     // entries of the sorted copy one workgroup fills
 
 // Fills entries [b kCopyTile, (b + 1) kCopyTile) of the sorted copy: entry e of sorted
-// row i is entry e - pptr[i] of row perm[i].  The tile's rows are located once, their
+// row i is entry e - pptr[i] of row order[i].  The tile's rows are located once, their
 // pointers staged in LDS, and every thread copies the entries e = tile start + t +
 // 256 k (writes are coalesced; reads are coalesced inside a row).
 __global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
-    const int32_t *__restrict__ perm, const int32_t *__restrict__ rowptr,
+    const int32_t *__restrict__ order, const int32_t *__restrict__ rowptr,
     const int32_t *__restrict__ col, const float *__restrict__ val,
     const int32_t *__restrict__ pptr, int32_t n, int64_t nnz, int32_t *__restrict__ pcol,
     float *__restrict__ pval) {
@@ -428,7 +447,7 @@ __global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
     if (rows <= kCopyTile) {
         for (int32_t k = threadIdx.x; k < rows; k += kThreads) {
             sh_ptr[k] = pptr[r_lo + k];
-            sh_src[k] = rowptr[perm[r_lo + k]];
+            sh_src[k] = rowptr[order[r_lo + k]];
         }
         __syncthreads();
         for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) {
@@ -441,7 +460,7 @@ __global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
         // more rows than entries (empty rows): search the row pointers in memory
         for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) {
             const int32_t r = row_of(pptr, r_lo, r_hi, e);
-            const int64_t src = rowptr[perm[r]] + (e - pptr[r]);
+            const int64_t src = rowptr[order[r]] + (e - pptr[r]);
             pcol[e] = col[src];
             pval[e] = val[src];
         }
@@ -667,7 +686,8 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                                         (static_cast<int64_t>(n) + 1 + kTile - 1) / kTile) + 1;
     Layout lp, ls;
     const size_t o_S = lp.take(sizeof(uint32_t) * un), o_K = lp.take(sizeof(uint64_t) * un),
-                 o_perm = lp.take(sizeof(int32_t) * un), o_pptr = lp.take(sizeof(int32_t) * (un + 1)),
+                 o_perm = lp.take(sizeof(int32_t) * un), o_order = lp.take(sizeof(int32_t) * un),
+                 o_pptr = lp.take(sizeof(int32_t) * (un + 1)),
                  o_pcol = lp.take(sizeof(int32_t) * unnz), o_pval = lp.take(sizeof(float) * unnz),
                  o_tasks = lp.take(sizeof(int32_t) * (un + 1)),
                  o_parts = lp.take(sizeof(SplitPart) * max_parts),
@@ -690,6 +710,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     p->S = reinterpret_cast<uint32_t *>(pm + o_S);
     p->K = reinterpret_cast<uint64_t *>(pm + o_K);
     p->perm = reinterpret_cast<int32_t *>(pm + o_perm);
+    p->order = reinterpret_cast<int32_t *>(pm + o_order);
     p->pptr = reinterpret_cast<int32_t *>(pm + o_pptr);
     p->pcol = reinterpret_cast<int32_t *>(pm + o_pcol);
     p->pval = reinterpret_cast<float *>(pm + o_pval);
@@ -790,13 +811,30 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     hipLaunchKernelGGL(lower_bound_kernel, dim3(1), dim3(1), 0, s, sorted, n, p->kstar, forced, dsum);
     const unsigned grid_n1 = static_cast<unsigned>((static_cast<int64_t>(n) + 1 + kThreads - 1) / kThreads);
     const unsigned grid_n = static_cast<unsigned>((static_cast<int64_t>(n) + kThreads - 1) / kThreads);
+    // processing order: one stable 8-bit pass over the node ids (keys < 64); the buffer of
+    // the sorted keys is free again once lower_bound has run (same stream)
+    {
+        const int32_t region = th.force_mode == DUALGCN_FORCE_SPARSE ? 0
+                               : th.force_mode == DUALGCN_FORCE_DENSE ? 1 : -1;
+        uint64_t *okey = sorted == kb0 ? kb1 : kb0;
+        uint64_t *okey_out = sorted == kb0 ? kb0 : kb1;
+        hipLaunchKernelGGL(order_key_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->K, p->kstar,
+                           region, csr->rowptr, n, okey);
+        hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, okey, n, 0, hist,
+                           nblocks);
+        if ((st = exclusive_scan(hist, static_cast<int64_t>(kRadix) * nblocks, scan_sums, nullptr, s)))
+            return st;
+        hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblocks), dim3(kThreads), 0, s, okey, nullptr, n,
+                           0, hist, nblocks, okey_out, p->order);
+        if ((st = hip_status(hipGetLastError()))) return st;
+    }
     uint32_t *pptr_u = reinterpret_cast<uint32_t *>(p->pptr);
-    hipLaunchKernelGGL(sorted_degree_kernel, dim3(grid_n1), dim3(kThreads), 0, s, p->perm, csr->rowptr,
+    hipLaunchKernelGGL(sorted_degree_kernel, dim3(grid_n1), dim3(kThreads), 0, s, p->order, csr->rowptr,
                        n, pptr_u);
     if ((st = exclusive_scan(pptr_u, static_cast<int64_t>(n) + 1, scan_sums, nullptr, s))) return st;
     if (nnz > 0) {
         const unsigned grid_e = static_cast<unsigned>((nnz + kCopyTile - 1) / kCopyTile);
-        hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_e), dim3(kThreads), 0, s, p->perm,
+        hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_e), dim3(kThreads), 0, s, p->order,
                            csr->rowptr, csr->col, csr->val, p->pptr, n, nnz, p->pcol, p->pval);
     }
     hipLaunchKernelGGL(task_flag_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt,

@@ -1,8 +1,9 @@
 // Dual-path aggregation SpMM Y = A X on gfx950 (DualGCN Sec. 3.3).
 //
 // The kernels stream the plan's sorted copy of the matrix: row i of the copy is
-// row perm[i] of A, the sparse region is rows [0, n_sparse) and the dense region
-// rows [n_sparse, n) (Eq. (1) was applied when the plan was built).  One launch
+// row order[i] of A, the sparse region is rows [0, n_sparse) and the dense region
+// rows [n_sparse, n) (Eq. (1) was applied when the plan was built; inside a region
+// rows go by row-length octave, then node id).  One launch
 // covers both paths; every workgroup picks its path from its index:
 //
 //   parts      rows of the dense region longer than one chunk, split into parts
@@ -88,7 +89,7 @@ struct Args {
     const int32_t *pptr;        // sorted copy of the matrix
     const int32_t *pcol;
     const float *pval;
-    const int32_t *perm;        // output row of each sorted row
+    const int32_t *perm;        // output row of each sorted row (the plan's order)
     const int32_t *tasks;
     const SplitPart *parts;
     int32_t *counters;
@@ -340,7 +341,7 @@ int launch_spmm(const Plan &p, const float *X, float *Y, int32_t F, bool relu, h
     a.pptr = p.pptr;
     a.pcol = p.pcol;
     a.pval = p.pval;
-    a.perm = p.perm;
+    a.perm = p.order;
     a.tasks = p.tasks;
     a.parts = p.parts;
     a.counters = p.counters;
