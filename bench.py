@@ -138,6 +138,51 @@ def cpu_baseline(w, g, X, weights, part_budget_s=2.5):
             "est_step_s": round(t_total, 3)}
 
 
+# Partition variants of the ablation: the paper's dual metric, its degree-only analogue
+# (the baseline partitioning of the paper's DualGCN_0 experiment), density only, and a
+# single path for every row.
+ABLATION = [("dual-metric alpha=1/2", (1, 2), "auto"),
+            ("degree only alpha=0", (0, 1), "auto"),
+            ("density only alpha=1", (1, 1), "auto"),
+            ("all rows sparse path", (1, 2), "sparse"),
+            ("all rows dense path", (1, 2), "dense")]
+
+
+def ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev):
+    """Times partition and the dominant SpMM for each variant; prints one JSON line each."""
+    X = Xd if not w.is_gcn else torch.randn((g.n, F_dom), dtype=torch.float32, device=Xd.device,
+                                            generator=torch.Generator(device=Xd.device).manual_seed(0))
+    Y = torch.empty_like(X)
+    for name, alpha, force in ABLATION:
+        part_ms, spmm_ms = [], []
+        for rep in range(args.warmup + args.steps):
+            a, b = ev(), ev()
+            a.record(stream)
+            plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps,
+                           alpha=alpha, force_mode=force)
+            b.record(stream)
+            c, d = ev(), ev()
+            c.record(stream)
+            dg.spmm(plan, X, Y, relu=w.is_gcn)
+            d.record(stream)
+            torch.cuda.synchronize()
+            if rep >= args.warmup:
+                part_ms.append(a.elapsed_time(b))
+                spmm_ms.append(c.elapsed_time(d))
+            info = plan.info()
+            plan.destroy()
+        ms = float(np.mean(spmm_ms))
+        print(json.dumps({"ablation": name, "workload": w.name, "F": F_dom, "alpha": list(alpha),
+                          "force_mode": force, "n_sparse": info["n_sparse"],
+                          "n_dense": info["n_dense"], "kstar": info["kstar"],
+                          "partition_ms": round(float(np.mean(part_ms)), 4),
+                          "spmm_ms": round(ms, 4),
+                          "spmm_ge_s": round(g.nnz * F_dom / (ms * 1e-3) / 1e9, 2),
+                          "spmm_hbm_frac_bmin": round(spmm_bytes(g.n, g.nnz, F_dom) / (ms * 1e-3)
+                                                      / (PEAK_HBM_GBS * 1e9), 4),
+                          "walks_per_node": w.walks, "walk_len": w.steps}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -150,6 +195,10 @@ def main():
                     help="spmm: one partition, then only the dominant SpMM launches (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device to device (a dispatch of known traffic)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="time partition + dominant SpMM for each partition variant (one JSON line each)")
+    ap.add_argument("--walks", type=int, default=None, help="walks per node (default: the workload's)")
+    ap.add_argument("--walk-len", type=int, default=None, help="steps per walk (default: the workload's)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -162,6 +211,9 @@ def main():
     from graphgen import configs
 
     w = configs.WORKLOADS[args.config]
+    if args.walks is not None or args.walk_len is not None:
+        import dataclasses
+        w = dataclasses.replace(w, walks=args.walks or w.walks, steps=args.walk_len or w.steps)
     t0 = time.time()
     g = configs.load_graph(w.name)
     X = configs.load_features(w.name)
@@ -207,6 +259,9 @@ def main():
         return
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
+    if args.ablation:
+        ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
+        return
     if w.is_gcn:
         Ts = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for _, fo in w.layers]
         Hs = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for _, fo in w.layers]

@@ -191,6 +191,34 @@ def test_spmm_configs_full(dg, device, cfg):
     assert_spmm_close(Y, Yr, B, what=cfg)
 
 
+@pytest.mark.parametrize("alpha,force", [((1, 2), "auto"), ((0, 1), "auto"), ((1, 1), "auto"),
+                                         ((1, 2), "sparse"), ((1, 2), "dense")])
+def test_ablation_variants_c2(dg, device, alpha, force):
+    """Every partition variant of the ablation: its plan matches the oracle and its SpMM
+    (with the variant's schedule) matches the plan-independent oracle product."""
+    w = configs.WORKLOADS["c2"]
+    g = configs.load_graph("c2")
+    X = configs.load_features("c2")
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps,
+                   alpha=alpha, force_mode=force)
+    assert_plan_matches(dg, plan, g, 0, w.walks, w.steps, alpha, (1, 2),
+                        {"auto": 0, "sparse": 1, "dense": 2}[force])
+    Y = dg.spmm(plan, torch.from_numpy(X).to(device)).cpu().numpy()
+    Yr, B = oracle.spmm(g, X)
+    assert_spmm_close(Y, Yr, B, what=f"c2 alpha={alpha} {force}")
+
+
+@pytest.mark.parametrize("k,d", [(50, 30), (16, 30), (50, 5)])
+def test_paper_walk_parameters_c1(dg, device, k, d):
+    """The paper's preprocessing uses 50 walks of 30 steps per node: bit-exact patterns and plan."""
+    g = configs.load_graph("c1")
+    rp, c, v = to_dev(g, device)
+    P = dg.arw_patterns(rp, c, v, seed=3, walks_per_node=k, walk_len=d).cpu().numpy()
+    assert np.array_equal(P, oracle.patterns(g, 3, k, d))
+    plan = dg.Plan(rp, c, v, seed=3, walks_per_node=k, walk_len=d)
+    assert_plan_matches(dg, plan, g, 3, k, d)
+
+
 def _sample_rows(g, plan_info_perm, n_sparse, count, seed):
     """Random rows plus the heaviest dense rows and the rows around the region boundary."""
     gen = np.random.default_rng(seed)
