@@ -138,8 +138,9 @@ void dualgcn_plan_destroy(dualgcn_plan *plan);
  * X and Y are float32 row-major n x F, contiguous (leading dimension F), and
  * must not overlap.  Rows of the sparse region are computed by the sparse
  * path (runs of up to 8 short rows per lane group of a wavefront); rows of the
- * dense region by the dense path (one wavefront per row; rows longer than the
- * dense chunk are split over several wavefronts and combined in a fixed order).
+ * dense region by the dense path (a lane group per row under 512 entries, a
+ * wavefront per longer row; rows longer than the dense chunk are split over
+ * several wavefronts and combined in a fixed order).
  * Every row of Y is written, rows without entries with zeros.  Products are
  * float32; sums are formed in float32 over at most 16 terms and then in
  * float64, and each output is rounded once to float32, so results do not
@@ -216,6 +217,8 @@ typedef struct dualgcn_plan_info {
     int32_t n_split_rows;    /* dense rows longer than dense_chunk */
     int32_t n_split_parts;   /* wavefronts those rows are split over */
     int32_t n_tasks;         /* sparse-region tasks (runs of at most 8 short rows) */
+    int32_t n_long_rows;     /* dense rows of >= 512 entries (a wavefront each; the
+                                shorter dense rows get a lane group each) */
 } dualgcn_plan_info;
 
 /* Fills *out from host-side copies kept in the plan (no device use). */

@@ -56,7 +56,7 @@ class PlanInfo(ctypes.Structure):
                 ("walks_per_node", ctypes.c_uint32), ("walk_len", ctypes.c_uint32),
                 ("max_degree", ctypes.c_int32), ("dense_chunk", ctypes.c_int32),
                 ("n_split_rows", ctypes.c_int32), ("n_split_parts", ctypes.c_int32),
-                ("n_tasks", ctypes.c_int32)]
+                ("n_tasks", ctypes.c_int32), ("n_long_rows", ctypes.c_int32)]
 
 
 def _load():

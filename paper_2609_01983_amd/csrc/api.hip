@@ -323,6 +323,7 @@ int dualgcn_plan_query(const dualgcn_plan *plan, dualgcn_plan_info *out) {
     i.n_split_rows = p->n_split_rows;
     i.n_split_parts = p->n_split_parts;
     i.n_tasks = p->n_tasks;
+    i.n_long_rows = p->n_long;
     *out = i;
     return DUALGCN_OK;
 }

@@ -19,6 +19,9 @@ constexpr int kDenseChunk = 4096;
 constexpr int kMaxSlice = 256;
 // Feature slices of one window are at most this many (arrival counters per part).
 constexpr int kMaxSlices = 8;
+// Dense rows of at least 2^kLongRowOctave entries get a wavefront each; shorter dense
+// rows get one lane group each.
+constexpr int kLongRowOctave = 9;
 // A sparse-region task is a run of at most kTaskRows consecutive rows of the sorted
 // order whose first entries fall in one window of kTaskEntries entries.
 constexpr int kTaskRows = 8;
@@ -59,6 +62,7 @@ struct Plan {
 
     int32_t n_sparse = 0;
     int32_t n_tasks = 0;
+    int32_t n_long = 0;                // dense rows of >= 2^kLongRowOctave entries (the last ones)
     int32_t n_split_rows = 0;
     int32_t n_split_parts = 0;
     SplitPart *parts = nullptr;        // [n_split_parts]

@@ -360,6 +360,8 @@ struct SplitSummary {
     int32_t split_rows;
     uint32_t parts;
     uint32_t tasks;
+    int32_t long_rows;
+    int32_t pad;
 };
 
 // n_sparse = first position whose key is >= K* (one thread; keys are sorted).
@@ -375,6 +377,21 @@ __global__ void lower_bound_kernel(const uint64_t *__restrict__ sorted, int32_t 
     out->split_rows = 0;
     out->parts = 0;
     out->tasks = 0;
+    out->long_rows = 0;
+}
+
+// long_rows = rows of the dense region with at least 2^kLongRowOctave entries: the keys of
+// the processing order are sorted, so they are the rows from the first key >= that class.
+__global__ void long_rows_kernel(const uint64_t *__restrict__ okey, int32_t n,
+                                 SplitSummary *__restrict__ out) {
+    const uint64_t first_long = 32u + kLongRowOctave;
+    int32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (okey[mid] < first_long) lo = mid + 1;
+        else hi = mid;
+    }
+    out->long_rows = n - lo;
 }
 
 // Processing order of the SpMM (the row order of the sorted copy): region first (sparse
@@ -826,6 +843,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
             return st;
         hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblocks), dim3(kThreads), 0, s, okey, nullptr, n,
                            0, hist, nblocks, okey_out, p->order);
+        hipLaunchKernelGGL(long_rows_kernel, dim3(1), dim3(1), 0, s, okey_out, n, dsum);
         if ((st = hip_status(hipGetLastError()))) return st;
     }
     uint32_t *pptr_u = reinterpret_cast<uint32_t *>(p->pptr);
@@ -856,6 +874,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if (ss.parts > max_parts) return DUALGCN_ERR_HIP;    // impossible: bounded above
     p->n_sparse = ss.n_sparse;
     p->n_tasks = static_cast<int32_t>(ss.tasks);
+    p->n_long = ss.long_rows;
     p->n_split_rows = ss.split_rows;
     p->n_split_parts = static_cast<int32_t>(ss.parts);
     guard.p = nullptr;
