@@ -8,13 +8,15 @@ already resident in HBM:
   c5        partition + 2 GCN layers (256 -> 128 -> 64); each layer is the update
             X W on the bf16 matrix cores then the SpMM, ReLU after layer 1; layer 1's
             update does not depend on the partition and runs on a second stream
-            while the partition is built
+            while the partition is built; layer 1 writes its output in bfloat16, which
+            layer 2's update reads (bit-identical to a float32 intermediate)
 Metric: edge-features per second, GE/s = sum over the step's SpMMs of nnz F / step time.
 
 The JSON line also carries
   roofline      the dominant kernel, the F=128 SpMM (the F=64 one for c2, F=16 for c1),
                 against 8 TB/s: algorithmic bytes
-                B_min = 4(n+1) + 8 nnz + 4 n F (X once) + 4 n F (Y) + 4 n (perm)
+                B_min = 4(n+1) + 8 nnz + 4 n F (X once) + 4 or 2 n F (Y, float32 or
+                bfloat16) + 4 n (order)
                 per launch over its mean duration, timed with HIP events on its
                 stream around every launch of it inside the timed steps;
                 `traffic` is the HBM bytes per launch from the rocprofv3 FETCH_SIZE /
@@ -41,8 +43,9 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_01983_amd", "csrc", f)
                   for f in ("spmm.hip", "internal.h")]
 
 
-def spmm_bytes(n, nnz, F):
-    return 4 * (n + 1) + 8 * nnz + 4 * n * F + 4 * n * F + 4 * n
+def spmm_bytes(n, nnz, F, ybytes=4):
+    """B_min of one SpMM launch: row pointers, (column, value) pairs, X once, Y once, order."""
+    return 4 * (n + 1) + 8 * nnz + 4 * n * F + ybytes * n * F + 4 * n
 
 
 def kernel_source_hash():
@@ -152,7 +155,7 @@ def ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
     """Times partition and the dominant SpMM for each variant; prints one JSON line each."""
     X = Xd if not w.is_gcn else torch.randn((g.n, F_dom), dtype=torch.float32, device=Xd.device,
                                             generator=torch.Generator(device=Xd.device).manual_seed(0))
-    Y = torch.empty_like(X)
+    Y = torch.empty(X.shape, dtype=torch.bfloat16 if w.is_gcn else torch.float32, device=X.device)
     for name, alpha, force in ABLATION:
         part_ms, spmm_ms = [], []
         for rep in range(args.warmup + args.steps):
@@ -163,7 +166,7 @@ def ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
             b.record(stream)
             c, d = ev(), ev()
             c.record(stream)
-            dg.spmm(plan, X, Y, relu=w.is_gcn)
+            dg.spmm(plan, X, Y, relu=w.is_gcn, out_bf16=w.is_gcn)
             d.record(stream)
             torch.cuda.synchronize()
             if rep >= args.warmup:
@@ -178,8 +181,8 @@ def ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
                           "partition_ms": round(float(np.mean(part_ms)), 4),
                           "spmm_ms": round(ms, 4),
                           "spmm_ge_s": round(g.nnz * F_dom / (ms * 1e-3) / 1e9, 2),
-                          "spmm_hbm_frac_bmin": round(spmm_bytes(g.n, g.nnz, F_dom) / (ms * 1e-3)
-                                                      / (PEAK_HBM_GBS * 1e9), 4),
+                          "spmm_hbm_frac_bmin": round(spmm_bytes(g.n, g.nnz, F_dom, 2 if w.is_gcn else 4)
+                                                      / (ms * 1e-3) / (PEAK_HBM_GBS * 1e9), 4),
                           "walks_per_node": w.walks, "walk_len": w.steps}), flush=True)
 
 
@@ -242,19 +245,19 @@ def main():
     if args.mode == "spmm":
         plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
         Xs = torch.randn((g.n, F_dom), dtype=torch.float32, device=dev) if w.is_gcn else Xd
-        Ys = torch.empty_like(Xs)
+        Ys = torch.empty(Xs.shape, dtype=torch.bfloat16 if w.is_gcn else torch.float32, device=dev)
         times = []
         for _ in range(args.spmm_reps):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            dg.spmm(plan, Xs, Ys, relu=w.is_gcn)
+            dg.spmm(plan, Xs, Ys, relu=w.is_gcn, out_bf16=w.is_gcn)
             b.record(stream)
             times.append((a, b))
         torch.cuda.synchronize()
         ms = [a.elapsed_time(b) for a, b in times]
         print(json.dumps({"mode": "spmm", "config": w.name, "F": F_dom,
                           "ms": [round(x, 4) for x in ms],
-                          "bytes_min": spmm_bytes(g.n, g.nnz, F_dom)}), flush=True)
+                          "bytes_min": spmm_bytes(g.n, g.nnz, F_dom, 2 if w.is_gcn else 4)}), flush=True)
         plan.destroy()
         return
 
@@ -263,8 +266,11 @@ def main():
         ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
         return
     if w.is_gcn:
+        # every layer but the last writes its output in bfloat16: the next update rounds its
+        # input to bfloat16 anyway, so the final output is bit-identical (tested)
         Ts = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for _, fo in w.layers]
-        Hs = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for _, fo in w.layers]
+        Hs = [torch.empty((g.n, fo), dtype=torch.bfloat16 if li < len(w.layers) - 1 else torch.float32,
+                          device=dev) for li, (_, fo) in enumerate(w.layers)]
     else:
         Y = torch.empty_like(Xd)
     holder = {"plan": None}
@@ -306,9 +312,10 @@ def main():
                     dg.update(Hs[li - 1], Wd[li], Ts[li])
                     b.record(stream)
                     marks[f"update_{li + 1}"] = [(a, b)]
+                last = li == len(w.layers) - 1
                 a, b = ev(), ev()
                 a.record(stream)
-                dg.spmm(plan, Ts[li], Hs[li], relu=li < len(w.layers) - 1)
+                dg.spmm(plan, Ts[li], Hs[li], relu=not last, out_bf16=not last)
                 b.record(stream)
                 marks[f"spmm_{li + 1}_F{fout}"] = [(a, b)]
         else:
@@ -340,18 +347,19 @@ def main():
 
     ge_per_step = g.nnz * (sum(fo for _, fo in w.layers) if w.is_gcn else w.F)
     value = ge_per_step / (ms_per_step * 1e-3) / 1e9
-    bmin = spmm_bytes(g.n, g.nnz, F_dom)
+    ybytes = 2 if w.is_gcn else 4                    # the dominant SpMM of c5 writes bfloat16
+    bmin = spmm_bytes(g.n, g.nnz, F_dom, ybytes)
     achieved = bmin / (spmm_ms * 1e-3) / 1e9
     traffic, traffic_src = counter_traffic(w.name)
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-            "kernel": f"spmm_dual_kernel<{min(64, max(1, F_dom // 4))}, 4> "
-                      f"(F={F_dom}{', ReLU' if w.is_gcn else ''})",
+            "kernel": f"spmm_dual_kernel<{min(64, max(1, F_dom // 4))}, 4, {'true' if w.is_gcn else 'false'}> "
+                      f"(F={F_dom}{', ReLU, bfloat16 output' if w.is_gcn else ''})",
             "bytes_per_launch": bmin, "ms_per_launch": round(spmm_ms, 4),
             "launches_timed": len(phases[dom_key]),
             "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
             "gather_bytes_per_launch": 4 * (g.n + 1) + 8 * g.nnz + 4 * g.nnz * F_dom
-                                       + 4 * g.n * F_dom + 4 * g.n,
+                                       + ybytes * g.n * F_dom + 4 * g.n,
             "spmm_ge_s": round(g.nnz * F_dom / (spmm_ms * 1e-3) / 1e9, 2)}
     out = {
         "metric": METRIC,

@@ -151,32 +151,42 @@ int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, 
 
 /* ------------------------------------------------------------------ GCN layer */
 
-#define DUALGCN_RELU 1u
+/* Flags of the GCN-layer entry points. */
+#define DUALGCN_RELU 1u       /* act = ReLU (else the identity) */
+#define DUALGCN_OUT_BF16 2u   /* the output is stored as bfloat16: the nearest-even rounding of
+                                 the float32 result (2 bytes per element, same row-major layout) */
+#define DUALGCN_IN_BF16 4u    /* the input X of the update holds bfloat16 values */
 
 /*
  * dualgcn_spmm_act -- Y = act(A X): dualgcn_spmm with the activation of a GCN
  * layer applied to every output before it is stored (Sec. 1: a layer ends with
- * a non-linearity).  act is ReLU if `flags & DUALGCN_RELU`, else the identity;
- * other flag bits are DUALGCN_ERR_INVALID_ARG.  Same layout, summation and
- * errors as dualgcn_spmm.  Asynchronous.
+ * a non-linearity).  act is ReLU if `flags & DUALGCN_RELU`, else the identity.
+ * With DUALGCN_OUT_BF16, Y receives the bfloat16 rounding of each float32 output
+ * (after the activation): exactly what the next layer's update rounds its input
+ * to, so a layer chain through a bfloat16 intermediate gives bit-identical
+ * results with half the intermediate's bytes.  Other flag bits are
+ * DUALGCN_ERR_INVALID_ARG.  Same summation and errors as dualgcn_spmm.
+ * Asynchronous.
  */
-int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, float *Y, int32_t F,
+int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, void *Y, int32_t F,
                      uint32_t flags, void *stream);
 
 /*
  * dualgcn_update -- the update phase of a GCN layer alone, T = X W (Sec. 1: the
  * aggregated features are multiplied by a small dense weight matrix).
  *
- * X is float32 n x F_in row-major (16-byte aligned), W float32 F_in x F_out
- * row-major, T float32 n x F_out row-major, n >= 1.  Computed on the matrix
- * cores with X and W rounded to bfloat16 (nearest-even) and float32
+ * X is float32 n x F_in row-major (16-byte aligned) -- or bfloat16 when `flags`
+ * holds DUALGCN_IN_BF16 --, W float32 F_in x F_out row-major, T float32
+ * n x F_out row-major, n >= 1.  Computed on the matrix cores with X and W rounded
+ * to bfloat16 (nearest-even; bfloat16 X is used as stored) and float32
  * accumulation.  F_in and F_out must be multiples of 32 with F_in <= 1024 and
- * F_out <= 256 (else DUALGCN_ERR_UNSUPPORTED).  X and T must not overlap.  No
- * plan and no workspace: the update does not depend on the partition, so it may
- * run on another stream while dualgcn_partition works.  Asynchronous.
+ * F_out <= 256 (else DUALGCN_ERR_UNSUPPORTED).  X and T must not overlap; other
+ * flag bits are DUALGCN_ERR_INVALID_ARG.  No plan and no workspace: the update
+ * does not depend on the partition, so it may run on another stream while
+ * dualgcn_partition works.  Asynchronous.
  */
-int dualgcn_update(const float *X, const float *W, float *T, int32_t n, int32_t F_in,
-                   int32_t F_out, void *stream);
+int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F_in,
+                   int32_t F_out, uint32_t flags, void *stream);
 
 /* Bytes of device workspace dualgcn_gcn_layer needs (host-only, no device use):
  * room for the float32 n x F_out product T. */
@@ -187,13 +197,16 @@ int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t 
  * dualgcn_gcn_layer -- one GCN layer Y = act(A (X W)): dualgcn_update into the
  * workspace followed by dualgcn_spmm_act (Sec. 1: update, aggregation, no bias).
  *
- * X is float32 n x F_in row-major, W float32 F_in x F_out row-major, Y float32
- * n x F_out row-major; X and Y may be the same buffer.  `workspace` is
- * caller-owned device memory of at least dualgcn_gcn_layer_workspace() bytes,
- * 256-byte aligned, overlapping neither X nor Y (else DUALGCN_ERR_INVALID_ARG).
- * Shape limits as for dualgcn_update.  Asynchronous.
+ * X is n x F_in row-major (float32, or bfloat16 with DUALGCN_IN_BF16), W float32
+ * F_in x F_out row-major, Y n x F_out row-major (float32, or bfloat16 with
+ * DUALGCN_OUT_BF16); X and Y may be the same buffer.  flags: DUALGCN_RELU,
+ * DUALGCN_IN_BF16, DUALGCN_OUT_BF16 (others are DUALGCN_ERR_INVALID_ARG).
+ * `workspace` is caller-owned device memory of at least
+ * dualgcn_gcn_layer_workspace() bytes, 256-byte aligned, overlapping neither X
+ * nor Y (else DUALGCN_ERR_INVALID_ARG).  Shape limits as for dualgcn_update.
+ * Asynchronous.
  */
-int dualgcn_gcn_layer(const dualgcn_plan *plan, const float *X, const float *W, float *Y,
+int dualgcn_gcn_layer(const dualgcn_plan *plan, const void *X, const float *W, void *Y,
                       int32_t F_in, int32_t F_out, uint32_t flags, void *workspace,
                       size_t workspace_bytes, void *stream);
 

@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libdualgcn.so")
 OK, ERR_INVALID_ARG, ERR_BAD_CSR, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP, ERR_NO_DEVICE = \
     0, -1, -2, -3, -4, -5, -6
 FORCE_AUTO, FORCE_SPARSE, FORCE_DENSE = 0, 1, 2
-RELU = 1
+RELU, OUT_BF16, IN_BF16 = 1, 2, 4
 
 _FORCE = {"auto": FORCE_AUTO, "sparse": FORCE_SPARSE, "dense": FORCE_DENSE,
           FORCE_AUTO: FORCE_AUTO, FORCE_SPARSE: FORCE_SPARSE, FORCE_DENSE: FORCE_DENSE}
@@ -73,7 +73,7 @@ def _load():
         "dualgcn_plan_destroy": ([P], None),
         "dualgcn_spmm": ([P, P, P, I32, P], ctypes.c_int),
         "dualgcn_spmm_act": ([P, P, P, I32, U32, P], ctypes.c_int),
-        "dualgcn_update": ([P, P, P, I32, I32, I32, P], ctypes.c_int),
+        "dualgcn_update": ([P, P, P, I32, I32, I32, U32, P], ctypes.c_int),
         "dualgcn_gcn_layer_workspace": ([P, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "dualgcn_gcn_layer": ([P, P, P, P, I32, I32, U32, P, SZ, P], ctypes.c_int),
         "dualgcn_plan_query": ([P, ctypes.POINTER(PlanInfo)], ctypes.c_int),
@@ -179,18 +179,22 @@ class Plan:
             pass
 
 
-def spmm(plan, X, Y=None, relu=False, stream=None):
-    """Y = A X (or relu(A X)) on the plan's matrix.  X: float32 [n, F] on the device."""
+def spmm(plan, X, Y=None, relu=False, out_bf16=False, stream=None):
+    """Y = A X (or relu(A X)) on the plan's matrix.  X: float32 [n, F] on the device.
+
+    With out_bf16, Y is bfloat16: the nearest-even rounding of the float32 result."""
     _dev(X, torch.float32, "X")
     if X.dim() != 2 or X.shape[0] != plan.n:
         raise ValueError("X must be [n, F]")
+    ydt = torch.bfloat16 if out_bf16 else torch.float32
     if Y is None:
-        Y = torch.empty_like(X)
-    _dev(Y, torch.float32, "Y")
+        Y = torch.empty(X.shape, dtype=ydt, device=X.device)
+    _dev(Y, ydt, "Y")
     if Y.shape != X.shape:
         raise ValueError("Y must have X's shape")
-    if relu:
-        _check(_lib.dualgcn_spmm_act(plan.handle, X.data_ptr(), Y.data_ptr(), X.shape[1], RELU,
+    if relu or out_bf16:
+        flags = (RELU if relu else 0) | (OUT_BF16 if out_bf16 else 0)
+        _check(_lib.dualgcn_spmm_act(plan.handle, X.data_ptr(), Y.data_ptr(), X.shape[1], flags,
                                      _stream(stream)), "dualgcn_spmm_act")
     else:
         _check(_lib.dualgcn_spmm(plan.handle, X.data_ptr(), Y.data_ptr(), X.shape[1],
@@ -199,10 +203,13 @@ def spmm(plan, X, Y=None, relu=False, stream=None):
 
 
 def update(X, W, T=None, stream=None):
-    """T = X W on the bf16 matrix cores (float32 accumulation).  X: [n, F_in], W: [F_in, F_out].
+    """T = X W on the bf16 matrix cores (float32 accumulation).  X: [n, F_in] float32 or
+    bfloat16, W: [F_in, F_out] float32.
 
     Needs no plan: it may run on another stream while a partition is built."""
-    _dev(X, torch.float32, "X")
+    if not isinstance(X, torch.Tensor) or X.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("X must be a float32 or bfloat16 tensor")
+    _dev(X, X.dtype, "X")
     _dev(W, torch.float32, "W")
     F_in, F_out = W.shape
     if X.dim() != 2 or X.shape[1] != F_in:
@@ -213,7 +220,8 @@ def update(X, W, T=None, stream=None):
     _dev(T, torch.float32, "T")
     if T.shape != (n, F_out):
         raise ValueError("T must be [n, F_out]")
-    _check(_lib.dualgcn_update(X.data_ptr(), W.data_ptr(), T.data_ptr(), n, F_in, F_out,
+    flags = IN_BF16 if X.dtype == torch.bfloat16 else 0
+    _check(_lib.dualgcn_update(X.data_ptr(), W.data_ptr(), T.data_ptr(), n, F_in, F_out, flags,
                                _stream(stream)), "dualgcn_update")
     return T
 
@@ -225,22 +233,29 @@ def gcn_layer_workspace_bytes(plan, F_in, F_out):
     return nbytes.value
 
 
-def gcn_layer(plan, X, W, relu=False, Y=None, workspace=None, stream=None):
-    """Y = act(A (X W)) with X W on the bf16 matrix cores (float32 accumulation)."""
-    _dev(X, torch.float32, "X")
+def gcn_layer(plan, X, W, relu=False, Y=None, workspace=None, out_bf16=False, stream=None):
+    """Y = act(A (X W)) with X W on the bf16 matrix cores (float32 accumulation).
+
+    X may be float32 or bfloat16; with out_bf16 Y is the bfloat16 rounding of the result."""
+    if not isinstance(X, torch.Tensor) or X.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("X must be a float32 or bfloat16 tensor")
+    _dev(X, X.dtype, "X")
     _dev(W, torch.float32, "W")
     F_in, F_out = W.shape
     if X.shape != (plan.n, F_in):
         raise ValueError("X must be [n, F_in]")
+    ydt = torch.bfloat16 if out_bf16 else torch.float32
     if Y is None:
-        Y = torch.empty((plan.n, F_out), dtype=torch.float32, device=X.device)
-    _dev(Y, torch.float32, "Y")
+        Y = torch.empty((plan.n, F_out), dtype=ydt, device=X.device)
+    _dev(Y, ydt, "Y")
     need = gcn_layer_workspace_bytes(plan, F_in, F_out)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
     _dev(workspace, torch.uint8, "workspace")
+    flags = (RELU if relu else 0) | (IN_BF16 if X.dtype == torch.bfloat16 else 0) | \
+        (OUT_BF16 if out_bf16 else 0)
     _check(_lib.dualgcn_gcn_layer(plan.handle, X.data_ptr(), W.data_ptr(), Y.data_ptr(), F_in,
-                                  F_out, RELU if relu else 0, workspace.data_ptr(),
+                                  F_out, flags, workspace.data_ptr(),
                                   workspace.numel(), _stream(stream)), "dualgcn_gcn_layer")
     return Y
 
@@ -257,4 +272,4 @@ def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
 
 __all__ = ["Plan", "spmm", "update", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
            "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
-           "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU"]
+           "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16"]

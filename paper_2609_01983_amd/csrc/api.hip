@@ -168,7 +168,7 @@ bool overlaps(const void *a, size_t abytes, const void *b, size_t bbytes) {
 }
 
 // Shapes of the update phase T = X W handled by the matrix-core kernel.
-int check_update(const float *X, const float *W, const float *T, int32_t F_in, int32_t F_out) {
+int check_update(const void *X, const float *W, const void *T, int32_t F_in, int32_t F_out) {
     if (!X || !W || !T || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
     if (F_in % 32 || F_out % 32 || F_in > 1024 || F_out > 256) return DUALGCN_ERR_UNSUPPORTED;
     if (reinterpret_cast<uintptr_t>(X) % 16) return DUALGCN_ERR_INVALID_ARG;
@@ -226,42 +226,37 @@ void dualgcn_plan_destroy(dualgcn_plan *plan) {
 }
 
 int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, void *stream) {
-    int st = check_plan(plan);
-    if (st) return st;
-    if (!X || !Y || F < 1) return DUALGCN_ERR_INVALID_ARG;
-    if (F >= (1 << 20)) return DUALGCN_ERR_UNSUPPORTED;
-    const Plan *p = as_plan(plan);
-    const size_t bytes = static_cast<size_t>(p->n) * F * sizeof(float);
-    if (overlaps(X, bytes, Y, bytes)) return DUALGCN_ERR_INVALID_ARG;
-    if ((st = dgc::device_status())) return st;
-    return dgc::launch_spmm(*p, X, Y, F, false, static_cast<hipStream_t>(stream));
+    return dualgcn_spmm_act(plan, X, Y, F, 0u, stream);
 }
 
-int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, float *Y, int32_t F,
+int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, void *Y, int32_t F,
                      uint32_t flags, void *stream) {
     int st = check_plan(plan);
     if (st) return st;
     if (!X || !Y || F < 1) return DUALGCN_ERR_INVALID_ARG;
-    if (flags & ~DUALGCN_RELU) return DUALGCN_ERR_INVALID_ARG;
+    if (flags & ~(DUALGCN_RELU | DUALGCN_OUT_BF16)) return DUALGCN_ERR_INVALID_ARG;
     if (F >= (1 << 20)) return DUALGCN_ERR_UNSUPPORTED;
     const Plan *p = as_plan(plan);
-    const size_t bytes = static_cast<size_t>(p->n) * F * sizeof(float);
-    if (overlaps(X, bytes, Y, bytes)) return DUALGCN_ERR_INVALID_ARG;
+    const bool bf = (flags & DUALGCN_OUT_BF16) != 0;
+    const size_t elems = static_cast<size_t>(p->n) * F;
+    if (overlaps(X, elems * sizeof(float), Y, elems * (bf ? 2 : 4))) return DUALGCN_ERR_INVALID_ARG;
     if ((st = dgc::device_status())) return st;
-    return dgc::launch_spmm(*p, X, Y, F, (flags & DUALGCN_RELU) != 0,
+    return dgc::launch_spmm(*p, X, Y, F, (flags & DUALGCN_RELU) != 0, bf,
                             static_cast<hipStream_t>(stream));
 }
 
-int dualgcn_update(const float *X, const float *W, float *T, int32_t n, int32_t F_in,
-                   int32_t F_out, void *stream) {
+int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F_in,
+                   int32_t F_out, uint32_t flags, void *stream) {
     if (n < 1) return DUALGCN_ERR_INVALID_ARG;
     int st = check_update(X, W, T, F_in, F_out);
     if (st) return st;
+    if (flags & ~DUALGCN_IN_BF16) return DUALGCN_ERR_INVALID_ARG;
+    const bool bf = (flags & DUALGCN_IN_BF16) != 0;
     const size_t un = static_cast<size_t>(n);
-    if (overlaps(X, un * F_in * sizeof(float), T, un * F_out * sizeof(float)))
+    if (overlaps(X, un * F_in * (bf ? 2 : 4), T, un * F_out * sizeof(float)))
         return DUALGCN_ERR_INVALID_ARG;
     if ((st = dgc::device_status())) return st;
-    return dgc::launch_xw(X, W, T, n, F_in, F_out, static_cast<hipStream_t>(stream));
+    return dgc::launch_xw(X, bf, W, T, n, F_in, F_out, static_cast<hipStream_t>(stream));
 }
 
 int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,
@@ -273,24 +268,26 @@ int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t 
     return DUALGCN_OK;
 }
 
-int dualgcn_gcn_layer(const dualgcn_plan *plan, const float *X, const float *W, float *Y,
+int dualgcn_gcn_layer(const dualgcn_plan *plan, const void *X, const float *W, void *Y,
                       int32_t F_in, int32_t F_out, uint32_t flags, void *workspace,
                       size_t workspace_bytes, void *stream) {
     int st = check_plan(plan);
     if (st) return st;
     if (!Y || !workspace) return DUALGCN_ERR_INVALID_ARG;
     if ((st = check_update(X, W, Y, F_in, F_out))) return st;
-    if (flags & ~DUALGCN_RELU) return DUALGCN_ERR_INVALID_ARG;
+    if (flags & ~(DUALGCN_RELU | DUALGCN_IN_BF16 | DUALGCN_OUT_BF16)) return DUALGCN_ERR_INVALID_ARG;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return DUALGCN_ERR_INVALID_ARG;
     const Plan *p = as_plan(plan);
     const size_t ws = dgc::xw_workspace_bytes(p->n, F_out);
     if (workspace_bytes < ws) return DUALGCN_ERR_INVALID_ARG;
     const size_t n = static_cast<size_t>(p->n);
-    if (overlaps(X, n * F_in * sizeof(float), workspace, ws) ||
-        overlaps(Y, n * F_out * sizeof(float), workspace, ws))
+    const bool in_bf = (flags & DUALGCN_IN_BF16) != 0, out_bf = (flags & DUALGCN_OUT_BF16) != 0;
+    if (overlaps(X, n * F_in * (in_bf ? 2 : 4), workspace, ws) ||
+        overlaps(Y, n * F_out * (out_bf ? 2 : 4), workspace, ws))
         return DUALGCN_ERR_INVALID_ARG;
     if ((st = dgc::device_status())) return st;
-    return dgc::launch_gcn_layer(*p, X, W, Y, F_in, F_out, (flags & DUALGCN_RELU) != 0, workspace,
+    return dgc::launch_gcn_layer(*p, X, in_bf, W, Y, out_bf, F_in, F_out,
+                                 (flags & DUALGCN_RELU) != 0, workspace,
                                  static_cast<hipStream_t>(stream));
 }
 

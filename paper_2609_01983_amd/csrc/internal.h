@@ -111,18 +111,28 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                const dualgcn_thresholds &th, hipStream_t stream, Plan **out);
 void free_plan(Plan *p);
 
-// ---- SpMM (spmm.hip): Y = A X on one plan, optional ReLU on the result.
-int launch_spmm(const Plan &p, const float *X, float *Y, int32_t F, bool relu,
+// float32 -> bfloat16 bits, round to nearest even; NaNs stay NaN.
+__device__ __forceinline__ unsigned short to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return static_cast<unsigned short>((u >> 16) | 0x40u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return static_cast<unsigned short>(u >> 16);
+}
+
+// ---- SpMM (spmm.hip): Y = A X on one plan, optional ReLU on the result; with out_bf16
+// Y holds the bfloat16 rounding (nearest-even) of the float32 results.
+int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool out_bf16,
                 hipStream_t stream);
 
 // ---- update phase (xw.hip)
 // Bytes of the float32 T = X W buffer a layer keeps in its workspace (256-byte multiple).
 size_t xw_workspace_bytes(int32_t n, int32_t F_out);
-// T = bf16(X) bf16(W) with float32 accumulation.
-int launch_xw(const float *X, const float *W, float *T, int32_t n, int32_t F_in, int32_t F_out,
-              hipStream_t stream);
+// T = bf16(X) bf16(W) with float32 accumulation; X is float32, or bfloat16 if in_bf16.
+int launch_xw(const void *X, bool in_bf16, const float *W, float *T, int32_t n, int32_t F_in,
+              int32_t F_out, hipStream_t stream);
 // Y = act(A (X W)): launch_xw into the workspace, then launch_spmm.
-int launch_gcn_layer(const Plan &p, const float *X, const float *W, float *Y, int32_t F_in,
-                     int32_t F_out, bool relu, void *workspace, hipStream_t stream);
+int launch_gcn_layer(const Plan &p, const void *X, bool in_bf16, const float *W, void *Y,
+                     bool out_bf16, int32_t F_in, int32_t F_out, bool relu, void *workspace,
+                     hipStream_t stream);
 
 }  // namespace dgc

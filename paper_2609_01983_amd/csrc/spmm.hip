@@ -72,20 +72,37 @@ __device__ __forceinline__ void load_x(const float *__restrict__ p, float (&x)[V
     }
 }
 
-template <int VEC>
-__device__ __forceinline__ void store_y(float *__restrict__ p, const double (&s)[VEC], bool relu) {
+// Stores the rounded sums of one lane's VEC features at element offset `at` of Y
+// (float32, or bfloat16 rounded from the float32 value when BF).
+template <int VEC, bool BF>
+__device__ __forceinline__ void store_y(void *__restrict__ Y, int64_t at, const double (&s)[VEC],
+                                        bool relu) {
     float o[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
         o[j] = static_cast<float>(s[j]);
         if (relu) o[j] = o[j] > 0.f ? o[j] : 0.f;
     }
-    if constexpr (VEC == 4) {
-        const f32x4 v = {o[0], o[1], o[2], o[3]};
-        __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(p));
-    } else {
+    if constexpr (BF) {
+        unsigned short *p = static_cast<unsigned short *>(Y) + at;
+        if constexpr (VEC == 4) {
+            const uint2 v = make_uint2(static_cast<uint32_t>(to_bf16(o[0])) | (static_cast<uint32_t>(to_bf16(o[1])) << 16),
+                                       static_cast<uint32_t>(to_bf16(o[2])) | (static_cast<uint32_t>(to_bf16(o[3])) << 16));
+            __builtin_nontemporal_store(v.x, reinterpret_cast<uint32_t *>(p));
+            __builtin_nontemporal_store(v.y, reinterpret_cast<uint32_t *>(p) + 1);
+        } else {
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) __builtin_nontemporal_store(o[j], p + j);
+            for (int j = 0; j < VEC; ++j) __builtin_nontemporal_store(to_bf16(o[j]), p + j);
+        }
+    } else {
+        float *p = static_cast<float *>(Y) + at;
+        if constexpr (VEC == 4) {
+            const f32x4 v = {o[0], o[1], o[2], o[3]};
+            __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(p));
+        } else {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) __builtin_nontemporal_store(o[j], p + j);
+        }
     }
 }
 
@@ -99,7 +116,7 @@ struct Args {
     int32_t *counters;
     double *partials;
     const float *X;
-    float *Y;
+    void *Y;                    // float32, or bfloat16 when the kernel's BF is set
     int32_t n, n_sparse, n_tasks, n_parts, n_long;
     int32_t ld;                 // leading dimension of X and Y (= F)
     int32_t f0;                 // first feature of this launch window
@@ -190,7 +207,7 @@ __device__ __forceinline__ int32_t task_meta(const int32_t (&m)[N], int j, int g
     return __shfl(x, gbase + j % LPR, 64);
 }
 
-template <int LPR, int VEC>
+template <int LPR, int VEC, bool BF>
 __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
     constexpr int GPW = 64 / LPR;                 // lane groups per wavefront
     constexpr int SW = LPR * VEC;                 // features per slice
@@ -230,7 +247,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
 #pragma unroll
             for (int j = 0; j < VEC; ++j) tot[j] += static_cast<double>(acc[j]);
         }
-        if (fin) store_y<VEC>(a.Y + static_cast<int64_t>(a.perm[i]) * a.ld + f, tot, a.relu);
+        if (fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(a.perm[i]) * a.ld + f, tot, a.relu);
         return;
     }
     if (lb < a.nb_parts + a.nb_long) {
@@ -257,7 +274,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
         double tot[VEC];
         dense_row<LPR, VEC>(a, e0, e1, li, gw, gbase, f, fin, tot);
         if (part < 0) {
-            if (gw == 0 && fin) store_y<VEC>(a.Y + static_cast<int64_t>(a.perm[i]) * a.ld + f, tot, a.relu);
+            if (gw == 0 && fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(a.perm[i]) * a.ld + f, tot, a.relu);
             return;
         }
         double *pp = a.partials + static_cast<int64_t>(first) * kMaxSlice + (f - a.f0);
@@ -283,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
                 for (int j = 0; j < VEC; ++j)
                     s[j] += __hip_atomic_load(pp + static_cast<int64_t>(q) * kMaxSlice + j,
                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            store_y<VEC>(a.Y + static_cast<int64_t>(a.perm[i]) * a.ld + f, s, a.relu);
+            store_y<VEC, BF>(a.Y, static_cast<int64_t>(a.perm[i]) * a.ld + f, s, a.relu);
         }
         if (lane == 0) *counter = 0;          // ready for the next call on this plan
         return;
@@ -307,7 +324,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
         double z[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; ++j) z[j] = 0.0;
-        if (fin) store_y<VEC>(a.Y + static_cast<int64_t>(task_meta<LPR>(rout, 0, gbase)) * a.ld + f, z, a.relu);
+        if (fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(task_meta<LPR>(rout, 0, gbase)) * a.ld + f, z, a.relu);
         return;
     }
     int cur = 0;                              // every row of a task with entries is non-empty
@@ -335,7 +352,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
                     tot[j] += static_cast<double>(part[j]);
                     part[j] = 0.f;
                 }
-                if (fin) store_y<VEC>(a.Y + static_cast<int64_t>(cur_out) * a.ld + f, tot, a.relu);
+                if (fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(cur_out) * a.ld + f, tot, a.relu);
 #pragma unroll
                 for (int j = 0; j < VEC; ++j) tot[j] = 0.0;
                 if (++cur < m) {
@@ -353,7 +370,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
 }
 
 template <int LPR, int VEC>
-int launch_window(Args a, hipStream_t s) {
+int launch_window(Args a, bool bf, hipStream_t s) {
     constexpr int GPB = kThreads / LPR;       // sparse tasks per workgroup
     a.nb_parts = (a.n_parts + kWaves - 1) / kWaves;
     a.nb_long = (a.n_long + kWaves - 1) / kWaves;
@@ -362,14 +379,19 @@ int launch_window(Args a, hipStream_t s) {
     const int64_t blocks = (static_cast<int64_t>(a.nb_parts) + a.nb_dense + nb_sparse) * a.S;
     if (blocks == 0) return DUALGCN_OK;
     if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(kThreads), 0, s, a);
+    if (bf)
+        hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC, true>), dim3(static_cast<unsigned>(blocks)),
+                           dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC, false>), dim3(static_cast<unsigned>(blocks)),
+                           dim3(kThreads), 0, s, a);
     return hip_status(hipGetLastError());
 }
 
 }  // namespace
 
-int launch_spmm(const Plan &p, const float *X, float *Y, int32_t F, bool relu, hipStream_t s) {
+int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool bf,
+                hipStream_t s) {
     Args a{};
     a.pptr = p.pptr;
     a.pcol = p.pcol;
@@ -390,7 +412,7 @@ int launch_spmm(const Plan &p, const float *X, float *Y, int32_t F, bool relu, h
     a.relu = relu ? 1 : 0;
 
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
-                     (reinterpret_cast<uintptr_t>(Y) % 16 == 0) && (F % 4 == 0);
+                     (reinterpret_cast<uintptr_t>(Y) % (bf ? 8 : 16) == 0) && (F % 4 == 0);
     int st = DUALGCN_OK;
     for (int32_t f0 = 0; f0 < F && !st; f0 += kMaxSlice) {
         const int32_t w = F - f0 < kMaxSlice ? F - f0 : kMaxSlice;
@@ -399,17 +421,17 @@ int launch_spmm(const Plan &p, const float *X, float *Y, int32_t F, bool relu, h
         if (vec) {
             // whole rows: the smallest power-of-two lane group with 4 features per lane
             a.S = 1;
-            if (w <= 4) st = launch_window<1, 4>(a, s);
-            else if (w <= 8) st = launch_window<2, 4>(a, s);
-            else if (w <= 16) st = launch_window<4, 4>(a, s);
-            else if (w <= 32) st = launch_window<8, 4>(a, s);
-            else if (w <= 64) st = launch_window<16, 4>(a, s);
-            else if (w <= 128) st = launch_window<32, 4>(a, s);
-            else st = launch_window<64, 4>(a, s);
+            if (w <= 4) st = launch_window<1, 4>(a, bf, s);
+            else if (w <= 8) st = launch_window<2, 4>(a, bf, s);
+            else if (w <= 16) st = launch_window<4, 4>(a, bf, s);
+            else if (w <= 32) st = launch_window<8, 4>(a, bf, s);
+            else if (w <= 64) st = launch_window<16, 4>(a, bf, s);
+            else if (w <= 128) st = launch_window<32, 4>(a, bf, s);
+            else st = launch_window<64, 4>(a, bf, s);
         } else {
             // any other width or alignment: one feature per lane, 64-feature slices
             a.S = (w + 63) / 64;
-            st = launch_window<64, 1>(a, s);
+            st = launch_window<64, 1>(a, bf, s);
         }
     }
     return st;

@@ -1,7 +1,9 @@
 // Update phase T = X W of a GCN layer on the gfx950 matrix cores (DualGCN Sec. 1:
 // after aggregation a layer multiplies by a small dense weight matrix).
 //
-// X (n x F_in, float32) is rounded to bfloat16 (nearest-even) in registers, W is
+// X (n x F_in, float32) is rounded to bfloat16 (nearest-even) in registers -- or is
+// read as stored when it already holds bfloat16 (the output of a previous layer's
+// aggregation written in bfloat16: the same values this rounding would give) --, W is
 // rounded to bfloat16 while each workgroup stages its transpose in LDS, and
 // v_mfma_f32_16x16x32_bf16 accumulates in float32.  The product is memory-bound
 // (it reads 4 F_in and writes 4 F_out bytes per row for 2 F_in F_out flops, far
@@ -35,17 +37,44 @@ constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
 constexpr int kLdsElems = 32768;     // bf16 elements of W^T one workgroup stages (64 KiB)
 constexpr int kPad = 8;              // bf16 padding per LDS row (spreads LDS banks)
 
-// float32 -> bfloat16 bits, round to nearest even; NaNs stay NaN.
-__device__ __forceinline__ unsigned short to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return static_cast<unsigned short>((u >> 16) | 0x40u);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return static_cast<unsigned short>(u >> 16);
-}
+// The bfloat16 A fragment of a lane at k-step ks: eight consecutive k of row `arow`
+// (zeros past the last row), from float32 X rounded here or from bfloat16 X as stored.
+template <bool XBF>
+struct XFrag {
+    f32x4 lo, hi;      // float32 X
+    uint4 raw;         // bfloat16 X
+
+    __device__ __forceinline__ void load(const void *X, int64_t arow, bool ok, int F_in, int kk) {
+        if constexpr (XBF) {
+            raw = make_uint4(0u, 0u, 0u, 0u);
+            if (ok) raw = *reinterpret_cast<const uint4 *>(static_cast<const unsigned short *>(X) + arow * F_in + kk);
+        } else {
+            lo = f32x4{0.f, 0.f, 0.f, 0.f};
+            hi = lo;
+            if (ok) {
+                const float *xr = static_cast<const float *>(X) + arow * F_in + kk;
+                lo = *reinterpret_cast<const f32x4 *>(xr);
+                hi = *reinterpret_cast<const f32x4 *>(xr + 4);
+            }
+        }
+    }
+    __device__ __forceinline__ bf16x8 bf16() const {
+        if constexpr (XBF) {
+            return __builtin_bit_cast(bf16x8, raw);
+        } else {
+            u16x8 a16;
+            a16[0] = to_bf16(lo[0]); a16[1] = to_bf16(lo[1]);
+            a16[2] = to_bf16(lo[2]); a16[3] = to_bf16(lo[3]);
+            a16[4] = to_bf16(hi[0]); a16[5] = to_bf16(hi[1]);
+            a16[6] = to_bf16(hi[2]); a16[7] = to_bf16(hi[3]);
+            return __builtin_bit_cast(bf16x8, a16);
+        }
+    }
+};
 
 // T[:, c0 : c0 + 16 ntiles] = bf16(X) bf16(W[:, c0 : ..]) for every row tile; F_in % 32 == 0.
-template <int NTMAX>
-__global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const float *__restrict__ X,
+template <int NTMAX, bool XBF>
+__global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const void *__restrict__ X,
                                                            const float *__restrict__ W,
                                                            float *__restrict__ T, int32_t n,
                                                            int32_t F_in, int32_t F_out,
@@ -72,25 +101,12 @@ __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const float *__restri
         f32x4 acc[NTMAX];
 #pragma unroll
         for (int t = 0; t < NTMAX; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-        const float *xr = X + arow * F_in + kgrp * 8;
         // k-step ks + 1 is requested while the MFMAs of k-step ks run
-        f32x4 lo = f32x4{0.f, 0.f, 0.f, 0.f}, hi = lo;
-        if (arow_ok) {
-            lo = *reinterpret_cast<const f32x4 *>(xr);
-            hi = *reinterpret_cast<const f32x4 *>(xr + 4);
-        }
+        XFrag<XBF> cur, nxt;
+        cur.load(X, arow, arow_ok, F_in, kgrp * 8);
         for (int ks = 0; ks < ksteps; ++ks) {
-            f32x4 nlo = f32x4{0.f, 0.f, 0.f, 0.f}, nhi = nlo;
-            if (arow_ok && ks + 1 < ksteps) {
-                nlo = *reinterpret_cast<const f32x4 *>(xr + (ks + 1) * 32);
-                nhi = *reinterpret_cast<const f32x4 *>(xr + (ks + 1) * 32 + 4);
-            }
-            u16x8 a16;
-            a16[0] = to_bf16(lo[0]); a16[1] = to_bf16(lo[1]);
-            a16[2] = to_bf16(lo[2]); a16[3] = to_bf16(lo[3]);
-            a16[4] = to_bf16(hi[0]); a16[5] = to_bf16(hi[1]);
-            a16[6] = to_bf16(hi[2]); a16[7] = to_bf16(hi[3]);
-            const bf16x8 av = __builtin_bit_cast(bf16x8, a16);
+            nxt.load(X, arow, arow_ok && ks + 1 < ksteps, F_in, (ks + 1) * 32 + kgrp * 8);
+            const bf16x8 av = cur.bf16();
             const int kk = ks * 32 + kgrp * 8;
 #pragma unroll
             for (int t = 0; t < NTMAX; ++t) {
@@ -100,8 +116,7 @@ __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const float *__restri
                         av, __builtin_bit_cast(bf16x8, b16), acc[t], 0, 0, 0);
                 }
             }
-            lo = nlo;
-            hi = nhi;
+            cur = nxt;
         }
 #pragma unroll
         for (int t = 0; t < NTMAX; ++t) {
@@ -135,16 +150,16 @@ int allow_lds(const void *kernel, size_t bytes) {
                                           static_cast<int>(bytes)));
 }
 
-template <int NT>
-int launch_xw(const float *X, const float *W, float *T, int32_t n, int32_t F_in, int32_t F_out,
+template <int NT, bool XBF>
+int launch_xw(const void *X, const float *W, float *T, int32_t n, int32_t F_in, int32_t F_out,
               int c0, int ntiles, size_t lds, hipStream_t s) {
-    int st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<NT>), lds);
+    int st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<NT, XBF>), lds);
     if (st) return st;
     // workgroups per CU allowed by the LDS of one CU (160 KiB) and by 2048 threads per CU
     const int per_cu = std::max<int>(1, std::min<int>(2048 / kThreads, static_cast<int>((160 * 1024) / lds)));
     const int64_t tiles = (static_cast<int64_t>(n) + kRowsPerBlock - 1) / kRowsPerBlock;
     const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(tiles, static_cast<int64_t>(num_cus()) * per_cu));
-    hipLaunchKernelGGL((xw_mfma_kernel<NT>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
+    hipLaunchKernelGGL((xw_mfma_kernel<NT, XBF>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
                        lds, s, X, W, T, n, F_in, F_out, c0, ntiles);
     return hip_status(hipGetLastError());
 }
@@ -155,8 +170,8 @@ size_t xw_workspace_bytes(int32_t n, int32_t F_out) {
     return (static_cast<size_t>(n) * F_out * sizeof(float) + 255) / 256 * 256;
 }
 
-int launch_xw(const float *X, const float *W, float *T, int32_t n, int32_t F_in, int32_t F_out,
-              hipStream_t s) {
+int launch_xw(const void *X, bool in_bf16, const float *W, float *T, int32_t n, int32_t F_in,
+              int32_t F_out, hipStream_t s) {
     // column blocks whose W^T slice fits the LDS budget
     const int cb = std::min<int>(F_out, (kLdsElems / F_in) / 16 * 16);
     if (cb < 16) return DUALGCN_ERR_UNSUPPORTED;
@@ -165,20 +180,27 @@ int launch_xw(const float *X, const float *W, float *T, int32_t n, int32_t F_in,
         const int ntiles = width / 16;
         const size_t lds = static_cast<size_t>(width) * (F_in + kPad) * sizeof(unsigned short);
         int st;
-        if (ntiles <= 4) st = launch_xw<4>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
-        else if (ntiles <= 8) st = launch_xw<8>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
-        else st = launch_xw<16>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+        if (in_bf16) {
+            if (ntiles <= 4) st = launch_xw<4, true>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+            else if (ntiles <= 8) st = launch_xw<8, true>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+            else st = launch_xw<16, true>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+        } else {
+            if (ntiles <= 4) st = launch_xw<4, false>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+            else if (ntiles <= 8) st = launch_xw<8, false>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+            else st = launch_xw<16, false>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
+        }
         if (st) return st;
     }
     return DUALGCN_OK;
 }
 
-int launch_gcn_layer(const Plan &p, const float *X, const float *W, float *Y, int32_t F_in,
-                     int32_t F_out, bool relu, void *workspace, hipStream_t s) {
+int launch_gcn_layer(const Plan &p, const void *X, bool in_bf16, const float *W, void *Y,
+                     bool out_bf16, int32_t F_in, int32_t F_out, bool relu, void *workspace,
+                     hipStream_t s) {
     float *T = static_cast<float *>(workspace);
-    const int st = launch_xw(X, W, T, p.n, F_in, F_out, s);
+    const int st = launch_xw(X, in_bf16, W, T, p.n, F_in, F_out, s);
     if (st) return st;
-    return launch_spmm(p, T, Y, F_out, relu, s);
+    return launch_spmm(p, T, Y, F_out, relu, out_bf16, s);
 }
 
 }  // namespace dgc

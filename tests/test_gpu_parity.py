@@ -272,6 +272,54 @@ def test_update_alone(dg, device, fin, fout):
     assert np.max(np.abs(T - _bf16(X) @ _bf16(W)) / (BT + 1e-30)) < 1e-5
 
 
+def _bf16_t(t):
+    """torch float32 -> bfloat16 (nearest-even) -> float64 numpy, done with integer ops."""
+    return _bf16(t.cpu().numpy())
+
+
+@pytest.mark.parametrize("F", [128, 64, 16, 12])
+def test_spmm_bf16_output_is_rounded_fp32(dg, device, F):
+    """DUALGCN_OUT_BF16 stores exactly the nearest-even bfloat16 of the float32 result."""
+    g = small.random_graph(500, 0.03, seed=13)
+    X = torch.from_numpy(dense.features_normal(g.n, F, seed=F, stream_id=32)).to(device)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=8, walk_len=4)
+    for relu in (False, True):
+        Y32 = dg.spmm(plan, X, relu=relu)
+        Y16 = dg.spmm(plan, X, relu=relu, out_bf16=True)
+        assert Y16.dtype == torch.bfloat16
+        assert np.array_equal(Y16.float().cpu().numpy().astype(np.float64), _bf16_t(Y32))
+
+
+def test_update_bf16_input_is_the_rounding_of_fp32_input(dg, device):
+    X = dense.features_normal(777, 128, seed=5, stream_id=33)
+    W = dense.glorot(128, 64, seed=5, stream_id=34)
+    Xd, Wd = torch.from_numpy(X).to(device), torch.from_numpy(W).to(device)
+    T32 = dg.update(Xd, Wd)
+    T16 = dg.update(Xd.to(torch.bfloat16), Wd)       # torch's conversion is nearest-even too
+    assert torch.equal(T32, T16)
+
+
+def test_two_layers_through_bf16_intermediate_are_bit_identical(dg, device):
+    """Layer 1 writing its output in bfloat16 and layer 2 reading it gives the same bits as
+    the float32 intermediate, because the update rounds its input to bfloat16 anyway."""
+    g = configs.load_graph("c2")
+    X = torch.from_numpy(dense.features_normal(g.n, 256, seed=0, stream_id=27)).to(device)
+    W1 = torch.from_numpy(dense.glorot(256, 128, seed=0, stream_id=4)).to(device)
+    W2 = torch.from_numpy(dense.glorot(128, 64, seed=0, stream_id=5)).to(device)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=16, walk_len=5)
+    H32 = dg.gcn_layer(plan, X, W1, relu=True)
+    Y32 = dg.gcn_layer(plan, H32, W2)
+    H16 = dg.gcn_layer(plan, X, W1, relu=True, out_bf16=True)
+    Y16 = dg.gcn_layer(plan, H16, W2)
+    assert H16.dtype == torch.bfloat16 and torch.equal(H16.float(), H32.to(torch.bfloat16).float())
+    assert torch.equal(Y16, Y32)
+    # the split entry points give the same bits
+    T1 = dg.update(X, W1)
+    H = dg.spmm(plan, T1, relu=True, out_bf16=True)
+    Y = dg.spmm(plan, dg.update(H, W2))
+    assert torch.equal(Y, Y32)
+
+
 # ---------------------------------------------------------------- GCN layer (bf16 MFMA)
 
 @pytest.mark.parametrize("fin,fout", [(32, 32), (64, 32), (256, 128), (128, 64), (96, 160)])
