@@ -17,8 +17,6 @@ using u128 = unsigned __int128;
 constexpr int kDenseChunk = 4096;
 // Widest feature window one SpMM launch covers; wider F is processed in windows.
 constexpr int kMaxSlice = 256;
-// Feature slices of one window are at most this many (arrival counters per part).
-constexpr int kMaxSlices = 8;
 // Dense rows of at least 2^kLongRowOctave entries get a wavefront each; shorter dense
 // rows get one lane group each.
 constexpr int kLongRowOctave = 9;
@@ -28,7 +26,7 @@ constexpr int kTaskRows = 8;
 constexpr int kTaskEntries = 32;
 
 // One part of a split dense row: position of the row in the sorted order, part index,
-// number of parts, index of the row's first part (which owns the arrival counters).
+// number of parts, index of the row's first part.
 struct SplitPart {
     int32_t row;
     int32_t part;
@@ -66,7 +64,6 @@ struct Plan {
     int32_t n_split_rows = 0;
     int32_t n_split_parts = 0;
     SplitPart *parts = nullptr;        // [n_split_parts]
-    int32_t *counters = nullptr;       // [n_split_parts][kMaxSlices] arrival counters (zero between calls)
     double *partials = nullptr;        // [n_split_parts][kMaxSlice]
 
     uint64_t kstar = 0, kmax = 0;

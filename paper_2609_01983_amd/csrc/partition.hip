@@ -708,7 +708,6 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_pcol = lp.take(sizeof(int32_t) * unnz), o_pval = lp.take(sizeof(float) * unnz),
                  o_tasks = lp.take(sizeof(int32_t) * (un + 1)),
                  o_parts = lp.take(sizeof(SplitPart) * max_parts),
-                 o_cnt = lp.take(sizeof(int32_t) * max_parts * kMaxSlices),
                  o_partials = lp.take(sizeof(double) * max_parts * kMaxSlice);
     const size_t o_flags = ls.take(2 * sizeof(int32_t)), o_mom = ls.take(sizeof(Moments) * nb_keys),
                  o_sum = ls.take(sizeof(Summary)), o_kb0 = ls.take(sizeof(uint64_t) * un),
@@ -733,7 +732,6 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     p->pval = reinterpret_cast<float *>(pm + o_pval);
     p->tasks = reinterpret_cast<int32_t *>(pm + o_tasks);
     p->parts = reinterpret_cast<SplitPart *>(pm + o_parts);
-    p->counters = reinterpret_cast<int32_t *>(pm + o_cnt);
     p->partials = reinterpret_cast<double *>(pm + o_partials);
     int32_t *bad = reinterpret_cast<int32_t *>(sm + o_flags);
     Moments *moments = reinterpret_cast<Moments *>(sm + o_mom);
@@ -750,8 +748,6 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     int32_t *blockmax = reinterpret_cast<int32_t *>(sm + o_bmax);
 
     if ((st = hip_status(hipMemsetAsync(bad, 0, 2 * sizeof(int32_t), s)))) return st;
-    if ((st = hip_status(hipMemsetAsync(p->counters, 0, sizeof(int32_t) * max_parts * kMaxSlices, s))))
-        return st;
     if ((st = validate_csr(csr, bad, nodeinfo, blockmax, s))) return st;
     // walks: the lockstep walker where it applies, else one walk per lane
     st = launch_density(nodeinfo, csr->col, n, seed, k, d, p->S, bad, s);

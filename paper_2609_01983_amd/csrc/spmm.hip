@@ -35,10 +35,12 @@
 // row gets a wavefront whose groups take rounds of the row in turn and are summed
 // with a butterfly over the lanes; a dense row shorter than 2^kLongRowOctave
 // entries gets one lane group, which fills its rounds better (measured: the SBM
-// workload's dense rows of 100-250 entries run 9% faster than with a wavefront).  A split row's parts each write a
-// float64 partial; the last part to arrive (integer counter per row and slice)
-// sums them in part order, writes the row and clears its counter.  No
-// floating-point atomics: Y is bit-reproducible.
+// workload's dense rows of 100-250 entries run 9% faster than with a wavefront).
+// A split row's parts each write a float64 partial, and a small second kernel
+// sums them in part order and writes the row.  The kernel boundary makes the
+// partials visible: a fence inside the SpMM would write back and invalidate the
+// XCD's L2 once per part, which the gathers live on.  No floating-point atomics:
+// Y is bit-reproducible.
 //
 // Sparse path (tasks): the group walks the task's entries as one stream, so even
 // rows with one or two entries share a round of kRound gathers; a row is written
@@ -113,7 +115,6 @@ struct Args {
     const int32_t *perm;        // output row of each sorted row (the plan's order)
     const int32_t *tasks;
     const SplitPart *parts;
-    int32_t *counters;
     double *partials;
     const float *X;
     void *Y;                    // float32, or bfloat16 when the kernel's BF is set
@@ -254,13 +255,12 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
         // ---------------- dense path, long rows: one wavefront per row or per part of a split row
         const int w = lb * kWaves + wave;
         int32_t i, e0, e1;
-        int part = -1, nparts = 1, first = 0;
+        int part = -1, first = 0;
         if (lb < a.nb_parts) {
             if (w >= a.n_parts) return;
             const SplitPart sp = a.parts[a.n_parts - 1 - w];
             i = sp.row;
             part = sp.part;
-            nparts = sp.nparts;
             first = sp.first;
             e0 = a.pptr[i] + part * kDenseChunk;
             e1 = min(e0 + kDenseChunk, a.pptr[i + 1]);
@@ -277,32 +277,12 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
             if (gw == 0 && fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(a.perm[i]) * a.ld + f, tot, a.relu);
             return;
         }
-        double *pp = a.partials + static_cast<int64_t>(first) * kMaxSlice + (f - a.f0);
+        // a part of a split row: its float64 partial, summed by combine_kernel after this launch
         if (gw == 0 && fin) {
+            double *pp = a.partials + static_cast<int64_t>(first + part) * kMaxSlice + (f - a.f0);
 #pragma unroll
-            for (int j = 0; j < VEC; ++j)
-                __hip_atomic_store(pp + static_cast<int64_t>(part) * kMaxSlice + j, tot[j],
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (int j = 0; j < VEC; ++j) pp[j] = tot[j];
         }
-        __threadfence();      // publish this part before counting it
-        int32_t *counter = a.counters + static_cast<int64_t>(first) * kMaxSlices + slice;
-        int last = 0;
-        if (lane == 0) last = atomicAdd(counter, 1) == nparts - 1;
-        last = __shfl(last, 0, 64);
-        if (!last) return;
-        __threadfence();      // see every other part
-        if (gw == 0 && fin) {
-            double s[VEC];
-#pragma unroll
-            for (int j = 0; j < VEC; ++j) s[j] = 0.0;
-            for (int q = 0; q < nparts; ++q)
-#pragma unroll
-                for (int j = 0; j < VEC; ++j)
-                    s[j] += __hip_atomic_load(pp + static_cast<int64_t>(q) * kMaxSlice + j,
-                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            store_y<VEC, BF>(a.Y, static_cast<int64_t>(a.perm[i]) * a.ld + f, s, a.relu);
-        }
-        if (lane == 0) *counter = 0;          // ready for the next call on this plan
         return;
     }
 
@@ -369,6 +349,22 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
     }
 }
 
+// The rows split into parts: row = the sum of its parts' float64 partials, in part order.
+// One workgroup per part; only a row's first part does the work (a kernel boundary after
+// the SpMM makes every partial visible, so no fence or counter is needed).
+template <bool BF>
+__global__ __launch_bounds__(kThreads) void combine_kernel(const Args a) {
+    const SplitPart sp = a.parts[blockIdx.x];
+    if (sp.part != 0) return;
+    const int t = static_cast<int>(threadIdx.x);
+    const int f = a.f0 + t;
+    if (f >= a.fend) return;
+    const double *pp = a.partials + static_cast<int64_t>(sp.first) * kMaxSlice + t;
+    double s[1] = {0.0};
+    for (int q = 0; q < sp.nparts; ++q) s[0] += pp[static_cast<int64_t>(q) * kMaxSlice];
+    store_y<1, BF>(a.Y, static_cast<int64_t>(a.perm[sp.row]) * a.ld + f, s, a.relu);
+}
+
 template <int LPR, int VEC>
 int launch_window(Args a, bool bf, hipStream_t s) {
     constexpr int GPB = kThreads / LPR;       // sparse tasks per workgroup
@@ -385,6 +381,14 @@ int launch_window(Args a, bool bf, hipStream_t s) {
     else
         hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC, false>), dim3(static_cast<unsigned>(blocks)),
                            dim3(kThreads), 0, s, a);
+    if (a.n_parts > 0) {
+        if (bf)
+            hipLaunchKernelGGL((combine_kernel<true>), dim3(static_cast<unsigned>(a.n_parts)),
+                               dim3(kThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL((combine_kernel<false>), dim3(static_cast<unsigned>(a.n_parts)),
+                               dim3(kThreads), 0, s, a);
+    }
     return hip_status(hipGetLastError());
 }
 
@@ -399,7 +403,6 @@ int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bo
     a.perm = p.order;
     a.tasks = p.tasks;
     a.parts = p.parts;
-    a.counters = p.counters;
     a.partials = p.partials;
     a.X = X;
     a.Y = Y;
