@@ -440,32 +440,39 @@ __device__ __forceinline__ int32_t row_of(const P &ptr, int32_t lo, int32_t hi, 
 
 constexpr int kCopyTile = 4096;     // entries of the sorted copy one workgroup fills
 
+// tile_row[t] = the sorted row that holds entry t kCopyTile (for every tile start below nnz):
+// each non-empty row writes the tiles that start inside it.
+__global__ __launch_bounds__(kThreads) void tile_row_kernel(const int32_t *__restrict__ pptr,
+                                                            int32_t n, int32_t *__restrict__ tile_row) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int64_t b = pptr[i], e = pptr[i + 1];
+    for (int64_t t = (b + kCopyTile - 1) / kCopyTile; t * kCopyTile < e; ++t)
+        tile_row[t] = static_cast<int32_t>(i);
+}
+
 // Fills entries [b kCopyTile, (b + 1) kCopyTile) of the sorted copy: entry e of sorted
-// row i is entry e - pptr[i] of row order[i].  The tile's rows are located once, their
-// pointers staged in LDS, and every thread copies the entries e = tile start + t +
-// 256 k (writes are coalesced; reads are coalesced inside a row).
+// row i is entry e - pptr[i] of row order[i].  The tile's rows come from tile_row and have
+// their pointers staged in LDS; thread t copies entries e0 + t + 256 k, so reads inside a
+// row and all writes are coalesced, and finds each entry's row by binary search in LDS.
 __global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
     const int32_t *__restrict__ order, const int32_t *__restrict__ rowptr,
     const int32_t *__restrict__ col, const float *__restrict__ val,
-    const int32_t *__restrict__ pptr, int32_t n, int64_t nnz, int32_t *__restrict__ pcol,
-    float *__restrict__ pval) {
-    __shared__ int32_t sh_ptr[kCopyTile + 1];
-    __shared__ int32_t sh_src[kCopyTile];
-    __shared__ int32_t sh_rows[2];
+    const int32_t *__restrict__ pptr, const int32_t *__restrict__ tile_row, int32_t n,
+    int64_t nnz, int32_t *__restrict__ pcol, float *__restrict__ pval) {
+    __shared__ int32_t sh_ptr[kCopyTile + 2];
+    __shared__ int32_t sh_src[kCopyTile + 1];
     const int64_t e0 = static_cast<int64_t>(blockIdx.x) * kCopyTile;
     const int64_t e1 = e0 + kCopyTile < nnz ? e0 + kCopyTile : nnz;
-    if (threadIdx.x == 0) {
-        sh_rows[0] = row_of(pptr, 0, n - 1, e0);
-        sh_rows[1] = row_of(pptr, sh_rows[0], n - 1, e1 - 1);
-    }
-    __syncthreads();
-    const int32_t r_lo = sh_rows[0], r_hi = sh_rows[1];
+    const int32_t r_lo = tile_row[blockIdx.x];
+    const int32_t r_hi = e1 < nnz ? tile_row[blockIdx.x + 1] : n - 1;   // holds e1 or the end
     const int32_t rows = r_hi - r_lo + 1;
-    if (rows <= kCopyTile) {
+    if (rows <= kCopyTile + 1) {
         for (int32_t k = threadIdx.x; k < rows; k += kThreads) {
             sh_ptr[k] = pptr[r_lo + k];
             sh_src[k] = rowptr[order[r_lo + k]];
         }
+        if (threadIdx.x == 0) sh_ptr[rows] = pptr[r_lo + rows];
         __syncthreads();
         for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) {
             const int32_t k = row_of(sh_ptr, 0, rows - 1, e);
@@ -715,6 +722,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_scan = ls.take(sizeof(uint32_t) * static_cast<size_t>(scan_tiles)),
                  o_hist = ls.take(sizeof(uint32_t) * kRadix * static_cast<size_t>(nblocks)),
                  o_ssum = ls.take(sizeof(SplitSummary)), o_counts = ls.take(sizeof(uint32_t) * 2 * un),
+                 o_tiles = ls.take(sizeof(int32_t) * (unnz / kCopyTile + 2)),
                  o_info = ls.take(sizeof(int2) * un),
                  o_bmax = ls.take(sizeof(int32_t) * kValidateBlocks);
     if ((st = alloc_block(&p->mem, &p->mem_bytes, lp.bytes))) return st;
@@ -848,8 +856,11 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if ((st = exclusive_scan(pptr_u, static_cast<int64_t>(n) + 1, scan_sums, nullptr, s))) return st;
     if (nnz > 0) {
         const unsigned grid_e = static_cast<unsigned>((nnz + kCopyTile - 1) / kCopyTile);
+        int32_t *tile_row = reinterpret_cast<int32_t *>(sm + o_tiles);
+        hipLaunchKernelGGL(tile_row_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, tile_row);
         hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_e), dim3(kThreads), 0, s, p->order,
-                           csr->rowptr, csr->col, csr->val, p->pptr, n, nnz, p->pcol, p->pval);
+                           csr->rowptr, csr->col, csr->val, p->pptr, tile_row, n, nnz, p->pcol,
+                           p->pval);
     }
     hipLaunchKernelGGL(task_flag_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt,
                        off);
