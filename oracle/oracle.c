@@ -23,11 +23,13 @@
  *                      its magnitude bound |x_i| |W|.
  *
  * Random stream of a walk (the paper does not say how a neighbour is drawn):
- * walk w of node v takes, at step s (0-based), 64-bit word (s mod 4) of the
- * Philox block with counter (v, w, floor(s/4), 0) and key (seed, 0); the
- * neighbour is entry floor(r * deg / 2^64) of the current row, i.e. uniform
- * over the row's entries as stored (self-loops and duplicates included).  A
- * row with no entries keeps the walk in place.
+ * walk w of node v takes, at step s (0-based), the 32-bit half r of 64-bit
+ * word floor(s/2) mod 4 of the Philox block with counter (v, w, floor(s/8), 0)
+ * and key (seed, 0) -- the low half for even s, the high half for odd s --;
+ * the neighbour is entry floor(r * deg / 2^32) of the current row, i.e.
+ * uniform over the row's entries as stored (self-loops and duplicates
+ * included).  One block serves eight steps.  A row with no entries keeps the
+ * walk in place.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -72,12 +74,10 @@ void philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]
     out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
 }
 
-/* floor(r * m / 2^64): maps a uniform 64-bit word onto [0, m). */
-static uint64_t scale_word(uint64_t r, uint64_t m)
+/* floor(r * m / 2^32): maps a uniform 32-bit word onto [0, m), m < 2^32. */
+static uint64_t scale_half(uint32_t r, uint64_t m)
 {
-    uint64_t hi, lo;
-    mul_hi_lo(r, m, &hi, &lo);
-    return hi;
+    return ((uint64_t)r * m) >> 32;
 }
 
 /* ---------------- anonymous random walks (Sec. 3.2) ---------------- */
@@ -105,15 +105,16 @@ uint32_t oracle_walk(const int32_t *rowptr, const int32_t *col, int32_t n,
     uint64_t key[2] = {seed, 0};
     uint64_t block[4] = {0, 0, 0, 0};
     for (uint32_t s = 0; s < steps; ++s) {
-        if (s % 4 == 0) {
-            uint64_t ctr[4] = {(uint64_t)(uint32_t)start, walk, s / 4, 0};
+        if (s % 8 == 0) {
+            uint64_t ctr[4] = {(uint64_t)(uint32_t)start, walk, s / 8, 0};
             philox4x64_10(ctr, key, block);
         }
-        uint64_t r = block[s % 4];
+        uint64_t word = block[(s / 2) % 4];
+        uint32_t r = (s % 2 == 0) ? (uint32_t)(word & 0xFFFFFFFFu) : (uint32_t)(word >> 32);
         int64_t deg = (int64_t)rowptr[cur + 1] - rowptr[cur];
         int32_t next = cur;
         if (deg > 0)
-            next = col[rowptr[cur] + (int64_t)scale_word(r, (uint64_t)deg)];
+            next = col[rowptr[cur] + (int64_t)scale_half(r, (uint64_t)deg)];
         uint32_t label = 0;
         for (uint32_t i = 0; i < distinct; ++i)
             if (seen[i] == next) { label = i + 1; break; }

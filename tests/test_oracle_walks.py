@@ -209,15 +209,17 @@ def test_neighbour_choice_is_uniform_over_row_entries():
 
 
 def test_walk_counter_layout():
-    """Step s of walk w from v uses word s mod 4 of Philox block (v, w, s div 4, 0), key (seed, 0)."""
+    """Step s of walk w from v uses the 32-bit half (low for even s) of word (s div 2) mod 4 of
+    Philox block (v, w, s div 8, 0), key (seed, 0); the blocks come from numpy's Philox."""
     g = small.clique(9)                       # 8 neighbours per row, no self-loops
-    seed, v, w, d = 77, 3, 5, 6
+    seed, v, w, d = 77, 3, 5, 19              # three blocks, odd and even steps
     lab = oracle.walk(g, v, w, seed, d)
     cur, seen, expect = v, [v], [1]
     for s in range(d):
-        word = oracle.philox([v, w, s // 4, 0], [seed, 0])[s % 4]
+        word = int(_numpy_block([v, w, s // 8, 0], [seed, 0])[(s // 2) % 4])
+        half = (word >> (32 * (s % 2))) & 0xFFFFFFFF
         row = g.col[g.rowptr[cur]:g.rowptr[cur + 1]]
-        idx = (int(word) * len(row)) >> 64
+        idx = (half * len(row)) >> 32
         cur = int(row[idx])
         if cur not in seen:
             seen.append(cur)
