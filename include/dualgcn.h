@@ -101,9 +101,10 @@ typedef struct dualgcn_plan dualgcn_plan;
  * For every node v, `walks_per_node` (k) anonymous random walks of `walk_len`
  * (d) steps give S_v = sum over the walks of the number of distinct nodes seen
  * (start included), so the neighbour density of Theorem 1 is N_v = S_v / k.
- * A step moves to entry floor(r * deg / 2^64) of the current CSR row, r being
- * 64-bit word (s mod 4) of Philox-4x64-10 (Salmon et al., SC'11) with counter
- * (v, w, floor(s / 4), 0) and key (seed, 0); an empty row keeps the walk in place.
+ * A step moves to entry floor(r * deg / 2^32) of the current CSR row, r being
+ * the 32-bit half (low for even s, high for odd s) of 64-bit word floor(s/2) mod 4
+ * of Philox-4x64-10 (Salmon et al., SC'11) with counter (v, w, floor(s / 8), 0)
+ * and key (seed, 0); an empty row keeps the walk in place.
  * D_v is the row length.  With alpha = p/q the hybrid metric is kept as the
  * exact integer K_v = q k H_v = p S_v + (q - p) k D_v.  The threshold key K* is
  * the least integer with K* >= mu_K + beta sigma_K (population statistics over

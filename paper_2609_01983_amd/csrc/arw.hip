@@ -12,11 +12,13 @@
 // written with one plain store; otherwise each lane adds its count with an
 // integer atomic (order-independent, hence exact).
 //
-// Random stream: step s of walk w from v uses 64-bit word (s mod 4) of the
-// Philox-4x64-10 block (Salmon, Moraes, Dror & Shaw, SC'11) with counter
-// (v, w, floor(s/4), 0) and key (seed, 0).  The neighbour is entry
-// floor(r * deg / 2^64) of the current row (uniform over stored entries); an
-// empty row keeps the walk in place.
+// Random stream: step s of walk w from v uses the 32-bit half r (low for even s,
+// high for odd s) of 64-bit word floor(s/2) mod 4 of the Philox-4x64-10 block
+// (Salmon, Moraes, Dror & Shaw, SC'11) with counter (v, w, floor(s/8), 0) and key
+// (seed, 0); one block serves eight steps.  The neighbour is entry
+// floor(r * deg / 2^32) of the current row (uniform over stored entries); an
+// empty row keeps the walk in place.  The 64-bit products of the Philox rounds
+// dominate the walk kernel, so halving the blocks per walk halves its time.
 #include "internal.h"
 
 namespace dgc {
@@ -31,6 +33,12 @@ constexpr uint64_t kPhiloxW1 = 0xBB67AE8584CAA73Bull;
 struct Block4 {
     uint64_t w[4];
 };
+
+// The 32-bit half of the block spent on step s (s is a compile-time index after unrolling).
+__device__ __forceinline__ uint32_t half_word(const Block4 &b, int s) {
+    const uint64_t word = b.w[(s >> 1) & 3];
+    return (s & 1) ? static_cast<uint32_t>(word >> 32) : static_cast<uint32_t>(word);
+}
 
 __device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2,
                                                 uint64_t c3, uint64_t k0, uint64_t k1) {
@@ -73,12 +81,12 @@ __device__ __forceinline__ uint32_t walk_one(const int32_t *__restrict__ rowptr,
 #pragma unroll kUnrollSteps
     for (int s = 0; s < MAXD; ++s) {
         if (static_cast<uint32_t>(s) >= d) break;
-        if ((s & 3) == 0) blk = philox4x64_10(v, w, static_cast<uint64_t>(s >> 2), 0, seed, 0);
-        const uint64_t r = blk.w[s & 3];
+        if ((s & 7) == 0) blk = philox4x64_10(v, w, static_cast<uint64_t>(s >> 3), 0, seed, 0);
+        const uint32_t r = half_word(blk, s);
         const int32_t b = rowptr[cur];
         const int32_t e = rowptr[cur + 1];
         int32_t nxt = cur;
-        if (e > b) nxt = col[b + static_cast<int32_t>(__umul64hi(r, static_cast<uint64_t>(e - b)))];
+        if (e > b) nxt = col[b + static_cast<int32_t>(__umulhi(r, static_cast<uint32_t>(e - b)))];
         uint8_t label = 0;
 #pragma unroll kUnrollSteps
         for (int i = 0; i <= s; ++i)
@@ -122,7 +130,7 @@ __device__ __forceinline__ void walk_lockstep(const int2 *__restrict__ nodeinfo,
         for (int j = 0; j < WPL; ++j) {
             ni[j] = make_int2(0, 0);
             if (live[j]) {
-                if ((s & 3) == 0) blk[j] = philox4x64_10(v, w0 + j, static_cast<uint64_t>(s >> 2), 0, seed, 0);
+                if ((s & 7) == 0) blk[j] = philox4x64_10(v, w0 + j, static_cast<uint64_t>(s >> 3), 0, seed, 0);
                 ni[j] = nodeinfo[cur[j]];
             }
         }
@@ -131,8 +139,8 @@ __device__ __forceinline__ void walk_lockstep(const int2 *__restrict__ nodeinfo,
         for (int j = 0; j < WPL; ++j) {
             nxt[j] = cur[j];
             if (live[j] && ni[j].y > 0) {
-                const uint64_t r = blk[j].w[s & 3];
-                nxt[j] = col[ni[j].x + static_cast<int32_t>(__umul64hi(r, static_cast<uint64_t>(ni[j].y)))];
+                const uint32_t r = half_word(blk[j], s);
+                nxt[j] = col[ni[j].x + static_cast<int32_t>(__umulhi(r, static_cast<uint32_t>(ni[j].y)))];
             }
         }
 #pragma unroll
