@@ -11,6 +11,8 @@ Pieces and the passages they follow (DualGCN paper):
 * degree -- Sec. 3.2 "Node Degree": the row length read from the row pointers.
 * hybrid metric -- Sec. 3.2: H_v = alpha N_v + (1 - alpha) D_v.  With
   alpha = p/q this is kept as the exact integer K_v = q k H_v = p S_v + (q-p) k D_v.
+  The adaptive alpha (Sec. 3.2, "Time Complexity") is Var(N) / (Var(N) + Var(D)),
+  rounded down to a multiple of 1/q.
 * threshold and mode -- Sec. 3.3 Eq. (1): dense iff H_v >= tau with
   tau = mu_H + 0.5 sigma_H (population statistics over all nodes).  Evaluated
   exactly with Python integers: H >= mu + (b/c) sigma  <=>  c (n K - S1) >= b sqrt(V)
@@ -135,6 +137,28 @@ def hybrid_keys(S, D, k, alpha=(1, 2)):
     return K
 
 
+ALPHA_ADAPTIVE = 0xFFFFFFFF   # alpha numerator that asks for the adaptive weight
+
+
+def adaptive_alpha(S, D, k, q):
+    """Adaptive alpha = p/q (Sec. 3.2, "Time Complexity and Overhead Analysis": alpha
+    follows a variance analysis and defaults to 1/2; the paper states no formula).
+
+    Reading: each metric gets its share of the total spread,
+    alpha = Var(N) / (Var(N) + Var(D)) with N_v = S_v / k and population variances
+    over all nodes, and 1/2 when neither metric varies.  Exact in integers: with
+    V_X = n sum X^2 - (sum X)^2 (n^2 times the variance), Var(N) / Var(D) =
+    V_S / (k^2 V_D), so p = floor(q V_S / (V_S + k^2 V_D)).
+    """
+    S = [int(x) for x in np.asarray(S).ravel()]
+    D = [int(x) for x in np.asarray(D).ravel()]
+    n = len(S)
+    VS = n * sum(x * x for x in S) - sum(S) ** 2
+    VD = n * sum(x * x for x in D) - sum(D) ** 2
+    den = VS + k * k * VD
+    return q // 2 if den == 0 else q * VS // den
+
+
 def moments(K):
     """(S1, S2) = (sum K, sum K^2) as exact Python integers."""
     values, counts = np.unique(np.asarray(K, dtype=np.uint64), return_counts=True)
@@ -167,10 +191,15 @@ def threshold_key(n, S1, S2, beta=(1, 2)):
 
 
 def partition(g, seed, k, steps, alpha=(1, 2), beta=(1, 2), force=FORCE_AUTO, S=None):
-    """The whole plan: S, K, K*, dense flags, perm (sorted by (K, v)) and n_sparse."""
+    """The whole plan: S, K, K*, dense flags, perm (sorted by (K, v)) and n_sparse.
+
+    alpha = (ALPHA_ADAPTIVE, q) takes the adaptive weight p/q; the alpha used is
+    returned under "alpha"."""
     if S is None:
         S = density_sums(g, seed, k, steps)
     D = degrees(g)
+    if alpha[0] == ALPHA_ADAPTIVE:
+        alpha = (adaptive_alpha(S, D, k, alpha[1]), alpha[1])
     K = hybrid_keys(S, D, k, alpha)
     n = g.n
     S1, S2 = moments(K)
@@ -186,7 +215,7 @@ def partition(g, seed, k, steps, alpha=(1, 2), beta=(1, 2), force=FORCE_AUTO, S=
     else:
         n_sparse = int(n - dense.sum())
     return dict(S=S, D=D, K=K, S1=S1, S2=S2, kstar=kstar, dense=dense, perm=perm,
-                n_sparse=n_sparse)
+                n_sparse=n_sparse, alpha=alpha)
 
 
 # ------------------------------------------------------------------ SpMM (Sec. 1, 2.1)

@@ -113,3 +113,86 @@ def test_c1_plan_invariants_and_moments():
     assert 0 < P["n_sparse"] < g.n
     S = P["S"]
     assert np.all(S >= 8) and np.all(S <= 8 * 5)        # 1 <= distinct <= d+1 per walk
+
+
+# ---------------------------------------------------------------- adaptive alpha
+# The adaptive weight is alpha = Var(N) / (Var(N) + Var(D)) (population variances,
+# N = S / k), 1/2 when neither varies.  Graphs whose walks are deterministic (every
+# row has at most one entry) fix N and D by hand, independently of the walk stream.
+
+def _pairs_and_empties(pairs, empties):
+    """`pairs` 2-cycles u <-> v (one entry per row, no self-loops) and `empties` empty rows."""
+    rows = []
+    for i in range(pairs):
+        rows += [[2 * i + 1], [2 * i]]
+    return small.from_rows(rows + [[] for _ in range(empties)])
+
+
+def _triangles_and_empties(tri, empties):
+    """`tri` directed 3-cycles a -> b -> c -> a and `empties` empty rows."""
+    rows = []
+    for i in range(tri):
+        a = 3 * i
+        rows += [[a + 1], [a + 2], [a]]
+    return small.from_rows(rows + [[] for _ in range(empties)])
+
+
+@pytest.mark.parametrize("k,q", [(4, 1024), (7, 1000), (1, 2)])
+def test_adaptive_alpha_equal_spreads_is_half(k, q):
+    # N is 2 on the paired rows and 1 on the empty ones; D is 1 and 0: the same
+    # spread, so alpha = 1/2 whatever the mix
+    g = _pairs_and_empties(5, 13)
+    S = oracle.density_sums(g, 9, k, 3)
+    assert sorted(set(S.tolist())) == [k, 2 * k]
+    assert oracle.adaptive_alpha(S, oracle.degrees(g), k, q) == q // 2
+
+
+@pytest.mark.parametrize("k", [3, 8])
+def test_adaptive_alpha_triangles_closed_form(k):
+    # N is 3 or 1 (d >= 2), D is 1 or 0 on the same rows: Var(N) = 4 Var(D), alpha = 4/5
+    g = _triangles_and_empties(4, 9)
+    S = oracle.density_sums(g, 2, k, 4)
+    assert sorted(set(S.tolist())) == [k, 3 * k]
+    D = oracle.degrees(g)
+    for q in (5, 1000, 1024, 65535):
+        assert oracle.adaptive_alpha(S, D, k, q) == (4 * q) // 5
+    # Fraction check of the same closed form on the raw values
+    N = [Fraction(int(s), k) for s in S]
+    mN = sum(N) / len(N)
+    vN = sum((x - mN) ** 2 for x in N) / len(N)
+    mD = Fraction(int(D.sum()), len(D))
+    vD = sum((int(x) - mD) ** 2 for x in D) / len(D)
+    assert vN / (vN + vD) == Fraction(4, 5)
+
+
+def test_adaptive_alpha_degenerate_cases():
+    # neither metric varies: the default 1/2
+    g = small.edgeless(12, self_loops=False, normalise=False)
+    S = oracle.density_sums(g, 0, 4, 3)
+    assert oracle.adaptive_alpha(S, oracle.degrees(g), 4, 1024) == 512
+    # constant degree, varying density: alpha = 1 (density alone separates nodes)
+    g = small.cycle(20, self_loops=True, normalise=True)
+    S = oracle.density_sums(g, 1, 6, 4)
+    assert len(set(S.tolist())) > 1
+    assert oracle.adaptive_alpha(S, oracle.degrees(g), 6, 1024) == 1024
+    # constant density, varying degree: alpha = 0 (rows holding only repeated
+    # self-loops keep every walk at its start, while their lengths differ)
+    g = small.from_rows([[0] * 3, [1], [2] * 5, [3] * 2])
+    S = oracle.density_sums(g, 0, 4, 3)
+    assert set(S.tolist()) == {4}
+    assert oracle.adaptive_alpha(S, oracle.degrees(g), 4, 1024) == 0
+
+
+def test_adaptive_partition_uses_the_chosen_alpha():
+    g = small.random_graph(80, 0.07, seed=11)
+    P = oracle.partition(g, 5, 8, 4, alpha=(oracle.ALPHA_ADAPTIVE, 1024))
+    p = P["alpha"][0]
+    assert P["alpha"][1] == 1024 and 0 <= p <= 1024
+    fixed = oracle.partition(g, 5, 8, 4, alpha=(p, 1024))
+    assert np.array_equal(P["perm"], fixed["perm"]) and P["kstar"] == fixed["kstar"]
+    # the weight against a float evaluation of the variances
+    N = P["S"] / 8.0
+    D = P["D"].astype(np.float64)
+    a = N.var() / (N.var() + D.var())
+    assert p <= a * 1024 < p + 1 + 1e-9
+    _check_plan(P, g.n)
