@@ -143,8 +143,9 @@ def cpu_baseline(w, g, X, weights, part_budget_s=2.5):
 
 # Partition variants of the ablation: the paper's dual metric, its degree-only analogue
 # (the baseline partitioning of the paper's DualGCN_0 experiment), density only, and a
-# single path for every row.
+# single path for every row, and the adaptive weight (each metric's share of the spread).
 ABLATION = [("dual-metric alpha=1/2", (1, 2), "auto"),
+            ("dual-metric adaptive alpha", (0xFFFFFFFF, 1024), "auto"),
             ("degree only alpha=0", (0, 1), "auto"),
             ("density only alpha=1", (1, 1), "auto"),
             ("all rows sparse path", (1, 2), "sparse"),
@@ -175,7 +176,8 @@ def ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
             info = plan.info()
             plan.destroy()
         ms = float(np.mean(spmm_ms))
-        print(json.dumps({"ablation": name, "workload": w.name, "F": F_dom, "alpha": list(alpha),
+        print(json.dumps({"ablation": name, "workload": w.name, "F": F_dom,
+                          "alpha": [info["alpha_num"], info["alpha_den"]],
                           "force_mode": force, "n_sparse": info["n_sparse"],
                           "n_dense": info["n_dense"], "kstar": info["kstar"],
                           "partition_ms": round(float(np.mean(part_ms)), 4),

@@ -10,6 +10,8 @@ RELABEL = 2    # vertex relabelling permutation
 FEATURES = 3   # X
 W1 = 4         # first weight matrix
 W2 = 5         # second weight matrix
+LABELS = 6     # node classes for the training loss
+GRADS = 7      # upstream gradients fed to single backward steps
 
 
 def stream(seed: int, stream_id: int) -> np.random.Generator:

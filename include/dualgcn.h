@@ -73,11 +73,22 @@ typedef struct dualgcn_csr {
 
 enum { DUALGCN_FORCE_AUTO = 0, DUALGCN_FORCE_SPARSE = 1, DUALGCN_FORCE_DENSE = 2 };
 
+/* alpha_num that selects the adaptive weight (see dualgcn_thresholds). */
+#define DUALGCN_ALPHA_ADAPTIVE 0xFFFFFFFFu
+
 /*
  * Partition parameters, as exact rationals.
  *   alpha = alpha_num / alpha_den, the weight of density against degree in the
  *           hybrid metric H_v = alpha N_v + (1 - alpha) D_v (Sec. 3.2); the
  *           paper's default is 1/2.  Requires alpha_num <= alpha_den, den > 0.
+ *           alpha_num = DUALGCN_ALPHA_ADAPTIVE asks for the adaptive weight of
+ *           Sec. 3.2 ("Time Complexity and Overhead Analysis"), for which the
+ *           paper gives no formula.  This library takes each metric's share of
+ *           the total spread, alpha = Var(N) / (Var(N) + Var(D)) (population
+ *           variances over all nodes), rounded down to a multiple of
+ *           1 / alpha_den, and 1/2 (alpha_num = floor(alpha_den / 2)) when
+ *           neither metric varies.  The weight chosen is reported by
+ *           dualgcn_plan_query.
  *   beta  = beta_num / beta_den, the threshold tau = mu_H + beta sigma_H of
  *           Eq. (1) (Sec. 3.3); the paper uses 1/2.  Requires den > 0.
  *   force_mode  DUALGCN_FORCE_AUTO applies Eq. (1); FORCE_SPARSE / FORCE_DENSE
@@ -123,7 +134,8 @@ typedef struct dualgcn_plan dualgcn_plan;
  * released inside the call.  The processing order keeps perm's split into the
  * sparse and the dense region; inside a region rows go by row-length octave,
  * then node id (balanced work, and the locality of the node numbering).  The
- * call waits for `stream` twice (to read the moment sums and the schedule sizes).
+ * call waits for `stream` twice (to read the moment sums and the schedule sizes),
+ * and once more with the adaptive weight (to read the moments of S and D).
  * *out is set to NULL on error.
  */
 int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,

@@ -335,3 +335,101 @@ def gcn_forward_rows(g, X, weights, rows):
             H, Hbound = Y, BY
         prev_nodes = out_nodes
     return H, Hbound
+
+
+# ------------------------------------------------------------------ training (Sec. 1)
+# The paper accelerates GCN training: each layer H = act(A (X W)) is followed, in the
+# backward pass, by the products of the chain rule.  With G = dL/dH:
+#   G_P = G * act'(P)        (P = A (X W); ReLU' is [P > 0])
+#   G_T = A^T G_P            (the aggregation transposed)
+#   dW  = X^T G_T
+#   dX  = G_T W^T            (masked by the previous layer's ReLU')
+# The loss is the mean softmax cross-entropy over the labeled rows.
+
+def softmax_xent(Y, labels, scale):
+    """(loss, G): loss = scale * sum over labeled rows of -log softmax(Y_v)[label_v] and
+    G = dloss/dY = scale (softmax(Y_v) - e_label) on labeled rows, 0 elsewhere.
+    Rows whose label is outside [0, C) are unlabeled.  float64."""
+    Y = np.asarray(Y, dtype=np.float64)
+    labels = np.asarray(labels).astype(np.int64)
+    n, C = Y.shape
+    m = Y.max(axis=1, keepdims=True)
+    e = np.exp(Y - m)
+    s = e.sum(axis=1, keepdims=True)
+    P = e / s
+    on = (labels >= 0) & (labels < C)
+    rows = np.flatnonzero(on)
+    G = np.zeros_like(Y)
+    G[rows] = P[rows]
+    G[rows, labels[rows]] -= 1.0
+    G *= scale
+    logp = Y[rows, labels[rows]] - m[rows, 0] - np.log(s[rows, 0])
+    return float(-scale * logp.sum()), G
+
+
+def transpose_csr(g):
+    """The transposed matrix A^T as a CSR graph (entries of column c become row c, in
+    row order of A)."""
+    from types import SimpleNamespace
+    rowptr, col, val = _csr(g)
+    rows = np.repeat(np.arange(g.n, dtype=np.int64), np.diff(rowptr.astype(np.int64)))
+    order = np.argsort(col, kind="stable")
+    tcol = rows[order].astype(np.int32)
+    tval = np.asarray(val)[order]
+    tptr = np.zeros(g.n + 1, dtype=np.int64)
+    np.add.at(tptr, col.astype(np.int64) + 1, 1)
+    return SimpleNamespace(n=g.n, rowptr=np.cumsum(tptr).astype(np.int32), col=tcol, val=tval)
+
+
+def spmm_f64(g, X):
+    """A X for a float64 X (every row), float64."""
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    return _spmm_f64(g, X, np.arange(g.n, dtype=np.int64), np.arange(g.n, dtype=np.int32))
+
+
+def weight_grad(X, G):
+    """(dW, B) = (X^T G, |X|^T |G|) in float64."""
+    X = np.asarray(X, dtype=np.float64)
+    G = np.asarray(G, dtype=np.float64)
+    return X.T @ G, np.abs(X).T @ np.abs(G)
+
+
+def backward_data(G, W, M=None):
+    """(dX, B) = ((G W^T) * [M > 0], (|G| |W|^T) * [M > 0]) in float64; no mask if M is None."""
+    G = np.asarray(G, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    dX = G @ W.T
+    B = np.abs(G) @ np.abs(W).T
+    if M is not None:
+        keep = np.asarray(M, dtype=np.float64) > 0
+        dX = dX * keep
+        B = B * keep
+    return dX, B
+
+
+def gcn_train_grads(g, X, weights, labels, scale):
+    """Forward and backward of a GCN (ReLU after every layer but the last, softmax
+    cross-entropy on the last) in float64.  Returns a dict with the loss, the weight
+    gradients "dW" (one per layer) and the intermediates: per layer "T", "P", "H" of
+    the forward and "GP", "GT" of the backward; "G" holds dL/dH of every layer."""
+    X = np.asarray(X, dtype=np.float64)
+    gt = transpose_csr(g)
+    L = len(weights)
+    Ws = [np.asarray(W, dtype=np.float64) for W in weights]
+    inp, T, P, H = [X], [], [], []
+    for li, W in enumerate(Ws):
+        T.append(inp[-1] @ W)
+        P.append(spmm_f64(g, T[-1]))
+        H.append(np.maximum(P[-1], 0.0) if li < L - 1 else P[-1])
+        inp.append(H[-1])
+    loss, G_last = softmax_xent(H[-1], labels, scale)
+    G = [None] * L
+    G[L - 1] = G_last
+    GP, GT, dW = [None] * L, [None] * L, [None] * L
+    for li in range(L - 1, -1, -1):
+        GP[li] = G[li] * (P[li] > 0) if li < L - 1 else G[li]
+        GT[li] = spmm_f64(gt, GP[li])
+        dW[li] = inp[li].T @ GT[li]
+        if li > 0:
+            G[li - 1] = GT[li] @ Ws[li].T
+    return dict(loss=loss, dW=dW, T=T, P=P, H=H, G=G, GP=GP, GT=GT)

@@ -22,6 +22,7 @@ OK, ERR_INVALID_ARG, ERR_BAD_CSR, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP, ERR_NO_DEVI
     0, -1, -2, -3, -4, -5, -6
 FORCE_AUTO, FORCE_SPARSE, FORCE_DENSE = 0, 1, 2
 RELU, OUT_BF16, IN_BF16 = 1, 2, 4
+ALPHA_ADAPTIVE = 0xFFFFFFFF      # alpha = (ALPHA_ADAPTIVE, q): adaptive weight in steps of 1/q
 
 _FORCE = {"auto": FORCE_AUTO, "sparse": FORCE_SPARSE, "dense": FORCE_DENSE,
           FORCE_AUTO: FORCE_AUTO, FORCE_SPARSE: FORCE_SPARSE, FORCE_DENSE: FORCE_DENSE}
@@ -272,4 +273,5 @@ def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
 
 __all__ = ["Plan", "spmm", "update", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
            "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
-           "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16"]
+           "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16",
+           "ALPHA_ADAPTIVE"]

@@ -204,7 +204,9 @@ int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_
     if ((st = check_walks(walks_per_node, walk_len))) return st;
     dualgcn_thresholds t{1, 2, 1, 2, DUALGCN_FORCE_AUTO};
     if (th) t = *th;
-    if (t.alpha_den == 0 || t.beta_den == 0 || t.alpha_num > t.alpha_den) return DUALGCN_ERR_INVALID_ARG;
+    if (t.alpha_den == 0 || t.beta_den == 0 ||
+        (t.alpha_num > t.alpha_den && t.alpha_num != DUALGCN_ALPHA_ADAPTIVE))
+        return DUALGCN_ERR_INVALID_ARG;
     if (t.alpha_den >= kMaxRational || t.beta_den >= kMaxRational || t.beta_num >= kMaxRational)
         return DUALGCN_ERR_INVALID_ARG;
     if (t.force_mode < DUALGCN_FORCE_AUTO || t.force_mode > DUALGCN_FORCE_DENSE)

@@ -17,8 +17,9 @@
 // (Salmon, Moraes, Dror & Shaw, SC'11) with counter (v, w, floor(s/8), 0) and key
 // (seed, 0); one block serves eight steps.  The neighbour is entry
 // floor(r * deg / 2^32) of the current row (uniform over stored entries); an
-// empty row keeps the walk in place.  The 64-bit products of the Philox rounds
-// dominate the walk kernel, so halving the blocks per walk halves its time.
+// empty row keeps the walk in place.  A walk of up to eight steps thus costs one
+// Philox evaluation; what bounds the kernel is the chain of dependent random reads
+// (row bounds, then a column entry) at every step.
 #include "internal.h"
 
 namespace dgc {

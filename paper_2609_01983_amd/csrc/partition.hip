@@ -657,6 +657,46 @@ int threshold_key(int32_t n, u128 s1, u128 s2, uint32_t b, uint32_t c, uint64_t 
     return DUALGCN_OK;
 }
 
+// n^2 times the population variance of values with sums s1, s2: V = n s2 - s1^2.
+int scaled_variance(int32_t n, u128 s1, u128 s2, u128 *V) {
+    u128 ns2, s1sq;
+    if (mul_overflows(static_cast<u128>(n), s2, &ns2)) return DUALGCN_ERR_UNSUPPORTED;
+    if (mul_overflows(s1, s1, &s1sq)) return DUALGCN_ERR_UNSUPPORTED;
+    if (ns2 < s1sq) return DUALGCN_ERR_HIP;  // impossible for exact sums
+    *V = ns2 - s1sq;
+    return DUALGCN_OK;
+}
+
+// Adaptive weight p/q = Var(N) / (Var(N) + Var(D)) rounded down (N = S / k), and
+// q / 2 when neither metric varies: since Var(N) / Var(D) = V_S / (k^2 V_D),
+// p = floor(q V_S / (V_S + k^2 V_D)).
+int adaptive_weight(int32_t n, uint32_t k, uint32_t q, const Moments &ms, const Moments &md,
+                    uint64_t *p) {
+    u128 vs, vd, kvd, num;
+    int st;
+    if ((st = scaled_variance(n, join(ms.s1_lo, ms.s1_hi), join(ms.s2_lo, ms.s2_hi), &vs)))
+        return st;
+    if ((st = scaled_variance(n, join(md.s1_lo, md.s1_hi), join(md.s2_lo, md.s2_hi), &vd)))
+        return st;
+    if (mul_overflows(static_cast<u128>(k) * k, vd, &kvd)) return DUALGCN_ERR_UNSUPPORTED;
+    const u128 den = vs + kvd;
+    if (den < vs) return DUALGCN_ERR_UNSUPPORTED;
+    if (den == 0) {
+        *p = q / 2;
+        return DUALGCN_OK;
+    }
+    if (mul_overflows(static_cast<u128>(q), vs, &num)) return DUALGCN_ERR_UNSUPPORTED;
+    *p = static_cast<uint64_t>(num / den);
+    return DUALGCN_OK;
+}
+
+// s2 = sum K^2 is accumulated modulo 2^128; it cannot have wrapped when
+// kmax * s1 (an upper bound of it) fits.
+bool square_sum_fits(const Moments &m) {
+    u128 bound;
+    return !mul_overflows(static_cast<u128>(m.kmax), join(m.s1_lo, m.s1_hi), &bound);
+}
+
 }  // namespace
 
 int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t *blockmax,
@@ -717,7 +757,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_parts = lp.take(sizeof(SplitPart) * max_parts),
                  o_partials = lp.take(sizeof(double) * max_parts * kMaxSlice);
     const size_t o_flags = ls.take(2 * sizeof(int32_t)), o_mom = ls.take(sizeof(Moments) * nb_keys),
-                 o_sum = ls.take(sizeof(Summary)), o_kb0 = ls.take(sizeof(uint64_t) * un),
+                 o_sum = ls.take(2 * sizeof(Summary)), o_kb0 = ls.take(sizeof(uint64_t) * un),
                  o_kb1 = ls.take(sizeof(uint64_t) * un), o_vb0 = ls.take(sizeof(int32_t) * un),
                  o_scan = ls.take(sizeof(uint32_t) * static_cast<size_t>(scan_tiles)),
                  o_hist = ls.take(sizeof(uint32_t) * kRadix * static_cast<size_t>(nblocks)),
@@ -762,8 +802,29 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if (st == DUALGCN_ERR_UNSUPPORTED)
         st = launch_arw(csr->rowptr, csr->col, n, seed, k, d, p->S, nullptr, bad, s);
     if (st) return st;
+    // adaptive alpha: moments of S and of D (two passes of the key kernel with the
+    // weights (1, 0) and (0, 1)), one more host wait, the weight chosen on the host
+    uint64_t pa = th.alpha_num;
+    const uint64_t qa = th.alpha_den;
+    if (th.alpha_num == DUALGCN_ALPHA_ADAPTIVE) {
+        const uint64_t weights[2][2] = {{1, 0}, {0, 1}};
+        for (int m = 0; m < 2; ++m) {
+            hipLaunchKernelGGL(keys_kernel, dim3(nb_keys), dim3(kThreads), 0, s, csr->rowptr, p->S,
+                               n, weights[m][0], weights[m][1], p->K, moments, bad);
+            hipLaunchKernelGGL(fold_kernel, dim3(1), dim3(kThreads), 0, s, moments, nb_keys, bad,
+                               blockmax, summary + m);
+        }
+        if ((st = hip_status(hipGetLastError()))) return st;
+        Summary two[2];
+        if ((st = hip_status(hipMemcpyAsync(two, summary, sizeof(two), hipMemcpyDeviceToHost, s))))
+            return st;
+        if ((st = hip_status(hipStreamSynchronize(s)))) return st;       // adaptive alpha only
+        if (two[0].flag) return DUALGCN_ERR_BAD_CSR;
+        if (!square_sum_fits(two[0].m) || !square_sum_fits(two[1].m)) return DUALGCN_ERR_UNSUPPORTED;
+        if ((st = adaptive_weight(n, k, th.alpha_den, two[0].m, two[1].m, &pa))) return st;
+        p->th.alpha_num = static_cast<uint32_t>(pa);
+    }
     // keys and moments
-    const uint64_t pa = th.alpha_num, qa = th.alpha_den;
     hipLaunchKernelGGL(keys_kernel, dim3(nb_keys), dim3(kThreads), 0, s, csr->rowptr, p->S, n,
                        pa, (qa - pa) * k, p->K, moments, bad);
     hipLaunchKernelGGL(fold_kernel, dim3(1), dim3(kThreads), 0, s, moments, nb_keys, bad, blockmax,
@@ -779,6 +840,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     p->s1 = join(sum.m.s1_lo, sum.m.s1_hi);
     p->s2 = join(sum.m.s2_lo, sum.m.s2_hi);
     p->kmax = sum.m.kmax;
+    if (!square_sum_fits(sum.m)) return DUALGCN_ERR_UNSUPPORTED;
     if ((st = threshold_key(n, p->s1, p->s2, th.beta_num, th.beta_den, &p->kstar))) return st;
 
     // stable radix sort of (K, v) on the bits the keys use; every entry of perm is a

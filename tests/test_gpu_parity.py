@@ -39,6 +39,7 @@ def assert_plan_matches(dg, plan, g, seed, k, d, alpha=(1, 2), beta=(1, 2), forc
     assert info["kstar"] == ref["kstar"]
     assert info["n_sparse"] == ref["n_sparse"]
     assert np.array_equal(perm, ref["perm"])
+    assert (info["alpha_num"], info["alpha_den"]) == tuple(ref["alpha"])
     return ref
 
 
@@ -100,6 +101,38 @@ def test_partition_parameters(dg, device, alpha, beta, force):
     plan = dg.Plan(*to_dev(g, device), seed=1, walks_per_node=8, walk_len=4, alpha=alpha,
                    beta=beta, force_mode=force)
     assert_plan_matches(dg, plan, g, 1, 8, 4, alpha, beta, force)
+
+
+ADAPTIVE_TINY = {
+    # deterministic walks: Var(N) = Var(D) (alpha 1/2) and Var(N) = 4 Var(D) (alpha 4/5)
+    "pairs": lambda: small.from_rows([[1], [0], [3], [2]] + [[] for _ in range(7)]),
+    "triangles": lambda: small.from_rows([[1], [2], [0], [4], [5], [3]] + [[] for _ in range(5)]),
+    "edgeless_bare": lambda: small.edgeless(9, self_loops=False, normalise=False),
+    "self_loops_only": lambda: small.from_rows([[0] * 3, [1], [2] * 5, [3] * 2]),
+}
+
+
+@pytest.mark.parametrize("name", sorted(TINY) + sorted(ADAPTIVE_TINY))
+@pytest.mark.parametrize("q", [1024, 7, 65535])
+def test_adaptive_alpha_bitexact_tiny(dg, device, name, q):
+    g = (TINY.get(name) or ADAPTIVE_TINY[name])()
+    alpha = (dg.ALPHA_ADAPTIVE, q)
+    plan = dg.Plan(*to_dev(g, device), seed=7, walks_per_node=8, walk_len=4, alpha=alpha)
+    ref = assert_plan_matches(dg, plan, g, 7, 8, 4, alpha)
+    if name == "pairs":
+        assert ref["alpha"][0] == q // 2
+    elif name == "triangles":
+        assert ref["alpha"][0] == 4 * q // 5
+
+
+@pytest.mark.parametrize("cfg", ["c1", "c2"])
+def test_adaptive_alpha_bitexact_configs(dg, device, cfg):
+    w = configs.WORKLOADS[cfg]
+    g = configs.load_graph(cfg)
+    alpha = (dg.ALPHA_ADAPTIVE, 1024)
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps,
+                   alpha=alpha)
+    assert_plan_matches(dg, plan, g, 0, w.walks, w.steps, alpha)
 
 
 @pytest.mark.parametrize("cfg", ["c1", "c2"])
@@ -192,7 +225,8 @@ def test_spmm_configs_full(dg, device, cfg):
 
 
 @pytest.mark.parametrize("alpha,force", [((1, 2), "auto"), ((0, 1), "auto"), ((1, 1), "auto"),
-                                         ((1, 2), "sparse"), ((1, 2), "dense")])
+                                         ((1, 2), "sparse"), ((1, 2), "dense"),
+                                         ((0xFFFFFFFF, 1024), "auto")])
 def test_ablation_variants_c2(dg, device, alpha, force):
     """Every partition variant of the ablation: its plan matches the oracle and its SpMM
     (with the variant's schedule) matches the plan-independent oracle product."""
