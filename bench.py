@@ -188,6 +188,88 @@ def ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
                           "walks_per_node": w.walks, "walk_len": w.steps}), flush=True)
 
 
+def train(args, w, g, dg, torch, np, rowptr, col, val, Xd, Wd, stream, ev):
+    """GCN training steps on one plan (the partition is amortised over the epochs, Sec. 3.2):
+    forward with bfloat16 intermediates, softmax cross-entropy on 10% labeled rows,
+    backward (A^T = A: the same plan), SGD on every weight.  One JSON line."""
+    from graphgen import dense
+    if not w.is_gcn:
+        raise SystemExit("--mode train needs a GCN workload")
+    dev = Xd.device
+    L = len(w.layers)
+    C = w.layers[-1][1]
+    labels = torch.from_numpy(dense.labels(g.n, C, seed=0, labeled_fraction=0.1)).to(dev)
+    scale = 1.0 / max(1, int((labels >= 0).sum().item()))
+    plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    Ws = [W.clone() for W in Wd]
+    T = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for _, fo in w.layers]
+    H = [torch.empty((g.n, fo), dtype=torch.bfloat16 if li < L - 1 else torch.float32, device=dev)
+         for li, (_, fo) in enumerate(w.layers)]
+    G = torch.empty((g.n, C), dtype=torch.float32, device=dev)
+    loss = torch.empty(dg.LOSS_SLOTS, dtype=torch.float64, device=dev)
+    dT = [torch.empty((g.n, fo), dtype=torch.bfloat16, device=dev) for _, fo in w.layers]
+    dH = [torch.empty((g.n, fo), dtype=torch.float32, device=dev) for _, fo in w.layers[:-1]]
+    dW = [torch.empty_like(W) for W in Ws]
+    ws = torch.empty(max(dg.weight_grad_workspace_bytes(g.n, fi, fo) for fi, fo in w.layers),
+                     dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        marks = {}
+
+        def mark(name, fn):
+            a, b = ev(), ev()
+            a.record(stream)
+            fn()
+            b.record(stream)
+            marks.setdefault(name, []).append((a, b))
+
+        inp = [Xd] + H[:-1]
+        for li in range(L):
+            mark("forward_update", lambda: dg.update(inp[li], Ws[li], T[li]))
+            mark("forward_spmm", lambda: dg.spmm(plan, T[li], H[li], relu=li < L - 1,
+                                                 out_bf16=li < L - 1))
+        mark("loss", lambda: dg.softmax_xent(H[-1], labels, scale, G, loss))
+        grad = G
+        for li in range(L - 1, -1, -1):
+            mark("backward_spmm", lambda: dg.spmm(plan, grad, dT[li], out_bf16=True))
+            if li > 0:          # dX before the step changes W
+                mark("backward_data", lambda: dg.backward_data(dT[li], Ws[li], H[li - 1], dH[li - 1]))
+            mark("weight_grad_sgd", lambda: dg.weight_grad(inp[li], dT[li], dW[li], args.lr, Ws[li], ws))
+            if li > 0:
+                grad = dH[li - 1]
+        return marks
+
+    losses = []
+    for _ in range(args.warmup):
+        step()
+        losses.append(loss[0].item())
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    all_marks = []
+    for _ in range(args.steps):
+        all_marks.append(step())
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    losses.append(loss[0].item())
+    phases = {}
+    for m in all_marks:
+        for k, v in m.items():
+            phases[k] = phases.get(k, 0.0) + sum(a.elapsed_time(b) for a, b in v)
+    ms = elapsed * 1e3 / args.steps
+    aggregated = 2 * g.nnz * sum(fo for _, fo in w.layers)      # forward + backward SpMMs
+    print(json.dumps({"mode": "train", "workload": w.desc, "config": w.name, "n": g.n,
+                      "nnz": g.nnz, "layers": w.layers, "steps": args.steps, "warmup": args.warmup,
+                      "ms_per_step": round(ms, 4),
+                      "spmm_ge_s": round(aggregated / (ms * 1e-3) / 1e9, 1),
+                      "phases_ms": {k: round(v / args.steps, 4) for k, v in phases.items()},
+                      "labeled_rows": int((labels >= 0).sum().item()), "lr": args.lr,
+                      "loss_first": losses[0], "loss_last": losses[-1],
+                      "note": "partition built once before the timed steps (amortised over epochs)"}),
+          flush=True)
+    plan.destroy()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -196,8 +278,10 @@ def main():
     ap.add_argument("--config", default=os.environ.get("DUALGCN_BENCH_CONFIG", "c5"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--spmm-reps", type=int, default=20)
-    ap.add_argument("--mode", choices=["full", "spmm"], default="full",
-                    help="spmm: one partition, then only the dominant SpMM launches (for counter runs)")
+    ap.add_argument("--mode", choices=["full", "spmm", "train"], default="full",
+                    help="spmm: one partition, then only the dominant SpMM launches (for counter "
+                         "runs); train: GCN training steps on one plan (forward, loss, backward, SGD)")
+    ap.add_argument("--lr", type=float, default=0.5, help="SGD step of --mode train")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device to device (a dispatch of known traffic)")
     ap.add_argument("--ablation", action="store_true",
@@ -264,6 +348,9 @@ def main():
         return
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
+    if args.mode == "train":
+        train(args, w, g, dg, torch, np, rowptr, col, val, Xd, Wd, stream, ev)
+        return
     if args.ablation:
         ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
         return

@@ -85,3 +85,14 @@ def from_undirected_edges(n: int, lo: np.ndarray, hi: np.ndarray, relabel=None,
     del rows, cols
     val = normalised_values(rowptr, col)
     return Graph(n=n, rowptr=rowptr, col=col, val=val, meta=dict(meta or {}))
+
+
+def transposed(g: Graph) -> Graph:
+    """The CSR of the transposed matrix (column c of g becomes row c, entries in row order)."""
+    rows = np.repeat(np.arange(g.n, dtype=np.int64), np.diff(g.rowptr.astype(np.int64)))
+    order = np.argsort(g.col, kind="stable")
+    counts = np.bincount(g.col.astype(np.int64), minlength=g.n)
+    rowptr = np.zeros(g.n + 1, dtype=np.int64)
+    rowptr[1:] = np.cumsum(counts)
+    return Graph(n=g.n, rowptr=rowptr.astype(np.int32), col=rows[order].astype(np.int32),
+                 val=np.asarray(g.val)[order].astype(np.float32), meta=dict(g.meta, transposed=True))

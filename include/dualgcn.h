@@ -151,8 +151,9 @@ void dualgcn_plan_destroy(dualgcn_plan *plan);
  * X and Y are float32 row-major n x F, contiguous (leading dimension F), and
  * must not overlap.  Rows of the sparse region are computed by the sparse
  * path (runs of up to 8 short rows per lane group of a wavefront); rows of the
- * dense region by the dense path (a lane group per row under 512 entries, a
- * wavefront per longer row; rows longer than the dense chunk are split over
+ * dense region by the dense path (a lane group per row under 512 entries -- 256,
+ * 128, 64 for F <= 64, 32, 16 --, a wavefront per longer row; rows longer than the
+ * dense chunk are split over
  * several wavefronts and combined in a fixed order).
  * Every row of Y is written, rows without entries with zeros.  Products are
  * float32; sums are formed in float32 over at most 16 terms and then in
@@ -223,6 +224,81 @@ int dualgcn_gcn_layer(const dualgcn_plan *plan, const void *X, const float *W, v
                       int32_t F_in, int32_t F_out, uint32_t flags, void *workspace,
                       size_t workspace_bytes, void *stream);
 
+/* ------------------------------------------------------------------ training */
+
+/*
+ * The backward pass of a GCN layer H = act(P), P = A T, T = X W (Sec. 1: the paper
+ * accelerates GCN training, whose gradients repeat the aggregation).  With
+ * G = dL/dH the chain rule gives, in order:
+ *   G_P = G * act'(P)          ReLU' = [P > 0]; folded into the product that makes G
+ *   G_T = A^T G_P              dualgcn_spmm_act on a plan of A^T.  The symmetric
+ *                              normalised adjacency is its own transpose, so there
+ *                              the forward plan serves; for another matrix, partition
+ *                              its transpose.
+ *   dW  = X^T G_T              dualgcn_weight_grad
+ *   dX  = (G_T W^T) * [M > 0]  dualgcn_backward_data, M the previous layer's output
+ * and the loss gradient of the last layer comes from dualgcn_softmax_xent.
+ */
+
+/* Flag of the training entry points: the gradient operand G holds bfloat16 values. */
+#define DUALGCN_GRAD_BF16 8u
+
+/* float64 slots of the loss buffer of dualgcn_softmax_xent. */
+#define DUALGCN_LOSS_SLOTS 1025
+
+/*
+ * dualgcn_softmax_xent -- mean softmax cross-entropy over labeled rows.
+ *
+ * Y (device, float32 n x C row-major) holds the logits, labels (device, int32[n])
+ * the class of every row; rows whose label is outside [0, C) are unlabeled.
+ * Writes G (device, float32 n x C) = scale * (softmax(Y_v) - e_label_v) on labeled
+ * rows and 0 on the others, and loss[0] = scale * sum over labeled rows of
+ * -log softmax(Y_v)[label_v]; pass scale = 1 / (number of labeled rows) for the
+ * mean.  loss is a device float64 buffer of DUALGCN_LOSS_SLOTS entries: the others
+ * receive per-workgroup partial sums, added in a fixed order, so the loss does not
+ * depend on timing.  float32 arithmetic (expf, logf), the loss summed in float64.
+ * G must not overlap Y.  1 <= C < 2^20.  Asynchronous.
+ */
+int dualgcn_softmax_xent(const float *Y, const int32_t *labels, int32_t n, int32_t C,
+                         float scale, float *G, double *loss, void *stream);
+
+/* Bytes of the workspace dualgcn_weight_grad needs for n rows (host only). */
+int dualgcn_weight_grad_workspace(int32_t n, int32_t F_in, int32_t F_out, size_t *bytes);
+
+/*
+ * dualgcn_weight_grad -- dW = X^T G, the weight gradient of the update phase.
+ *
+ * X (device, n x F_in) is float32, or bfloat16 with DUALGCN_IN_BF16; G (device,
+ * n x F_out) is float32, or bfloat16 with DUALGCN_GRAD_BF16; dW (device, float32
+ * F_in x F_out row-major).  Both operands are rounded to bfloat16 (nearest-even)
+ * and multiplied on the matrix cores with float32 accumulation over chunks of
+ * rows; the per-workgroup partial matrices (in `workspace`, device, 256-byte
+ * aligned, at least dualgcn_weight_grad_workspace bytes) are summed in a fixed
+ * order in float64, so results do not depend on timing.  If W (device, float32
+ * F_in x F_out) is not NULL, the same call applies the SGD step W -= lr dW.
+ * Shapes: F_in and F_out multiples of 32, F_in <= 1024, F_out <= 256 (else
+ * DUALGCN_ERR_UNSUPPORTED); X and G 16-byte aligned.  Asynchronous.
+ */
+int dualgcn_weight_grad(const void *X, const void *G, float *dW, int32_t n, int32_t F_in,
+                        int32_t F_out, uint32_t flags, float lr, float *W, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+/*
+ * dualgcn_backward_data -- dX = (G W^T) * [M > 0], the gradient that flows from a
+ * layer's update phase to its input, masked by the ReLU that produced that input.
+ *
+ * G (device, n x F_out) is float32, or bfloat16 with DUALGCN_GRAD_BF16; W (device,
+ * float32 F_in x F_out, the layer's weights as used forward); M (device, n x F_in)
+ * is the previous layer's output H (float32, or bfloat16 with DUALGCN_IN_BF16), or
+ * NULL for no mask; dX (device, float32 n x F_in).  G and W are rounded to
+ * bfloat16 and multiplied on the matrix cores with float32 accumulation (the
+ * kernel of dualgcn_update).  dX must not overlap G or M.  Shape limits as for
+ * dualgcn_update (F_in and F_out multiples of 32, F_in <= 1024, F_out <= 256); G
+ * 16-byte aligned.  Asynchronous.
+ */
+int dualgcn_backward_data(const void *G, const float *W, const void *M, float *dX, int32_t n,
+                          int32_t F_in, int32_t F_out, uint32_t flags, void *stream);
+
 /* ------------------------------------------------------------------ introspection */
 
 typedef struct dualgcn_plan_info {
@@ -244,7 +320,8 @@ typedef struct dualgcn_plan_info {
     int32_t n_split_parts;   /* wavefronts those rows are split over */
     int32_t n_tasks;         /* sparse-region tasks (runs of at most 8 short rows) */
     int32_t n_long_rows;     /* dense rows of >= 512 entries (a wavefront each; the
-                                shorter dense rows get a lane group each) */
+                                shorter dense rows get a lane group each; for F <= 64
+                                the bound is 256, for F <= 32 128, for F <= 16 64) */
 } dualgcn_plan_info;
 
 /* Fills *out from host-side copies kept in the plan (no device use). */

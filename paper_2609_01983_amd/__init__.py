@@ -21,7 +21,8 @@ LIB_PATH = os.path.join(_HERE, "libdualgcn.so")
 OK, ERR_INVALID_ARG, ERR_BAD_CSR, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP, ERR_NO_DEVICE = \
     0, -1, -2, -3, -4, -5, -6
 FORCE_AUTO, FORCE_SPARSE, FORCE_DENSE = 0, 1, 2
-RELU, OUT_BF16, IN_BF16 = 1, 2, 4
+RELU, OUT_BF16, IN_BF16, GRAD_BF16 = 1, 2, 4, 8
+LOSS_SLOTS = 1025                # float64 entries of the loss buffer of softmax_xent
 ALPHA_ADAPTIVE = 0xFFFFFFFF      # alpha = (ALPHA_ADAPTIVE, q): adaptive weight in steps of 1/q
 
 _FORCE = {"auto": FORCE_AUTO, "sparse": FORCE_SPARSE, "dense": FORCE_DENSE,
@@ -80,6 +81,11 @@ def _load():
         "dualgcn_plan_query": ([P, ctypes.POINTER(PlanInfo)], ctypes.c_int),
         "dualgcn_plan_export": ([P, P, P, P], ctypes.c_int),
         "dualgcn_arw_patterns": ([ctypes.POINTER(Csr), U64, U32, U32, P, P], ctypes.c_int),
+        "dualgcn_softmax_xent": ([P, P, I32, I32, ctypes.c_float, P, P, P], ctypes.c_int),
+        "dualgcn_weight_grad_workspace": ([I32, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
+        "dualgcn_weight_grad": ([P, P, P, I32, I32, I32, U32, ctypes.c_float, P, P, SZ, P],
+                                ctypes.c_int),
+        "dualgcn_backward_data": ([P, P, P, P, I32, I32, I32, U32, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -261,6 +267,106 @@ def gcn_layer(plan, X, W, relu=False, Y=None, workspace=None, out_bf16=False, st
     return Y
 
 
+# ------------------------------------------------------------------ training
+
+def _float_or_bf16(t, name):
+    if not isinstance(t, torch.Tensor) or t.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError(f"{name} must be a float32 or bfloat16 tensor")
+    _dev(t, t.dtype, name)
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D")
+
+
+def softmax_xent(Y, labels, scale=None, G=None, loss=None, stream=None):
+    """Softmax cross-entropy over the rows whose label is in [0, C).
+
+    Returns (G, loss): G = dloss/dY (float32 [n, C]) and a float64 device tensor of
+    LOSS_SLOTS entries whose entry 0 is the loss.  scale defaults to 1 / (labeled rows),
+    counted on the host from `labels` only when not given."""
+    _dev(Y, torch.float32, "Y")
+    _dev(labels, torch.int32, "labels")
+    n, C = Y.shape
+    if labels.shape != (n,):
+        raise ValueError("labels must be [n]")
+    if scale is None:
+        scale = 1.0 / max(1, int(((labels >= 0) & (labels < C)).sum().item()))
+    if G is None:
+        G = torch.empty_like(Y)
+    _dev(G, torch.float32, "G")
+    if loss is None:
+        loss = torch.empty(LOSS_SLOTS, dtype=torch.float64, device=Y.device)
+    _dev(loss, torch.float64, "loss")
+    if G.shape != Y.shape or loss.numel() < LOSS_SLOTS:
+        raise ValueError("G must match Y and loss must hold LOSS_SLOTS entries")
+    _check(_lib.dualgcn_softmax_xent(Y.data_ptr(), labels.data_ptr(), n, C, float(scale),
+                                     G.data_ptr(), loss.data_ptr(), _stream(stream)),
+           "dualgcn_softmax_xent")
+    return G, loss
+
+
+def weight_grad_workspace_bytes(n, F_in, F_out):
+    nbytes = ctypes.c_size_t()
+    _check(_lib.dualgcn_weight_grad_workspace(n, F_in, F_out, ctypes.byref(nbytes)),
+           "dualgcn_weight_grad_workspace")
+    return nbytes.value
+
+
+def weight_grad(X, G, dW=None, lr=0.0, W=None, workspace=None, stream=None):
+    """dW = X^T G on the bf16 matrix cores; with W, also the SGD step W -= lr dW.
+    X: [n, F_in] and G: [n, F_out], each float32 or bfloat16."""
+    _float_or_bf16(X, "X")
+    _float_or_bf16(G, "G")
+    n, F_in = X.shape
+    if G.shape[0] != n:
+        raise ValueError("X and G must have the same rows")
+    F_out = G.shape[1]
+    if dW is None:
+        dW = torch.empty((F_in, F_out), dtype=torch.float32, device=X.device)
+    _dev(dW, torch.float32, "dW")
+    if W is not None:
+        _dev(W, torch.float32, "W")
+        if W.shape != (F_in, F_out):
+            raise ValueError("W must be [F_in, F_out]")
+    if dW.shape != (F_in, F_out):
+        raise ValueError("dW must be [F_in, F_out]")
+    need = weight_grad_workspace_bytes(n, F_in, F_out)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    flags = (IN_BF16 if X.dtype == torch.bfloat16 else 0) | \
+            (GRAD_BF16 if G.dtype == torch.bfloat16 else 0)
+    _check(_lib.dualgcn_weight_grad(X.data_ptr(), G.data_ptr(), dW.data_ptr(), n, F_in, F_out,
+                                    flags, float(lr), W.data_ptr() if W is not None else None,
+                                    workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                    _stream(stream)), "dualgcn_weight_grad")
+    return dW
+
+
+def backward_data(G, W, M=None, dX=None, stream=None):
+    """dX = (G W^T) * [M > 0] on the bf16 matrix cores (no mask without M).
+    G: [n, F_out] float32 or bfloat16, W: [F_in, F_out] float32, M: [n, F_in]."""
+    _float_or_bf16(G, "G")
+    _dev(W, torch.float32, "W")
+    F_in, F_out = W.shape
+    n = G.shape[0]
+    if G.shape[1] != F_out:
+        raise ValueError("G must be [n, F_out]")
+    flags = GRAD_BF16 if G.dtype == torch.bfloat16 else 0
+    if M is not None:
+        _float_or_bf16(M, "M")
+        if M.shape != (n, F_in):
+            raise ValueError("M must be [n, F_in]")
+        flags |= IN_BF16 if M.dtype == torch.bfloat16 else 0
+    if dX is None:
+        dX = torch.empty((n, F_in), dtype=torch.float32, device=G.device)
+    _dev(dX, torch.float32, "dX")
+    if dX.shape != (n, F_in):
+        raise ValueError("dX must be [n, F_in]")
+    _check(_lib.dualgcn_backward_data(G.data_ptr(), W.data_ptr(),
+                                      M.data_ptr() if M is not None else None, dX.data_ptr(), n,
+                                      F_in, F_out, flags, _stream(stream)), "dualgcn_backward_data")
+    return dX
+
+
 def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
     """uint8 [n, k, d+1] anonymous walks (labels) of every node, on the device."""
     csr = make_csr(rowptr, col, val)
@@ -274,4 +380,5 @@ def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
 __all__ = ["Plan", "spmm", "update", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
            "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
            "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16",
-           "ALPHA_ADAPTIVE"]
+           "ALPHA_ADAPTIVE", "GRAD_BF16", "LOSS_SLOTS", "softmax_xent", "weight_grad",
+           "weight_grad_workspace_bytes", "backward_data"]

@@ -293,6 +293,71 @@ int dualgcn_gcn_layer(const dualgcn_plan *plan, const void *X, const float *W, v
                                  static_cast<hipStream_t>(stream));
 }
 
+int dualgcn_softmax_xent(const float *Y, const int32_t *labels, int32_t n, int32_t C,
+                         float scale, float *G, double *loss, void *stream) {
+    if (!Y || !labels || !G || !loss || n < 1 || C < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (C >= (1 << 20)) return DUALGCN_ERR_UNSUPPORTED;
+    const size_t elems = static_cast<size_t>(n) * C;
+    const size_t lbytes = sizeof(double) * DUALGCN_LOSS_SLOTS;
+    if (overlaps(Y, elems * sizeof(float), G, elems * sizeof(float)) ||
+        overlaps(loss, lbytes, Y, elems * sizeof(float)) ||
+        overlaps(loss, lbytes, G, elems * sizeof(float)) ||
+        overlaps(loss, lbytes, labels, sizeof(int32_t) * n) ||
+        overlaps(G, elems * sizeof(float), labels, sizeof(int32_t) * n))
+        return DUALGCN_ERR_INVALID_ARG;
+    int st = dgc::device_status();
+    if (st) return st;
+    return dgc::launch_softmax_xent(Y, labels, n, C, scale, G, loss, static_cast<hipStream_t>(stream));
+}
+
+int dualgcn_weight_grad_workspace(int32_t n, int32_t F_in, int32_t F_out, size_t *bytes) {
+    if (!bytes || n < 1 || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
+    *bytes = dgc::wgrad_workspace_bytes(n, F_in, F_out);
+    return DUALGCN_OK;
+}
+
+int dualgcn_weight_grad(const void *X, const void *G, float *dW, int32_t n, int32_t F_in,
+                        int32_t F_out, uint32_t flags, float lr, float *W, void *workspace,
+                        size_t workspace_bytes, void *stream) {
+    if (!G || !dW || !workspace || n < 1) return DUALGCN_ERR_INVALID_ARG;
+    int st = check_update(X, W ? W : dW, dW, F_in, F_out);
+    if (st) return st;
+    if (flags & ~(DUALGCN_IN_BF16 | DUALGCN_GRAD_BF16)) return DUALGCN_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(G) % 16 || reinterpret_cast<uintptr_t>(workspace) % 256)
+        return DUALGCN_ERR_INVALID_ARG;
+    const size_t ws = dgc::wgrad_workspace_bytes(n, F_in, F_out);
+    if (workspace_bytes < ws) return DUALGCN_ERR_INVALID_ARG;
+    const bool xbf = (flags & DUALGCN_IN_BF16) != 0, gbf = (flags & DUALGCN_GRAD_BF16) != 0;
+    const size_t un = static_cast<size_t>(n);
+    const size_t xb = un * F_in * (xbf ? 2 : 4), gb = un * F_out * (gbf ? 2 : 4);
+    const size_t wb = static_cast<size_t>(F_in) * F_out * sizeof(float);
+    if (overlaps(dW, wb, X, xb) || overlaps(dW, wb, G, gb) || overlaps(dW, wb, workspace, ws) ||
+        overlaps(workspace, ws, X, xb) || overlaps(workspace, ws, G, gb))
+        return DUALGCN_ERR_INVALID_ARG;
+    if (W && (overlaps(W, wb, X, xb) || overlaps(W, wb, G, gb) || overlaps(W, wb, dW, wb) ||
+              overlaps(W, wb, workspace, ws)))
+        return DUALGCN_ERR_INVALID_ARG;
+    if ((st = dgc::device_status())) return st;
+    return dgc::launch_weight_grad(X, xbf, G, gbf, dW, n, F_in, F_out, lr, W, workspace,
+                                   static_cast<hipStream_t>(stream));
+}
+
+int dualgcn_backward_data(const void *G, const float *W, const void *M, float *dX, int32_t n,
+                          int32_t F_in, int32_t F_out, uint32_t flags, void *stream) {
+    if (!G || n < 1) return DUALGCN_ERR_INVALID_ARG;
+    int st = check_update(G, W, dX, F_in, F_out);
+    if (st) return st;
+    if (flags & ~(DUALGCN_IN_BF16 | DUALGCN_GRAD_BF16)) return DUALGCN_ERR_INVALID_ARG;
+    const bool mbf = (flags & DUALGCN_IN_BF16) != 0, gbf = (flags & DUALGCN_GRAD_BF16) != 0;
+    const size_t un = static_cast<size_t>(n);
+    const size_t xb = un * F_in * sizeof(float);
+    if (overlaps(dX, xb, G, un * F_out * (gbf ? 2 : 4))) return DUALGCN_ERR_INVALID_ARG;
+    if (M && overlaps(dX, xb, M, un * F_in * (mbf ? 2 : 4))) return DUALGCN_ERR_INVALID_ARG;
+    if ((st = dgc::device_status())) return st;
+    return dgc::launch_backward_data(G, gbf, W, M, mbf, dX, n, F_in, F_out,
+                                     static_cast<hipStream_t>(stream));
+}
+
 int dualgcn_plan_query(const dualgcn_plan *plan, dualgcn_plan_info *out) {
     int st = check_plan(plan);
     if (st) return st;
@@ -322,7 +387,7 @@ int dualgcn_plan_query(const dualgcn_plan *plan, dualgcn_plan_info *out) {
     i.n_split_rows = p->n_split_rows;
     i.n_split_parts = p->n_split_parts;
     i.n_tasks = p->n_tasks;
-    i.n_long_rows = p->n_long;
+    i.n_long_rows = p->n_long[0];
     *out = i;
     return DUALGCN_OK;
 }

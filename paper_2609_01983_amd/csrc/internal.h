@@ -18,8 +18,12 @@ constexpr int kDenseChunk = 4096;
 // Widest feature window one SpMM launch covers; wider F is processed in windows.
 constexpr int kMaxSlice = 256;
 // Dense rows of at least 2^kLongRowOctave entries get a wavefront each; shorter dense
-// rows get one lane group each.
+// rows get one lane group each.  Narrow features mean small lane groups (more of them per
+// wavefront), so the SpMM lowers the bound by one octave per halving of the group below
+// 32 lanes, down to 2^(kLongRowOctave - kLongRowClasses + 1) entries: a group then never
+// walks more than 64 / (groups per wavefront) rounds of 16 entries alone.
 constexpr int kLongRowOctave = 9;
+constexpr int kLongRowClasses = 4;
 // A sparse-region task is a run of at most kTaskRows consecutive rows of the sorted
 // order whose first entries fall in one window of kTaskEntries entries.
 constexpr int kTaskRows = 8;
@@ -60,7 +64,8 @@ struct Plan {
 
     int32_t n_sparse = 0;
     int32_t n_tasks = 0;
-    int32_t n_long = 0;                // dense rows of >= 2^kLongRowOctave entries (the last ones)
+    int32_t n_long[kLongRowClasses] = {};   // dense rows of >= 2^(kLongRowOctave - c) entries
+                                            // (the last ones of the order)
     int32_t n_split_rows = 0;
     int32_t n_split_parts = 0;
     SplitPart *parts = nullptr;        // [n_split_parts]
@@ -131,5 +136,22 @@ int launch_xw(const void *X, bool in_bf16, const float *W, float *T, int32_t n, 
 int launch_gcn_layer(const Plan &p, const void *X, bool in_bf16, const float *W, void *Y,
                      bool out_bf16, int32_t F_in, int32_t F_out, bool relu, void *workspace,
                      hipStream_t stream);
+
+// dX = (bf16(G) bf16(W)^T) * [M > 0] (no mask when M is null); G is n x F_out (float32,
+// or bfloat16 if g_bf16), W is F_in x F_out, M and dX are n x F_in.
+int launch_backward_data(const void *G, bool g_bf16, const float *W, const void *M, bool m_bf16,
+                         float *dX, int32_t n, int32_t F_in, int32_t F_out, hipStream_t stream);
+
+// ---- training (train.hip)
+// Workgroups of the loss kernel; loss[1 .. kLossBlocks] hold their partial sums.
+constexpr int kLossBlocks = DUALGCN_LOSS_SLOTS - 1;
+int launch_softmax_xent(const float *Y, const int32_t *labels, int32_t n, int32_t C, float scale,
+                        float *G, double *loss, hipStream_t stream);
+// Bytes of the partial dW matrices of launch_weight_grad.
+size_t wgrad_workspace_bytes(int32_t n, int32_t F_in, int32_t F_out);
+// dW = bf16(X)^T bf16(G), summed over rows in a fixed order; with W, W -= lr dW.
+int launch_weight_grad(const void *X, bool x_bf16, const void *G, bool g_bf16, float *dW,
+                       int32_t n, int32_t F_in, int32_t F_out, float lr, float *W, void *workspace,
+                       hipStream_t stream);
 
 }  // namespace dgc

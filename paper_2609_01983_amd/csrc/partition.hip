@@ -360,8 +360,7 @@ struct SplitSummary {
     int32_t split_rows;
     uint32_t parts;
     uint32_t tasks;
-    int32_t long_rows;
-    int32_t pad;
+    int32_t long_rows[kLongRowClasses];   // dense rows of >= 2^(kLongRowOctave - c) entries
 };
 
 // n_sparse = first position whose key is >= K* (one thread; keys are sorted).
@@ -377,21 +376,24 @@ __global__ void lower_bound_kernel(const uint64_t *__restrict__ sorted, int32_t 
     out->split_rows = 0;
     out->parts = 0;
     out->tasks = 0;
-    out->long_rows = 0;
+    for (int c = 0; c < kLongRowClasses; ++c) out->long_rows[c] = 0;
 }
 
-// long_rows = rows of the dense region with at least 2^kLongRowOctave entries: the keys of
-// the processing order are sorted, so they are the rows from the first key >= that class.
+// long_rows[c] = rows of the dense region with at least 2^(kLongRowOctave - c) entries: the
+// keys of the processing order are sorted, so they are the rows from the first key >= that
+// class.
 __global__ void long_rows_kernel(const uint64_t *__restrict__ okey, int32_t n,
                                  SplitSummary *__restrict__ out) {
-    const uint64_t first_long = 32u + kLongRowOctave;
-    int32_t lo = 0, hi = n;
-    while (lo < hi) {
-        const int32_t mid = lo + (hi - lo) / 2;
-        if (okey[mid] < first_long) lo = mid + 1;
-        else hi = mid;
+    for (int c = 0; c < kLongRowClasses; ++c) {
+        const uint64_t first_long = 32u + kLongRowOctave - c;
+        int32_t lo = 0, hi = n;
+        while (lo < hi) {
+            const int32_t mid = lo + (hi - lo) / 2;
+            if (okey[mid] < first_long) lo = mid + 1;
+            else hi = mid;
+        }
+        out->long_rows[c] = n - lo;
     }
-    out->long_rows = n - lo;
 }
 
 // Processing order of the SpMM (the row order of the sorted copy): region first (sparse
@@ -943,7 +945,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if (ss.parts > max_parts) return DUALGCN_ERR_HIP;    // impossible: bounded above
     p->n_sparse = ss.n_sparse;
     p->n_tasks = static_cast<int32_t>(ss.tasks);
-    p->n_long = ss.long_rows;
+    for (int c = 0; c < kLongRowClasses; ++c) p->n_long[c] = ss.long_rows[c];
     p->n_split_rows = ss.split_rows;
     p->n_split_parts = static_cast<int32_t>(ss.parts);
     guard.p = nullptr;

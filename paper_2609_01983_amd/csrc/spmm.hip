@@ -410,7 +410,7 @@ int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bo
     a.n_sparse = p.n_sparse;
     a.n_tasks = p.n_tasks;
     a.n_parts = p.n_split_parts;
-    a.n_long = p.n_long;
+    a.n_long = p.n_long[0];
     a.ld = F;
     a.relu = relu ? 1 : 0;
 
@@ -422,8 +422,13 @@ int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bo
         a.f0 = f0;
         a.fend = f0 + w;
         if (vec) {
-            // whole rows: the smallest power-of-two lane group with 4 features per lane
+            // whole rows: the smallest power-of-two lane group with 4 features per lane;
+            // groups under 32 lanes hand rows from a lower length bound to wavefronts
             a.S = 1;
+            const int lpr = w <= 4 ? 1 : w <= 8 ? 2 : w <= 16 ? 4 : w <= 32 ? 8 : w <= 64 ? 16 : 32;
+            int cls = 0;
+            for (int g = lpr; g < 32 && cls < kLongRowClasses - 1; g *= 2) ++cls;
+            a.n_long = p.n_long[cls];
             if (w <= 4) st = launch_window<1, 4>(a, bf, s);
             else if (w <= 8) st = launch_window<2, 4>(a, bf, s);
             else if (w <= 16) st = launch_window<4, 4>(a, bf, s);

@@ -1,5 +1,7 @@
 // Update phase T = X W of a GCN layer on the gfx950 matrix cores (DualGCN Sec. 1:
-// after aggregation a layer multiplies by a small dense weight matrix).
+// after aggregation a layer multiplies by a small dense weight matrix), and the same
+// kernel for the backward product dX = (G_T W^T) * [M > 0] of training, which reads W
+// transposed and zeroes the outputs that the previous layer's ReLU did not pass.
 //
 // X (n x F_in, float32) is rounded to bfloat16 (nearest-even) in registers -- or is
 // read as stored when it already holds bfloat16 (the output of a previous layer's
@@ -36,6 +38,7 @@ constexpr int kRowsPerWave = 16;
 constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
 constexpr int kLdsElems = 32768;     // bf16 elements of W^T one workgroup stages (64 KiB)
 constexpr int kPad = 8;              // bf16 padding per LDS row (spreads LDS banks)
+constexpr int kMaxTiles = 16;        // 16-column output tiles per wavefront and launch
 
 // The bfloat16 A fragment of a lane at k-step ks: eight consecutive k of row `arow`
 // (zeros past the last row), from float32 X rounded here or from bfloat16 X as stored.
@@ -44,15 +47,15 @@ struct XFrag {
     f32x4 lo, hi;      // float32 X
     uint4 raw;         // bfloat16 X
 
-    __device__ __forceinline__ void load(const void *X, int64_t arow, bool ok, int F_in, int kk) {
+    __device__ __forceinline__ void load(const void *X, int64_t arow, bool ok, int ld, int kk) {
         if constexpr (XBF) {
             raw = make_uint4(0u, 0u, 0u, 0u);
-            if (ok) raw = *reinterpret_cast<const uint4 *>(static_cast<const unsigned short *>(X) + arow * F_in + kk);
+            if (ok) raw = *reinterpret_cast<const uint4 *>(static_cast<const unsigned short *>(X) + arow * ld + kk);
         } else {
             lo = f32x4{0.f, 0.f, 0.f, 0.f};
             hi = lo;
             if (ok) {
-                const float *xr = static_cast<const float *>(X) + arow * F_in + kk;
+                const float *xr = static_cast<const float *>(X) + arow * ld + kk;
                 lo = *reinterpret_cast<const f32x4 *>(xr);
                 hi = *reinterpret_cast<const f32x4 *>(xr + 4);
             }
@@ -72,26 +75,52 @@ struct XFrag {
     }
 };
 
-// T[:, c0 : c0 + 16 ntiles] = bf16(X) bf16(W[:, c0 : ..]) for every row tile; F_in % 32 == 0.
-template <int NTMAX, bool XBF>
+// Where the output keeps a product: no mask, or M > 0 for a float32 or bfloat16 M.
+enum MaskKind { kNoMask = 0, kMaskF32 = 1, kMaskBF16 = 2 };
+
+template <int MASK>
+__device__ __forceinline__ bool keep(const void *M, int64_t at) {
+    if constexpr (MASK == kMaskF32) {
+        return static_cast<const float *>(M)[at] > 0.f;
+    } else if constexpr (MASK == kMaskBF16) {
+        const uint32_t bits = static_cast<uint32_t>(static_cast<const unsigned short *>(M)[at]) << 16;
+        return __builtin_bit_cast(float, bits) > 0.f;
+    } else {
+        return true;
+    }
+}
+
+// Out[:, c0 : c0 + 16 ntiles] = bf16(A) bf16(B[:, c0 : ..]) for every row tile, where A is
+// n x K (row-major) and B(k, j) = W[k sk + j sn] is K x N: (sk, sn) = (N, 1) multiplies by
+// W, (1, K) by the transpose of a row-major N x K matrix W.  With a mask, outputs whose
+// M element (n x N, row-major) is not positive are written as zeros.  K % 32 == 0.
+template <int NTMAX, bool XBF, int MASK>
 __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const void *__restrict__ X,
                                                            const float *__restrict__ W,
+                                                           const void *__restrict__ M,
                                                            float *__restrict__ T, int32_t n,
-                                                           int32_t F_in, int32_t F_out,
-                                                           int32_t c0, int32_t ntiles) {
-    extern __shared__ unsigned short w_lds[];   // [16 ntiles][F_in + kPad]: W^T in bf16
-    const int ldw = F_in + kPad;
+                                                           int32_t K, int32_t N, int32_t sk,
+                                                           int32_t sn, int32_t c0, int32_t ntiles) {
+    extern __shared__ unsigned short w_lds[];   // [16 ntiles][K + kPad]: B^T in bf16
+    const int ldw = K + kPad;
     const int ncols = 16 * ntiles;
-    for (int idx = threadIdx.x; idx < F_in * ncols; idx += kThreads) {
-        const int c = idx / ncols, j = idx % ncols;
-        w_lds[j * ldw + c] = to_bf16(W[static_cast<int64_t>(c) * F_out + c0 + j]);
+    if (sn == 1) {          // consecutive threads read consecutive columns of W
+        for (int idx = threadIdx.x; idx < K * ncols; idx += kThreads) {
+            const int c = idx / ncols, j = idx % ncols;
+            w_lds[j * ldw + c] = to_bf16(W[static_cast<int64_t>(c) * sk + c0 + j]);
+        }
+    } else {                // consecutive threads read consecutive k of W's rows
+        for (int idx = threadIdx.x; idx < K * ncols; idx += kThreads) {
+            const int j = idx / K, c = idx % K;
+            w_lds[j * ldw + c] = to_bf16(W[static_cast<int64_t>(c0 + j) * sn + c]);
+        }
     }
     __syncthreads();
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lrow = lane & 15;          // A row / B column / D column inside the tile
     const int kgrp = lane >> 4;          // which 8-wide k group this lane supplies
-    const int ksteps = F_in / 32;
+    const int ksteps = K / 32;
     const int64_t tiles = (static_cast<int64_t>(n) + kRowsPerBlock - 1) / kRowsPerBlock;
 
     for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
@@ -103,9 +132,9 @@ __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const void *__restric
         for (int t = 0; t < NTMAX; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
         // k-step ks + 1 is requested while the MFMAs of k-step ks run
         XFrag<XBF> cur, nxt;
-        cur.load(X, arow, arow_ok, F_in, kgrp * 8);
+        cur.load(X, arow, arow_ok, K, kgrp * 8);
         for (int ks = 0; ks < ksteps; ++ks) {
-            nxt.load(X, arow, arow_ok && ks + 1 < ksteps, F_in, (ks + 1) * 32 + kgrp * 8);
+            nxt.load(X, arow, arow_ok && ks + 1 < ksteps, K, (ks + 1) * 32 + kgrp * 8);
             const bf16x8 av = cur.bf16();
             const int kk = ks * 32 + kgrp * 8;
 #pragma unroll
@@ -124,7 +153,10 @@ __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const void *__restric
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int64_t orow = row0 + kgrp * 4 + j;
-                    if (orow < n) T[orow * F_out + c0 + t * 16 + lrow] = acc[t][j];
+                    if (orow < n) {
+                        const int64_t at = orow * N + c0 + t * 16 + lrow;
+                        T[at] = keep<MASK>(M, at) ? acc[t][j] : 0.f;
+                    }
                 }
             }
         }
@@ -150,18 +182,51 @@ int allow_lds(const void *kernel, size_t bytes) {
                                           static_cast<int>(bytes)));
 }
 
-template <int NT, bool XBF>
-int launch_xw(const void *X, const float *W, float *T, int32_t n, int32_t F_in, int32_t F_out,
-              int c0, int ntiles, size_t lds, hipStream_t s) {
-    int st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<NT, XBF>), lds);
+template <int NT, bool XBF, int MASK>
+int launch_tiles(const void *X, const float *W, const void *M, float *T, int32_t n, int32_t K,
+                 int32_t N, int32_t sk, int32_t sn, int c0, int ntiles, size_t lds, hipStream_t s) {
+    int st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<NT, XBF, MASK>), lds);
     if (st) return st;
     // workgroups per CU allowed by the LDS of one CU (160 KiB) and by 2048 threads per CU
     const int per_cu = std::max<int>(1, std::min<int>(2048 / kThreads, static_cast<int>((160 * 1024) / lds)));
     const int64_t tiles = (static_cast<int64_t>(n) + kRowsPerBlock - 1) / kRowsPerBlock;
     const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(tiles, static_cast<int64_t>(num_cus()) * per_cu));
-    hipLaunchKernelGGL((xw_mfma_kernel<NT, XBF>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                       lds, s, X, W, T, n, F_in, F_out, c0, ntiles);
+    hipLaunchKernelGGL((xw_mfma_kernel<NT, XBF, MASK>), dim3(static_cast<unsigned>(grid)),
+                       dim3(kThreads), lds, s, X, W, M, T, n, K, N, sk, sn, c0, ntiles);
     return hip_status(hipGetLastError());
+}
+
+template <bool XBF, int MASK>
+int launch_nt(const void *X, const float *W, const void *M, float *T, int32_t n, int32_t K,
+              int32_t N, int32_t sk, int32_t sn, int c0, int ntiles, size_t lds, hipStream_t s) {
+    if (ntiles <= 4) return launch_tiles<4, XBF, MASK>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+    if (ntiles <= 8) return launch_tiles<8, XBF, MASK>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+    return launch_tiles<16, XBF, MASK>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+}
+
+// Out (n x N) = A (n x K) B (K x N) with B(k, j) = W[k sk + j sn], in column blocks whose
+// B^T slice fits the LDS budget.
+int launch_mm(const void *X, bool in_bf16, const float *W, int32_t sk, int32_t sn,
+              const void *M, int mask, float *T, int32_t n, int32_t K, int32_t N, hipStream_t s) {
+    const int cb = std::min<int>(std::min<int>(N, 16 * kMaxTiles), (kLdsElems / K) / 16 * 16);
+    if (cb < 16) return DUALGCN_ERR_UNSUPPORTED;
+    for (int c0 = 0; c0 < N; c0 += cb) {
+        const int width = std::min(cb, N - c0);
+        const int ntiles = width / 16;
+        const size_t lds = static_cast<size_t>(width) * (K + kPad) * sizeof(unsigned short);
+        int st;
+        if (in_bf16) {
+            if (mask == kMaskF32) st = launch_nt<true, kMaskF32>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+            else if (mask == kMaskBF16) st = launch_nt<true, kMaskBF16>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+            else st = launch_nt<true, kNoMask>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+        } else {
+            if (mask == kMaskF32) st = launch_nt<false, kMaskF32>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+            else if (mask == kMaskBF16) st = launch_nt<false, kMaskBF16>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+            else st = launch_nt<false, kNoMask>(X, W, M, T, n, K, N, sk, sn, c0, ntiles, lds, s);
+        }
+        if (st) return st;
+    }
+    return DUALGCN_OK;
 }
 
 }  // namespace
@@ -172,26 +237,13 @@ size_t xw_workspace_bytes(int32_t n, int32_t F_out) {
 
 int launch_xw(const void *X, bool in_bf16, const float *W, float *T, int32_t n, int32_t F_in,
               int32_t F_out, hipStream_t s) {
-    // column blocks whose W^T slice fits the LDS budget
-    const int cb = std::min<int>(F_out, (kLdsElems / F_in) / 16 * 16);
-    if (cb < 16) return DUALGCN_ERR_UNSUPPORTED;
-    for (int c0 = 0; c0 < F_out; c0 += cb) {
-        const int width = std::min(cb, F_out - c0);
-        const int ntiles = width / 16;
-        const size_t lds = static_cast<size_t>(width) * (F_in + kPad) * sizeof(unsigned short);
-        int st;
-        if (in_bf16) {
-            if (ntiles <= 4) st = launch_xw<4, true>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
-            else if (ntiles <= 8) st = launch_xw<8, true>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
-            else st = launch_xw<16, true>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
-        } else {
-            if (ntiles <= 4) st = launch_xw<4, false>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
-            else if (ntiles <= 8) st = launch_xw<8, false>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
-            else st = launch_xw<16, false>(X, W, T, n, F_in, F_out, c0, ntiles, lds, s);
-        }
-        if (st) return st;
-    }
-    return DUALGCN_OK;
+    return launch_mm(X, in_bf16, W, F_out, 1, nullptr, kNoMask, T, n, F_in, F_out, s);
+}
+
+int launch_backward_data(const void *G, bool g_bf16, const float *W, const void *M, bool m_bf16,
+                         float *dX, int32_t n, int32_t F_in, int32_t F_out, hipStream_t s) {
+    const int mask = M == nullptr ? kNoMask : (m_bf16 ? kMaskBF16 : kMaskF32);
+    return launch_mm(G, g_bf16, W, 1, F_out, M, mask, dX, n, F_out, F_in, s);
 }
 
 int launch_gcn_layer(const Plan &p, const void *X, bool in_bf16, const float *W, void *Y,

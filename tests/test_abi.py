@@ -86,6 +86,40 @@ def test_other_entry_points_reject_null(dg):
     L.dualgcn_plan_destroy(None)                     # no-op
 
 
+def test_training_entry_points_check_arguments(dg):
+    L = dg.lib()
+    # softmax cross-entropy: null pointers, empty shapes, overlapping outputs
+    assert L.dualgcn_softmax_xent(None, 64, 10, 4, 1.0, 1 << 20, 1 << 24, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_softmax_xent(1 << 20, 64, 0, 4, 1.0, 1 << 24, 1 << 28, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_softmax_xent(1 << 20, 64, 10, 1 << 20, 1.0, 1 << 34, 1 << 40, None) == dg.ERR_UNSUPPORTED
+    assert L.dualgcn_softmax_xent(1 << 20, 64, 10, 4, 1.0, (1 << 20) + 16, 1 << 28, None) == dg.ERR_INVALID_ARG
+    # weight gradient: workspace query, shapes, flags, alignment, workspace size
+    nbytes = ctypes.c_size_t()
+    assert L.dualgcn_weight_grad_workspace(0, 32, 32, ctypes.byref(nbytes)) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad_workspace(100, 32, 32, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad_workspace(100, 32, 64, ctypes.byref(nbytes)) == dg.OK
+    assert nbytes.value == 2 * 32 * 64 * 4                  # two 64-row chunks: two partials
+    assert L.dualgcn_weight_grad_workspace(1 << 22, 256, 128, ctypes.byref(nbytes)) == dg.OK
+    assert nbytes.value == 512 * 256 * 128 * 4
+    X, G, dW, ws = 1 << 30, 1 << 31, 1 << 32, 1 << 33
+    big = 1 << 28
+    assert L.dualgcn_weight_grad(None, G, dW, 100, 32, 32, 0, 0.0, None, ws, big, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad(X, G, dW, 100, 48, 32, 0, 0.0, None, ws, big, None) == dg.ERR_UNSUPPORTED
+    assert L.dualgcn_weight_grad(X, G, dW, 100, 32, 32, 1, 0.0, None, ws, big, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad(X, G + 8, dW, 100, 32, 32, 0, 0.0, None, ws, big, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad(X, G, dW, 100, 32, 32, 0, 0.0, None, ws + 16, big, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad(X, G, dW, 100, 32, 32, 0, 0.0, None, ws, 16, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad(X, G, X, 100, 32, 32, 0, 0.0, None, ws, big, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad(X, G, dW, 100, 32, 32, 0, 0.1, dW, ws, big, None) == dg.ERR_INVALID_ARG
+    # backward data
+    M, dX = 1 << 34, 1 << 35
+    assert L.dualgcn_backward_data(None, 16, M, dX, 10, 32, 32, 0, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_backward_data(G, 16, M, dX, 10, 32, 48, 0, None) == dg.ERR_UNSUPPORTED
+    assert L.dualgcn_backward_data(G, 16, M, dX, 10, 32, 32, 1, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_backward_data(G, 16, M, G, 10, 32, 32, 0, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_backward_data(G, 16, M, M, 10, 32, 32, 0, None) == dg.ERR_INVALID_ARG
+
+
 @pytest.mark.skipif(gpu_available(), reason="checks the no-device path")
 def test_valid_arguments_without_device_report_no_device(dg):
     L = dg.lib()

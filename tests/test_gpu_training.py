@@ -1,0 +1,301 @@
+"""GPU parity of the training path: the HIP kernels (through the C ABI) against the
+oracle's float64 chain rule.
+
+* softmax cross-entropy: G within 1e-5 * scale per element, the loss within 1e-5 of
+  scale * sum |terms|;
+* weight gradient and backward data (bf16 matrix cores): within 1e-2 * (|X|^T |G|)
+  and 1e-2 * (|G| |W|^T) per element, masks exact;
+* the transposed aggregation on a plan of A^T: the SpMM bound 1e-5 * sum |a||g|;
+* a whole two-layer training step on the c2 graph: within bounds propagated through
+  the chain from the per-stage budgets above.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from graphgen import configs, dense, small
+from graphgen.csr import transposed
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 1e-2
+
+
+@pytest.fixture(scope="module")
+def dg(device):
+    import paper_2609_01983_amd as dg
+    return dg
+
+
+def to_dev(g, device):
+    return (torch.from_numpy(np.ascontiguousarray(g.rowptr)).to(device),
+            torch.from_numpy(np.ascontiguousarray(g.col)).to(device),
+            torch.from_numpy(np.ascontiguousarray(g.val)).to(device))
+
+
+def _bf16_values(a):
+    """float32 array of the bfloat16 values torch stores for `a` (the test's own rounding,
+    used only to build inputs)."""
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16).float().numpy()
+
+
+def _within(got, want, bound, tol, what):
+    got = np.asarray(got, dtype=np.float64)
+    err = np.abs(got - want)
+    bad = ~(err <= tol * bound)
+    if bad.any():
+        i = tuple(np.argwhere(bad)[0])
+        raise AssertionError(f"{what}: {bad.sum()} outside; first at {i}: got {got[i]!r} "
+                             f"want {want[i]!r} bound {bound[i]!r}")
+
+
+# ---------------------------------------------------------------- softmax cross-entropy
+
+def _labels(n, C, seed):
+    y = dense.labels(n, C, seed, labeled_fraction=0.7)
+    y[::97] = C + 3                                   # out of range: unlabeled as well
+    return y
+
+
+def _loss_bound(Y, labels, scale):
+    Y = np.asarray(Y, dtype=np.float64)
+    C = Y.shape[1]
+    on = np.flatnonzero((labels >= 0) & (labels < C))
+    m = np.abs(Y).max(axis=1)
+    return scale * float((np.abs(Y[on, labels[on]]) + m[on] + np.log(C) + 1.0).sum())
+
+
+@pytest.mark.parametrize("n,C", [(1, 1), (300, 3), (1000, 16), (777, 17), (4096, 64), (513, 100)])
+def test_softmax_xent(dg, device, n, C):
+    Y = dense.features_normal(n, C, seed=n + C) * np.float32(3.0)
+    labels = _labels(n, C, seed=C)
+    scale = 1.0 / max(1, int(((labels >= 0) & (labels < C)).sum()))
+    G, loss = dg.softmax_xent(torch.from_numpy(Y).to(device), torch.from_numpy(labels).to(device),
+                              scale)
+    ref_loss, ref_G = oracle.softmax_xent(Y, labels, scale)
+    _within(G.cpu().numpy(), ref_G, np.full(ref_G.shape, scale), 1e-5, "G")
+    assert abs(loss[0].item() - ref_loss) <= 1e-5 * _loss_bound(Y, labels, scale)
+    # unlabeled rows get exactly zero gradient
+    off = (labels < 0) | (labels >= C)
+    assert np.all(G.cpu().numpy()[off] == 0.0)
+    # bit-reproducible
+    G2, loss2 = dg.softmax_xent(torch.from_numpy(Y).to(device), torch.from_numpy(labels).to(device),
+                                scale)
+    assert torch.equal(G, G2) and loss[0].item() == loss2[0].item()
+
+
+def test_softmax_xent_c5_shape(dg, device):
+    """The last layer of c5: n = 2^22 rows of 64 classes; every G row sampled, the loss whole."""
+    n, C = 1 << 22, 64
+    Y = dense.features_normal(n, C, seed=5, stream_id=7)
+    labels = _labels(n, C, seed=5)
+    scale = 1.0 / max(1, int(((labels >= 0) & (labels < C)).sum()))
+    G, loss = dg.softmax_xent(torch.from_numpy(Y).to(device), torch.from_numpy(labels).to(device),
+                              scale)
+    Gh = G.cpu().numpy()
+    rows = np.random.default_rng(1).choice(n, 4096, replace=False)
+    rows = np.concatenate([rows, [0, n - 1]])
+    _, ref_G = oracle.softmax_xent(Y[rows], labels[rows], scale)
+    _within(Gh[rows], ref_G, np.full(ref_G.shape, scale), 1e-5, "G sampled")
+    total = 0.0
+    for lo in range(0, n, 1 << 20):
+        total += oracle.softmax_xent(Y[lo:lo + (1 << 20)], labels[lo:lo + (1 << 20)], scale)[0]
+    assert abs(loss[0].item() - total) <= 1e-5 * _loss_bound(Y, labels, scale)
+
+
+# ---------------------------------------------------------------- weight gradient
+
+@pytest.mark.parametrize("n,fin,fout", [(1, 32, 32), (64, 32, 32), (1000, 32, 64), (4133, 256, 128),
+                                        (777, 128, 64), (2050, 1024, 256), (300, 96, 160),
+                                        (129, 512, 32)])
+@pytest.mark.parametrize("xbf,gbf", [(False, False), (True, True), (False, True), (True, False)])
+def test_weight_grad(dg, device, n, fin, fout, xbf, gbf):
+    X = dense.features_normal(n, fin, seed=fin + n)
+    G = dense.features_normal(n, fout, seed=fout + 7, stream_id=7)
+    Xt = torch.from_numpy(X).to(device)
+    Gt = torch.from_numpy(G).to(device)
+    if xbf:
+        Xt = Xt.to(torch.bfloat16)
+        X = _bf16_values(X)
+    if gbf:
+        Gt = Gt.to(torch.bfloat16)
+        G = _bf16_values(G)
+    dW = dg.weight_grad(Xt, Gt).cpu().numpy()
+    ref, B = oracle.weight_grad(X, G)
+    _within(dW, ref, B, BF16_TOL, f"dW {n}x{fin}x{fout}")
+    _check_rounded_operands(dW, X, G)
+    again = dg.weight_grad(Xt, Gt).cpu().numpy()
+    assert np.array_equal(dW, again)
+
+
+def _check_rounded_operands(dW, X, G):
+    """Against the exact product of the bfloat16 operands: only float32 accumulation is
+    left, at most (rows per partial / 32 + 34) 2^-24 of sum |x||g| with at most 2^13 rows
+    per partial below n = 2^22; 1e-4 of that sum covers it, and normwise 1e-4."""
+    Xr, Gr = _bf16_values(X), _bf16_values(G)
+    ref, B = oracle.weight_grad(Xr, Gr)
+    _within(dW, ref, B, 1e-4, "dW vs bf16 operands")
+    assert np.linalg.norm(dW - ref) <= 1e-4 * np.linalg.norm(ref) + 1e-30
+
+
+def test_weight_grad_sgd_step(dg, device):
+    n, fin, fout = 3000, 128, 64
+    X = torch.from_numpy(dense.features_normal(n, fin, seed=1)).to(device)
+    G = torch.from_numpy(dense.features_normal(n, fout, seed=2, stream_id=7)).to(device)
+    W0 = torch.from_numpy(dense.glorot(fin, fout, seed=3)).to(device)
+    W = W0.clone()
+    dW = dg.weight_grad(X, G, lr=0.05, W=W)
+    want = (W0.double() - 0.05 * dW.double()).cpu().numpy()
+    got = W.double().cpu().numpy()
+    assert np.all(np.abs(got - want) <= 1e-7 * (np.abs(want) + 0.05 * np.abs(dW.double().cpu().numpy())))
+
+
+def test_weight_grad_c5_layer1_shape(dg, device):
+    """dW1 at c5's shape (n = 2^22, 256 -> 128), X as the c5 features, G seeded."""
+    n, fin, fout = 1 << 22, 256, 128
+    X = dense.features_normal(n, fin, seed=0)
+    G = _bf16_values(dense.features_normal(n, fout, seed=9, stream_id=7) * np.float32(1e-3))
+    dW = dg.weight_grad(torch.from_numpy(X).to(device),
+                        torch.from_numpy(G).to(device).to(torch.bfloat16)).cpu().numpy()
+    ref = np.zeros((fin, fout))
+    B = np.zeros((fin, fout))
+    refr = np.zeros((fin, fout))
+    Br = np.zeros((fin, fout))
+    for lo in range(0, n, 1 << 19):
+        Xc, Gc = X[lo:lo + (1 << 19)], G[lo:lo + (1 << 19)]
+        r, b = oracle.weight_grad(Xc, Gc)
+        ref += r
+        B += b
+        r, b = oracle.weight_grad(_bf16_values(Xc), Gc)
+        refr += r
+        Br += b
+    _within(dW, ref, B, BF16_TOL, "dW c5 layer 1")
+    _within(dW, refr, Br, 1e-4, "dW c5 layer 1 vs bf16 operands")
+    assert np.linalg.norm(dW - refr) <= 1e-4 * np.linalg.norm(refr)
+
+
+# ---------------------------------------------------------------- backward data
+
+@pytest.mark.parametrize("n,fin,fout", [(1, 32, 32), (1000, 64, 32), (4133, 256, 128), (777, 128, 64),
+                                        (500, 1024, 64), (300, 96, 160), (65, 32, 256)])
+@pytest.mark.parametrize("mask", [None, "f32", "bf16"])
+@pytest.mark.parametrize("gbf", [False, True])
+def test_backward_data(dg, device, n, fin, fout, mask, gbf):
+    G = dense.features_normal(n, fout, seed=fout, stream_id=7)
+    W = dense.glorot(fin, fout, seed=fin)
+    Gt = torch.from_numpy(G).to(device)
+    if gbf:
+        Gt = Gt.to(torch.bfloat16)
+        G = _bf16_values(G)
+    M = Mt = None
+    if mask is not None:
+        M = dense.features_normal(n, fin, seed=3, stream_id=6)
+        M[::5] = 0.0                                   # zeros are masked, like negatives
+        Mt = torch.from_numpy(M).to(device)
+        if mask == "bf16":
+            Mt = Mt.to(torch.bfloat16)
+            M = _bf16_values(M)
+    dX = dg.backward_data(Gt, torch.from_numpy(W).to(device), Mt).cpu().numpy()
+    ref, B = oracle.backward_data(G, W, M)
+    _within(dX, ref, B, BF16_TOL, f"dX {n}x{fin}x{fout} mask={mask}")
+    # exact product of the bfloat16 operands: float32 sums over F_out <= 256 terms only
+    ref, B = oracle.backward_data(_bf16_values(G), _bf16_values(W), M)
+    _within(dX, ref, B, 1e-5, f"dX vs bf16 operands {n}x{fin}x{fout}")
+    if M is not None:
+        assert np.all(dX[M <= 0] == 0.0)
+
+
+# ---------------------------------------------------------------- transposed aggregation
+
+def test_transposed_aggregation_on_plan_of_transpose(dg, device):
+    rs = np.random.default_rng(3)
+    rows = [list(rs.choice(400, size=rs.integers(0, 30), replace=True)) for _ in range(400)]
+    rows[7] = list(range(400)) * 3                    # a hub row with duplicates
+    g = small.from_rows(rows)
+    g.val[:] = rs.uniform(-1, 1, g.col.size).astype(np.float32)
+    gt = transposed(g)
+    plan_t = dg.Plan(*to_dev(gt, device), seed=1, walks_per_node=8, walk_len=4)
+    G = dense.features_normal(400, 48, seed=2, stream_id=7)
+    got = dg.spmm(plan_t, torch.from_numpy(G).to(device)).cpu().numpy()
+    want = oracle.spmm_f64(oracle.transpose_csr(g), G)
+    gabs = small.from_rows(rows)
+    gabs.val[:] = np.abs(g.val)
+    B = oracle.spmm_f64(oracle.transpose_csr(gabs), np.abs(G))
+    _within(got, want, B, 1e-5, "A^T G")
+
+
+# ---------------------------------------------------------------- whole training step
+
+R_MFMA = 1e-2       # one bf16 matrix-core product (two roundings and float32 sums)
+R_SPMM = 1e-5       # one float32 aggregation
+R_STORE = 2.0 ** -8  # one bfloat16 store (nearest-even: at most 2^-9 relative)
+
+
+def test_two_layer_training_step_c2(dg, device):
+    g = configs.load_graph("c2")
+    w = configs.WORKLOADS["c2"]
+    X = configs.load_features("c2")
+    F0, F1, C = X.shape[1], 32, 32
+    W1 = dense.glorot(F0, F1, seed=0)
+    W2 = dense.glorot(F1, C, seed=0, stream_id=5)
+    labels = dense.labels(g.n, C, seed=0, labeled_fraction=0.1)
+    scale = 1.0 / int((labels >= 0).sum())
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    Xd = torch.from_numpy(X).to(device)
+    W1d = torch.from_numpy(W1).to(device)
+    W2d = torch.from_numpy(W2).to(device)
+    ld = torch.from_numpy(labels).to(device)
+    # forward
+    T1 = dg.update(Xd, W1d)
+    H1 = dg.spmm(plan, T1, relu=True, out_bf16=True)
+    T2 = dg.update(H1, W2d)
+    Y2 = dg.spmm(plan, T2)
+    # loss and backward
+    G2, loss = dg.softmax_xent(Y2, ld, scale)
+    dT2 = dg.spmm(plan, G2, out_bf16=True)
+    dW2 = dg.weight_grad(H1, dT2).cpu().numpy()
+    dH1 = dg.backward_data(dT2, W2d, H1)
+    dT1 = dg.spmm(plan, dH1, out_bf16=True)
+    dW1 = dg.weight_grad(Xd, dT1).cpu().numpy()
+
+    ref = oracle.gcn_train_grads(g, X, [W1, W2], labels, scale)
+    # error budgets propagated through the chain (float64, with |A| for every aggregation)
+    ga = type(g)(n=g.n, rowptr=g.rowptr, col=g.col, val=np.abs(g.val))
+    agg = lambda M: oracle.spmm_f64(ga, M)            # |A| M (= |A|^T M: symmetric)
+    aX, aW1, aW2 = np.abs(X.astype(np.float64)), np.abs(W1.astype(np.float64)), np.abs(W2.astype(np.float64))
+    E_T1 = R_MFMA * aX @ aW1
+    E_P1 = agg(E_T1) + R_SPMM * agg(aX @ aW1)
+    H1r = ref["H"][0]
+    E_H1 = E_P1 + R_STORE * (np.abs(H1r) + E_P1)
+    aH1 = np.abs(H1r) + E_H1
+    E_T2 = E_H1 @ aW2 + R_MFMA * aH1 @ aW2
+    E_Y2 = agg(E_T2) + R_SPMM * agg(aH1 @ aW2)
+    on = (labels >= 0) & (labels < C)
+    rowE = E_Y2.max(axis=1)
+    E_G2 = np.where(on[:, None], scale * (0.5 * rowE[:, None] + 1e-6), 0.0)
+    E_loss = scale * float((2 * rowE[on]).sum()) + 1e-5 * _loss_bound(ref["H"][1], labels, scale)
+    assert abs(loss[0].item() - ref["loss"]) <= E_loss
+    G2r = ref["G"][1]
+    dT2r = ref["GT"][1]
+    E_dT2 = agg(E_G2) + R_SPMM * agg(np.abs(G2r)) + R_STORE * (np.abs(dT2r) + agg(E_G2))
+    adT2 = np.abs(dT2r) + E_dT2
+    E_dW2 = E_H1.T @ adT2 + np.abs(H1r).T @ E_dT2 + R_MFMA * aH1.T @ adT2
+    _within(dW2, ref["dW"][1], E_dW2, 1.0, "dW2")
+    P1r = ref["P"][0]
+    ambiguous = np.abs(P1r) <= E_P1
+    keep = (P1r > 0) & ~ambiguous
+    full = adT2 @ aW2.T
+    E_dH1 = np.where(keep, E_dT2 @ aW2.T + R_MFMA * full, 0.0) + np.where(ambiguous, full * (1 + R_MFMA), 0.0)
+    dT1r = ref["GT"][0]
+    dH1r = ref["GP"][0]
+    E_dT1 = agg(E_dH1) + R_SPMM * agg(np.abs(dH1r)) + R_STORE * (np.abs(dT1r) + agg(E_dH1))
+    E_dW1 = aX.T @ E_dT1 + R_MFMA * aX.T @ (np.abs(dT1r) + E_dT1)
+    _within(dW1, ref["dW"][0], E_dW1, 1.0, "dW1")
+    # Those bounds hold whatever the signs, so over the n-row sums of dW they are loose.
+    # Normwise, r bfloat16 roundings of at most 2^-9 each perturb every product term by
+    # at most r 2^-9 (r <= 8 on any path here: 1.6%) and independent perturbations do not
+    # add up coherently: 3% normwise, 1% for the loss.
+    for got, want in ((dW1, ref["dW"][0]), (dW2, ref["dW"][1])):
+        assert np.linalg.norm(got - want) <= 3e-2 * np.linalg.norm(want)
+    assert abs(loss[0].item() - ref["loss"]) <= 1e-2 * abs(ref["loss"])
