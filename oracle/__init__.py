@@ -433,3 +433,29 @@ def gcn_train_grads(g, X, weights, labels, scale):
         if li > 0:
             G[li - 1] = GT[li] @ Ws[li].T
     return dict(loss=loss, dW=dW, T=T, P=P, H=H, G=G, GP=GP, GT=GT)
+
+
+# ------------------------------------------------------------------ aggregators (Sec. 2.1)
+# The aggregation phase multiplies by a matrix built from the adjacency; the paper's
+# general message-passing form admits other aggregators than the GCN normalisation.
+# Values are defined from the row lengths d of the matrix as given (self-loops included
+# when present), computed in float64 and rounded once to float32.
+AGG_GCN, AGG_MEAN, AGG_SUM = 0, 1, 2
+
+
+def aggregator_values(g, kind, eps=0.0):
+    """float32 values for the structure of g: GCN 1/sqrt(d_r d_c), mean 1/d_r, sum 1
+    (1 + eps on self-loop entries, the GIN form)."""
+    rowptr = np.asarray(g.rowptr, dtype=np.int64)
+    col = np.asarray(g.col, dtype=np.int64)
+    d = np.diff(rowptr).astype(np.float64)
+    rows = np.repeat(np.arange(g.n, dtype=np.int64), np.diff(rowptr))
+    if kind == AGG_GCN:
+        v = 1.0 / np.sqrt(d[rows] * d[col])
+    elif kind == AGG_MEAN:
+        v = 1.0 / d[rows]
+    elif kind == AGG_SUM:
+        v = np.where(rows == col, 1.0 + float(np.float32(eps)), 1.0)
+    else:
+        raise ValueError(kind)
+    return v.astype(np.float32)
