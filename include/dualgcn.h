@@ -146,6 +146,27 @@ int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_
 void dualgcn_plan_destroy(dualgcn_plan *plan);
 
 /*
+ * dualgcn_plan_save / dualgcn_plan_load -- keep a partition across runs (Sec. 3.2: the
+ * preprocessing is amortised over the training epochs).  The saved form is a host byte
+ * buffer: a header (parameters, the weight an adaptive alpha chose, the sizes and a
+ * 64-bit checksum of the row pointers and columns) and the density sums S (4 n bytes).
+ * Loading rebuilds the plan from S on the given CSR without walking: keys, threshold,
+ * sort and schedule are recomputed, so the plan equals the saved one exactly.
+ *
+ * save: with buf NULL, *bytes receives the size needed; otherwise *bytes must be at
+ * least that (else DUALGCN_ERR_INVALID_ARG, *bytes set to it) and receives the size
+ * written.  Waits for the device.
+ * load: csr must hold the same structure as the saved plan's matrix (same n, nnz and
+ * checksum, else DUALGCN_ERR_INVALID_ARG; the values may differ, e.g. another
+ * aggregator); a buffer that is not a saved plan (magic, version, size) is
+ * DUALGCN_ERR_INVALID_ARG.  Waits for `stream` like dualgcn_partition.  *out is NULL
+ * on error.
+ */
+int dualgcn_plan_save(const dualgcn_plan *plan, void *buf, size_t *bytes);
+int dualgcn_plan_load(const dualgcn_csr *csr, const void *buf, size_t bytes, void *stream,
+                      dualgcn_plan **out);
+
+/*
  * dualgcn_spmm -- Y = A X, the aggregation SpMM (Sec. 1, Sec. 2.1).
  *
  * X and Y are float32 row-major n x F, contiguous (leading dimension F), and
@@ -223,6 +244,29 @@ int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t 
 int dualgcn_gcn_layer(const dualgcn_plan *plan, const void *X, const float *W, void *Y,
                       int32_t F_in, int32_t F_out, uint32_t flags, void *workspace,
                       size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------ aggregators */
+
+enum { DUALGCN_AGG_GCN = 0, DUALGCN_AGG_MEAN = 1, DUALGCN_AGG_SUM = 2 };
+
+/*
+ * dualgcn_aggregator_values -- fills val (device, float32[nnz]) with the values of an
+ * aggregation matrix on the structure of csr (its rowptr and col; csr->val is not read
+ * and may be the same buffer as val).  Sec. 2.1: the aggregation phase multiplies by a
+ * matrix derived from the adjacency; the SpMM kernels take any values, so other
+ * aggregators run on the same plan.  With d_v the row length of v in the matrix as
+ * given (self-loops included when present):
+ *   DUALGCN_AGG_GCN   1 / sqrt(d_r d_c)                      (symmetric normalisation)
+ *   DUALGCN_AGG_MEAN  1 / d_r                                (GraphSAGE mean)
+ *   DUALGCN_AGG_SUM   1, and 1 + eps on self-loop entries    (GIN: A + (1 + eps) I
+ *                     when every row holds its self-loop once)
+ * computed in float64 and rounded once to float32.  The CSR is validated on the device
+ * first and the call waits for `stream` to report DUALGCN_ERR_BAD_CSR (val is then
+ * undefined).  A plan built before keeps its own copy of the values: build it again, or
+ * build it after filling val.
+ */
+int dualgcn_aggregator_values(const dualgcn_csr *csr, int32_t kind, float eps, float *val,
+                              void *stream);
 
 /* ------------------------------------------------------------------ training */
 

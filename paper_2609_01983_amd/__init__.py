@@ -81,6 +81,9 @@ def _load():
         "dualgcn_plan_query": ([P, ctypes.POINTER(PlanInfo)], ctypes.c_int),
         "dualgcn_plan_export": ([P, P, P, P], ctypes.c_int),
         "dualgcn_arw_patterns": ([ctypes.POINTER(Csr), U64, U32, U32, P, P], ctypes.c_int),
+        "dualgcn_plan_save": ([P, P, ctypes.POINTER(SZ)], ctypes.c_int),
+        "dualgcn_plan_load": ([ctypes.POINTER(Csr), P, SZ, P, ctypes.POINTER(P)], ctypes.c_int),
+        "dualgcn_aggregator_values": ([ctypes.POINTER(Csr), I32, ctypes.c_float, P, P], ctypes.c_int),
         "dualgcn_softmax_xent": ([P, P, I32, I32, ctypes.c_float, P, P, P], ctypes.c_int),
         "dualgcn_weight_grad_workspace": ([I32, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "dualgcn_weight_grad": ([P, P, P, I32, I32, I32, U32, ctypes.c_float, P, P, SZ, P],
@@ -174,6 +177,28 @@ class Plan:
                                         K.ctypes.data), "dualgcn_plan_export")
         return perm, S, K
 
+    def save(self):
+        """The plan as bytes (parameters, checksum of the structure, density sums)."""
+        nbytes = ctypes.c_size_t()
+        _check(_lib.dualgcn_plan_save(self.handle, None, ctypes.byref(nbytes)), "dualgcn_plan_save")
+        buf = ctypes.create_string_buffer(nbytes.value)
+        _check(_lib.dualgcn_plan_save(self.handle, buf, ctypes.byref(nbytes)), "dualgcn_plan_save")
+        return buf.raw[:nbytes.value]
+
+    @classmethod
+    def load(cls, rowptr, col, val, blob, stream=None):
+        """Rebuilds a saved plan on the same structure (values may differ), without walks."""
+        self = cls.__new__(cls)
+        self._keep = (rowptr, col, val)
+        self.csr = make_csr(rowptr, col, val)
+        self.n = self.csr.n
+        out = ctypes.c_void_p()
+        buf = ctypes.create_string_buffer(bytes(blob), len(blob))
+        _check(_lib.dualgcn_plan_load(ctypes.byref(self.csr), buf, len(blob), _stream(stream),
+                                      ctypes.byref(out)), "dualgcn_plan_load")
+        self._h = out
+        return self
+
     def destroy(self):
         if getattr(self, "_h", None):
             _lib.dualgcn_plan_destroy(self._h)
@@ -265,6 +290,25 @@ def gcn_layer(plan, X, W, relu=False, Y=None, workspace=None, out_bf16=False, st
                                   F_out, flags, workspace.data_ptr(),
                                   workspace.numel(), _stream(stream)), "dualgcn_gcn_layer")
     return Y
+
+
+# ------------------------------------------------------------------ aggregators
+
+AGG_GCN, AGG_MEAN, AGG_SUM = 0, 1, 2
+_AGG = {"gcn": AGG_GCN, "mean": AGG_MEAN, "sum": AGG_SUM,
+        AGG_GCN: AGG_GCN, AGG_MEAN: AGG_MEAN, AGG_SUM: AGG_SUM}
+
+
+def aggregator_values(rowptr, col, kind="gcn", eps=0.0, val=None, stream=None):
+    """float32 values of an aggregation matrix on this structure: "gcn" 1/sqrt(d_r d_c),
+    "mean" 1/d_r, "sum" 1 with 1 + eps on self-loops (GIN).  Validates the CSR (waits)."""
+    if val is None:
+        val = torch.empty(col.numel(), dtype=torch.float32, device=col.device)
+    csr = make_csr(rowptr, col, val)
+    _check(_lib.dualgcn_aggregator_values(ctypes.byref(csr), _AGG[kind], float(eps),
+                                          val.data_ptr() if val.numel() else None,
+                                          _stream(stream)), "dualgcn_aggregator_values")
+    return val
 
 
 # ------------------------------------------------------------------ training
@@ -381,4 +425,5 @@ __all__ = ["Plan", "spmm", "update", "gcn_layer", "gcn_layer_workspace_bytes", "
            "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
            "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16",
            "ALPHA_ADAPTIVE", "GRAD_BF16", "LOSS_SLOTS", "softmax_xent", "weight_grad",
-           "weight_grad_workspace_bytes", "backward_data"]
+           "weight_grad_workspace_bytes", "backward_data", "aggregator_values", "AGG_GCN",
+           "AGG_MEAN", "AGG_SUM"]

@@ -1,5 +1,6 @@
 // C ABI of libdualgcn: argument checks, status codes and dispatch to the kernels.
 // Every check that needs no device runs before the device is touched.
+#include <cstring>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -214,7 +215,7 @@ int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_
     if (!keys_fit(t.alpha_den, walks_per_node, walk_len, csr->nnz)) return DUALGCN_ERR_UNSUPPORTED;
     if ((st = dgc::device_status())) return st;
     Plan *p = nullptr;
-    st = dgc::build_plan(csr, seed, walks_per_node, walk_len, t,
+    st = dgc::build_plan(csr, seed, walks_per_node, walk_len, t, nullptr,
                          static_cast<hipStream_t>(stream), &p);
     if (st) return st;
     *out = reinterpret_cast<dualgcn_plan *>(p);
@@ -426,6 +427,118 @@ int dualgcn_arw_patterns(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_p
     if (!st)
         st = dgc::launch_arw(csr->rowptr, csr->col, csr->n, seed, walks_per_node, walk_len, S, out,
                              flags, s);
+    int32_t bad = 0;
+    if (!st) st = dgc::hip_status(hipMemcpyAsync(&bad, flags, sizeof(bad), hipMemcpyDeviceToHost, s));
+    if (!st) st = dgc::hip_status(hipStreamSynchronize(s));
+    (void)hipFree(scratch);
+    if (!st && bad) st = DUALGCN_ERR_BAD_CSR;
+    return st;
+}
+
+// Saved plans: this header, then the n density sums S (uint32).
+struct PlanFileHeader {
+    char magic[8];
+    uint32_t version;
+    uint32_t header_bytes;
+    int32_t n;
+    int32_t reserved;
+    int64_t nnz;
+    uint64_t seed;
+    uint32_t k, d;
+    dualgcn_thresholds th;
+    int32_t reserved2;
+    uint64_t checksum;
+};
+constexpr char kPlanMagic[8] = {'D', 'G', 'C', 'N', 'P', 'L', 'A', 'N'};
+constexpr uint32_t kPlanVersion = 1;
+
+int dualgcn_plan_save(const dualgcn_plan *plan, void *buf, size_t *bytes) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if (!bytes) return DUALGCN_ERR_INVALID_ARG;
+    const Plan *p = as_plan(plan);
+    const size_t need = sizeof(PlanFileHeader) + sizeof(uint32_t) * static_cast<size_t>(p->n);
+    if (!buf) {
+        *bytes = need;
+        return DUALGCN_OK;
+    }
+    if (*bytes < need) {
+        *bytes = need;
+        return DUALGCN_ERR_INVALID_ARG;
+    }
+    PlanFileHeader h{};
+    std::memcpy(h.magic, kPlanMagic, sizeof(h.magic));
+    h.version = kPlanVersion;
+    h.header_bytes = sizeof(PlanFileHeader);
+    h.n = p->n;
+    h.nnz = p->nnz;
+    h.seed = p->seed;
+    h.k = p->k;
+    h.d = p->d;
+    h.th = p->th;               // with an adaptive alpha: the weight it chose
+    if ((st = dgc::structure_checksum(p->rowptr, p->col, p->n, p->nnz, nullptr, &h.checksum)))
+        return st;
+    std::memcpy(buf, &h, sizeof(h));
+    if ((st = dgc::hip_status(hipMemcpy(static_cast<char *>(buf) + sizeof(h), p->S,
+                                        sizeof(uint32_t) * static_cast<size_t>(p->n),
+                                        hipMemcpyDeviceToHost))))
+        return st;
+    *bytes = need;
+    return DUALGCN_OK;
+}
+
+int dualgcn_plan_load(const dualgcn_csr *csr, const void *buf, size_t bytes, void *stream,
+                      dualgcn_plan **out) {
+    if (!out) return DUALGCN_ERR_INVALID_ARG;
+    *out = nullptr;
+    int st = check_csr(csr);
+    if (st) return st;
+    if (!buf || bytes < sizeof(PlanFileHeader)) return DUALGCN_ERR_INVALID_ARG;
+    PlanFileHeader h;
+    std::memcpy(&h, buf, sizeof(h));
+    if (std::memcmp(h.magic, kPlanMagic, sizeof(h.magic)) || h.version != kPlanVersion ||
+        h.header_bytes != sizeof(PlanFileHeader))
+        return DUALGCN_ERR_INVALID_ARG;
+    if (h.n != csr->n || h.nnz != csr->nnz ||
+        bytes != sizeof(PlanFileHeader) + sizeof(uint32_t) * static_cast<size_t>(h.n))
+        return DUALGCN_ERR_INVALID_ARG;
+    const dualgcn_thresholds &t = h.th;
+    if ((st = check_walks(h.k, h.d))) return st;
+    if (t.alpha_den == 0 || t.beta_den == 0 || t.alpha_num > t.alpha_den ||
+        t.alpha_den >= kMaxRational || t.beta_den >= kMaxRational || t.beta_num >= kMaxRational ||
+        t.force_mode < DUALGCN_FORCE_AUTO || t.force_mode > DUALGCN_FORCE_DENSE)
+        return DUALGCN_ERR_INVALID_ARG;
+    if (!keys_fit(t.alpha_den, h.k, h.d, csr->nnz)) return DUALGCN_ERR_UNSUPPORTED;
+    if ((st = dgc::device_status())) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint64_t sum = 0;
+    if ((st = dgc::structure_checksum(csr->rowptr, csr->col, csr->n, csr->nnz, s, &sum))) return st;
+    if (sum != h.checksum) return DUALGCN_ERR_INVALID_ARG;
+    const uint32_t *S = reinterpret_cast<const uint32_t *>(static_cast<const char *>(buf) + sizeof(h));
+    Plan *p = nullptr;
+    if ((st = dgc::build_plan(csr, h.seed, h.k, h.d, t, S, s, &p))) return st;
+    *out = reinterpret_cast<dualgcn_plan *>(p);
+    return DUALGCN_OK;
+}
+
+int dualgcn_aggregator_values(const dualgcn_csr *csr, int32_t kind, float eps, float *val,
+                              void *stream) {
+    int st = check_csr(csr);
+    if (st) return st;
+    if (!val || kind < DUALGCN_AGG_GCN || kind > DUALGCN_AGG_SUM) return DUALGCN_ERR_INVALID_ARG;
+    if (overlaps(val, sizeof(float) * static_cast<size_t>(csr->nnz), csr->rowptr,
+                 sizeof(int32_t) * (static_cast<size_t>(csr->n) + 1)) ||
+        (csr->nnz > 0 && overlaps(val, sizeof(float) * static_cast<size_t>(csr->nnz), csr->col,
+                                  sizeof(int32_t) * static_cast<size_t>(csr->nnz))))
+        return DUALGCN_ERR_INVALID_ARG;
+    if ((st = dgc::device_status())) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *scratch = nullptr;   // 2 validation words
+    if ((st = dgc::alloc_bytes(&scratch, 2 * sizeof(int32_t)))) return st;
+    int32_t *flags = static_cast<int32_t *>(scratch);
+    st = dgc::hip_status(hipMemsetAsync(flags, 0, 2 * sizeof(int32_t), s));
+    if (!st) st = dgc::validate_csr(csr, flags, nullptr, nullptr, s);
+    if (!st) st = dgc::launch_aggregator_values(csr, kind, eps, val, s);
     int32_t bad = 0;
     if (!st) st = dgc::hip_status(hipMemcpyAsync(&bad, flags, sizeof(bad), hipMemcpyDeviceToHost, s));
     if (!st) st = dgc::hip_status(hipStreamSynchronize(s));

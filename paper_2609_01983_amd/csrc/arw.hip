@@ -159,6 +159,59 @@ __device__ __forceinline__ void walk_lockstep(const int2 *__restrict__ nodeinfo,
     }
 }
 
+// The same lockstep walks over successor records: succ[e] = (col[e], first entry of that
+// node, its degree), so one read per step yields the next node together with what the
+// step after it needs -- one dependent random read per step instead of two.
+template <int MAXD, int WPL>
+__device__ __forceinline__ void walk_lockstep_succ(const int2 *__restrict__ nodeinfo,
+                                                   const int4 *__restrict__ succ, uint32_t v,
+                                                   uint32_t w0, uint32_t d, uint64_t seed,
+                                                   uint32_t (&u)[WPL]) {
+    int32_t path[WPL][MAXD + 1];
+    int32_t cur[WPL], first[WPL], deg[WPL];
+    bool live[WPL];
+    Block4 blk[WPL];
+    const int2 start = nodeinfo[v];
+#pragma unroll
+    for (int j = 0; j < WPL; ++j) {
+        path[j][0] = static_cast<int32_t>(v);
+        cur[j] = static_cast<int32_t>(v);
+        first[j] = start.x;
+        deg[j] = start.y;
+        live[j] = true;
+        u[j] = 1;
+    }
+#pragma unroll
+    for (int s = 0; s < MAXD; ++s) {
+        if (static_cast<uint32_t>(s) >= d) break;
+        int4 rec[WPL];            // (next node, its first entry, its degree, unused)
+#pragma unroll
+        for (int j = 0; j < WPL; ++j) {
+            rec[j] = make_int4(cur[j], first[j], deg[j], 0);
+            if (live[j] && deg[j] > 0) {
+                if ((s & 7) == 0) blk[j] = philox4x64_10(v, w0 + j, static_cast<uint64_t>(s >> 3), 0, seed, 0);
+                const uint32_t r = half_word(blk[j], s);
+                rec[j] = succ[first[j] + static_cast<int32_t>(__umulhi(r, static_cast<uint32_t>(deg[j])))];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < WPL; ++j) {
+            const int32_t nxt = rec[j].x;
+            if (live[j]) {
+                bool seen = false;
+#pragma unroll
+                for (int i = 0; i <= s; ++i) seen |= path[j][i] == nxt;
+                if (!seen) ++u[j];
+                live[j] = !(deg[j] <= 1 && nxt == cur[j]);   // absorbed: stays put for good
+            }
+            path[j][s + 1] = nxt;
+            cur[j] = nxt;
+            first[j] = rec[j].y;
+            deg[j] = rec[j].z;
+        }
+    }
+}
+
 // One lane per (node, walk); with `patterns` the labels are written out.
 template <int MAXD, bool UNROLL>
 __global__ __launch_bounds__(256) void arw_kernel(const int32_t *__restrict__ rowptr,
@@ -197,6 +250,7 @@ __global__ __launch_bounds__(256) void arw_kernel(const int32_t *__restrict__ ro
 template <int MAXD, int WPL>
 __global__ __launch_bounds__(256) void arw_sum_kernel(const int2 *__restrict__ nodeinfo,
                                                       const int32_t *__restrict__ col,
+                                                      const int4 *__restrict__ succ,
                                                       int32_t n, uint64_t seed, uint32_t d,
                                                       int k_log2, uint32_t *__restrict__ S,
                                                       const int32_t *__restrict__ bad_flag) {
@@ -209,7 +263,10 @@ __global__ __launch_bounds__(256) void arw_sum_kernel(const int2 *__restrict__ n
     uint32_t u = 0;
     if (valid) {
         uint32_t uj[WPL];
-        walk_lockstep<MAXD, WPL>(nodeinfo, col, v, w0, d, seed, uj);
+        if (succ)
+            walk_lockstep_succ<MAXD, WPL>(nodeinfo, succ, v, w0, d, seed, uj);
+        else
+            walk_lockstep<MAXD, WPL>(nodeinfo, col, v, w0, d, seed, uj);
 #pragma unroll
         for (int j = 0; j < WPL; ++j) u += uj[j];
     }
@@ -219,8 +276,8 @@ __global__ __launch_bounds__(256) void arw_sum_kernel(const int2 *__restrict__ n
 
 }  // namespace
 
-int launch_density(const int2 *nodeinfo, const int32_t *col, int32_t n, uint64_t seed,
-                   uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
+int launch_density(const int2 *nodeinfo, const int32_t *col, const int4 *succ, int32_t n,
+                   uint64_t seed, uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
                    hipStream_t stream) {
     int k_log2 = -1;
     if ((k & (k - 1)) == 0) {
@@ -231,7 +288,7 @@ int launch_density(const int2 *nodeinfo, const int32_t *col, int32_t n, uint64_t
     const int64_t blocks = (static_cast<int64_t>(n) * k / 2 + 255) / 256;   // two walks per lane
     if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
     hipLaunchKernelGGL((arw_sum_kernel<8, 2>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                       stream, nodeinfo, col, n, seed, d, k_log2, S, bad_flag);
+                       stream, nodeinfo, col, succ, n, seed, d, k_log2, S, bad_flag);
     return hip_status(hipGetLastError());
 }
 

@@ -95,10 +95,12 @@ int launch_arw(const int32_t *rowptr, const int32_t *col, int32_t n, uint64_t se
                uint32_t d, uint32_t *S, uint8_t *patterns, const int32_t *bad_flag,
                hipStream_t stream);
 // The same sums from nodeinfo (every node's (first entry, degree), as validate_csr writes
-// it), two walks per lane advanced in lockstep.  DUALGCN_ERR_UNSUPPORTED (nothing
-// launched) unless d <= 8 and k is a power of two in [2, 128].
-int launch_density(const int2 *nodeinfo, const int32_t *col, int32_t n, uint64_t seed,
-                   uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
+// it), two walks per lane advanced in lockstep.  With succ (succ[e] = (col[e], first entry
+// and degree of that node)) each step reads one record instead of a node's bounds and then
+// a column.  DUALGCN_ERR_UNSUPPORTED (nothing launched) unless d <= 8 and k is a power of
+// two in [2, 128].
+int launch_density(const int2 *nodeinfo, const int32_t *col, const int4 *succ, int32_t n,
+                   uint64_t seed, uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
                    hipStream_t stream);
 
 // ---- partition (partition.hip)
@@ -109,8 +111,13 @@ int launch_density(const int2 *nodeinfo, const int32_t *col, int32_t n, uint64_t
 constexpr int kValidateBlocks = 2048;
 int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t *blockmax,
                  hipStream_t stream);
+// S_host (host, n sums), when given, replaces the walks: the density sums of a saved plan.
 int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
-               const dualgcn_thresholds &th, hipStream_t stream, Plan **out);
+               const dualgcn_thresholds &th, const uint32_t *S_host, hipStream_t stream,
+               Plan **out);
+// An order-free 64-bit checksum of a CSR structure (row pointers and columns); waits.
+int structure_checksum(const int32_t *rowptr, const int32_t *col, int32_t n, int64_t nnz,
+                       hipStream_t stream, uint64_t *out);
 void free_plan(Plan *p);
 
 // float32 -> bfloat16 bits, round to nearest even; NaNs stay NaN.
@@ -141,6 +148,11 @@ int launch_gcn_layer(const Plan &p, const void *X, bool in_bf16, const float *W,
 // or bfloat16 if g_bf16), W is F_in x F_out, M and dX are n x F_in.
 int launch_backward_data(const void *G, bool g_bf16, const float *W, const void *M, bool m_bf16,
                          float *dX, int32_t n, int32_t F_in, int32_t F_out, hipStream_t stream);
+
+// ---- aggregator values (aggregate.hip): val[e] for the structure of csr (no validation;
+// out-of-range columns read nothing).
+int launch_aggregator_values(const dualgcn_csr *csr, int kind, float eps, float *val,
+                             hipStream_t stream);
 
 // ---- training (train.hip)
 // Workgroups of the loss kernel; loss[1 .. kLossBlocks] hold their partial sums.

@@ -95,6 +95,70 @@ __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__res
     }
 }
 
+// Successor records of the walks: succ[e] = (c, first entry of c, degree of c) for
+// c = col[e], from the node records validate_kernel wrote.  A column out of range (the
+// validation flags it, and nothing walks then) gets a record without reading them.
+__global__ __launch_bounds__(kThreads) void successor_kernel(const int2 *__restrict__ nodeinfo,
+                                                             const int32_t *__restrict__ col,
+                                                             int32_t n, int64_t nnz,
+                                                             int4 *__restrict__ succ) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < nnz;
+         e += stride) {
+        const int32_t c = col[e];
+        int4 r = make_int4(c, 0, 0, 0);
+        if (c >= 0 && c < n) {
+            const int2 ni = nodeinfo[c];
+            r.y = ni.x;
+            r.z = ni.y;
+        }
+        succ[e] = r;
+    }
+}
+
+// ------------------------------------------------------------------ structure checksum
+
+// splitmix64's output function (Steele, Lea & Flood, OOPSLA'14): a bijective mix of one
+// 64-bit word.
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+constexpr int kSumBlocks = 1024;
+
+// partial[b] = sum (mod 2^64) of mix64 over this workgroup's entries of rowptr (tagged by
+// position) and col (tagged by position and a different constant): order-free, exact.
+__global__ __launch_bounds__(kThreads) void checksum_kernel(const int32_t *__restrict__ rowptr,
+                                                            const int32_t *__restrict__ col,
+                                                            int32_t n, int64_t nnz,
+                                                            uint64_t *__restrict__ partial) {
+    __shared__ uint64_t sh[kThreads];
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    uint64_t acc = 0;
+    for (int64_t i = t0; i <= n; i += stride)
+        acc += mix64((static_cast<uint64_t>(i) << 32) ^ static_cast<uint32_t>(rowptr[i]));
+    for (int64_t e = t0; e < nnz; e += stride)
+        acc += mix64(((static_cast<uint64_t>(e) << 32) ^ static_cast<uint32_t>(col[e])) +
+                     0x9E3779B97F4A7C15ull);
+    const int t = threadIdx.x;
+    sh[t] = acc;
+    __syncthreads();
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        if (t < h) sh[t] += sh[t + h];
+        __syncthreads();
+    }
+    if (t == 0) partial[blockIdx.x] = sh[0];
+}
+
+__global__ void checksum_fold_kernel(uint64_t *__restrict__ partial) {
+    uint64_t s = 0;
+    for (int i = 0; i < kSumBlocks; ++i) s += partial[i];
+    partial[kSumBlocks] = s;
+}
+
 // ------------------------------------------------------------------ keys and moments
 
 struct Moments {
@@ -714,8 +778,25 @@ void free_plan(Plan *p) {
     delete p;
 }
 
+int structure_checksum(const int32_t *rowptr, const int32_t *col, int32_t n, int64_t nnz,
+                       hipStream_t s, uint64_t *out) {
+    void *buf = nullptr;
+    int st = alloc_bytes(&buf, sizeof(uint64_t) * (kSumBlocks + 1));
+    if (st) return st;
+    uint64_t *partial = static_cast<uint64_t *>(buf);
+    hipLaunchKernelGGL(checksum_kernel, dim3(kSumBlocks), dim3(kThreads), 0, s, rowptr, col, n, nnz,
+                       partial);
+    hipLaunchKernelGGL(checksum_fold_kernel, dim3(1), dim3(1), 0, s, partial);
+    st = hip_status(hipGetLastError());
+    if (!st) st = hip_status(hipMemcpyAsync(out, partial + kSumBlocks, sizeof(uint64_t),
+                                            hipMemcpyDeviceToHost, s));
+    if (!st) st = hip_status(hipStreamSynchronize(s));
+    (void)hipFree(buf);
+    return st;
+}
+
 int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
-               const dualgcn_thresholds &th, hipStream_t s, Plan **out) {
+               const dualgcn_thresholds &th, const uint32_t *S_host, hipStream_t s, Plan **out) {
     const int32_t n = csr->n;
     const int64_t nnz = csr->nnz;
     const size_t un = static_cast<size_t>(n), unnz = static_cast<size_t>(nnz);
@@ -746,6 +827,10 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     // build in another: two allocations per plan.  Split parts are bounded by
     // sum over rows longer than C of ceil(deg / C) < 2 nnz / C + 1.
     const size_t max_parts = unnz / kDenseChunk * 2 + 1;
+    // The lockstep walker reads successor records (16 bytes per entry, scratch) when the
+    // walks take at least 16 steps per node: building them costs one random read per entry
+    // and saves one dependent random read per step.
+    const bool use_succ = S_host == nullptr && static_cast<uint64_t>(k) * d >= 16;
     const int32_t nb_keys = static_cast<int32_t>(std::min<int64_t>((n + kThreads - 1) / kThreads, 1024));
     const int32_t nblocks = static_cast<int32_t>((static_cast<int64_t>(n) + kTile - 1) / kTile);
     const int64_t scan_tiles = std::max((static_cast<int64_t>(kRadix) * nblocks + kTile - 1) / kTile,
@@ -766,6 +851,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_ssum = ls.take(sizeof(SplitSummary)), o_counts = ls.take(sizeof(uint32_t) * 2 * un),
                  o_tiles = ls.take(sizeof(int32_t) * (unnz / kCopyTile + 2)),
                  o_info = ls.take(sizeof(int2) * un),
+                 o_succ = ls.take(use_succ ? sizeof(int4) * unnz : 0),
                  o_bmax = ls.take(sizeof(int32_t) * kValidateBlocks);
     if ((st = alloc_block(&p->mem, &p->mem_bytes, lp.bytes))) return st;
     ScratchBlock scratch;
@@ -799,11 +885,25 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
 
     if ((st = hip_status(hipMemsetAsync(bad, 0, 2 * sizeof(int32_t), s)))) return st;
     if ((st = validate_csr(csr, bad, nodeinfo, blockmax, s))) return st;
-    // walks: the lockstep walker where it applies, else one walk per lane
-    st = launch_density(nodeinfo, csr->col, n, seed, k, d, p->S, bad, s);
-    if (st == DUALGCN_ERR_UNSUPPORTED)
-        st = launch_arw(csr->rowptr, csr->col, n, seed, k, d, p->S, nullptr, bad, s);
-    if (st) return st;
+    int4 *succ = nullptr;
+    if (use_succ && nnz > 0) {
+        succ = reinterpret_cast<int4 *>(sm + o_succ);
+        const int64_t sblocks = std::min<int64_t>((nnz + kThreads - 1) / kThreads, 65536);
+        hipLaunchKernelGGL(successor_kernel, dim3(static_cast<unsigned>(sblocks)), dim3(kThreads), 0,
+                           s, nodeinfo, csr->col, n, nnz, succ);
+    }
+    if (S_host) {
+        // the density sums of a saved plan of this matrix: no walks
+        if ((st = hip_status(hipMemcpyAsync(p->S, S_host, sizeof(uint32_t) * un,
+                                            hipMemcpyHostToDevice, s))))
+            return st;
+    } else {
+        // walks: the lockstep walker where it applies, else one walk per lane
+        st = launch_density(nodeinfo, csr->col, succ, n, seed, k, d, p->S, bad, s);
+        if (st == DUALGCN_ERR_UNSUPPORTED)
+            st = launch_arw(csr->rowptr, csr->col, n, seed, k, d, p->S, nullptr, bad, s);
+        if (st) return st;
+    }
     // adaptive alpha: moments of S and of D (two passes of the key kernel with the
     // weights (1, 0) and (0, 1)), one more host wait, the weight chosen on the host
     uint64_t pa = th.alpha_num;

@@ -19,6 +19,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace dgc {
 namespace {
@@ -81,11 +82,98 @@ __global__ __launch_bounds__(kThreads) void softmax_xent_kernel(
     if (threadIdx.x == 0) partial[blockIdx.x] = sh[0];
 }
 
-// loss[0] = scale * sum of the partials, in workgroup order.
-__global__ void loss_total_kernel(double *__restrict__ loss, int32_t count, float scale) {
+// The same for C % 4 == 0, C <= 64 QPL, 16-byte aligned rows: every lane keeps QPL float4 of
+// each of RPG rows in registers (one read of Y, one write of G), and a group has the loads
+// of all RPG rows in flight before it reduces any of them.
+template <int QPL, int RPG>
+__global__ __launch_bounds__(kThreads) void softmax_xent_vec_kernel(
+    const float *__restrict__ Y, const int32_t *__restrict__ labels, int32_t n, int32_t C,
+    float scale, float *__restrict__ G, double *__restrict__ partial) {
+    __shared__ double sh[kThreads];
+    const int g = threadIdx.x / kGroup, l = threadIdx.x % kGroup;
+    const int quads = C / 4;
+    constexpr int kRowsPerIter = kRowsPerBlock * RPG;
+    double acc = 0.0;
+    for (int64_t base = static_cast<int64_t>(blockIdx.x) * kRowsPerIter; base < n;
+         base += static_cast<int64_t>(gridDim.x) * kRowsPerIter) {
+        f32x4 v[RPG][QPL];
+        int32_t lab[RPG];
+#pragma unroll
+        for (int r = 0; r < RPG; ++r) {
+            const int64_t row = base + r * kRowsPerBlock + g;
+            lab[r] = row < n ? labels[row] : -1;
+#pragma unroll
+            for (int q = 0; q < QPL; ++q) {
+                const int j = l + q * kGroup;
+                v[r][q] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+                if (row < n && j < quads) v[r][q] = *reinterpret_cast<const f32x4 *>(Y + row * C + 4 * j);
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < RPG; ++r) {
+            const int64_t row = base + r * kRowsPerBlock + g;
+            float m = -INFINITY;
+#pragma unroll
+            for (int q = 0; q < QPL; ++q)
+                m = fmaxf(m, fmaxf(fmaxf(v[r][q][0], v[r][q][1]), fmaxf(v[r][q][2], v[r][q][3])));
+            m = group_max(m);
+            float s = 0.f;
+            float ylab = 0.f;
+#pragma unroll
+            for (int q = 0; q < QPL; ++q) {
+                const int j = l + q * kGroup;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    if (4 * j + c == lab[r]) ylab = v[r][q][c];
+                    const float e = j < quads ? expf(v[r][q][c] - m) : 0.f;
+                    v[r][q][c] = e;
+                    s += e;
+                }
+            }
+            s = group_sum(s);
+            ylab = group_sum(ylab);
+            const bool labeled = lab[r] >= 0 && lab[r] < C;
+            const float inv = 1.f / s;
+            if (row < n) {
+#pragma unroll
+                for (int q = 0; q < QPL; ++q) {
+                    const int j = l + q * kGroup;
+                    if (j < quads) {
+                        f32x4 o;
+#pragma unroll
+                        for (int c = 0; c < 4; ++c)
+                            o[c] = labeled ? scale * (v[r][q][c] * inv - (4 * j + c == lab[r] ? 1.f : 0.f)) : 0.f;
+                        __builtin_nontemporal_store(o, reinterpret_cast<f32x4 *>(G + row * C + 4 * j));
+                    }
+                }
+                if (labeled && l == 0) acc += static_cast<double>(logf(s) + m - ylab);
+            }
+        }
+    }
+    const int t = threadIdx.x;
+    sh[t] = acc;
+    __syncthreads();
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        if (t < h) sh[t] += sh[t + h];
+        __syncthreads();
+    }
+    if (t == 0) partial[blockIdx.x] = sh[0];
+}
+
+// loss[0] = scale * sum of the partials, by a fixed tree over workgroup order.
+__global__ __launch_bounds__(kThreads) void loss_total_kernel(double *__restrict__ loss,
+                                                              int32_t count, float scale) {
+    __shared__ double sh[kThreads];
+    const int t = threadIdx.x;
     double s = 0.0;
-    for (int i = 0; i < count; ++i) s += loss[1 + i];
-    loss[0] = static_cast<double>(scale) * s;
+    for (int i = t; i < count; i += kThreads) s += loss[1 + i];
+    sh[t] = s;
+    __syncthreads();
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        if (t < h) sh[t] += sh[t + h];
+        __syncthreads();
+    }
+    if (t == 0) loss[0] = static_cast<double>(scale) * sh[0];
 }
 
 // ------------------------------------------------------------------ weight gradient
@@ -93,67 +181,101 @@ __global__ void loss_total_kernel(double *__restrict__ loss, int32_t count, floa
 constexpr int kWgThreads = 512;
 constexpr int kWgWaves = kWgThreads / 64;
 constexpr int kChunk = 64;                       // rows per LDS stage (two k-steps of 32)
-constexpr int kLdsPad = 8;                       // bf16 padding per transposed row
-constexpr int kLdsRow = kChunk + kLdsPad;
+// A transposed LDS row holds the chunk's 64 rows of one column as bfloat16, padded to 68:
+// consecutive lanes of a store then hit 64 different banks, and every 8-byte fragment
+// read stays aligned.
+constexpr int kLdsRow = 68;
+constexpr int kLdsRow2 = kLdsRow / 2;            // the same row in 32-bit words
 constexpr int kMaxIB = 256;                      // dW rows (X columns) per pass
 constexpr int kMaxJB = 128;                      // dW columns (G columns) per pass
-constexpr int kMaxPartials = 512;                // workgroups, hence partial dW matrices
+constexpr int kMaxPartials = 1024;               // workgroups, hence partial dW matrices
 
-// Four consecutive elements of one row as float32, from float32 or bfloat16 storage.
 template <bool BF>
-__device__ __forceinline__ f32x4 load4(const void *base, int64_t at) {
-    if constexpr (BF) {
-        const uint2 r = *reinterpret_cast<const uint2 *>(static_cast<const unsigned short *>(base) + at);
-        return f32x4{__builtin_bit_cast(float, r.x << 16), __builtin_bit_cast(float, r.x & 0xFFFF0000u),
-                     __builtin_bit_cast(float, r.y << 16), __builtin_bit_cast(float, r.y & 0xFFFF0000u)};
-    } else {
-        return *reinterpret_cast<const f32x4 *>(static_cast<const float *>(base) + at);
-    }
-}
+struct RawQuad {           // four consecutive elements of a row as stored
+    using type = f32x4;
+};
+template <>
+struct RawQuad<true> {
+    using type = uint2;
+};
 
-// One staged operand: `width` columns (starting at col0) of a 64-row chunk, held by each
-// thread as up to ITEMS (row pair, column quad) items between the global load and the
-// transposed LDS write t[col][row].
+// One staged operand: `width` columns (from col0, width % 32 == 0) of a 64-row chunk, held
+// by each thread as up to ITEMS items of (row pair, column quad) between the global load
+// and the transposed LDS store t[col][row].  Items come in blocks of 8 row pairs x 8
+// quads, one block per wavefront instruction: each row's 8 quads are one contiguous
+// 128-byte (float32) or 64-byte (bfloat16) segment of memory, and the 64 LDS words a
+// store instruction writes fall in 64 different banks.
 template <bool BF, int ITEMS>
 struct Stage {
-    f32x4 v[ITEMS][2];
+    typename RawQuad<BF>::type v[ITEMS][2];
+
+    __device__ __forceinline__ static bool item(int it, int width, int &rp, int &cq) {
+        const int w = static_cast<int>(threadIdx.x) + it * kWgThreads;
+        const int blk = w >> 6, sub = w & 63;
+        const int qb = blk >> 2;
+        rp = 8 * (blk & 3) + (sub & 7);
+        cq = 8 * qb + (sub >> 3);
+        return qb < width / 32;
+    }
 
     __device__ __forceinline__ void load(const void *src, int64_t ld, int64_t n, int64_t r0,
                                          int col0, int width) {
-        const int quads = width / 4;
 #pragma unroll
         for (int it = 0; it < ITEMS; ++it) {
-            const int w = threadIdx.x + it * kWgThreads;
-            const int rp = w / quads, cq = w % quads;
+            int rp, cq;
+            const bool ok = item(it, width, rp, cq);
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int64_t r = r0 + 2 * rp + h;
-                v[it][h] = f32x4{0.f, 0.f, 0.f, 0.f};
-                if (rp < kChunk / 2 && r < n) v[it][h] = load4<BF>(src, r * ld + col0 + 4 * cq);
+                if constexpr (BF) {
+                    v[it][h] = make_uint2(0u, 0u);
+                    if (ok && r < n)
+                        v[it][h] = *reinterpret_cast<const uint2 *>(static_cast<const unsigned short *>(src) +
+                                                                    r * ld + col0 + 4 * cq);
+                } else {
+                    v[it][h] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    if (ok && r < n)
+                        v[it][h] = *reinterpret_cast<const f32x4 *>(static_cast<const float *>(src) +
+                                                                    r * ld + col0 + 4 * cq);
+                }
             }
         }
     }
 
+    __device__ __forceinline__ static uint32_t bits(const typename RawQuad<BF>::type &q, int c) {
+        if constexpr (BF) {
+            const uint32_t word = c < 2 ? q.x : q.y;
+            return (c & 1) ? word >> 16 : word & 0xFFFFu;
+        } else {
+            return to_bf16(q[c]);
+        }
+    }
+
     __device__ __forceinline__ void store(uint32_t *t, int width) const {
-        const int quads = width / 4;
 #pragma unroll
         for (int it = 0; it < ITEMS; ++it) {
-            const int w = threadIdx.x + it * kWgThreads;
-            const int rp = w / quads, cq = w % quads;
-            if (rp < kChunk / 2) {
+            int rp, cq;
+            if (item(it, width, rp, cq)) {
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const uint32_t lo = to_bf16(v[it][0][c]), hi = to_bf16(v[it][1][c]);
-                    t[((4 * cq + c) * kLdsRow + 2 * rp) / 2] = lo | (hi << 16);
-                }
+                for (int c = 0; c < 4; ++c)
+                    t[(4 * cq + c) * kLdsRow2 + rp] = bits(v[it][0], c) | (bits(v[it][1], c) << 16);
             }
         }
     }
 };
 
+// Eight consecutive k (rows of the chunk) of transposed row `row`, from two aligned 8-byte
+// LDS reads.
+__device__ __forceinline__ bf16x8 fragment(const uint32_t *t, int row, int kk) {
+    const uint2 *q = reinterpret_cast<const uint2 *>(t + row * kLdsRow2 + kk / 2);
+    const uint2 a = q[0], b = q[1];
+    return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+}
+
 // partial[blockIdx.x] (F_in x F_out, only the block [i0, i0 + IB) x [j0, j0 + JB)) =
 // sum over this workgroup's chunks of bf16(X)^T bf16(G).  Tiles of 16 x 16 go to the
-// wavefronts in row-major order, NT per wavefront.
+// wavefronts in row-major order, NT per wavefront.  The loads of chunk c + gridDim.x are
+// in flight while chunk c is stored to LDS and multiplied.
 template <int NT, bool XBF, bool GBF>
 __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restrict__ X,
                                                            const void *__restrict__ G,
@@ -162,9 +284,7 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restric
                                                            int32_t IB, int32_t j0, int32_t JB) {
     extern __shared__ uint32_t lds[];
     uint32_t *xt = lds;                                    // [IB][kLdsRow] bf16
-    uint32_t *gt = lds + IB * kLdsRow / 2;                 // [JB][kLdsRow] bf16
-    const unsigned short *xt16 = reinterpret_cast<const unsigned short *>(xt);
-    const unsigned short *gt16 = reinterpret_cast<const unsigned short *>(gt);
+    uint32_t *gt = lds + IB * kLdsRow2;                    // [JB][kLdsRow] bf16
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lrow = lane & 15, kgrp = lane >> 4;
@@ -177,8 +297,8 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restric
 
     constexpr int kXItems = (kChunk / 2) * (kMaxIB / 4) / kWgThreads;   // 4
     constexpr int kGItems = (kChunk / 2) * (kMaxJB / 4) / kWgThreads;   // 2
-    Stage<XBF, kXItems> xs;
-    Stage<GBF, kGItems> gs;
+    Stage<XBF, kXItems> xs, xn;
+    Stage<GBF, kGItems> gs, gn;
     const int64_t chunks = (static_cast<int64_t>(n) + kChunk - 1) / kChunk;
     int64_t c = blockIdx.x;
     if (c < chunks) {
@@ -186,15 +306,15 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restric
         gs.load(G, F_out, n, c * kChunk, j0, JB);
     }
     for (; c < chunks; c += gridDim.x) {
+        const int64_t next = c + gridDim.x;
+        if (next < chunks) {
+            xn.load(X, F_in, n, next * kChunk, i0, IB);
+            gn.load(G, F_out, n, next * kChunk, j0, JB);
+        }
         __syncthreads();                     // the previous chunk's MFMAs are done with LDS
         xs.store(xt, IB);
         gs.store(gt, JB);
         __syncthreads();
-        const int64_t next = c + gridDim.x;
-        if (next < chunks) {                 // the next chunk is requested during the MFMAs
-            xs.load(X, F_in, n, next * kChunk, i0, IB);
-            gs.load(G, F_out, n, next * kChunk, j0, JB);
-        }
 #pragma unroll
         for (int ks = 0; ks < kChunk / 32; ++ks) {
             const int kk = ks * 32 + kgrp * 8;
@@ -203,13 +323,13 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restric
                 const int t = wave * NT + u;
                 if (t < tiles) {
                     const int it = t / jt_count, jt = t % jt_count;
-                    const u16x8 a = *reinterpret_cast<const u16x8 *>(xt16 + (it * 16 + lrow) * kLdsRow + kk);
-                    const u16x8 b = *reinterpret_cast<const u16x8 *>(gt16 + (jt * 16 + lrow) * kLdsRow + kk);
                     acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc[u], 0, 0, 0);
+                        fragment(xt, it * 16 + lrow, kk), fragment(gt, jt * 16 + lrow, kk), acc[u], 0, 0, 0);
                 }
             }
         }
+        xs = xn;
+        gs = gn;
     }
     float *out = partial + static_cast<int64_t>(blockIdx.x) * F_in * F_out;
 #pragma unroll
@@ -224,83 +344,153 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restric
     }
 }
 
-// dW[e] = sum over workgroups b (in order) of partial[b][e]; with W, also W[e] -= lr dW[e].
+// dW[e] = sum over workgroups b of partial[b][e] in float64: eight threads sum consecutive
+// eighths of the partials in order, then the eight sums are added in order; with W, also
+// W[e] -= lr dW[e].  A workgroup covers 32 consecutive elements.
+constexpr int kReduceSegs = 8;
+constexpr int kReduceElems = kThreads / kReduceSegs;
 __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float *__restrict__ partial,
                                                                 int32_t count, int64_t elems,
                                                                 float *__restrict__ dW, float lr,
                                                                 float *__restrict__ W) {
-    for (int64_t e = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; e < elems;
-         e += static_cast<int64_t>(gridDim.x) * kThreads) {
+    __shared__ double sh[kReduceSegs][kReduceElems];
+    const int el = threadIdx.x % kReduceElems, seg = threadIdx.x / kReduceElems;
+    const int per = (count + kReduceSegs - 1) / kReduceSegs;
+    for (int64_t e0 = static_cast<int64_t>(blockIdx.x) * kReduceElems; e0 < elems;
+         e0 += static_cast<int64_t>(gridDim.x) * kReduceElems) {
+        const int64_t e = e0 + el;
         double s = 0.0;
-        for (int b = 0; b < count; ++b) s += static_cast<double>(partial[b * elems + e]);
-        const float d = static_cast<float>(s);
-        dW[e] = d;
-        if (W) W[e] -= lr * d;
+        if (e < elems) {
+            const int b1 = min(count, (seg + 1) * per);
+            for (int b = seg * per; b < b1; ++b) s += static_cast<double>(partial[b * elems + e]);
+        }
+        sh[seg][el] = s;
+        __syncthreads();
+        if (seg == 0 && e < elems) {
+            double t = 0.0;
+#pragma unroll
+            for (int k = 0; k < kReduceSegs; ++k) t += sh[k][el];
+            const float d = static_cast<float>(t);
+            dW[e] = d;
+            if (W) W[e] -= lr * d;
+        }
+        __syncthreads();
     }
 }
 
-int wgrad_blocks(int32_t n) {
+// Upper bound of the workgroups (partials) of one product over n rows.
+int wgrad_max_blocks(int32_t n) {
     const int64_t chunks = (static_cast<int64_t>(n) + kChunk - 1) / kChunk;
     return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(chunks, kMaxPartials)));
 }
 
+int device_cus() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+    }
+    return cus;
+}
+
+size_t wgrad_lds_bytes(int IB, int JB) {
+    return static_cast<size_t>(IB + JB) * kLdsRow * sizeof(unsigned short);
+}
+
+// One pass over the rows for the dW block [i0, i0 + IB) x [j0, j0 + JB).  With `blocks`
+// == 0 nothing is launched: *resident receives how many workgroups of this kernel a CU
+// holds at once (registers, LDS and threads).
 template <int NT, bool XBF, bool GBF>
-int launch_wgrad_pass(const void *X, const void *G, float *partial, int blocks, int32_t n,
-                      int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB, hipStream_t s) {
-    const size_t lds = static_cast<size_t>(IB + JB) * kLdsRow * sizeof(unsigned short);
+int launch_wgrad_pass(const void *X, const void *G, float *partial, int blocks, int *resident,
+                      int32_t n, int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB,
+                      hipStream_t s) {
+    const size_t lds = wgrad_lds_bytes(IB, JB);
+    if (blocks == 0) {
+        int per_cu = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wgrad_kernel<NT, XBF, GBF>,
+                                                         kWgThreads, lds) != hipSuccess || per_cu < 1)
+            per_cu = 1;
+        *resident = per_cu;
+        return DUALGCN_OK;
+    }
     hipLaunchKernelGGL((wgrad_kernel<NT, XBF, GBF>), dim3(blocks), dim3(kWgThreads), lds, s, X, G,
                        partial, n, F_in, F_out, i0, IB, j0, JB);
     return hip_status(hipGetLastError());
 }
 
 template <bool XBF, bool GBF>
-int launch_wgrad_nt(const void *X, const void *G, float *partial, int blocks, int32_t n,
-                    int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB, hipStream_t s) {
+int launch_wgrad_nt(const void *X, const void *G, float *partial, int blocks, int *resident,
+                    int32_t n, int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB,
+                    hipStream_t s) {
     const int per_wave = ((IB / 16) * (JB / 16) + kWgWaves - 1) / kWgWaves;
-    if (per_wave <= 4) return launch_wgrad_pass<4, XBF, GBF>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s);
-    if (per_wave <= 8) return launch_wgrad_pass<8, XBF, GBF>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s);
-    return launch_wgrad_pass<16, XBF, GBF>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s);
+    if (per_wave <= 4)
+        return launch_wgrad_pass<4, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
+    if (per_wave <= 8)
+        return launch_wgrad_pass<8, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
+    return launch_wgrad_pass<16, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
+}
+
+int launch_wgrad_any(bool x_bf16, bool g_bf16, const void *X, const void *G, float *partial,
+                     int blocks, int *resident, int32_t n, int32_t F_in, int32_t F_out, int i0,
+                     int IB, int j0, int JB, hipStream_t s) {
+    if (x_bf16)
+        return g_bf16 ? launch_wgrad_nt<true, true>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s)
+                      : launch_wgrad_nt<true, false>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
+    return g_bf16 ? launch_wgrad_nt<false, true>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s)
+                  : launch_wgrad_nt<false, false>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
 }
 
 }  // namespace
 
 int launch_softmax_xent(const float *Y, const int32_t *labels, int32_t n, int32_t C, float scale,
                         float *G, double *loss, hipStream_t s) {
-    const int64_t need = (static_cast<int64_t>(n) + kRowsPerBlock - 1) / kRowsPerBlock;
+    const bool vec = C % 4 == 0 && C <= 4 * 4 * kGroup && reinterpret_cast<uintptr_t>(Y) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(G) % 16 == 0;
+    const int rows_per_block = vec && C <= 4 * kGroup ? kRowsPerBlock * 4 : kRowsPerBlock;
+    const int64_t need = (static_cast<int64_t>(n) + rows_per_block - 1) / rows_per_block;
     const int blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(need, kLossBlocks)));
-    hipLaunchKernelGGL(softmax_xent_kernel, dim3(blocks), dim3(kThreads), 0, s, Y, labels, n, C,
-                       scale, G, loss + 1);
-    hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1), 0, s, loss, blocks, scale);
+    if (vec && C <= 4 * kGroup)
+        hipLaunchKernelGGL((softmax_xent_vec_kernel<1, 4>), dim3(blocks), dim3(kThreads), 0, s, Y,
+                           labels, n, C, scale, G, loss + 1);
+    else if (vec)
+        hipLaunchKernelGGL((softmax_xent_vec_kernel<4, 1>), dim3(blocks), dim3(kThreads), 0, s, Y,
+                           labels, n, C, scale, G, loss + 1);
+    else
+        hipLaunchKernelGGL(softmax_xent_kernel, dim3(blocks), dim3(kThreads), 0, s, Y, labels, n, C,
+                           scale, G, loss + 1);
+    hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(kThreads), 0, s, loss, blocks, scale);
     return hip_status(hipGetLastError());
 }
 
 size_t wgrad_workspace_bytes(int32_t n, int32_t F_in, int32_t F_out) {
-    return static_cast<size_t>(wgrad_blocks(n)) * F_in * F_out * sizeof(float);
+    return static_cast<size_t>(wgrad_max_blocks(n)) * F_in * F_out * sizeof(float);
 }
 
 int launch_weight_grad(const void *X, bool x_bf16, const void *G, bool g_bf16, float *dW,
                        int32_t n, int32_t F_in, int32_t F_out, float lr, float *W, void *workspace,
                        hipStream_t s) {
     float *partial = static_cast<float *>(workspace);
-    const int blocks = wgrad_blocks(n);
     const int JB = std::min<int>(F_out, kMaxJB);
     const int IB = std::min<int>(F_in, kMaxIB);
+    // workgroups: as many as the CUs hold at once for the widest pass, at most one per
+    // chunk and kMaxPartials; every pass uses the same count, fixed for a device, so the
+    // reduction order is fixed too
+    int resident = 1;
+    launch_wgrad_any(x_bf16, g_bf16, X, G, partial, 0, &resident, n, F_in, F_out, 0, IB, 0, JB, s);
+    const int blocks = std::min(wgrad_max_blocks(n), device_cus() * resident);
     for (int j0 = 0; j0 < F_out; j0 += JB) {
         for (int i0 = 0; i0 < F_in; i0 += IB) {
             const int ib = std::min(IB, F_in - i0), jb = std::min(JB, F_out - j0);
-            int st;
-            if (x_bf16) {
-                st = g_bf16 ? launch_wgrad_nt<true, true>(X, G, partial, blocks, n, F_in, F_out, i0, ib, j0, jb, s)
-                            : launch_wgrad_nt<true, false>(X, G, partial, blocks, n, F_in, F_out, i0, ib, j0, jb, s);
-            } else {
-                st = g_bf16 ? launch_wgrad_nt<false, true>(X, G, partial, blocks, n, F_in, F_out, i0, ib, j0, jb, s)
-                            : launch_wgrad_nt<false, false>(X, G, partial, blocks, n, F_in, F_out, i0, ib, j0, jb, s);
-            }
+            const int st = launch_wgrad_any(x_bf16, g_bf16, X, G, partial, blocks, nullptr, n, F_in,
+                                            F_out, i0, ib, j0, jb, s);
             if (st) return st;
         }
     }
     const int64_t elems = static_cast<int64_t>(F_in) * F_out;
-    const int rblocks = static_cast<int>(std::min<int64_t>((elems + kThreads - 1) / kThreads, 4096));
+    const int rblocks = static_cast<int>(std::min<int64_t>((elems + kReduceElems - 1) / kReduceElems, 8192));
     hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(rblocks), dim3(kThreads), 0, s, partial, blocks,
                        elems, dW, lr, W);
     return hip_status(hipGetLastError());

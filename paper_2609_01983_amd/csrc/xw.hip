@@ -78,15 +78,15 @@ struct XFrag {
 // Where the output keeps a product: no mask, or M > 0 for a float32 or bfloat16 M.
 enum MaskKind { kNoMask = 0, kMaskF32 = 1, kMaskBF16 = 2 };
 
+// The mask element at `at` as float32.
 template <int MASK>
-__device__ __forceinline__ bool keep(const void *M, int64_t at) {
+__device__ __forceinline__ float mask_value(const void *M, int64_t at) {
     if constexpr (MASK == kMaskF32) {
-        return static_cast<const float *>(M)[at] > 0.f;
+        return static_cast<const float *>(M)[at];
     } else if constexpr (MASK == kMaskBF16) {
-        const uint32_t bits = static_cast<uint32_t>(static_cast<const unsigned short *>(M)[at]) << 16;
-        return __builtin_bit_cast(float, bits) > 0.f;
+        return __builtin_bit_cast(float, static_cast<uint32_t>(static_cast<const unsigned short *>(M)[at]) << 16);
     } else {
-        return true;
+        return 1.f;
     }
 }
 
@@ -155,7 +155,8 @@ __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const void *__restric
                     const int64_t orow = row0 + kgrp * 4 + j;
                     if (orow < n) {
                         const int64_t at = orow * N + c0 + t * 16 + lrow;
-                        T[at] = keep<MASK>(M, at) ? acc[t][j] : 0.f;
+                        if constexpr (MASK == kNoMask) T[at] = acc[t][j];
+                        else T[at] = mask_value<MASK>(M, at) > 0.f ? acc[t][j] : 0.f;
                     }
                 }
             }

@@ -86,6 +86,34 @@ def test_other_entry_points_reject_null(dg):
     L.dualgcn_plan_destroy(None)                     # no-op
 
 
+def test_plan_io_checks_arguments(dg):
+    L = dg.lib()
+    nbytes = ctypes.c_size_t(0)
+    out = ctypes.c_void_p(5)
+    assert L.dualgcn_plan_save(None, None, ctypes.byref(nbytes)) == dg.ERR_INVALID_ARG
+    c = _csr(dg, n=4, nnz=4)
+    assert L.dualgcn_plan_load(ctypes.byref(c), None, 0, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
+    assert out.value is None
+    junk = ctypes.create_string_buffer(b"NOTAPLAN" + bytes(72 + 16))
+    assert L.dualgcn_plan_load(ctypes.byref(c), junk, 96, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
+    # a well-formed header for another size of matrix: refused before any device use
+    import struct
+    hdr = b"DGCNPLAN" + struct.pack("<IIii q Q II IIIIi i Q", 1, 80, 5, 0, 4, 0, 8, 4, 1, 2, 1, 2, 0, 0, 0)
+    assert len(hdr) == 80
+    blob = ctypes.create_string_buffer(hdr + bytes(20), 100)
+    assert L.dualgcn_plan_load(ctypes.byref(c), blob, 100, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
+
+
+def test_aggregator_values_checks_arguments(dg):
+    L = dg.lib()
+    c = _csr(dg, rowptr=1 << 20, col=1 << 24, val=1 << 28)
+    assert L.dualgcn_aggregator_values(None, 0, 0.0, 1 << 30, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_aggregator_values(ctypes.byref(c), 0, 0.0, None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_aggregator_values(ctypes.byref(c), 3, 0.0, 1 << 30, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_aggregator_values(ctypes.byref(c), -1, 0.0, 1 << 30, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_aggregator_values(ctypes.byref(c), 0, 0.0, 1 << 24, None) == dg.ERR_INVALID_ARG
+
+
 def test_training_entry_points_check_arguments(dg):
     L = dg.lib()
     # softmax cross-entropy: null pointers, empty shapes, overlapping outputs
@@ -100,7 +128,7 @@ def test_training_entry_points_check_arguments(dg):
     assert L.dualgcn_weight_grad_workspace(100, 32, 64, ctypes.byref(nbytes)) == dg.OK
     assert nbytes.value == 2 * 32 * 64 * 4                  # two 64-row chunks: two partials
     assert L.dualgcn_weight_grad_workspace(1 << 22, 256, 128, ctypes.byref(nbytes)) == dg.OK
-    assert nbytes.value == 512 * 256 * 128 * 4
+    assert nbytes.value == 1024 * 256 * 128 * 4             # at most 1024 partials
     X, G, dW, ws = 1 << 30, 1 << 31, 1 << 32, 1 << 33
     big = 1 << 28
     assert L.dualgcn_weight_grad(None, G, dW, 100, 32, 32, 0, 0.0, None, ws, big, None) == dg.ERR_INVALID_ARG
@@ -128,6 +156,7 @@ def test_valid_arguments_without_device_report_no_device(dg):
     assert L.dualgcn_partition(ctypes.byref(c), 0, 4, 4, None, None, ctypes.byref(out)) == dg.ERR_NO_DEVICE
     assert out.value is None
     assert L.dualgcn_arw_patterns(ctypes.byref(c), 0, 4, 4, 1, None) == dg.ERR_NO_DEVICE
+    assert L.dualgcn_aggregator_values(ctypes.byref(c), 0, 0.0, 1 << 30, None) == dg.ERR_NO_DEVICE
 
 
 def test_binding_rejects_host_tensors(dg):
