@@ -278,7 +278,7 @@ def main():
     ap.add_argument("--config", default=os.environ.get("DUALGCN_BENCH_CONFIG", "c5"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--spmm-reps", type=int, default=20)
-    ap.add_argument("--mode", choices=["full", "spmm", "train"], default="full",
+    ap.add_argument("--mode", choices=["full", "spmm", "train", "planio"], default="full",
                     help="spmm: one partition, then only the dominant SpMM launches (for counter "
                          "runs); train: GCN training steps on one plan (forward, loss, backward, SGD)")
     ap.add_argument("--lr", type=float, default=0.5, help="SGD step of --mode train")
@@ -350,6 +350,30 @@ def main():
     ev = lambda: torch.cuda.Event(enable_timing=True)
     if args.mode == "train":
         train(args, w, g, dg, torch, np, rowptr, col, val, Xd, Wd, stream, ev)
+        return
+    if args.mode == "planio":
+        # partition against save + load of the same plan (wall clock, synchronised)
+        times = {"partition": [], "save": [], "load": []}
+        for rep in range(args.warmup + args.steps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            blob = plan.save()
+            t2 = time.perf_counter()
+            loaded = dg.Plan.load(rowptr, col, val, blob)
+            torch.cuda.synchronize()
+            t3 = time.perf_counter()
+            if rep >= args.warmup:
+                times["partition"].append(t1 - t0)
+                times["save"].append(t2 - t1)
+                times["load"].append(t3 - t2)
+            loaded.destroy()
+            plan.destroy()
+        print(json.dumps({"mode": "planio", "config": w.name, "saved_bytes": len(blob),
+                          **{k + "_ms": round(float(np.mean(v)) * 1e3, 3) for k, v in times.items()}}),
+              flush=True)
         return
     if args.ablation:
         ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
