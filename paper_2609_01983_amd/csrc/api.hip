@@ -155,6 +155,19 @@ bool keys_fit(uint32_t q, uint32_t k, uint32_t d, int64_t nnz) {
     return m < (static_cast<dgc::u128>(1) << 63);
 }
 
+// Thresholds of a partition: rationals below 2^16 with non-zero denominators, alpha <= 1
+// (or the adaptive marker when `adaptive_ok`), a known force mode.
+int check_thresholds(const dualgcn_thresholds &t, bool adaptive_ok) {
+    if (t.alpha_den == 0 || t.beta_den == 0) return DUALGCN_ERR_INVALID_ARG;
+    if (t.alpha_num > t.alpha_den && !(adaptive_ok && t.alpha_num == DUALGCN_ALPHA_ADAPTIVE))
+        return DUALGCN_ERR_INVALID_ARG;
+    if (t.alpha_den >= kMaxRational || t.beta_den >= kMaxRational || t.beta_num >= kMaxRational)
+        return DUALGCN_ERR_INVALID_ARG;
+    if (t.force_mode < DUALGCN_FORCE_AUTO || t.force_mode > DUALGCN_FORCE_DENSE)
+        return DUALGCN_ERR_INVALID_ARG;
+    return DUALGCN_OK;
+}
+
 int check_plan(const dualgcn_plan *plan) {
     return plan ? DUALGCN_OK : DUALGCN_ERR_INVALID_ARG;
 }
@@ -205,13 +218,7 @@ int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_
     if ((st = check_walks(walks_per_node, walk_len))) return st;
     dualgcn_thresholds t{1, 2, 1, 2, DUALGCN_FORCE_AUTO};
     if (th) t = *th;
-    if (t.alpha_den == 0 || t.beta_den == 0 ||
-        (t.alpha_num > t.alpha_den && t.alpha_num != DUALGCN_ALPHA_ADAPTIVE))
-        return DUALGCN_ERR_INVALID_ARG;
-    if (t.alpha_den >= kMaxRational || t.beta_den >= kMaxRational || t.beta_num >= kMaxRational)
-        return DUALGCN_ERR_INVALID_ARG;
-    if (t.force_mode < DUALGCN_FORCE_AUTO || t.force_mode > DUALGCN_FORCE_DENSE)
-        return DUALGCN_ERR_INVALID_ARG;
+    if ((st = check_thresholds(t, true))) return st;
     if (!keys_fit(t.alpha_den, walks_per_node, walk_len, csr->nnz)) return DUALGCN_ERR_UNSUPPORTED;
     if ((st = dgc::device_status())) return st;
     Plan *p = nullptr;
@@ -504,10 +511,7 @@ int dualgcn_plan_load(const dualgcn_csr *csr, const void *buf, size_t bytes, voi
         return DUALGCN_ERR_INVALID_ARG;
     const dualgcn_thresholds &t = h.th;
     if ((st = check_walks(h.k, h.d))) return st;
-    if (t.alpha_den == 0 || t.beta_den == 0 || t.alpha_num > t.alpha_den ||
-        t.alpha_den >= kMaxRational || t.beta_den >= kMaxRational || t.beta_num >= kMaxRational ||
-        t.force_mode < DUALGCN_FORCE_AUTO || t.force_mode > DUALGCN_FORCE_DENSE)
-        return DUALGCN_ERR_INVALID_ARG;
+    if ((st = check_thresholds(t, false))) return st;     // a saved plan holds a resolved alpha
     if (!keys_fit(t.alpha_den, h.k, h.d, csr->nnz)) return DUALGCN_ERR_UNSUPPORTED;
     if ((st = dgc::device_status())) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
