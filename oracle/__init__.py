@@ -407,20 +407,40 @@ def backward_data(G, W, M=None):
     return dX, B
 
 
-def gcn_train_grads(g, X, weights, labels, scale):
+def round_bf16(a):
+    """float64 array of the bfloat16 values nearest (ties to even) to the float32 rounding
+    of `a`: the 16 high bits of the float32 pattern after adding 0x7FFF plus the lowest
+    kept bit; NaN stays NaN."""
+    f = np.ascontiguousarray(a, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    out = (r & 0xFFFFFFFF).astype(np.uint32).view(np.float32).astype(np.float64)
+    return np.where(np.isnan(f), np.nan, out)
+
+
+def gcn_train_grads(g, X, weights, labels, scale, bf16=False):
     """Forward and backward of a GCN (ReLU after every layer but the last, softmax
     cross-entropy on the last) in float64.  Returns a dict with the loss, the weight
     gradients "dW" (one per layer) and the intermediates: per layer "T", "P", "H" of
-    the forward and "GP", "GT" of the backward; "G" holds dL/dH of every layer."""
+    the forward and "GP", "GT" of the backward; "G" holds dL/dH of every layer.
+
+    bf16=True applies the declared roundings of the matrix-core path and nothing else:
+    both operands of every dense product to bfloat16, hidden activations and aggregated
+    gradients stored as bfloat16, the last layer's output stored as float32; all other
+    arithmetic stays float64."""
     X = np.asarray(X, dtype=np.float64)
     gt = transpose_csr(g)
     L = len(weights)
+    r = round_bf16 if bf16 else (lambda a: a)
     Ws = [np.asarray(W, dtype=np.float64) for W in weights]
     inp, T, P, H = [X], [], [], []
     for li, W in enumerate(Ws):
-        T.append(inp[-1] @ W)
+        T.append(r(inp[-1]) @ r(W))
         P.append(spmm_f64(g, T[-1]))
-        H.append(np.maximum(P[-1], 0.0) if li < L - 1 else P[-1])
+        if li < L - 1:
+            H.append(r(np.maximum(P[-1], 0.0)))
+        else:
+            H.append(P[-1].astype(np.float32).astype(np.float64) if bf16 else P[-1])
         inp.append(H[-1])
     loss, G_last = softmax_xent(H[-1], labels, scale)
     G = [None] * L
@@ -428,10 +448,10 @@ def gcn_train_grads(g, X, weights, labels, scale):
     GP, GT, dW = [None] * L, [None] * L, [None] * L
     for li in range(L - 1, -1, -1):
         GP[li] = G[li] * (P[li] > 0) if li < L - 1 else G[li]
-        GT[li] = spmm_f64(gt, GP[li])
-        dW[li] = inp[li].T @ GT[li]
+        GT[li] = r(spmm_f64(gt, GP[li]))
+        dW[li] = r(inp[li]).T @ GT[li]
         if li > 0:
-            G[li - 1] = GT[li] @ Ws[li].T
+            G[li - 1] = GT[li] @ r(Ws[li]).T
     return dict(loss=loss, dW=dW, T=T, P=P, H=H, G=G, GP=GP, GT=GT)
 
 

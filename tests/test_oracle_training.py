@@ -149,3 +149,32 @@ def test_weight_grad_and_backward_data_brute_force():
             s = sum(G[r, j] * W[i, j] for j in range(3)) if M[r, i] > 0 else 0.0
             assert math.isclose(dX[r, i], s, rel_tol=1e-12, abs_tol=1e-12)
     assert np.array_equal(oracle.backward_data(G, W)[0] != 0, np.ones((9, 4), dtype=bool))
+
+
+def test_round_bf16_matches_torch_and_ties_go_even():
+    import torch
+    rs = np.random.default_rng(9)
+    x = np.concatenate([rs.standard_normal(20000).astype(np.float32) * 10.0 ** rs.integers(-30, 30, 20000),
+                        np.array([0.0, -0.0, np.inf, -np.inf, 3.4e38, -3.4e38, 1e-40, -1e-40], np.float32)])
+    want = torch.from_numpy(x).to(torch.bfloat16).float().numpy().astype(np.float64)
+    got = oracle.round_bf16(x)
+    assert np.array_equal(got, want)
+    # exact ties: 1 + 2^-8 lies halfway between 1 and 1 + 2^-7 and goes to the even 1
+    assert oracle.round_bf16(np.float32(1 + 2 ** -8)) == 1.0
+    assert oracle.round_bf16(np.float32(1 + 3 * 2 ** -8)) == 1 + 2 ** -6
+    assert np.isnan(oracle.round_bf16(np.float32(np.nan)))
+
+
+def test_bf16_chain_is_the_exact_chain_on_bf16_values():
+    # inputs, weights and every intermediate representable in bfloat16: the declared
+    # roundings change nothing, so both chains agree to float64 rounding
+    g = small.from_rows([[0], [1], [2], [3]])                 # identity: A = I
+    X = np.array([[1, 2], [0.5, -1], [-2, 0.25], [4, 1]], dtype=np.float32)
+    Ws = [np.array([[1, 0], [0, 1]], np.float32), np.array([[1, -1], [2, 0.5]], np.float32)]
+    labels = np.array([0, 1, -1, 1], np.int32)
+    a = oracle.gcn_train_grads(g, X, Ws, labels, 1.0)
+    b = oracle.gcn_train_grads(g, X, Ws, labels, 1.0, bf16=True)
+    assert np.array_equal(a["H"][0], b["H"][0])
+    # the aggregated gradients are rounded in the bf16 chain, not in the exact one
+    assert np.allclose(a["dW"][1], b["dW"][1], rtol=2 ** -7, atol=1e-12)
+    assert abs(a["loss"] - b["loss"]) < 1e-12
