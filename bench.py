@@ -152,6 +152,28 @@ ABLATION = [("dual-metric alpha=1/2", (1, 2), "auto"),
             ("all rows dense path", (1, 2), "dense")]
 
 
+def block_stats(g, perm, K, np, blocks=1024):
+    """Partition-quality statistics of the paper's objective (Sec. 3.2): cut the sorted order
+    into `blocks` contiguous blocks and report the work imbalance max/avg of the blocks'
+    entries (Theorem 2's measure) and the sum of the within-block variances of H (in
+    key units), next to the same for blocks of consecutive node ids."""
+    deg = np.diff(g.rowptr.astype(np.int64))
+    Kf = K.astype(np.float64)
+    out = {}
+    for name, order in (("sorted", perm.astype(np.int64)), ("node_id", np.arange(g.n))):
+        edges = np.linspace(0, g.n, blocks + 1).astype(np.int64)
+        work = np.add.reduceat(deg[order], edges[:-1])
+        kk = Kf[order]
+        s1 = np.add.reduceat(kk, edges[:-1])
+        s2 = np.add.reduceat(kk * kk, edges[:-1])
+        cnt = np.diff(edges)
+        var = s2 / cnt - (s1 / cnt) ** 2
+        out[name] = {"imbalance_max_over_avg": round(float(work.max() / work.mean()), 2),
+                     "sum_block_var_K": float(np.maximum(var, 0).sum())}
+    out["blocks"] = blocks
+    return out
+
+
 def ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev):
     """Times partition and the dominant SpMM for each variant; prints one JSON line each."""
     X = Xd if not w.is_gcn else torch.randn((g.n, F_dom), dtype=torch.float32, device=Xd.device,
@@ -174,14 +196,17 @@ def ablation(args, w, g, dg, torch, np, rowptr, col, val, Xd, F_dom, stream, ev)
                 part_ms.append(a.elapsed_time(b))
                 spmm_ms.append(c.elapsed_time(d))
             info = plan.info()
+            if rep == args.warmup + args.steps - 1:
+                plan_perm, _, plan_K = plan.export()
             plan.destroy()
         ms = float(np.mean(spmm_ms))
+        stats = block_stats(g, plan_perm, plan_K, np)
         print(json.dumps({"ablation": name, "workload": w.name, "F": F_dom,
                           "alpha": [info["alpha_num"], info["alpha_den"]],
                           "force_mode": force, "n_sparse": info["n_sparse"],
                           "n_dense": info["n_dense"], "kstar": info["kstar"],
                           "partition_ms": round(float(np.mean(part_ms)), 4),
-                          "spmm_ms": round(ms, 4),
+                          "spmm_ms": round(ms, 4), "block_stats": stats,
                           "spmm_ge_s": round(g.nnz * F_dom / (ms * 1e-3) / 1e9, 2),
                           "spmm_hbm_frac_bmin": round(spmm_bytes(g.n, g.nnz, F_dom, 2 if w.is_gcn else 4)
                                                       / (ms * 1e-3) / (PEAK_HBM_GBS * 1e9), 4),
@@ -490,6 +515,7 @@ def main():
         "config": {"workload": w.desc, "name": w.name, "n": g.n, "nnz": g.nnz,
                    "max_degree": g.max_degree(), "F": w.F, "walks_per_node": w.walks,
                    "walk_len": w.steps, "layers": [list(l) for l in w.layers],
+                   "seed": 0, "graph_sha256": g.sha256()[:16],
                    "parallelism": "single GPU"},
         "roofline": roof,
         "phases_ms": {k: round(float(np.mean(v)), 4) for k, v in phases.items()},

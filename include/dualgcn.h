@@ -38,7 +38,9 @@ typedef enum dualgcn_status {
     DUALGCN_ERR_BAD_CSR = -2,      /* row pointers not monotone, rowptr[0] != 0,
                                       rowptr[n] != nnz, or a column outside [0, n) */
     DUALGCN_ERR_UNSUPPORTED = -3,  /* sizes the library does not handle (see each call) */
-    DUALGCN_ERR_OOM = -4,          /* a device allocation failed */
+    DUALGCN_ERR_OOM = -4,          /* a device allocation failed (for tests, the environment
+                                      variable DUALGCN_TEST_FAIL_ALLOC=N makes the N-th
+                                      allocation after it is set fail) */
     DUALGCN_ERR_HIP = -5,          /* a HIP runtime call failed; see dualgcn_last_hip_error */
     DUALGCN_ERR_NO_DEVICE = -6     /* no usable HIP device */
 } dualgcn_status;

@@ -1,7 +1,9 @@
 // C ABI of libdualgcn: argument checks, status codes and dispatch to the kernels.
 // Every check that needs no device runs before the device is touched.
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
+#include <string>
 #include <new>
 #include <vector>
 
@@ -31,8 +33,28 @@ int device_status() {
     return DUALGCN_OK;
 }
 
+// Allocation-failure injection for tests: while DUALGCN_TEST_FAIL_ALLOC holds N > 0 (any
+// text may follow the number), the N-th device allocation request counted from the
+// moment the variable took its current text fails with DUALGCN_ERR_OOM (once) before HIP
+// is called.
+bool injected_failure() {
+    static std::mutex mu;
+    static std::string last;
+    static long count = 0;
+    const char *e = std::getenv("DUALGCN_TEST_FAIL_ALLOC");
+    const std::string cur = e ? e : "";
+    std::lock_guard<std::mutex> lock(mu);
+    if (cur != last) {
+        last = cur;
+        count = 0;
+    }
+    const long target = cur.empty() ? 0 : std::atol(cur.c_str());
+    return target > 0 && ++count == target;
+}
+
 int alloc_bytes(void **p, size_t bytes) {
     *p = nullptr;
+    if (injected_failure()) return DUALGCN_ERR_OOM;
     const hipError_t e = hipMalloc(p, bytes ? bytes : 1);
     if (e != hipSuccess) {
         *p = nullptr;
@@ -64,6 +86,7 @@ constexpr size_t kCachedBlocks = 4;
 int alloc_block(void **p, size_t *capacity, size_t bytes) {
     *p = nullptr;
     *capacity = 0;
+    if (injected_failure()) return DUALGCN_ERR_OOM;
     if (bytes == 0) bytes = 1;
     int dev = 0;
     int st = hip_status(hipGetDevice(&dev));
