@@ -57,7 +57,8 @@ def build(verbose=False):
     with ThreadPoolExecutor(workers) as ex:
         objs = list(ex.map(compile_one, SOURCES))
     cmd = [cc, f"--offload-arch={ARCH}", "-mcode-object-version=5", "-shared", "-fPIC", "-o",
-           LIB + ".tmp"] + objs
+           LIB + ".tmp"] + objs + ["-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx",
+                                   "-Wl,-rpath,/opt/rocm/lib"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True, capture_output=not verbose)

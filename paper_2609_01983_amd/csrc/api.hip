@@ -234,6 +234,7 @@ int dualgcn_last_hip_error(void) { return dgc::g_last_hip_error; }
 int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,
                       uint32_t walk_len, const dualgcn_thresholds *th, void *stream,
                       dualgcn_plan **out) {
+    dgc::TraceRange trace("dualgcn_partition");
     if (!out) return DUALGCN_ERR_INVALID_ARG;
     *out = nullptr;
     int st = check_csr(csr);
@@ -264,6 +265,7 @@ int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, 
 
 int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, void *Y, int32_t F,
                      uint32_t flags, void *stream) {
+    dgc::TraceRange trace("dualgcn_spmm");
     int st = check_plan(plan);
     if (st) return st;
     if (!X || !Y || F < 1) return DUALGCN_ERR_INVALID_ARG;
@@ -280,6 +282,7 @@ int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, void *Y, int32_t 
 
 int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F_in,
                    int32_t F_out, uint32_t flags, void *stream) {
+    dgc::TraceRange trace("dualgcn_update");
     if (n < 1) return DUALGCN_ERR_INVALID_ARG;
     int st = check_update(X, W, T, F_in, F_out);
     if (st) return st;
@@ -304,6 +307,7 @@ int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t 
 int dualgcn_gcn_layer(const dualgcn_plan *plan, const void *X, const float *W, void *Y,
                       int32_t F_in, int32_t F_out, uint32_t flags, void *workspace,
                       size_t workspace_bytes, void *stream) {
+    dgc::TraceRange trace("dualgcn_gcn_layer");
     int st = check_plan(plan);
     if (st) return st;
     if (!Y || !workspace) return DUALGCN_ERR_INVALID_ARG;
@@ -326,6 +330,7 @@ int dualgcn_gcn_layer(const dualgcn_plan *plan, const void *X, const float *W, v
 
 int dualgcn_softmax_xent(const float *Y, const int32_t *labels, int32_t n, int32_t C,
                          float scale, float *G, double *loss, void *stream) {
+    dgc::TraceRange trace("dualgcn_softmax_xent");
     if (!Y || !labels || !G || !loss || n < 1 || C < 1) return DUALGCN_ERR_INVALID_ARG;
     if (C >= (1 << 20)) return DUALGCN_ERR_UNSUPPORTED;
     const size_t elems = static_cast<size_t>(n) * C;
@@ -350,6 +355,7 @@ int dualgcn_weight_grad_workspace(int32_t n, int32_t F_in, int32_t F_out, size_t
 int dualgcn_weight_grad(const void *X, const void *G, float *dW, int32_t n, int32_t F_in,
                         int32_t F_out, uint32_t flags, float lr, float *W, void *workspace,
                         size_t workspace_bytes, void *stream) {
+    dgc::TraceRange trace("dualgcn_weight_grad");
     if (!G || !dW || !workspace || n < 1) return DUALGCN_ERR_INVALID_ARG;
     int st = check_update(X, W ? W : dW, dW, F_in, F_out);
     if (st) return st;
@@ -375,6 +381,7 @@ int dualgcn_weight_grad(const void *X, const void *G, float *dW, int32_t n, int3
 
 int dualgcn_backward_data(const void *G, const float *W, const void *M, float *dX, int32_t n,
                           int32_t F_in, int32_t F_out, uint32_t flags, void *stream) {
+    dgc::TraceRange trace("dualgcn_backward_data");
     if (!G || n < 1) return DUALGCN_ERR_INVALID_ARG;
     int st = check_update(G, W, dX, F_in, F_out);
     if (st) return st;
@@ -439,6 +446,7 @@ int dualgcn_plan_export(const dualgcn_plan *plan, int32_t *perm_h, uint32_t *S_h
 
 int dualgcn_arw_patterns(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,
                          uint32_t walk_len, uint8_t *out, void *stream) {
+    dgc::TraceRange trace("dualgcn_arw_patterns");
     int st = check_csr(csr);
     if (st) return st;
     if ((st = check_walks(walks_per_node, walk_len))) return st;
@@ -483,6 +491,7 @@ constexpr char kPlanMagic[8] = {'D', 'G', 'C', 'N', 'P', 'L', 'A', 'N'};
 constexpr uint32_t kPlanVersion = 1;
 
 int dualgcn_plan_save(const dualgcn_plan *plan, void *buf, size_t *bytes) {
+    dgc::TraceRange trace("dualgcn_plan_save");
     int st = check_plan(plan);
     if (st) return st;
     if (!bytes) return DUALGCN_ERR_INVALID_ARG;
@@ -519,6 +528,7 @@ int dualgcn_plan_save(const dualgcn_plan *plan, void *buf, size_t *bytes) {
 
 int dualgcn_plan_load(const dualgcn_csr *csr, const void *buf, size_t bytes, void *stream,
                       dualgcn_plan **out) {
+    dgc::TraceRange trace("dualgcn_plan_load");
     if (!out) return DUALGCN_ERR_INVALID_ARG;
     *out = nullptr;
     int st = check_csr(csr);
@@ -550,6 +560,7 @@ int dualgcn_plan_load(const dualgcn_csr *csr, const void *buf, size_t bytes, voi
 
 int dualgcn_aggregator_values(const dualgcn_csr *csr, int32_t kind, float eps, float *val,
                               void *stream) {
+    dgc::TraceRange trace("dualgcn_aggregator_values");
     int st = check_csr(csr);
     if (st) return st;
     if (!val || kind < DUALGCN_AGG_GCN || kind > DUALGCN_AGG_SUM) return DUALGCN_ERR_INVALID_ARG;

@@ -8,7 +8,23 @@
 
 #include "dualgcn.h"
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 namespace dgc {
+
+// A named range for tracers (roctx; a call into the marker library and nothing more when
+// no tool listens).  next() closes the current range and opens the following one.
+class TraceRange {
+   public:
+    explicit TraceRange(const char *name) { roctxRangePush(name); }
+    ~TraceRange() { roctxRangePop(); }
+    TraceRange(const TraceRange &) = delete;
+    TraceRange &operator=(const TraceRange &) = delete;
+    void next(const char *name) {
+        roctxRangePop();
+        roctxRangePush(name);
+    }
+};
 
 using u128 = unsigned __int128;
 

@@ -883,6 +883,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     int2 *nodeinfo = reinterpret_cast<int2 *>(sm + o_info);
     int32_t *blockmax = reinterpret_cast<int32_t *>(sm + o_bmax);
 
+    TraceRange phase("partition: validate + walks");
     if ((st = hip_status(hipMemsetAsync(bad, 0, 2 * sizeof(int32_t), s)))) return st;
     if ((st = validate_csr(csr, bad, nodeinfo, blockmax, s))) return st;
     int4 *succ = nullptr;
@@ -926,6 +927,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
         if ((st = adaptive_weight(n, k, th.alpha_den, two[0].m, two[1].m, &pa))) return st;
         p->th.alpha_num = static_cast<uint32_t>(pa);
     }
+    phase.next("partition: keys + threshold");
     // keys and moments
     hipLaunchKernelGGL(keys_kernel, dim3(nb_keys), dim3(kThreads), 0, s, csr->rowptr, p->S, n,
                        pa, (qa - pa) * k, p->K, moments, bad);
@@ -945,6 +947,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if (!square_sum_fits(sum.m)) return DUALGCN_ERR_UNSUPPORTED;
     if ((st = threshold_key(n, p->s1, p->s2, th.beta_num, th.beta_den, &p->kstar))) return st;
 
+    phase.next("partition: sort");
     // stable radix sort of (K, v) on the bits the keys use; every entry of perm is a
     // valid node id even before the sort writes it
     if ((st = hip_status(hipMemsetAsync(p->perm, 0, sizeof(int32_t) * un, s)))) return st;
@@ -1015,6 +1018,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
         if ((st = hip_status(hipGetLastError()))) return st;
     }
     uint32_t *pptr_u = reinterpret_cast<uint32_t *>(p->pptr);
+    phase.next("partition: sorted copy + schedule");
     hipLaunchKernelGGL(sorted_degree_kernel, dim3(grid_n1), dim3(kThreads), 0, s, p->order, csr->rowptr,
                        n, pptr_u);
     if ((st = exclusive_scan(pptr_u, static_cast<int64_t>(n) + 1, scan_sums, nullptr, s))) return st;
