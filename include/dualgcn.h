@@ -340,7 +340,7 @@ int dualgcn_weight_grad(const void *X, const void *G, float *dW, int32_t n, int3
  * bfloat16 and multiplied on the matrix cores with float32 accumulation (the
  * kernel of dualgcn_update).  dX must not overlap G or M.  Shape limits as for
  * dualgcn_update (F_in and F_out multiples of 32, F_in <= 1024, F_out <= 256); G
- * 16-byte aligned.  Asynchronous.
+ * 16-byte aligned, and with a mask M and dX too.  Asynchronous.
  */
 int dualgcn_backward_data(const void *G, const float *W, const void *M, float *dX, int32_t n,
                           int32_t F_in, int32_t F_out, uint32_t flags, void *stream);

@@ -391,6 +391,8 @@ int dualgcn_backward_data(const void *G, const float *W, const void *M, float *d
     const size_t xb = un * F_in * sizeof(float);
     if (overlaps(dX, xb, G, un * F_out * (gbf ? 2 : 4))) return DUALGCN_ERR_INVALID_ARG;
     if (M && overlaps(dX, xb, M, un * F_in * (mbf ? 2 : 4))) return DUALGCN_ERR_INVALID_ARG;
+    if (M && (reinterpret_cast<uintptr_t>(M) % 16 || reinterpret_cast<uintptr_t>(dX) % 16))
+        return DUALGCN_ERR_INVALID_ARG;
     if ((st = dgc::device_status())) return st;
     return dgc::launch_backward_data(G, gbf, W, M, mbf, dX, n, F_in, F_out,
                                      static_cast<hipStream_t>(stream));

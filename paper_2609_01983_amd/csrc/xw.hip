@@ -78,15 +78,43 @@ struct XFrag {
 // Where the output keeps a product: no mask, or M > 0 for a float32 or bfloat16 M.
 enum MaskKind { kNoMask = 0, kMaskF32 = 1, kMaskBF16 = 2 };
 
-// The mask element at `at` as float32.
+// Masked products leave the matrix cores through LDS: each wavefront stages its 16-row
+// tile 64 columns at a time (rows padded to 68 words), and every lane then finishes 16
+// consecutive outputs of one row -- the mask read and the output written with 16-byte
+// accesses instead of one element per lane and instruction.
+constexpr int kEpiCols = 64;
+constexpr int kEpiLd = kEpiCols + 4;
+constexpr int kEpiWaveWords = kRowsPerWave * kEpiLd;
+
+size_t epilogue_lds_bytes(int mask) {
+    return mask == kNoMask ? 0 : static_cast<size_t>(kWaves) * kEpiWaveWords * sizeof(float);
+}
+
+// Sixteen consecutive mask elements from `at` (16-byte aligned) as float32.
 template <int MASK>
-__device__ __forceinline__ float mask_value(const void *M, int64_t at) {
+__device__ __forceinline__ void load_mask16(const void *M, int64_t at, float (&m)[16]) {
     if constexpr (MASK == kMaskF32) {
-        return static_cast<const float *>(M)[at];
-    } else if constexpr (MASK == kMaskBF16) {
-        return __builtin_bit_cast(float, static_cast<uint32_t>(static_cast<const unsigned short *>(M)[at]) << 16);
+        const f32x4 *p = reinterpret_cast<const f32x4 *>(static_cast<const float *>(M) + at);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const f32x4 v = p[q];
+            m[4 * q] = v[0];
+            m[4 * q + 1] = v[1];
+            m[4 * q + 2] = v[2];
+            m[4 * q + 3] = v[3];
+        }
     } else {
-        return 1.f;
+        const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const unsigned short *>(M) + at);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const uint4 v = p[q];
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                m[8 * q + 2 * i] = __builtin_bit_cast(float, w[i] << 16);
+                m[8 * q + 2 * i + 1] = __builtin_bit_cast(float, w[i] & 0xFFFF0000u);
+            }
+        }
     }
 }
 
@@ -147,17 +175,51 @@ __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const void *__restric
             }
             cur = nxt;
         }
+        if constexpr (MASK == kNoMask) {
 #pragma unroll
-        for (int t = 0; t < NTMAX; ++t) {
-            if (t < ntiles) {
+            for (int t = 0; t < NTMAX; ++t) {
+                if (t < ntiles) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int64_t orow = row0 + kgrp * 4 + j;
-                    if (orow < n) {
-                        const int64_t at = orow * N + c0 + t * 16 + lrow;
-                        if constexpr (MASK == kNoMask) T[at] = acc[t][j];
-                        else T[at] = mask_value<MASK>(M, at) > 0.f ? acc[t][j] : 0.f;
+                    for (int j = 0; j < 4; ++j) {
+                        const int64_t orow = row0 + kgrp * 4 + j;
+                        if (orow < n) T[orow * N + c0 + t * 16 + lrow] = acc[t][j];
                     }
+                }
+            }
+        } else {
+            float *epi = reinterpret_cast<float *>(w_lds + ncols * ldw) + wave * kEpiWaveWords;
+            const int er = lane >> 2;                  // staged row this lane finishes
+            const int ec = (lane & 3) * 16;            // its first column inside a pass
+            const int64_t orow = row0 + er;
+#pragma unroll
+            for (int h = 0; h < (NTMAX + 3) / 4; ++h) {
+                if (4 * h < ntiles) {                  // uniform over the workgroup
+                    const int cl = h * kEpiCols + ec;  // column inside this launch's block
+                    const bool ok = orow < n && cl < ncols;
+                    const int64_t at = orow * N + c0 + cl;
+                    float mk[16];
+                    if (ok) load_mask16<MASK>(M, at, mk);
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int t = 4 * h + u;
+                        if (t < NTMAX && t < ntiles) {
+#pragma unroll
+                            for (int j = 0; j < 4; ++j) epi[(kgrp * 4 + j) * kEpiLd + u * 16 + lrow] = acc[t][j];
+                        }
+                    }
+                    __syncthreads();
+                    if (ok) {
+                        const f32x4 *src = reinterpret_cast<const f32x4 *>(epi + er * kEpiLd + ec);
+                        f32x4 *dst = reinterpret_cast<f32x4 *>(T + at);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            f32x4 v = src[q];
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) v[i] = mk[4 * q + i] > 0.f ? v[i] : 0.f;
+                            dst[q] = v;
+                        }
+                    }
+                    __syncthreads();
                 }
             }
         }
@@ -186,6 +248,7 @@ int allow_lds(const void *kernel, size_t bytes) {
 template <int NT, bool XBF, int MASK>
 int launch_tiles(const void *X, const float *W, const void *M, float *T, int32_t n, int32_t K,
                  int32_t N, int32_t sk, int32_t sn, int c0, int ntiles, size_t lds, hipStream_t s) {
+    lds += epilogue_lds_bytes(MASK);
     int st = allow_lds(reinterpret_cast<const void *>(&xw_mfma_kernel<NT, XBF, MASK>), lds);
     if (st) return st;
     // workgroups per CU allowed by the LDS of one CU (160 KiB) and by 2048 threads per CU
