@@ -178,7 +178,7 @@ __global__ __launch_bounds__(kThreads) void loss_total_kernel(double *__restrict
 
 // ------------------------------------------------------------------ weight gradient
 
-constexpr int kWgThreads = 512;
+constexpr int kWgThreads = 1024;
 constexpr int kWgWaves = kWgThreads / 64;
 constexpr int kChunk = 64;                       // rows per LDS stage (two k-steps of 32)
 // A transposed LDS row holds the chunk's 64 rows of one column as bfloat16, padded to 68:
@@ -295,8 +295,8 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restric
 #pragma unroll
     for (int u = 0; u < NT; ++u) acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    constexpr int kXItems = (kChunk / 2) * (kMaxIB / 4) / kWgThreads;   // 4
-    constexpr int kGItems = (kChunk / 2) * (kMaxJB / 4) / kWgThreads;   // 2
+    constexpr int kXItems = (kChunk / 2) * (kMaxIB / 4) / kWgThreads;   // 2
+    constexpr int kGItems = (kChunk / 2) * (kMaxJB / 4) / kWgThreads;   // 1
     Stage<XBF, kXItems> xs, xn;
     Stage<GBF, kGItems> gs, gn;
     const int64_t chunks = (static_cast<int64_t>(n) + kChunk - 1) / kChunk;
@@ -426,11 +426,11 @@ int launch_wgrad_nt(const void *X, const void *G, float *partial, int blocks, in
                     int32_t n, int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB,
                     hipStream_t s) {
     const int per_wave = ((IB / 16) * (JB / 16) + kWgWaves - 1) / kWgWaves;
+    if (per_wave <= 2)
+        return launch_wgrad_pass<2, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
     if (per_wave <= 4)
         return launch_wgrad_pass<4, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
-    if (per_wave <= 8)
-        return launch_wgrad_pass<8, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
-    return launch_wgrad_pass<16, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
+    return launch_wgrad_pass<8, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
 }
 
 int launch_wgrad_any(bool x_bf16, bool g_bf16, const void *X, const void *G, float *partial,
