@@ -1,0 +1,64 @@
+"""The largest matrix the library accepts: nnz = 2^31 - 2^24 (just under the 2^31 - 2^16
+bound), built on the device as a circulant (row r holds columns r + o mod n for 127
+fixed offsets, value 1/127).  The partition must cover every row exactly once, and the
+SpMM must match the closed form on sampled rows: entry indices near 2^31 exercise every
+32-bit index path of the kernels."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+N = 1 << 24
+DEG = 127
+F = 4
+
+
+@pytest.fixture(scope="module")
+def dg(device):
+    import paper_2609_01983_amd as dg
+    return dg
+
+
+def _x_value(c, f):
+    return ((c * (f + 1)) % 97) / 97.0 - 0.5
+
+
+def test_max_size_circulant(dg, device):
+    offsets = np.unique(np.concatenate([[0], (np.arange(1, DEG) ** 3) % N]))[:DEG]
+    assert offsets.size == DEG
+    nnz = N * DEG
+    assert nnz == 2 ** 31 - 2 ** 24
+    off = torch.from_numpy(offsets.astype(np.int64)).to(device)
+    rowptr = (torch.arange(N + 1, device=device, dtype=torch.int64) * DEG).to(torch.int32)
+    col = torch.empty(nnz, dtype=torch.int32, device=device)
+    step = 1 << 20                                   # rows per slice while building
+    for r0 in range(0, N, step):
+        rows = torch.arange(r0, min(N, r0 + step), device=device, dtype=torch.int64)
+        c = torch.sort((rows[:, None] + off[None, :]) % N, dim=1).values
+        col[r0 * DEG:(r0 + rows.numel()) * DEG] = c.reshape(-1).to(torch.int32)
+        del c, rows
+    val = torch.full((nnz,), 1.0 / DEG, dtype=torch.float32, device=device)
+    plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=4, walk_len=3)
+    info = plan.info()
+    assert info["nnz"] == nnz and info["n_sparse"] + info["n_dense"] == N
+    perm, S, K = plan.export()
+    assert np.array_equal(np.sort(perm), np.arange(N, dtype=np.int32))
+    assert S.min() >= 4 and S.max() <= 4 * 4
+    Ks = K[perm]
+    assert np.all(Ks[1:] >= Ks[:-1])
+    # X[c, f] from a closed form; Y[r] = (1/127) sum over the offsets of X[r + o]
+    cidx = torch.arange(N, device=device, dtype=torch.int64)
+    X = torch.stack([(((cidx * (f + 1)) % 97).to(torch.float32) / 97.0 - 0.5) for f in range(F)], 1)
+    Y = dg.spmm(plan, X.contiguous())
+    rows = np.concatenate([np.random.default_rng(0).choice(N, 2000, replace=False), [0, N - 1]])
+    Yh = Y[torch.from_numpy(rows).to(device)].cpu().numpy().astype(np.float64)
+    v32 = float(np.float32(1.0 / DEG))
+    for i, r in enumerate(rows):
+        cs = (r + offsets) % N
+        for f in range(F):
+            xs = np.array([np.float32(_x_value(int(c), f)) for c in cs], dtype=np.float64)
+            want = v32 * xs.sum()
+            bound = v32 * np.abs(xs).sum()
+            assert abs(Yh[i, f] - want) <= 1e-5 * bound + 1e-30, (r, f, Yh[i, f], want)
+    plan.destroy()
