@@ -5,14 +5,17 @@
  * product Y = A X of the DualGCN paper (Sec. 1 and Sec. 2.1), scheduled by the
  * paper's dual-metric partition (Sec. 3.2) and run by two kernels, one for the
  * sparse region and one for the dense region of the partition (Sec. 3.3), and
- * the update phase X W of a layer (Sec. 1).
+ * the update phase X W of a layer (Sec. 1); for training, the loss gradient and
+ * the backward products of a layer; the values of other aggregators on the same
+ * structure; and plans saved and loaded across runs.
  *
  * Conventions for every entry point
  *   - Pointers named *_h are host memory; every other array pointer is device
  *     memory on the current HIP device.  No entry point copies user arrays.
  *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
  *     Work is enqueued on that stream.  Only dualgcn_partition,
- *     dualgcn_plan_export and dualgcn_arw_patterns wait for it.
+ *     dualgcn_plan_load, dualgcn_plan_export, dualgcn_plan_save,
+ *     dualgcn_aggregator_values and dualgcn_arw_patterns wait for the device.
  *   - Every function returns a dualgcn_status (0 = success).  Arguments are
  *     checked before the device is touched.  Outputs are undefined after an
  *     error.  No C++ exception crosses this interface.
