@@ -828,9 +828,10 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     // sum over rows longer than C of ceil(deg / C) < 2 nnz / C + 1.
     const size_t max_parts = unnz / kDenseChunk * 2 + 1;
     // The lockstep walker reads successor records (16 bytes per entry, scratch) when the
-    // walks take at least 16 steps per node: building them costs one random read per entry
-    // and saves one dependent random read per step.
-    const bool use_succ = S_host == nullptr && static_cast<uint64_t>(k) * d >= 16;
+    // walks take at least twice as many steps as the matrix has entries: building them
+    // costs one random read per entry and saves one dependent random read per step.
+    const bool use_succ = S_host == nullptr &&
+                          static_cast<u128>(n) * k * d >= 2 * static_cast<u128>(unnz);
     const int32_t nb_keys = static_cast<int32_t>(std::min<int64_t>((n + kThreads - 1) / kThreads, 1024));
     const int32_t nblocks = static_cast<int32_t>((static_cast<int64_t>(n) + kTile - 1) / kTile);
     const int64_t scan_tiles = std::max((static_cast<int64_t>(kRadix) * nblocks + kTile - 1) / kTile,
