@@ -302,3 +302,24 @@ def test_two_layer_training_step_c2(dg, device):
     for got, want in ((dW1, ref16["dW"][0]), (dW2, ref16["dW"][1])):
         assert np.linalg.norm(got - want) <= 1e-3 * np.linalg.norm(want)
     assert abs(loss[0].item() - ref16["loss"]) <= 1e-5 * abs(ref16["loss"])
+
+
+def test_label_restricted_plan_gives_the_loss_gradient_aggregation(dg, device):
+    """The loss gradient vanishes on unlabeled rows, so A^T G = A G (A symmetric) needs only
+    the entries whose column is labeled: the column-restricted matrix's own plan gives the
+    same aggregation (the bench's training step uses it for the last layer)."""
+    g = configs.load_graph("c2")
+    w = configs.WORKLOADS["c2"]
+    labels = dense.labels(g.n, 32, seed=3, labeled_fraction=0.1)
+    Y = dense.features_normal(g.n, 32, seed=4)
+    scale = 1.0 / int((labels >= 0).sum())
+    _, G = oracle.softmax_xent(Y, labels, scale)
+    keep = (labels >= 0)[g.col]
+    rowptr_l = np.concatenate([[0], np.cumsum(keep)])[g.rowptr].astype(np.int32)
+    gl = type(g)(n=g.n, rowptr=rowptr_l, col=g.col[keep].copy(), val=g.val[keep].copy())
+    plan_l = dg.Plan(*to_dev(gl, device), seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    got = dg.spmm(plan_l, torch.from_numpy(G.astype(np.float32)).to(device)).cpu().numpy()
+    want = oracle.spmm_f64(oracle.transpose_csr(g), G)
+    ga = type(g)(n=g.n, rowptr=g.rowptr, col=g.col, val=np.abs(g.val))
+    B = oracle.spmm_f64(oracle.transpose_csr(ga), np.abs(G))
+    _within(got, want, B, 1e-5, "label-restricted A^T G")
