@@ -323,3 +323,23 @@ def test_label_restricted_plan_gives_the_loss_gradient_aggregation(dg, device):
     ga = type(g)(n=g.n, rowptr=g.rowptr, col=g.col, val=np.abs(g.val))
     B = oracle.spmm_f64(oracle.transpose_csr(ga), np.abs(G))
     _within(got, want, B, 1e-5, "label-restricted A^T G")
+
+
+def test_row_restricted_plan_gives_the_labeled_outputs(dg, device):
+    """The loss reads the last layer's output on labeled rows only: the plan of the
+    row-restricted matrix (unlabeled rows empty) gives those rows, and zeros elsewhere."""
+    g = configs.load_graph("c2")
+    w = configs.WORKLOADS["c2"]
+    labels = dense.labels(g.n, 32, seed=5, labeled_fraction=0.1)
+    lab = labels >= 0
+    deg = np.diff(g.rowptr) * lab
+    rowptr_r = np.concatenate([[0], np.cumsum(deg)]).astype(np.int32)
+    keep = np.repeat(lab, np.diff(g.rowptr))
+    gr = type(g)(n=g.n, rowptr=rowptr_r, col=g.col[keep].copy(), val=g.val[keep].copy())
+    plan_r = dg.Plan(*to_dev(gr, device), seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    T = dense.features_normal(g.n, 32, seed=6)
+    got = dg.spmm(plan_r, torch.from_numpy(T).to(device)).cpu().numpy()
+    rows = np.flatnonzero(lab).astype(np.int32)
+    want, B = oracle.spmm(g, T, rows)
+    _within(got[rows], want, B, 1e-5, "row-restricted A T on labeled rows")
+    assert np.all(got[~lab] == 0.0)
