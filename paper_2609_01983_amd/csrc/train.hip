@@ -408,6 +408,12 @@ int launch_wgrad_pass(const void *X, const void *G, float *partial, int blocks, 
                       int32_t n, int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB,
                       hipStream_t s) {
     const size_t lds = wgrad_lds_bytes(IB, JB);
+    if (lds > 64 * 1024) {                   // dynamic LDS above 64 KiB is requested per kernel
+        const int st = hip_status(hipFuncSetAttribute(
+            reinterpret_cast<const void *>(&wgrad_kernel<NT, XBF, GBF>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+        if (st) return st;
+    }
     if (blocks == 0) {
         int per_cu = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wgrad_kernel<NT, XBF, GBF>,
@@ -479,7 +485,9 @@ int launch_weight_grad(const void *X, bool x_bf16, const void *G, bool g_bf16, f
     // chunk and kMaxPartials; every pass uses the same count, fixed for a device, so the
     // reduction order is fixed too
     int resident = 1;
-    launch_wgrad_any(x_bf16, g_bf16, X, G, partial, 0, &resident, n, F_in, F_out, 0, IB, 0, JB, s);
+    const int st0 = launch_wgrad_any(x_bf16, g_bf16, X, G, partial, 0, &resident, n, F_in, F_out,
+                                     0, IB, 0, JB, s);
+    if (st0) return st0;
     const int blocks = std::min(wgrad_max_blocks(n), device_cus() * resident);
     for (int j0 = 0; j0 < F_out; j0 += JB) {
         for (int i0 = 0; i0 < F_in; i0 += IB) {
