@@ -342,6 +342,9 @@ def main():
                     help="spmm: one partition, then only the dominant SpMM launches (for counter "
                          "runs); train: GCN training steps on one plan (forward, loss, backward, SGD)")
     ap.add_argument("--lr", type=float, default=0.5, help="SGD step of --mode train")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="GCN workloads: build the next step's partition on a second stream while "
+                         "this step's updates and SpMMs run")
     ap.add_argument("--full-forward", action="store_true",
                     help="--mode train: compute the last layer's output on every row instead of "
                          "the labeled rows the loss reads")
@@ -458,9 +461,43 @@ def main():
                                  walk_len=w.steps)
 
     side = torch.cuda.Stream(device=dev)    # default priority, like the main stream
+    pipelined = args.pipeline and w.is_gcn
+    if pipelined:
+        # the partition of step k + 1 is built on the side stream while step k's updates and
+        # SpMMs run; the first one is built before the warm-up
+        holder["next"] = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks,
+                                 walk_len=w.steps, stream=side)
+
+    def step_pipelined():
+        marks = {}
+        plan = holder["next"]
+        for li, (fin, fout) in enumerate(w.layers):
+            a, b = ev(), ev()
+            a.record(stream)
+            dg.update(Xd if li == 0 else Hs[li - 1], Wd[li], Ts[li])
+            b.record(stream)
+            marks[f"update_{li + 1}"] = [(a, b)]
+            last = li == len(w.layers) - 1
+            a, b = ev(), ev()
+            a.record(stream)
+            dg.spmm(plan, Ts[li], Hs[li], relu=not last, out_bf16=not last)
+            b.record(stream)
+            marks[f"spmm_{li + 1}_F{fout}"] = [(a, b)]
+        a, b = ev(), ev()
+        a.record(side)
+        holder["next"] = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks,
+                                 walk_len=w.steps, stream=side)
+        b.record(side)
+        marks["partition"] = [(a, b)]
+        if holder["plan"] is not None:
+            holder["plan"].destroy()              # waits for this step's work
+        holder["plan"] = plan
+        return marks
 
     def step():
         """Enqueues one step; returns {phase: [(start, end) events]}."""
+        if pipelined:
+            return step_pipelined()
         marks = {}
         if w.is_gcn:
             # layer 1's update needs no plan: it runs on a second stream while the
@@ -523,6 +560,8 @@ def main():
     dom_key = f"spmm_1_F{F_dom}"
     spmm_ms = float(np.mean(phases[dom_key]))
     info = holder["plan"].info()
+    if holder.get("next") is not None:
+        holder["next"].destroy()
 
     ge_per_step = g.nnz * (sum(fo for _, fo in w.layers) if w.is_gcn else w.F)
     value = ge_per_step / (ms_per_step * 1e-3) / 1e9
@@ -557,7 +596,9 @@ def main():
                    "max_degree": g.max_degree(), "F": w.F, "walks_per_node": w.walks,
                    "walk_len": w.steps, "layers": [list(l) for l in w.layers],
                    "seed": 0, "graph_sha256": g.sha256()[:16],
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU",
+                   "steps_overlap": ("partition of the next step beside this step's updates and SpMMs"
+                                     if pipelined else "layer-1 update beside the partition")},
         "roofline": roof,
         "phases_ms": {k: round(float(np.mean(v)), 4) for k, v in phases.items()},
         "plan": {"n_sparse": info["n_sparse"], "n_dense": info["n_dense"],
