@@ -1,8 +1,11 @@
 // Dual-metric partition on gfx950 (DualGCN Sec. 3.2 and Sec. 3.3 Eq. (1)).
 //
-// Pipeline (one stream, two host waits):
-//   validate        rowptr / col checks and the largest degree        -> flag
-//   walks           S_v (arw.hip)
+// Pipeline (one stream, two host waits; three with the adaptive alpha):
+//   validate        rowptr / col checks, the largest degree, node records -> flag
+//   successors      (when walks outnumber entries twice) one record per entry:
+//                   the column and that node's first entry and degree
+//   walks           S_v (arw.hip), or S from a saved plan
+//   adaptive alpha  (optional) moments of S and D            -> extra host wait
 //   keys            K_v = p S_v + (q - p) k D_v, D_v from the row pointers, and the
 //                   exact 128-bit sums of K and K^2 per workgroup, then one
 //                   workgroup folds them                              -> host wait 1

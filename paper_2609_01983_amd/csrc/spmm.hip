@@ -8,7 +8,8 @@
 //
 //   parts      rows of the dense region longer than one chunk, split into parts
 //              of kDenseChunk entries (heaviest row first), one wavefront per part
-//   long       the other dense rows of at least 2^kLongRowOctave entries, one
+//   long       the other dense rows of at least 2^kLongRowOctave entries (one to
+//              three octaves fewer for groups narrower than 32 lanes), one
 //              wavefront per row, heaviest first
 //   medium     the remaining dense rows, one lane group per row, heaviest first
 //   sparse     tasks of up to kTaskRows short consecutive rows, one lane group per
