@@ -48,6 +48,12 @@ def spmm_bytes(n, nnz, F, ybytes=4):
     return 4 * (n + 1) + 8 * nnz + 4 * n * F + ybytes * n * F + 4 * n
 
 
+def fused_bytes(n, nnz, F_in, F_out):
+    """B_min of one aggregation fused with the next update: row pointers, (column, value)
+    pairs, X once, T (float32, F_out wide) once, order; W is negligible."""
+    return 4 * (n + 1) + 8 * nnz + 4 * n * F_in + 4 * n * F_out + 4 * n
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
@@ -56,16 +62,19 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def counter_traffic(workload):
-    """HBM bytes per SpMM launch from the committed counter summary, if still valid."""
+def counter_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, if still valid."""
     if not os.path.exists(COUNTER_SUMMARY):
         return None, "no counter summary"
     text = open(COUNTER_SUMMARY).read()
     m_w = re.search(r"^workload: (\S+)", text, re.M)
+    m_k = re.search(r"^kernel: (.+)$", text, re.M)
     m_t = re.search(r"^traffic_bytes_per_launch: (\d+)", text, re.M)
     m_h = re.search(r"^kernel_source_sha256: ([0-9a-f]{64})", text, re.M)
     if not (m_w and m_t and m_h) or m_w.group(1) != workload:
         return None, "no counters for this workload"
+    if not m_k or m_k.group(1).strip() != kernel:
+        return None, "no counters for this kernel"
     if m_h.group(1) != kernel_source_hash():
         return None, "kernel changed since the counters were taken"
     return int(m_t.group(1)), "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
@@ -351,6 +360,9 @@ def main():
     ap.add_argument("--full-backward", action="store_true",
                     help="--mode train: aggregate the loss gradient with the full plan instead of "
                          "the plan restricted to labeled columns")
+    ap.add_argument("--unfused", action="store_true",
+                    help="GCN steps: layer 1's aggregation and layer 2's update as two calls "
+                         "(by default one, dualgcn_spmm_update); --mode spmm: time the plain SpMM")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device to device (a dispatch of known traffic)")
     ap.add_argument("--ablation", action="store_true",
@@ -400,19 +412,29 @@ def main():
     if args.mode == "spmm":
         plan = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
         Xs = torch.randn((g.n, F_dom), dtype=torch.float32, device=dev) if w.is_gcn else Xd
-        Ys = torch.empty(Xs.shape, dtype=torch.bfloat16 if w.is_gcn else torch.float32, device=dev)
+        fused_w = not args.unfused and w.is_gcn and len(w.layers) > 1
+        if fused_w:
+            F_next = w.layers[1][1]
+            Ys = torch.empty((g.n, F_next), dtype=torch.float32, device=dev)
+        else:
+            Ys = torch.empty(Xs.shape, dtype=torch.bfloat16 if w.is_gcn else torch.float32, device=dev)
         times = []
         for _ in range(args.spmm_reps):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            dg.spmm(plan, Xs, Ys, relu=w.is_gcn, out_bf16=w.is_gcn)
+            if fused_w:
+                dg.spmm_update(plan, Xs, Wd[1], Ys, relu=True)
+            else:
+                dg.spmm(plan, Xs, Ys, relu=w.is_gcn, out_bf16=w.is_gcn)
             b.record(stream)
             times.append((a, b))
         torch.cuda.synchronize()
         ms = [a.elapsed_time(b) for a, b in times]
-        print(json.dumps({"mode": "spmm", "config": w.name, "F": F_dom,
+        print(json.dumps({"mode": "spmm", "config": w.name, "F": F_dom, "fused_update": fused_w,
                           "ms": [round(x, 4) for x in ms],
-                          "bytes_min": spmm_bytes(g.n, g.nnz, F_dom, 2 if w.is_gcn else 4)}), flush=True)
+                          "bytes_min": (fused_bytes(g.n, g.nnz, F_dom, F_next) if fused_w else
+                                        spmm_bytes(g.n, g.nnz, F_dom, 2 if w.is_gcn else 4))}),
+              flush=True)
         plan.destroy()
         return
 
@@ -468,21 +490,39 @@ def main():
         holder["next"] = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks,
                                  walk_len=w.steps, stream=side)
 
-    def step_pipelined():
-        marks = {}
-        plan = holder["next"]
-        for li, (fin, fout) in enumerate(w.layers):
-            a, b = ev(), ev()
-            a.record(stream)
-            dg.update(Xd if li == 0 else Hs[li - 1], Wd[li], Ts[li])
-            b.record(stream)
-            marks[f"update_{li + 1}"] = [(a, b)]
+    fused = not args.unfused and w.is_gcn
+
+    def layers(plan, marks, first):
+        """Layers `first`.. of the GCN on the main stream (layer 1's update, if first > 0,
+        is already in Ts[0]).  With `fused`, a layer's aggregation and the next layer's
+        update are one call that never stores the layer's output."""
+        for li in range(first, len(w.layers)):
+            fout = w.layers[li][1]
+            if li > 0 and not fused:
+                a, b = ev(), ev()
+                a.record(stream)
+                dg.update(Hs[li - 1], Wd[li], Ts[li])
+                b.record(stream)
+                marks[f"update_{li + 1}"] = [(a, b)]
             last = li == len(w.layers) - 1
             a, b = ev(), ev()
             a.record(stream)
-            dg.spmm(plan, Ts[li], Hs[li], relu=not last, out_bf16=not last)
+            if fused and not last:
+                dg.spmm_update(plan, Ts[li], Wd[li + 1], Ts[li + 1], relu=True)
+            else:
+                dg.spmm(plan, Ts[li], Hs[li], relu=not last, out_bf16=not last)
             b.record(stream)
             marks[f"spmm_{li + 1}_F{fout}"] = [(a, b)]
+
+    def step_pipelined():
+        marks = {}
+        plan = holder["next"]
+        a, b = ev(), ev()
+        a.record(stream)
+        dg.update(Xd, Wd[0], Ts[0])
+        b.record(stream)
+        marks["update_1"] = [(a, b)]
+        layers(plan, marks, 0)
         a, b = ev(), ev()
         a.record(side)
         holder["next"] = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks,
@@ -521,19 +561,7 @@ def main():
         plan = holder["plan"]
         if w.is_gcn:
             stream.wait_event(upd1_done)
-            for li, (fin, fout) in enumerate(w.layers):
-                if li > 0:
-                    a, b = ev(), ev()
-                    a.record(stream)
-                    dg.update(Hs[li - 1], Wd[li], Ts[li])
-                    b.record(stream)
-                    marks[f"update_{li + 1}"] = [(a, b)]
-                last = li == len(w.layers) - 1
-                a, b = ev(), ev()
-                a.record(stream)
-                dg.spmm(plan, Ts[li], Hs[li], relu=not last, out_bf16=not last)
-                b.record(stream)
-                marks[f"spmm_{li + 1}_F{fout}"] = [(a, b)]
+            layers(plan, marks, 0)
         else:
             a, b = ev(), ev()
             a.record(stream)
@@ -565,19 +593,30 @@ def main():
 
     ge_per_step = g.nnz * (sum(fo for _, fo in w.layers) if w.is_gcn else w.F)
     value = ge_per_step / (ms_per_step * 1e-3) / 1e9
-    ybytes = 2 if w.is_gcn else 4                    # the dominant SpMM of c5 writes bfloat16
-    bmin = spmm_bytes(g.n, g.nnz, F_dom, ybytes)
+    lpr = min(64, max(1, 1 << max(0, (F_dom - 1).bit_length() - 2)))
+    if fused:
+        # the dominant kernel is layer 1's aggregation with layer 2's update fused in: it
+        # writes T (float32, F_next wide) instead of the layer's output
+        F_next = w.layers[1][1]
+        out_bytes = 4 * g.n * F_next
+        bmin = fused_bytes(g.n, g.nnz, F_dom, F_next)
+        kname = f"spmm_xw_kernel<{lpr}>"
+        kdesc = f"{kname} (F={F_dom} -> {F_next}, ReLU, fused update)"
+    else:
+        out_bytes = (2 if w.is_gcn else 4) * g.n * F_dom   # every layer but the last: bfloat16
+        bmin = spmm_bytes(g.n, g.nnz, F_dom, 2 if w.is_gcn else 4)
+        kname = f"spmm_dual_kernel<{lpr}, 4, {'true' if w.is_gcn else 'false'}>"
+        kdesc = f"{kname} (F={F_dom}{', ReLU, bfloat16 output' if w.is_gcn else ''})"
     achieved = bmin / (spmm_ms * 1e-3) / 1e9
-    traffic, traffic_src = counter_traffic(w.name)
+    traffic, traffic_src = counter_traffic(w.name, kname)
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-            "kernel": f"spmm_dual_kernel<{min(64, max(1, F_dom // 4))}, 4, {'true' if w.is_gcn else 'false'}> "
-                      f"(F={F_dom}{', ReLU, bfloat16 output' if w.is_gcn else ''})",
+            "kernel": kdesc,
             "bytes_per_launch": bmin, "ms_per_launch": round(spmm_ms, 4),
             "launches_timed": len(phases[dom_key]),
             "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
             "gather_bytes_per_launch": 4 * (g.n + 1) + 8 * g.nnz + 4 * g.nnz * F_dom
-                                       + ybytes * g.n * F_dom + 4 * g.n,
+                                       + out_bytes + 4 * g.n,
             "spmm_ge_s": round(g.nnz * F_dom / (spmm_ms * 1e-3) / 1e9, 2)}
     out = {
         "metric": METRIC,
@@ -597,6 +636,7 @@ def main():
                    "walk_len": w.steps, "layers": [list(l) for l in w.layers],
                    "seed": 0, "graph_sha256": g.sha256()[:16],
                    "parallelism": "single GPU",
+                   "fused_update": bool(fused),
                    "steps_overlap": ("partition of the next step beside this step's updates and SpMMs"
                                      if pipelined else "layer-1 update beside the partition")},
         "roofline": roof,

@@ -228,6 +228,28 @@ int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, void *Y, int32_t 
 int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F_in,
                    int32_t F_out, uint32_t flags, void *stream);
 
+/*
+ * dualgcn_spmm_update -- the aggregation of one GCN layer fused with the update of the
+ * next: T = bf16(act(A X)) bf16(W), float32 accumulation (Sec. 1: a layer's aggregated
+ * output, after its non-linearity, is what the next layer multiplies by its weights).
+ *
+ * The same result as dualgcn_spmm_act with DUALGCN_OUT_BF16 into a buffer H followed
+ * by dualgcn_update of H with DUALGCN_IN_BF16 -- bit for bit: every row of act(A X) is
+ * summed as in dualgcn_spmm, rounded to bfloat16 (nearest-even), and multiplied on the
+ * matrix cores in the update's order --, without H: the n x F_in intermediate is never
+ * written to or read from device memory.
+ *
+ * X is float32 n x F_in row-major (16-byte aligned), W float32 F_in x F_out row-major
+ * (rounded to bfloat16 as in dualgcn_update), T float32 n x F_out row-major (4-byte
+ * aligned), overlapping neither X nor W.  flags: DUALGCN_RELU (others are
+ * DUALGCN_ERR_INVALID_ARG).  F_in and F_out must be multiples of 32, at most 256, and
+ * W^T in bfloat16 plus the row tiles must fit a workgroup's LDS (F_in = F_out = 256
+ * does not; everything with F_in <= 128 does), else DUALGCN_ERR_UNSUPPORTED.
+ * Asynchronous.
+ */
+int dualgcn_spmm_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
+                        int32_t F_in, int32_t F_out, uint32_t flags, void *stream);
+
 /* Bytes of device workspace dualgcn_gcn_layer needs (host-only, no device use):
  * room for the float32 n x F_out product T. */
 int dualgcn_gcn_layer_workspace(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,

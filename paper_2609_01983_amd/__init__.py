@@ -75,6 +75,7 @@ def _load():
         "dualgcn_plan_destroy": ([P], None),
         "dualgcn_spmm": ([P, P, P, I32, P], ctypes.c_int),
         "dualgcn_spmm_act": ([P, P, P, I32, U32, P], ctypes.c_int),
+        "dualgcn_spmm_update": ([P, P, P, P, I32, I32, U32, P], ctypes.c_int),
         "dualgcn_update": ([P, P, P, I32, I32, I32, U32, P], ctypes.c_int),
         "dualgcn_gcn_layer_workspace": ([P, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "dualgcn_gcn_layer": ([P, P, P, P, I32, I32, U32, P, SZ, P], ctypes.c_int),
@@ -258,6 +259,28 @@ def update(X, W, T=None, stream=None):
     return T
 
 
+def spmm_update(plan, X, W, T=None, relu=False, stream=None):
+    """T = bf16(act(A X)) bf16(W) (float32 accumulation) without storing act(A X): the
+    aggregation of one layer fused with the next layer's update.  X: float32 [n, F_in],
+    W: float32 [F_in, F_out], T: float32 [n, F_out]."""
+    _dev(X, torch.float32, "X")
+    _dev(W, torch.float32, "W")
+    if X.dim() != 2 or X.shape[0] != plan.n:
+        raise ValueError("X must be [n, F_in]")
+    F_in, F_out = W.shape
+    if X.shape[1] != F_in:
+        raise ValueError("W must be [F_in, F_out]")
+    if T is None:
+        T = torch.empty((plan.n, F_out), dtype=torch.float32, device=X.device)
+    _dev(T, torch.float32, "T")
+    if T.shape != (plan.n, F_out):
+        raise ValueError("T must be [n, F_out]")
+    _check(_lib.dualgcn_spmm_update(plan.handle, X.data_ptr(), W.data_ptr(), T.data_ptr(), F_in,
+                                    F_out, RELU if relu else 0, _stream(stream)),
+           "dualgcn_spmm_update")
+    return T
+
+
 def gcn_layer_workspace_bytes(plan, F_in, F_out):
     nbytes = ctypes.c_size_t()
     _check(_lib.dualgcn_gcn_layer_workspace(plan.handle, F_in, F_out, ctypes.byref(nbytes)),
@@ -421,7 +444,7 @@ def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
     return out
 
 
-__all__ = ["Plan", "spmm", "update", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
+__all__ = ["Plan", "spmm", "spmm_update", "update", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
            "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
            "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16",
            "ALPHA_ADAPTIVE", "GRAD_BF16", "LOSS_SLOTS", "softmax_xent", "weight_grad",

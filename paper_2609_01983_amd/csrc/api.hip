@@ -280,6 +280,29 @@ int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, void *Y, int32_t 
                             static_cast<hipStream_t>(stream));
 }
 
+int dualgcn_spmm_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
+                        int32_t F_in, int32_t F_out, uint32_t flags, void *stream) {
+    dgc::TraceRange trace("dualgcn_spmm_update");
+    int st = check_plan(plan);
+    if (st) return st;
+    if (!X || !W || !T || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (flags & ~DUALGCN_RELU) return DUALGCN_ERR_INVALID_ARG;
+    if (F_in % 32 || F_out % 32 || F_in > 256 || F_out > 256 ||
+        dgc::spmm_xw_lds_bytes(F_in, F_out) > 160 * 1024)
+        return DUALGCN_ERR_UNSUPPORTED;
+    if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(T) % 4)
+        return DUALGCN_ERR_INVALID_ARG;
+    const Plan *p = as_plan(plan);
+    const size_t n = static_cast<size_t>(p->n);
+    const size_t tbytes = n * F_out * sizeof(float);
+    if (overlaps(X, n * F_in * sizeof(float), T, tbytes) ||
+        overlaps(W, static_cast<size_t>(F_in) * F_out * sizeof(float), T, tbytes))
+        return DUALGCN_ERR_INVALID_ARG;
+    if ((st = dgc::device_status())) return st;
+    return dgc::launch_spmm_xw(*p, X, W, T, F_in, F_out, (flags & DUALGCN_RELU) != 0,
+                               static_cast<hipStream_t>(stream));
+}
+
 int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F_in,
                    int32_t F_out, uint32_t flags, void *stream) {
     dgc::TraceRange trace("dualgcn_update");

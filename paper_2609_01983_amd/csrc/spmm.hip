@@ -52,6 +52,8 @@
 // error of every element is below ~(kRound + 2) * 2^-24 * sum |a||x|.
 #include "internal.h"
 
+#include <algorithm>
+
 namespace dgc {
 namespace {
 
@@ -60,6 +62,8 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kRound = 16;            // entries a lane group gathers per round
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 
 template <int VEC>
 __device__ __forceinline__ void load_x(const float *__restrict__ p, float (&x)[VEC]) {
@@ -128,6 +132,50 @@ struct Args {
     int32_t nb_long;            // logical workgroups of long dense rows (a wavefront each)
     int32_t nb_dense;           // nb_long + those of the other dense rows (a group each)
     int32_t relu;
+};
+
+// Where a finished row goes.  Rows are emitted by whole lane groups (every lane of
+// the group calls row() with the same arguments except its features): `slot` numbers
+// the row inside the wavefront's current block of work (group gw, row j of its task:
+// gw * kTaskRows + j; a wavefront's long row: 0).
+//
+// StoreRows writes the row to Y at output row `out`.
+template <int VEC, bool BF>
+struct StoreRows {
+    void *Y;
+    int32_t ld;
+    bool relu;
+    __device__ __forceinline__ void row(int64_t out, int slot, const double (&tot)[VEC], int f,
+                                        bool fin) const {
+        (void)slot;
+        if (fin) store_y<VEC, BF>(Y, out * ld + f, tot, relu);
+    }
+};
+
+// StageRows keeps the row for the fused update instead: act(row) rounded to bfloat16
+// in the wavefront's LDS tile (row `slot`, ld elements apart), its output row in
+// outs[slot].  VEC = 4; the window starts at feature 0.
+struct StageRows {
+    unsigned short *h;
+    int32_t *outs;
+    int32_t ld;
+    bool relu;
+    bool lead;          // the group's first lane records the output row
+    __device__ __forceinline__ void row(int64_t out, int slot, const double (&tot)[4], int f,
+                                        bool fin) const {
+        if (fin) {
+            float o[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                o[j] = static_cast<float>(tot[j]);
+                if (relu) o[j] = o[j] > 0.f ? o[j] : 0.f;
+            }
+            *reinterpret_cast<uint2 *>(h + static_cast<int64_t>(slot) * ld + f) =
+                make_uint2(static_cast<uint32_t>(to_bf16(o[0])) | (static_cast<uint32_t>(to_bf16(o[1])) << 16),
+                           static_cast<uint32_t>(to_bf16(o[2])) | (static_cast<uint32_t>(to_bf16(o[3])) << 16));
+        }
+        if (lead) outs[slot] = static_cast<int32_t>(out);
+    }
 };
 
 // Entries [e, min(e + kRound, e_end)) of the sorted copy, as seen by lane li of a
@@ -209,16 +257,16 @@ __device__ __forceinline__ int32_t task_meta(const int32_t (&m)[N], int j, int g
     return __shfl(x, gbase + j % LPR, 64);
 }
 
-template <int LPR, int VEC, bool BF>
-__global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
+// The work of logical workgroup lb (feature slice `slice`) for wavefront `wave` of a
+// workgroup of WAVES wavefronts; finished rows go to `emit`.
+template <int LPR, int VEC, int WAVES, class Emit>
+__device__ __forceinline__ void spmm_block(const Args &a, int lb, int slice, int wave,
+                                           const Emit &emit) {
     constexpr int GPW = 64 / LPR;                 // lane groups per wavefront
     constexpr int SW = LPR * VEC;                 // features per slice
     constexpr int RPL = (kTaskRows + LPR - 1) / LPR;
 
-    const int slice = static_cast<int>(blockIdx.x) % a.S;
-    const int lb = static_cast<int>(blockIdx.x) / a.S;
     const int lane = static_cast<int>(threadIdx.x) & 63;
-    const int wave = static_cast<int>(threadIdx.x) >> 6;
     const int li = lane % LPR;
     const int gw = lane / LPR;
     const int gbase = lane - li;
@@ -227,7 +275,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
 
     if (lb >= a.nb_parts + a.nb_long && lb < a.nb_parts + a.nb_dense) {
         // ---------------- dense path, shorter rows: one lane group per row
-        const int64_t gi = (static_cast<int64_t>(lb - a.nb_parts - a.nb_long) * kWaves + wave) * GPW + gw;
+        const int64_t gi = (static_cast<int64_t>(lb - a.nb_parts - a.nb_long) * WAVES + wave) * GPW + gw;
         const int64_t i = a.n - a.n_long - 1 - gi;
         if (i < a.n_sparse) return;           // the whole group leaves together
         const int32_t e0 = a.pptr[i], e1 = a.pptr[i + 1];
@@ -249,12 +297,12 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
 #pragma unroll
             for (int j = 0; j < VEC; ++j) tot[j] += static_cast<double>(acc[j]);
         }
-        if (fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(a.perm[i]) * a.ld + f, tot, a.relu);
+        emit.row(a.perm[i], gw * kTaskRows, tot, f, fin);
         return;
     }
     if (lb < a.nb_parts + a.nb_long) {
         // ---------------- dense path, long rows: one wavefront per row or per part of a split row
-        const int w = lb * kWaves + wave;
+        const int w = lb * WAVES + wave;
         int32_t i, e0, e1;
         int part = -1, first = 0;
         if (lb < a.nb_parts) {
@@ -266,7 +314,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
             e0 = a.pptr[i] + part * kDenseChunk;
             e1 = min(e0 + kDenseChunk, a.pptr[i + 1]);
         } else {
-            i = a.n - 1 - (w - a.nb_parts * kWaves);
+            i = a.n - 1 - (w - a.nb_parts * WAVES);
             if (i < a.n - a.n_long) return;
             e0 = a.pptr[i];
             e1 = a.pptr[i + 1];
@@ -275,7 +323,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
         double tot[VEC];
         dense_row<LPR, VEC>(a, e0, e1, li, gw, gbase, f, fin, tot);
         if (part < 0) {
-            if (gw == 0 && fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(a.perm[i]) * a.ld + f, tot, a.relu);
+            if (gw == 0) emit.row(a.perm[i], 0, tot, f, fin);
             return;
         }
         // a part of a split row: its float64 partial, summed by combine_kernel after this launch
@@ -288,7 +336,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
     }
 
     // ---------------- sparse path: one task (up to kTaskRows short rows) per lane group
-    const int64_t t = (static_cast<int64_t>(lb - a.nb_parts - a.nb_dense) * kWaves + wave) * GPW + gw;
+    const int64_t t = (static_cast<int64_t>(lb - a.nb_parts - a.nb_dense) * WAVES + wave) * GPW + gw;
     if (t >= a.n_tasks) return;               // the whole group leaves together
     const int32_t r0 = a.tasks[t];
     const int m = a.tasks[t + 1] - r0;        // 1 .. kTaskRows rows
@@ -305,7 +353,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
         double z[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; ++j) z[j] = 0.0;
-        if (fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(task_meta<LPR>(rout, 0, gbase)) * a.ld + f, z, a.relu);
+        emit.row(task_meta<LPR>(rout, 0, gbase), gw * kTaskRows, z, f, fin);
         return;
     }
     int cur = 0;                              // every row of a task with entries is non-empty
@@ -333,7 +381,7 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
                     tot[j] += static_cast<double>(part[j]);
                     part[j] = 0.f;
                 }
-                if (fin) store_y<VEC, BF>(a.Y, static_cast<int64_t>(cur_out) * a.ld + f, tot, a.relu);
+                emit.row(cur_out, gw * kTaskRows + cur, tot, f, fin);
 #pragma unroll
                 for (int j = 0; j < VEC; ++j) tot[j] = 0.0;
                 if (++cur < m) {
@@ -348,6 +396,14 @@ __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
             part[j] = 0.f;
         }
     }
+}
+
+template <int LPR, int VEC, bool BF>
+__global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
+    const StoreRows<VEC, BF> emit{a.Y, a.ld, a.relu != 0};
+    spmm_block<LPR, VEC, kWaves>(a, static_cast<int>(blockIdx.x) / a.S,
+                                 static_cast<int>(blockIdx.x) % a.S,
+                                 static_cast<int>(threadIdx.x) >> 6, emit);
 }
 
 // The rows split into parts: row = the sum of its parts' float64 partials, in part order.
@@ -366,14 +422,186 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Args a) {
     store_y<1, BF>(a.Y, static_cast<int64_t>(a.perm[sp.row]) * a.ld + f, s, a.relu);
 }
 
-template <int LPR, int VEC>
-int launch_window(Args a, bool bf, hipStream_t s) {
+// ---------------- the aggregation fused with the next layer's update
+//
+// T = bf16(act(A X)) bf16(W), float32 accumulation: the product of a GCN layer's
+// aggregated output with the next layer's weights without storing the aggregated
+// features.  The aggregation is the plain kernel's (same schedule, same sums); a
+// finished row is rounded to bfloat16 into its wavefront's LDS tile instead of Y.
+// Every workgroup stages W^T in bfloat16 once and then takes logical workgroups
+// blockIdx.x, blockIdx.x + gridDim.x, ... of the plain kernel's schedule (heaviest
+// first as before); after each one, the wavefront multiplies its tile by W^T on the
+// matrix cores (v_mfma_f32_16x16x32_bf16, 16-row tiles, k in the update kernel's
+// order) and writes the finished rows of T.  Rows go through the same bfloat16
+// values and the same MFMA sequence as dualgcn_spmm_act with a bfloat16 output
+// followed by dualgcn_update, so both routes give identical T.
+//
+// MFMA 16x16x32 operands (l = lane): A row l % 16 and B column l % 16, eight
+// consecutive k of group l / 16; D rows 4 (l / 16) + j, j < 4, column l % 16.
+constexpr int kXwPad = 8;                     // bfloat16 padding per LDS row
+constexpr int kXwBlocksPerGroup = 8;          // logical workgroups per launched workgroup
+
+template <int LPR>
+struct XwTile {
+    static constexpr int kSlots = (64 / LPR) * kTaskRows;   // rows a wavefront finishes per block
+    static constexpr int kRows = kSlots < 16 ? 16 : kSlots; // rows of its LDS tile
+};
+
+size_t xw_lds_bytes(int lpr, int K, int N) {
+    const int slots = (64 / lpr) * kTaskRows;
+    const size_t rows = slots < 16 ? 16 : slots;
+    const size_t ld = static_cast<size_t>(K) + kXwPad;
+    return (static_cast<size_t>(N) + kWaves * rows) * ld * sizeof(unsigned short) +
+           kWaves * rows * sizeof(int32_t);
+}
+
+template <int LPR>
+__global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const float *__restrict__ W,
+                                                           float *__restrict__ T, int32_t K,
+                                                           int32_t N, int32_t nblocks) {
+    constexpr int ROWS = XwTile<LPR>::kRows;
+    extern __shared__ unsigned short xw_lds[];
+    const int ld = K + kXwPad;
+    const int ntiles = N / 16;
+    const int lane = static_cast<int>(threadIdx.x) & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    unsigned short *wt = xw_lds;                                   // [N][ld]: W^T in bfloat16
+    unsigned short *h = xw_lds + (N + wave * ROWS) * ld;           // this wavefront's rows
+    int32_t *outs = reinterpret_cast<int32_t *>(xw_lds + (N + kWaves * ROWS) * ld) + wave * ROWS;
+    for (int idx = static_cast<int>(threadIdx.x); idx < K * N; idx += kThreads) {
+        const int c = idx / N, j = idx % N;   // consecutive threads read consecutive columns
+        wt[j * ld + c] = to_bf16(W[idx]);
+    }
+    if (lane < ROWS) outs[lane] = -1;
+    __syncthreads();
+
+    const StageRows emit{h, outs, ld, a.relu != 0, lane % LPR == 0};
+    const int lrow = lane & 15, kgrp = lane >> 4;
+    for (int lb = static_cast<int>(blockIdx.x); lb < nblocks; lb += static_cast<int>(gridDim.x)) {
+        spmm_block<LPR, 4, kWaves>(a, lb, 0, wave, emit);
+        __syncwarp();
+#pragma unroll
+        for (int rt = 0; rt < ROWS / 16; ++rt) {
+            if (__ballot(outs[rt * 16 + lrow] >= 0) == 0) continue;   // no row in this tile
+            int32_t o[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) o[j] = outs[rt * 16 + kgrp * 4 + j];
+            const unsigned short *hrow = h + (rt * 16 + lrow) * ld + kgrp * 8;
+            // one 16-column tile of T at a time (the k order of each tile is the update's)
+            for (int t = 0; t < ntiles; ++t) {
+                const unsigned short *wrow = wt + (t * 16 + lrow) * ld + kgrp * 8;
+                f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int kk = 0; kk < K; kk += 32) {
+                    const u16x8 a16 = *reinterpret_cast<const u16x8 *>(hrow + kk);
+                    const u16x8 b16 = *reinterpret_cast<const u16x8 *>(wrow + kk);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a16),
+                                                                  __builtin_bit_cast(bf16x8, b16), acc,
+                                                                  0, 0, 0);
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (o[j] >= 0)
+                        __builtin_nontemporal_store(acc[j], T + static_cast<int64_t>(o[j]) * N + t * 16 + lrow);
+            }
+        }
+        __syncwarp();
+        if (lane < ROWS) outs[lane] = -1;
+        __syncwarp();
+    }
+}
+
+// The split rows of the fused product: the row from its parts' partials (as in
+// combine_kernel), rounded to bfloat16 as row 0 of a tile whose other rows are zero,
+// then the same MFMA sequence on the first wavefront with W read from memory.
+__global__ __launch_bounds__(kThreads) void combine_xw_kernel(const Args a, const float *__restrict__ W,
+                                                              float *__restrict__ T, int32_t K,
+                                                              int32_t N) {
+    __shared__ unsigned short hrow[kMaxSlice];
+    const SplitPart sp = a.parts[blockIdx.x];
+    if (sp.part != 0) return;
+    const int t = static_cast<int>(threadIdx.x);
+    if (t < K) {
+        const double *pp = a.partials + static_cast<int64_t>(sp.first) * kMaxSlice + t;
+        double sum = 0.0;
+        for (int q = 0; q < sp.nparts; ++q) sum += pp[static_cast<int64_t>(q) * kMaxSlice];
+        float o = static_cast<float>(sum);
+        if (a.relu) o = o > 0.f ? o : 0.f;
+        hrow[t] = to_bf16(o);
+    }
+    __syncthreads();
+    if (t >= 64) return;
+    const int lrow = t & 15, kgrp = t >> 4;
+    const int64_t out = static_cast<int64_t>(a.perm[sp.row]) * N;
+    for (int u = 0; u < N / 16; ++u) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kk = kgrp * 8; kk < K; kk += 32) {
+            u16x8 a16, b16;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                a16[e] = lrow == 0 ? hrow[kk + e] : static_cast<unsigned short>(0);
+                b16[e] = to_bf16(W[static_cast<int64_t>(kk + e) * N + u * 16 + lrow]);
+            }
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a16),
+                                                          __builtin_bit_cast(bf16x8, b16), acc, 0, 0, 0);
+        }
+        if (kgrp == 0) T[out + u * 16 + lrow] = acc[0];
+    }
+}
+
+// Logical workgroups of the plain kernel's schedule (sets the nb_* fields).
+template <int LPR>
+int64_t schedule_blocks(Args &a) {
     constexpr int GPB = kThreads / LPR;       // sparse tasks per workgroup
     a.nb_parts = (a.n_parts + kWaves - 1) / kWaves;
     a.nb_long = (a.n_long + kWaves - 1) / kWaves;
     a.nb_dense = a.nb_long + (a.n - a.n_sparse - a.n_long + GPB - 1) / GPB;
     const int64_t nb_sparse = (static_cast<int64_t>(a.n_tasks) + GPB - 1) / GPB;
-    const int64_t blocks = (static_cast<int64_t>(a.nb_parts) + a.nb_dense + nb_sparse) * a.S;
+    return static_cast<int64_t>(a.nb_parts) + a.nb_dense + nb_sparse;
+}
+
+int device_cus() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+    }
+    return cus;
+}
+
+template <int LPR>
+int launch_xw_window(Args a, const float *W, float *T, int32_t K, int32_t N, hipStream_t s) {
+    const int64_t blocks = schedule_blocks<LPR>(a);
+    if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
+    if (blocks > 0) {
+        const size_t lds = xw_lds_bytes(LPR, K, N);
+        const void *kern = reinterpret_cast<const void *>(&spmm_xw_kernel<LPR>);
+        if (lds > 64 * 1024) {
+            const int st = hip_status(hipFuncSetAttribute(
+                kern, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+            if (st) return st;
+        }
+        // about kXwBlocksPerGroup logical workgroups each, and at least as many workgroups
+        // as fit at once (LDS of one CU: 160 KiB; 2048 threads).  Measured on c5 (F 128 -> 64):
+        // one pass of resident workgroups over all blocks is 12% slower than this (its static
+        // share of blocks finishes unevenly); blocks of ~4 or fewer pay the W staging again.
+        const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(2048 / kThreads, (160 * 1024) / lds));
+        const int64_t grid = std::min<int64_t>(
+            blocks, std::max<int64_t>(per_cu * device_cus(), (blocks + kXwBlocksPerGroup - 1) / kXwBlocksPerGroup));
+        hipLaunchKernelGGL((spmm_xw_kernel<LPR>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
+                           lds, s, a, W, T, K, N, static_cast<int32_t>(blocks));
+    }
+    if (a.n_parts > 0)
+        hipLaunchKernelGGL(combine_xw_kernel, dim3(static_cast<unsigned>(a.n_parts)), dim3(kThreads),
+                           0, s, a, W, T, K, N);
+    return hip_status(hipGetLastError());
+}
+
+template <int LPR, int VEC>
+int launch_window(Args a, bool bf, hipStream_t s) {
+    const int64_t blocks = schedule_blocks<LPR>(a) * a.S;
     if (blocks == 0) return DUALGCN_OK;
     if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
     if (bf)
@@ -393,10 +621,7 @@ int launch_window(Args a, bool bf, hipStream_t s) {
     return hip_status(hipGetLastError());
 }
 
-}  // namespace
-
-int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool bf,
-                hipStream_t s) {
+Args plan_args(const Plan &p, const float *X, void *Y, int32_t F, bool relu) {
     Args a{};
     a.pptr = p.pptr;
     a.pcol = p.pcol;
@@ -414,6 +639,45 @@ int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bo
     a.n_long = p.n_long[0];
     a.ld = F;
     a.relu = relu ? 1 : 0;
+    return a;
+}
+
+// Lane-group width for a window of w features with four features per lane, and the
+// class of the long-row bound that goes with it.
+int window_lpr(int32_t w) {
+    return w <= 4 ? 1 : w <= 8 ? 2 : w <= 16 ? 4 : w <= 32 ? 8 : w <= 64 ? 16 : w <= 128 ? 32 : 64;
+}
+
+int long_row_class(int lpr) {
+    int cls = 0;
+    for (int g = lpr; g < 32 && cls < kLongRowClasses - 1; g *= 2) ++cls;
+    return cls;
+}
+
+}  // namespace
+
+size_t spmm_xw_lds_bytes(int32_t F_in, int32_t F_out) {
+    return xw_lds_bytes(window_lpr(F_in), F_in, F_out);
+}
+
+int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, int32_t F_in,
+                   int32_t F_out, bool relu, hipStream_t s) {
+    Args a = plan_args(p, X, nullptr, F_in, relu);
+    a.f0 = 0;
+    a.fend = F_in;
+    a.S = 1;
+    const int lpr = window_lpr(F_in);
+    a.n_long = p.n_long[long_row_class(lpr)];
+    if (lpr == 8) return launch_xw_window<8>(a, W, T, F_in, F_out, s);
+    if (lpr == 16) return launch_xw_window<16>(a, W, T, F_in, F_out, s);
+    if (lpr == 32) return launch_xw_window<32>(a, W, T, F_in, F_out, s);
+    if (lpr == 64) return launch_xw_window<64>(a, W, T, F_in, F_out, s);
+    return DUALGCN_ERR_UNSUPPORTED;
+}
+
+int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool bf,
+                hipStream_t s) {
+    Args a = plan_args(p, X, Y, F, relu);
 
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
                      (reinterpret_cast<uintptr_t>(Y) % (bf ? 8 : 16) == 0) && (F % 4 == 0);
@@ -426,10 +690,7 @@ int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bo
             // whole rows: the smallest power-of-two lane group with 4 features per lane;
             // groups under 32 lanes hand rows from a lower length bound to wavefronts
             a.S = 1;
-            const int lpr = w <= 4 ? 1 : w <= 8 ? 2 : w <= 16 ? 4 : w <= 32 ? 8 : w <= 64 ? 16 : 32;
-            int cls = 0;
-            for (int g = lpr; g < 32 && cls < kLongRowClasses - 1; g *= 2) ++cls;
-            a.n_long = p.n_long[cls];
+            a.n_long = p.n_long[long_row_class(window_lpr(w))];
             if (w <= 4) st = launch_window<1, 4>(a, bf, s);
             else if (w <= 8) st = launch_window<2, 4>(a, bf, s);
             else if (w <= 16) st = launch_window<4, 4>(a, bf, s);
