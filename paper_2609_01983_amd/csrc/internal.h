@@ -146,6 +146,9 @@ __device__ __forceinline__ unsigned short to_bf16(float f) {
 
 // ---- SpMM (spmm.hip): Y = A X on one plan, optional ReLU on the result; with out_bf16
 // Y holds the bfloat16 rounding (nearest-even) of the float32 results.
+// Host wait for the work queued on a stream, polling instead of blocking (partition.hip).
+int wait_stream(hipStream_t stream);
+
 int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool out_bf16,
                 hipStream_t stream);
 // T = bf16(act(A X)) bf16(W) (float32 accumulation) without storing act(A X):

@@ -25,6 +25,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <thread>
 
 namespace dgc {
 namespace {
@@ -652,10 +653,35 @@ struct ScratchBlock {
     hipStream_t stream = nullptr;
     ~ScratchBlock() {
         if (!p) return;
-        (void)hipStreamSynchronize(stream);
+        (void)wait_stream(stream);
         release_block(p, bytes);
     }
 };
+
+}  // namespace
+
+// Waits until the work queued on s so far has finished by polling an event: a wait
+// that blocks in the runtime resumes 50-150 us after the last kernel, which the
+// partition's host waits would otherwise add to every build (the GPU idles meanwhile).
+int wait_stream(hipStream_t s) {
+    hipEvent_t e = nullptr;
+    int st = hip_status(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    if (st) return st;
+    st = hip_status(hipEventRecord(e, s));
+    while (!st) {
+        const hipError_t q = hipEventQuery(e);
+        if (q == hipSuccess) break;
+        if (q != hipErrorNotReady) {
+            st = hip_status(q);
+            break;
+        }
+        std::this_thread::yield();
+    }
+    (void)hipEventDestroy(e);
+    return st;
+}
+
+namespace {
 
 // Exclusive scan of `count` u32 values in place; `sums` holds one word per tile.
 // Writes the grand total to *grand (device) when grand is not null.
@@ -925,7 +951,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
         Summary two[2];
         if ((st = hip_status(hipMemcpyAsync(two, summary, sizeof(two), hipMemcpyDeviceToHost, s))))
             return st;
-        if ((st = hip_status(hipStreamSynchronize(s)))) return st;       // adaptive alpha only
+        if ((st = wait_stream(s))) return st;                           // adaptive alpha only
         if (two[0].flag) return DUALGCN_ERR_BAD_CSR;
         if (!square_sum_fits(two[0].m) || !square_sum_fits(two[1].m)) return DUALGCN_ERR_UNSUPPORTED;
         if ((st = adaptive_weight(n, k, th.alpha_den, two[0].m, two[1].m, &pa))) return st;
@@ -941,7 +967,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     Summary sum{};
     if ((st = hip_status(hipMemcpyAsync(&sum, summary, sizeof(sum), hipMemcpyDeviceToHost, s))))
         return st;
-    if ((st = hip_status(hipStreamSynchronize(s)))) return st;           // host wait 1
+    if ((st = wait_stream(s))) return st;                               // host wait 1
     if (sum.flag) return DUALGCN_ERR_BAD_CSR;
 
     p->max_degree = sum.maxdeg;
@@ -1049,7 +1075,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     SplitSummary ss{};
     if ((st = hip_status(hipMemcpyAsync(&ss, dsum, sizeof(ss), hipMemcpyDeviceToHost, s)))) return st;
     // host wait 2: the region and schedule sizes; the scratch block is released after it
-    if ((st = hip_status(hipStreamSynchronize(s)))) return st;
+    if ((st = wait_stream(s))) return st;
     if (ss.parts > max_parts) return DUALGCN_ERR_HIP;    // impossible: bounded above
     p->n_sparse = ss.n_sparse;
     p->n_tasks = static_cast<int32_t>(ss.tasks);
