@@ -159,55 +159,59 @@ __device__ __forceinline__ void walk_lockstep(const int2 *__restrict__ nodeinfo,
     }
 }
 
-// The same lockstep walks over successor records: succ[e] = (col[e], first entry of that
-// node, its degree), so one read per step yields the next node together with what the
-// step after it needs -- one dependent random read per step instead of two.
+// The same lockstep walks over successor records: succ[e] = (first entry, degree) of
+// the node in column e, so one 8-byte read per step yields the next node together with
+// what the step after it needs -- one dependent random read per step instead of two.
+// A node is identified by its first entry, which is unique among nodes with entries;
+// a node without entries (it shares its first entry with the next node that has some)
+// gets bit 31 set.  A walk meets at most one such node, as its last, since it never
+// leaves it, so the keys tell apart every pair of nodes one walk can visit.
+__device__ __forceinline__ int32_t node_key(int2 rec) {
+    return rec.y > 0 ? rec.x : static_cast<int32_t>(static_cast<uint32_t>(rec.x) | 0x80000000u);
+}
+
 template <int MAXD, int WPL>
 __device__ __forceinline__ void walk_lockstep_succ(const int2 *__restrict__ nodeinfo,
-                                                   const int4 *__restrict__ succ, uint32_t v,
+                                                   const int2 *__restrict__ succ, uint32_t v,
                                                    uint32_t w0, uint32_t d, uint64_t seed,
                                                    uint32_t (&u)[WPL]) {
     int32_t path[WPL][MAXD + 1];
-    int32_t cur[WPL], first[WPL], deg[WPL];
+    int2 cur[WPL];                // (first entry, degree) of the current node
     bool live[WPL];
     Block4 blk[WPL];
     const int2 start = nodeinfo[v];
 #pragma unroll
     for (int j = 0; j < WPL; ++j) {
-        path[j][0] = static_cast<int32_t>(v);
-        cur[j] = static_cast<int32_t>(v);
-        first[j] = start.x;
-        deg[j] = start.y;
+        path[j][0] = node_key(start);
+        cur[j] = start;
         live[j] = true;
         u[j] = 1;
     }
 #pragma unroll
     for (int s = 0; s < MAXD; ++s) {
         if (static_cast<uint32_t>(s) >= d) break;
-        int4 rec[WPL];            // (next node, its first entry, its degree, unused)
+        int2 nxt[WPL];
 #pragma unroll
         for (int j = 0; j < WPL; ++j) {
-            rec[j] = make_int4(cur[j], first[j], deg[j], 0);
-            if (live[j] && deg[j] > 0) {
+            nxt[j] = cur[j];
+            if (live[j] && cur[j].y > 0) {
                 if ((s & 7) == 0) blk[j] = philox4x64_10(v, w0 + j, static_cast<uint64_t>(s >> 3), 0, seed, 0);
                 const uint32_t r = half_word(blk[j], s);
-                rec[j] = succ[first[j] + static_cast<int32_t>(__umulhi(r, static_cast<uint32_t>(deg[j])))];
+                nxt[j] = succ[cur[j].x + static_cast<int32_t>(__umulhi(r, static_cast<uint32_t>(cur[j].y)))];
             }
         }
 #pragma unroll
         for (int j = 0; j < WPL; ++j) {
-            const int32_t nxt = rec[j].x;
+            const int32_t key = node_key(nxt[j]);
             if (live[j]) {
                 bool seen = false;
 #pragma unroll
-                for (int i = 0; i <= s; ++i) seen |= path[j][i] == nxt;
+                for (int i = 0; i <= s; ++i) seen |= path[j][i] == key;
                 if (!seen) ++u[j];
-                live[j] = !(deg[j] <= 1 && nxt == cur[j]);   // absorbed: stays put for good
+                live[j] = !(cur[j].y <= 1 && key == path[j][s]);   // absorbed: stays put for good
             }
-            path[j][s + 1] = nxt;
-            cur[j] = nxt;
-            first[j] = rec[j].y;
-            deg[j] = rec[j].z;
+            path[j][s + 1] = key;
+            cur[j] = nxt[j];
         }
     }
 }
@@ -250,7 +254,7 @@ __global__ __launch_bounds__(256) void arw_kernel(const int32_t *__restrict__ ro
 template <int MAXD, int WPL>
 __global__ __launch_bounds__(256) void arw_sum_kernel(const int2 *__restrict__ nodeinfo,
                                                       const int32_t *__restrict__ col,
-                                                      const int4 *__restrict__ succ,
+                                                      const int2 *__restrict__ succ,
                                                       int32_t n, uint64_t seed, uint32_t d,
                                                       int k_log2, uint32_t *__restrict__ S,
                                                       const int32_t *__restrict__ bad_flag) {
@@ -276,7 +280,7 @@ __global__ __launch_bounds__(256) void arw_sum_kernel(const int2 *__restrict__ n
 
 }  // namespace
 
-int launch_density(const int2 *nodeinfo, const int32_t *col, const int4 *succ, int32_t n,
+int launch_density(const int2 *nodeinfo, const int32_t *col, const int2 *succ, int32_t n,
                    uint64_t seed, uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
                    hipStream_t stream) {
     int k_log2 = -1;

@@ -115,7 +115,7 @@ int launch_arw(const int32_t *rowptr, const int32_t *col, int32_t n, uint64_t se
 // and degree of that node)) each step reads one record instead of a node's bounds and then
 // a column.  DUALGCN_ERR_UNSUPPORTED (nothing launched) unless d <= 8 and k is a power of
 // two in [2, 128].
-int launch_density(const int2 *nodeinfo, const int32_t *col, const int4 *succ, int32_t n,
+int launch_density(const int2 *nodeinfo, const int32_t *col, const int2 *succ, int32_t n,
                    uint64_t seed, uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
                    hipStream_t stream);
 

@@ -3,7 +3,7 @@
 // Pipeline (one stream, two host waits; three with the adaptive alpha):
 //   validate        rowptr / col checks, the largest degree, node records -> flag
 //   successors      (when walks outnumber entries twice) one record per entry:
-//                   the column and that node's first entry and degree
+//                   the first entry and degree of the node in that column
 //   walks           S_v (arw.hip), or S from a saved plan
 //   adaptive alpha  (optional) moments of S and D            -> extra host wait
 //   keys            K_v = p S_v + (q - p) k D_v, D_v from the row pointers, and the
@@ -99,24 +99,18 @@ __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__res
     }
 }
 
-// Successor records of the walks: succ[e] = (c, first entry of c, degree of c) for
-// c = col[e], from the node records validate_kernel wrote.  A column out of range (the
+// Successor records of the walks: succ[e] = (first entry of c, degree of c) for
+// c = col[e], the node record validate_kernel wrote.  A column out of range (the
 // validation flags it, and nothing walks then) gets a record without reading them.
 __global__ __launch_bounds__(kThreads) void successor_kernel(const int2 *__restrict__ nodeinfo,
                                                              const int32_t *__restrict__ col,
                                                              int32_t n, int64_t nnz,
-                                                             int4 *__restrict__ succ) {
+                                                             int2 *__restrict__ succ) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
     for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < nnz;
          e += stride) {
         const int32_t c = col[e];
-        int4 r = make_int4(c, 0, 0, 0);
-        if (c >= 0 && c < n) {
-            const int2 ni = nodeinfo[c];
-            r.y = ni.x;
-            r.z = ni.y;
-        }
-        succ[e] = r;
+        succ[e] = c >= 0 && c < n ? nodeinfo[c] : make_int2(0, 0);
     }
 }
 
@@ -856,7 +850,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     // build in another: two allocations per plan.  Split parts are bounded by
     // sum over rows longer than C of ceil(deg / C) < 2 nnz / C + 1.
     const size_t max_parts = unnz / kDenseChunk * 2 + 1;
-    // The lockstep walker reads successor records (16 bytes per entry, scratch) when the
+    // The lockstep walker reads successor records (8 bytes per entry, scratch) when the
     // walks take at least twice as many steps as the matrix has entries: building them
     // costs one random read per entry and saves one dependent random read per step.
     const bool use_succ = S_host == nullptr &&
@@ -881,7 +875,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_ssum = ls.take(sizeof(SplitSummary)), o_counts = ls.take(sizeof(uint32_t) * 2 * un),
                  o_tiles = ls.take(sizeof(int32_t) * (unnz / kCopyTile + 2)),
                  o_info = ls.take(sizeof(int2) * un),
-                 o_succ = ls.take(use_succ ? sizeof(int4) * unnz : 0),
+                 o_succ = ls.take(use_succ ? sizeof(int2) * unnz : 0),
                  o_bmax = ls.take(sizeof(int32_t) * kValidateBlocks);
     if ((st = alloc_block(&p->mem, &p->mem_bytes, lp.bytes))) return st;
     ScratchBlock scratch;
@@ -916,9 +910,9 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     TraceRange phase("partition: validate + walks");
     if ((st = hip_status(hipMemsetAsync(bad, 0, 2 * sizeof(int32_t), s)))) return st;
     if ((st = validate_csr(csr, bad, nodeinfo, blockmax, s))) return st;
-    int4 *succ = nullptr;
+    int2 *succ = nullptr;
     if (use_succ && nnz > 0) {
-        succ = reinterpret_cast<int4 *>(sm + o_succ);
+        succ = reinterpret_cast<int2 *>(sm + o_succ);
         const int64_t sblocks = std::min<int64_t>((nnz + kThreads - 1) / kThreads, 65536);
         hipLaunchKernelGGL(successor_kernel, dim3(static_cast<unsigned>(sblocks)), dim3(kThreads), 0,
                            s, nodeinfo, csr->col, n, nnz, succ);
