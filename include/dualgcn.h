@@ -240,7 +240,7 @@ int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F
  * written to or read from device memory.
  *
  * X is float32 n x F_in row-major (16-byte aligned), W float32 F_in x F_out row-major
- * (rounded to bfloat16 as in dualgcn_update), T float32 n x F_out row-major (4-byte
+ * (rounded to bfloat16 as in dualgcn_update), T float32 n x F_out row-major (16-byte
  * aligned), overlapping neither X nor W.  flags: DUALGCN_RELU (others are
  * DUALGCN_ERR_INVALID_ARG).  F_in and F_out must be multiples of 32, at most 256, and
  * W^T in bfloat16 plus the row tiles must fit a workgroup's LDS (F_in = F_out = 256

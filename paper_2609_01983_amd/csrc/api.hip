@@ -290,7 +290,7 @@ int dualgcn_spmm_update(const dualgcn_plan *plan, const float *X, const float *W
     if (F_in % 32 || F_out % 32 || F_in > 256 || F_out > 256 ||
         dgc::spmm_xw_lds_bytes(F_in, F_out) > 160 * 1024)
         return DUALGCN_ERR_UNSUPPORTED;
-    if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(T) % 4)
+    if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(T) % 16)
         return DUALGCN_ERR_INVALID_ARG;
     const Plan *p = as_plan(plan);
     const size_t n = static_cast<size_t>(p->n);

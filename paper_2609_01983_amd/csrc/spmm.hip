@@ -440,6 +440,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Args a) {
 // consecutive k of group l / 16; D rows 4 (l / 16) + j, j < 4, column l % 16.
 constexpr int kXwPad = 8;                     // bfloat16 padding per LDS row
 constexpr int kXwBlocksPerGroup = 8;          // logical workgroups per launched workgroup
+constexpr int kXwStageLd = 68;                // floats per staged output row (64 + padding)
+constexpr int kXwStageWords = 16 * kXwStageLd; // a wavefront's output staging
 
 template <int LPR>
 struct XwTile {
@@ -452,7 +454,7 @@ size_t xw_lds_bytes(int lpr, int K, int N) {
     const size_t rows = slots < 16 ? 16 : slots;
     const size_t ld = static_cast<size_t>(K) + kXwPad;
     return (static_cast<size_t>(N) + kWaves * rows) * ld * sizeof(unsigned short) +
-           kWaves * rows * sizeof(int32_t);
+           kWaves * rows * sizeof(int32_t) + static_cast<size_t>(kWaves) * kXwStageWords * sizeof(float);
 }
 
 template <int LPR>
@@ -468,6 +470,8 @@ __global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const f
     unsigned short *wt = xw_lds;                                   // [N][ld]: W^T in bfloat16
     unsigned short *h = xw_lds + (N + wave * ROWS) * ld;           // this wavefront's rows
     int32_t *outs = reinterpret_cast<int32_t *>(xw_lds + (N + kWaves * ROWS) * ld) + wave * ROWS;
+    float *stage = reinterpret_cast<float *>(reinterpret_cast<int32_t *>(xw_lds + (N + kWaves * ROWS) * ld) +
+                                             kWaves * ROWS) + wave * kXwStageWords;
     for (int idx = static_cast<int>(threadIdx.x); idx < K * N; idx += kThreads) {
         const int c = idx / N, j = idx % N;   // consecutive threads read consecutive columns
         wt[j * ld + c] = to_bf16(W[idx]);
@@ -477,17 +481,20 @@ __global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const f
 
     const StageRows emit{h, outs, ld, a.relu != 0, lane % LPR == 0};
     const int lrow = lane & 15, kgrp = lane >> 4;
+    const int sr = lane >> 4, sc = (lane & 15) * 4;        // first staged row and the columns a lane stores
     for (int lb = static_cast<int>(blockIdx.x); lb < nblocks; lb += static_cast<int>(gridDim.x)) {
         spmm_block<LPR, 4, kWaves>(a, lb, 0, wave, emit);
         __syncwarp();
 #pragma unroll
         for (int rt = 0; rt < ROWS / 16; ++rt) {
             if (__ballot(outs[rt * 16 + lrow] >= 0) == 0) continue;   // no row in this tile
-            int32_t o[4];
+            int32_t orow[4];                                          // rows sr + 4 q of the tile
 #pragma unroll
-            for (int j = 0; j < 4; ++j) o[j] = outs[rt * 16 + kgrp * 4 + j];
+            for (int q = 0; q < 4; ++q) orow[q] = outs[rt * 16 + sr + 4 * q];
             const unsigned short *hrow = h + (rt * 16 + lrow) * ld + kgrp * 8;
-            // one 16-column tile of T at a time (the k order of each tile is the update's)
+            // one 16-column tile of T at a time (the k order of each tile is the update's),
+            // staged in LDS and stored 64 columns at a time: each store instruction writes
+            // four whole 256-byte row pieces (16 lanes x 16 bytes each)
             for (int t = 0; t < ntiles; ++t) {
                 const unsigned short *wrow = wt + (t * 16 + lrow) * ld + kgrp * 8;
                 f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -499,9 +506,22 @@ __global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const f
                                                                   0, 0, 0);
                 }
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (o[j] >= 0)
-                        __builtin_nontemporal_store(acc[j], T + static_cast<int64_t>(o[j]) * N + t * 16 + lrow);
+                for (int j = 0; j < 4; ++j) stage[(kgrp * 4 + j) * kXwStageLd + (t & 3) * 16 + lrow] = acc[j];
+                if ((t & 3) == 3 || t == ntiles - 1) {
+                    __syncwarp();
+                    const int c0 = (t & ~3) * 16;                      // first column of this pass
+                    if (c0 + sc < N) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            if (orow[q] >= 0) {
+                                const f32x4 v = *reinterpret_cast<const f32x4 *>(stage + (sr + 4 * q) * kXwStageLd + sc);
+                                __builtin_nontemporal_store(
+                                    v, reinterpret_cast<f32x4 *>(T + static_cast<int64_t>(orow[q]) * N + c0 + sc));
+                            }
+                        }
+                    }
+                    __syncwarp();
+                }
             }
         }
         __syncwarp();
