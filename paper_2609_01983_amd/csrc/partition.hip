@@ -516,37 +516,67 @@ __global__ __launch_bounds__(kThreads) void tile_row_kernel(const int32_t *__res
 }
 
 // Fills entries [b kCopyTile, (b + 1) kCopyTile) of the sorted copy: entry e of sorted
-// row i is entry e - pptr[i] of row order[i].  The tile's rows come from tile_row and have
-// their pointers staged in LDS; thread t copies entries e0 + t + 256 k, so reads inside a
-// row and all writes are coalesced, and finds each entry's row by binary search in LDS.
+// row i is entry e - pptr[i] of row order[i], i.e. entry e + delta[i] of the matrix with
+// delta[i] = rowptr[order[i]] - pptr[i].  The tile's rows come from tile_row; each counts
+// itself at the tile position where it starts (its first entry, or the tile's start), and
+// an inclusive scan of those counts gives every entry the index of its row (rows of no
+// entries start where the next row does and count before it).  Thread t then copies entries
+// e0 + t + 256 k, so reads inside a row and all writes are coalesced.
 __global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
     const int32_t *__restrict__ order, const int32_t *__restrict__ rowptr,
     const int32_t *__restrict__ col, const float *__restrict__ val,
     const int32_t *__restrict__ pptr, const int32_t *__restrict__ tile_row, int32_t n,
     int64_t nnz, int32_t *__restrict__ pcol, float *__restrict__ pval) {
-    __shared__ int32_t sh_ptr[kCopyTile + 2];
-    __shared__ int32_t sh_src[kCopyTile + 1];
+    constexpr int kPer = kCopyTile / kThreads;          // counters one thread scans
+    __shared__ int32_t sh_delta[kCopyTile + 1];
+    __shared__ __align__(16) uint32_t sh_cnt[kCopyTile];
+    __shared__ uint32_t sh_waves[kThreads / 64];
+    const int t = static_cast<int>(threadIdx.x);
     const int64_t e0 = static_cast<int64_t>(blockIdx.x) * kCopyTile;
     const int64_t e1 = e0 + kCopyTile < nnz ? e0 + kCopyTile : nnz;
     const int32_t r_lo = tile_row[blockIdx.x];
     const int32_t r_hi = e1 < nnz ? tile_row[blockIdx.x + 1] : n - 1;   // holds e1 or the end
     const int32_t rows = r_hi - r_lo + 1;
     if (rows <= kCopyTile + 1) {
-        for (int32_t k = threadIdx.x; k < rows; k += kThreads) {
-            sh_ptr[k] = pptr[r_lo + k];
-            sh_src[k] = rowptr[order[r_lo + k]];
-        }
-        if (threadIdx.x == 0) sh_ptr[rows] = pptr[r_lo + rows];
+        for (int k = t; k < kCopyTile; k += kThreads) sh_cnt[k] = 0;
         __syncthreads();
-        for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) {
-            const int32_t k = row_of(sh_ptr, 0, rows - 1, e);
-            const int64_t src = sh_src[k] + (e - sh_ptr[k]);
+        for (int32_t k = t; k < rows; k += kThreads) {
+            const int32_t b = pptr[r_lo + k];
+            sh_delta[k] = rowptr[order[r_lo + k]] - b;
+            const int64_t pos = b > e0 ? b - e0 : 0;
+            if (pos < e1 - e0) atomicAdd(&sh_cnt[pos], 1u);
+        }
+        __syncthreads();
+        uint32_t c[kPer];
+        uint32_t sum = 0;
+#pragma unroll
+        for (int q = 0; q < kPer / 4; ++q) {
+            const uint4 v = reinterpret_cast<const uint4 *>(sh_cnt + t * kPer)[q];
+            c[4 * q] = v.x;
+            c[4 * q + 1] = v.y;
+            c[4 * q + 2] = v.z;
+            c[4 * q + 3] = v.w;
+        }
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            sum += c[q];
+            c[q] = sum;
+        }
+        uint32_t total;
+        const uint32_t base = block_exclusive_scan(sum, &total, sh_waves);
+#pragma unroll
+        for (int q = 0; q < kPer / 4; ++q)
+            reinterpret_cast<uint4 *>(sh_cnt + t * kPer)[q] =
+                make_uint4(base + c[4 * q], base + c[4 * q + 1], base + c[4 * q + 2], base + c[4 * q + 3]);
+        __syncthreads();
+        for (int64_t e = e0 + t; e < e1; e += kThreads) {
+            const int64_t src = e + sh_delta[sh_cnt[e - e0] - 1];
             pcol[e] = col[src];
             pval[e] = val[src];
         }
     } else {
         // more rows than entries (empty rows): search the row pointers in memory
-        for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) {
+        for (int64_t e = e0 + t; e < e1; e += kThreads) {
             const int32_t r = row_of(pptr, r_lo, r_hi, e);
             const int64_t src = rowptr[order[r]] + (e - pptr[r]);
             pcol[e] = col[src];
@@ -555,6 +585,8 @@ __global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
     }
 }
 
+constexpr int32_t kTaskProbe = 64;
+
 // Does row i of the sorted order start a sparse-region task?  A task is a run of at most
 // kTaskRows consecutive rows whose first entries lie in one window of kTaskEntries entries;
 // an empty row forms a task of its own.
@@ -562,7 +594,13 @@ __device__ __forceinline__ bool starts_task(const int32_t *__restrict__ pptr, in
     const int32_t b = pptr[i];
     if (i == 0 || pptr[i + 1] == b || pptr[i - 1] == b) return true;
     const int32_t w0 = (b / kTaskEntries) * kTaskEntries;
-    int32_t lo = 0, hi = i;        // first row whose first entry is >= w0
+    // first row whose first entry is >= w0: it lies within the last kTaskProbe rows unless
+    // the window holds that many empty rows, so probe there before searching all of [0, i]
+    int32_t lo = 0, hi = i;
+    if (i >= kTaskProbe) {
+        if (pptr[i - kTaskProbe] < w0) lo = i - kTaskProbe + 1;
+        else hi = i - kTaskProbe;
+    }
     while (lo < hi) {
         const int32_t mid = lo + (hi - lo) / 2;
         if (pptr[mid] < w0) lo = mid + 1;
