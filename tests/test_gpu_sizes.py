@@ -5,7 +5,9 @@
   and the whole order), and the SpMM on sampled rows (random rows, the heaviest
   rows and the rows around the region boundary) within 1e-5 sum |a||x|;
 * c5 two-layer GCN forward (256 -> 128 -> 64, bf16 matrix cores): layer 1 on sampled
-  rows and the end-to-end output on a few rows, within the bf16 bound.
+  rows and the end-to-end output on a few rows, within the bf16 bound;
+* c5 fused layer junction (the benchmark's layer-1 kernel): bit-identical to the two-call
+  route on every row, and within the bf16 bound of the oracle on sampled rows.
 """
 import time
 
@@ -82,4 +84,39 @@ def test_c5_gcn_forward_sampled(dg, device):
     Yr, bound = oracle.gcn_forward_rows(g, X, [W1, W2], rows2)
     assert_spmm_close(Y2s, Yr, bound, tol=GCN_TOL, what="c5 two layers")
     _log(f"c5: two-layer output ok on {rows2.size} rows (oracle {time.time() - t0:.1f}s)")
+    plan.destroy()
+
+
+def test_c5_fused_junction_sampled(dg, device):
+    """The bench's fused layer junction at full size: T2 = bf16(relu(A T1)) bf16(W2) bit for bit
+    against the two-call route on every row, and against the oracle's float64 layer 1 on
+    sampled rows: |T2 - H W2| <= 2e-2 ((|H| + B_H) |W2|), which covers layer 1's bf16 bound
+    (1e-2 B_H), the bf16 rounding of H and W2 and the float32 accumulation."""
+    w = configs.WORKLOADS["c5"]
+    g = configs.load_graph("c5")
+    X = configs.load_features("c5")
+    W1, W2 = configs.load_weights("c5")
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    W2d = torch.from_numpy(W2).to(device)
+    Xd = torch.from_numpy(X).to(device)
+    T1 = dg.update(Xd, torch.from_numpy(W1).to(device))
+    del Xd
+    T2 = dg.spmm_update(plan, T1, W2d, relu=True)
+    T2_two = dg.update(dg.spmm(plan, T1, relu=True, out_bf16=True), W2d)
+    assert torch.equal(T2, T2_two), "fused and two-call results differ at full size"
+    _log("c5: fused junction bit-identical to the two calls on every row")
+    del T2_two, T1
+    perm = plan.export()[0]
+    gen = np.random.default_rng(17)
+    rows = np.unique(np.concatenate([gen.choice(g.n, 1000, replace=False), perm[-6:]])).astype(np.int32)
+    T2s = T2[torch.from_numpy(rows).long().to(device)].cpu().numpy().astype(np.float64)
+    t0 = time.time()
+    H, BH = oracle.gcn_layer(g, X, W1, relu=True, rows=rows)
+    W2a = np.abs(W2.astype(np.float64))
+    ref = H @ W2.astype(np.float64)
+    bound = (np.abs(H) + BH) @ W2a
+    err = np.abs(T2s - ref)
+    bad = ~(err <= 2e-2 * bound)
+    assert not bad.any(), f"{bad.sum()} outside; worst ratio {np.max(err / np.maximum(bound, 1e-300))}"
+    _log(f"c5: fused junction ok on {rows.size} rows (oracle {time.time() - t0:.1f}s)")
     plan.destroy()
