@@ -286,10 +286,16 @@ def train(args, w, g, dg, torch, np, rowptr, col, val, Xd, Wd, stream, ev):
 
         inp = [Xd] + H[:-1]
         for li in range(L):
-            mark("forward_update", lambda: dg.update(inp[li], Ws[li], T[li]))
             fplan = plan_out if (li == L - 1 and plan_out is not None) else plan
-            mark("forward_spmm", lambda: dg.spmm(fplan, T[li], H[li], relu=li < L - 1,
-                                                 out_bf16=li < L - 1))
+            if li == 0 or args.unfused:
+                mark("forward_update", lambda: dg.update(inp[li], Ws[li], T[li]))
+            if li < L - 1 and not args.unfused:
+                # aggregation fused with the next layer's update; H[li] is kept for the backward
+                mark("forward_spmm", lambda: dg.spmm_update(fplan, T[li], Ws[li + 1], T[li + 1],
+                                                            relu=True, H=H[li]))
+            else:
+                mark("forward_spmm", lambda: dg.spmm(fplan, T[li], H[li], relu=li < L - 1,
+                                                     out_bf16=li < L - 1))
         mark("loss", lambda: dg.softmax_xent(H[-1], labels, scale, G, loss))
         grad = G
         for li in range(L - 1, -1, -1):
@@ -331,6 +337,7 @@ def train(args, w, g, dg, torch, np, rowptr, col, val, Xd, Wd, stream, ev):
                                         if plan_lab is not None else "full plan"),
                       "last_forward": ("row-restricted plan of the labeled rows, nnz %d" % nnz_out
                                        if plan_out is not None else "full plan"),
+                      "fused_update": not args.unfused,
                       "note": "partition built once before the timed steps (amortised over epochs)"}),
           flush=True)
     plan.destroy()

@@ -5,7 +5,8 @@
  * product Y = A X of the DualGCN paper (Sec. 1 and Sec. 2.1), scheduled by the
  * paper's dual-metric partition (Sec. 3.2) and run by two kernels, one for the
  * sparse region and one for the dense region of the partition (Sec. 3.3), and
- * the update phase X W of a layer (Sec. 1); for training, the loss gradient and
+ * the update phase X W of a layer (Sec. 1), also fused with the aggregation of the
+ * layer before it; for training, the loss gradient and
  * the backward products of a layer; the values of other aggregators on the same
  * structure; and plans saved and loaded across runs.
  *
@@ -236,19 +237,21 @@ int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F
  * The same result as dualgcn_spmm_act with DUALGCN_OUT_BF16 into a buffer H followed
  * by dualgcn_update of H with DUALGCN_IN_BF16 -- bit for bit: every row of act(A X) is
  * summed as in dualgcn_spmm, rounded to bfloat16 (nearest-even), and multiplied on the
- * matrix cores in the update's order --, without H: the n x F_in intermediate is never
- * written to or read from device memory.
+ * matrix cores in the update's order --, without reading H back: with H = NULL the
+ * n x F_in intermediate never goes through device memory at all.
  *
  * X is float32 n x F_in row-major (16-byte aligned), W float32 F_in x F_out row-major
  * (rounded to bfloat16 as in dualgcn_update), T float32 n x F_out row-major (16-byte
- * aligned), overlapping neither X nor W.  flags: DUALGCN_RELU (others are
- * DUALGCN_ERR_INVALID_ARG).  F_in and F_out must be multiples of 32, at most 256, and
+ * aligned), overlapping neither X nor W.  H is NULL, or bfloat16 n x F_in row-major
+ * (8-byte aligned, overlapping none of X, W and T) that also receives bf16(act(A X)),
+ * the output dualgcn_spmm_act would write with DUALGCN_OUT_BF16 (training keeps it for
+ * the backward pass).  flags: DUALGCN_RELU (others are DUALGCN_ERR_INVALID_ARG).  F_in and F_out must be multiples of 32, at most 256, and
  * W^T in bfloat16 plus the row tiles must fit a workgroup's LDS (F_in = F_out = 256
  * does not; everything with F_in <= 128 does), else DUALGCN_ERR_UNSUPPORTED.
  * Asynchronous.
  */
 int dualgcn_spmm_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
-                        int32_t F_in, int32_t F_out, uint32_t flags, void *stream);
+                        void *H, int32_t F_in, int32_t F_out, uint32_t flags, void *stream);
 
 /* Bytes of device workspace dualgcn_gcn_layer needs (host-only, no device use):
  * room for the float32 n x F_out product T. */

@@ -75,7 +75,7 @@ def _load():
         "dualgcn_plan_destroy": ([P], None),
         "dualgcn_spmm": ([P, P, P, I32, P], ctypes.c_int),
         "dualgcn_spmm_act": ([P, P, P, I32, U32, P], ctypes.c_int),
-        "dualgcn_spmm_update": ([P, P, P, P, I32, I32, U32, P], ctypes.c_int),
+        "dualgcn_spmm_update": ([P, P, P, P, P, I32, I32, U32, P], ctypes.c_int),
         "dualgcn_update": ([P, P, P, I32, I32, I32, U32, P], ctypes.c_int),
         "dualgcn_gcn_layer_workspace": ([P, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "dualgcn_gcn_layer": ([P, P, P, P, I32, I32, U32, P, SZ, P], ctypes.c_int),
@@ -259,10 +259,11 @@ def update(X, W, T=None, stream=None):
     return T
 
 
-def spmm_update(plan, X, W, T=None, relu=False, stream=None):
-    """T = bf16(act(A X)) bf16(W) (float32 accumulation) without storing act(A X): the
-    aggregation of one layer fused with the next layer's update.  X: float32 [n, F_in],
-    W: float32 [F_in, F_out], T: float32 [n, F_out]."""
+def spmm_update(plan, X, W, T=None, relu=False, H=None, stream=None):
+    """T = bf16(act(A X)) bf16(W) (float32 accumulation): the aggregation of one layer fused
+    with the next layer's update.  X: float32 [n, F_in], W: float32 [F_in, F_out],
+    T: float32 [n, F_out].  H: None (act(A X) is not stored), or a bfloat16 [n, F_in]
+    tensor that receives bf16(act(A X))."""
     _dev(X, torch.float32, "X")
     _dev(W, torch.float32, "W")
     if X.dim() != 2 or X.shape[0] != plan.n:
@@ -275,8 +276,14 @@ def spmm_update(plan, X, W, T=None, relu=False, stream=None):
     _dev(T, torch.float32, "T")
     if T.shape != (plan.n, F_out):
         raise ValueError("T must be [n, F_out]")
-    _check(_lib.dualgcn_spmm_update(plan.handle, X.data_ptr(), W.data_ptr(), T.data_ptr(), F_in,
-                                    F_out, RELU if relu else 0, _stream(stream)),
+    hp = None
+    if H is not None:
+        _dev(H, torch.bfloat16, "H")
+        if H.shape != (plan.n, F_in):
+            raise ValueError("H must be [n, F_in]")
+        hp = H.data_ptr()
+    _check(_lib.dualgcn_spmm_update(plan.handle, X.data_ptr(), W.data_ptr(), T.data_ptr(), hp,
+                                    F_in, F_out, RELU if relu else 0, _stream(stream)),
            "dualgcn_spmm_update")
     return T
 

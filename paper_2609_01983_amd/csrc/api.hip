@@ -281,7 +281,7 @@ int dualgcn_spmm_act(const dualgcn_plan *plan, const float *X, void *Y, int32_t 
 }
 
 int dualgcn_spmm_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
-                        int32_t F_in, int32_t F_out, uint32_t flags, void *stream) {
+                        void *H, int32_t F_in, int32_t F_out, uint32_t flags, void *stream) {
     dgc::TraceRange trace("dualgcn_spmm_update");
     int st = check_plan(plan);
     if (st) return st;
@@ -295,11 +295,17 @@ int dualgcn_spmm_update(const dualgcn_plan *plan, const float *X, const float *W
     const Plan *p = as_plan(plan);
     const size_t n = static_cast<size_t>(p->n);
     const size_t tbytes = n * F_out * sizeof(float);
-    if (overlaps(X, n * F_in * sizeof(float), T, tbytes) ||
-        overlaps(W, static_cast<size_t>(F_in) * F_out * sizeof(float), T, tbytes))
+    const size_t xbytes = n * F_in * sizeof(float), wbytes = static_cast<size_t>(F_in) * F_out * sizeof(float);
+    if (overlaps(X, xbytes, T, tbytes) || overlaps(W, wbytes, T, tbytes))
         return DUALGCN_ERR_INVALID_ARG;
+    if (H) {
+        const size_t hbytes = n * F_in * sizeof(uint16_t);
+        if (reinterpret_cast<uintptr_t>(H) % 8 || overlaps(H, hbytes, X, xbytes) ||
+            overlaps(H, hbytes, W, wbytes) || overlaps(H, hbytes, T, tbytes))
+            return DUALGCN_ERR_INVALID_ARG;
+    }
     if ((st = dgc::device_status())) return st;
-    return dgc::launch_spmm_xw(*p, X, W, T, F_in, F_out, (flags & DUALGCN_RELU) != 0,
+    return dgc::launch_spmm_xw(*p, X, W, T, H, F_in, F_out, (flags & DUALGCN_RELU) != 0,
                                static_cast<hipStream_t>(stream));
 }
 

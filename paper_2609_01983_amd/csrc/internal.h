@@ -151,10 +151,11 @@ int wait_stream(hipStream_t stream);
 
 int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool out_bf16,
                 hipStream_t stream);
-// T = bf16(act(A X)) bf16(W) (float32 accumulation) without storing act(A X):
-// 32 <= F_in <= 256 and 32 <= F_out <= 256 multiples of 32, X 16-byte aligned.
-int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, int32_t F_in,
-                   int32_t F_out, bool relu, hipStream_t stream);
+// T = bf16(act(A X)) bf16(W) (float32 accumulation), act(A X) stored as bfloat16 to H
+// only if H is not null: 32 <= F_in <= 256 and 32 <= F_out <= 256 multiples of 32,
+// X and T 16-byte aligned, H 8-byte aligned.
+int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, void *H,
+                   int32_t F_in, int32_t F_out, bool relu, hipStream_t stream);
 // LDS bytes a workgroup of launch_spmm_xw takes (at most 160 KiB are supported).
 size_t spmm_xw_lds_bytes(int32_t F_in, int32_t F_out);
 

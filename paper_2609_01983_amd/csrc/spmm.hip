@@ -1,4 +1,5 @@
-// Dual-path aggregation SpMM Y = A X on gfx950 (DualGCN Sec. 3.3).
+// Dual-path aggregation SpMM Y = A X on gfx950 (DualGCN Sec. 3.3), and the same
+// aggregation fused with the next layer's update, T = bf16(act(A X)) W (further below).
 //
 // The kernels stream the plan's sorted copy of the matrix: row i of the copy is
 // row order[i] of A, the sparse region is rows [0, n_sparse) and the dense region
@@ -154,13 +155,17 @@ struct StoreRows {
 
 // StageRows keeps the row for the fused update instead: act(row) rounded to bfloat16
 // in the wavefront's LDS tile (row `slot`, ld elements apart), its output row in
-// outs[slot].  VEC = 4; the window starts at feature 0.
+// outs[slot]; when H is set, the same bfloat16 row is also stored to H (row `out`,
+// ldH elements apart), as the plain kernel stores a bfloat16 Y.  VEC = 4; the window
+// starts at feature 0.
 struct StageRows {
     unsigned short *h;
     int32_t *outs;
     int32_t ld;
     bool relu;
     bool lead;          // the group's first lane records the output row
+    unsigned short *H;
+    int32_t ldH;
     __device__ __forceinline__ void row(int64_t out, int slot, const double (&tot)[4], int f,
                                         bool fin) const {
         if (fin) {
@@ -170,9 +175,15 @@ struct StageRows {
                 o[j] = static_cast<float>(tot[j]);
                 if (relu) o[j] = o[j] > 0.f ? o[j] : 0.f;
             }
-            *reinterpret_cast<uint2 *>(h + static_cast<int64_t>(slot) * ld + f) =
+            const uint2 pk =
                 make_uint2(static_cast<uint32_t>(to_bf16(o[0])) | (static_cast<uint32_t>(to_bf16(o[1])) << 16),
                            static_cast<uint32_t>(to_bf16(o[2])) | (static_cast<uint32_t>(to_bf16(o[3])) << 16));
+            *reinterpret_cast<uint2 *>(h + static_cast<int64_t>(slot) * ld + f) = pk;
+            if (H) {
+                uint32_t *g = reinterpret_cast<uint32_t *>(H + out * ldH + f);
+                __builtin_nontemporal_store(pk.x, g);
+                __builtin_nontemporal_store(pk.y, g + 1);
+            }
         }
         if (lead) outs[slot] = static_cast<int32_t>(out);
     }
@@ -427,7 +438,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Args a) {
 // T = bf16(act(A X)) bf16(W), float32 accumulation: the product of a GCN layer's
 // aggregated output with the next layer's weights without storing the aggregated
 // features.  The aggregation is the plain kernel's (same schedule, same sums); a
-// finished row is rounded to bfloat16 into its wavefront's LDS tile instead of Y.
+// finished row is rounded to bfloat16 into its wavefront's LDS tile (and, if asked,
+// also stored to H as the plain kernel's bfloat16 output) instead of Y.
 // Every workgroup stages W^T in bfloat16 once and then takes logical workgroups
 // blockIdx.x, blockIdx.x + gridDim.x, ... of the plain kernel's schedule (heaviest
 // first as before); after each one, the wavefront multiplies its tile by W^T on the
@@ -479,7 +491,7 @@ __global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const f
     if (lane < ROWS) outs[lane] = -1;
     __syncthreads();
 
-    const StageRows emit{h, outs, ld, a.relu != 0, lane % LPR == 0};
+    const StageRows emit{h, outs, ld, a.relu != 0, lane % LPR == 0, static_cast<unsigned short *>(a.Y), a.ld};
     const int lrow = lane & 15, kgrp = lane >> 4;
     const int sr = lane >> 4, sc = (lane & 15) * 4;        // first staged row and the columns a lane stores
     for (int lb = static_cast<int>(blockIdx.x); lb < nblocks; lb += static_cast<int>(gridDim.x)) {
@@ -547,6 +559,7 @@ __global__ __launch_bounds__(kThreads) void combine_xw_kernel(const Args a, cons
         float o = static_cast<float>(sum);
         if (a.relu) o = o > 0.f ? o : 0.f;
         hrow[t] = to_bf16(o);
+        if (a.Y) static_cast<unsigned short *>(a.Y)[static_cast<int64_t>(a.perm[sp.row]) * K + t] = hrow[t];
     }
     __syncthreads();
     if (t >= 64) return;
@@ -680,9 +693,9 @@ size_t spmm_xw_lds_bytes(int32_t F_in, int32_t F_out) {
     return xw_lds_bytes(window_lpr(F_in), F_in, F_out);
 }
 
-int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, int32_t F_in,
-                   int32_t F_out, bool relu, hipStream_t s) {
-    Args a = plan_args(p, X, nullptr, F_in, relu);
+int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, void *H,
+                   int32_t F_in, int32_t F_out, bool relu, hipStream_t s) {
+    Args a = plan_args(p, X, H, F_in, relu);
     a.f0 = 0;
     a.fend = F_in;
     a.S = 1;

@@ -74,7 +74,7 @@ def test_other_entry_points_reject_null(dg):
     assert L.dualgcn_update(16, 32, 1 << 20, 8, 48, 32, 0, None) == dg.ERR_UNSUPPORTED
     assert L.dualgcn_update(16, 32, 1 << 20, 8, 32, 32, 8, None) == dg.ERR_INVALID_ARG   # bad flag
     assert L.dualgcn_spmm_act(None, 16, 32, 8, 8, None) == dg.ERR_INVALID_ARG
-    assert L.dualgcn_spmm_update(None, 16, 32, 48, 128, 64, dg.RELU, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_spmm_update(None, 16, 32, 48, None, 128, 64, dg.RELU, None) == dg.ERR_INVALID_ARG
     nbytes = ctypes.c_size_t()
     assert L.dualgcn_gcn_layer_workspace(None, 32, 32, ctypes.byref(nbytes)) == dg.ERR_INVALID_ARG
     assert L.dualgcn_gcn_layer(None, 1, 2, 3, 32, 32, 0, 256, 1 << 20, None) == dg.ERR_INVALID_ARG

@@ -76,6 +76,11 @@ def test_fused_equals_two_calls_and_oracle(dg, device, name, F_in, F_out, relu):
     got = T.cpu().numpy()
     assert np.array_equal(got.view(np.uint32), T2.cpu().numpy().view(np.uint32)), \
         f"{name} {F_in}->{F_out}: fused and two-call results differ"
+    # with H kept: the same T, and H is the plain kernel's bfloat16 output bit for bit
+    Hk = torch.full((g.n, F_in), float("nan"), dtype=torch.bfloat16, device=device)
+    Tk = dg.spmm_update(plan, Xd, Wd, relu=relu, H=Hk)
+    assert torch.equal(Tk, T)
+    assert torch.equal(Hk.view(torch.int16), dg.spmm(plan, Xd, relu=relu, out_bf16=True).view(torch.int16))
     # the oracle (rows sampled on the larger graphs)
     rows = np.arange(g.n, dtype=np.int32)
     if g.n > 4096:
@@ -123,20 +128,42 @@ def test_fused_argument_checks(dg, device):
     T = torch.zeros((g.n, 256), dtype=torch.float32, device=device)
     h = plan.handle
     call = L.dualgcn_spmm_update
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), 128, 64, dg.RELU, None) == 0
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), 128, 64, 2, None) == dg.ERR_INVALID_ARG
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), 48, 64, 0, None) == dg.ERR_UNSUPPORTED
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), 128, 48, 0, None) == dg.ERR_UNSUPPORTED
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), 288, 64, 0, None) == dg.ERR_UNSUPPORTED
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), 256, 256, 0, None) == dg.ERR_UNSUPPORTED
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), 256, 224, 0, None) == dg.ERR_UNSUPPORTED
-    assert call(h, X.data_ptr() + 4, W.data_ptr(), T.data_ptr(), 128, 64, 0, None) == dg.ERR_INVALID_ARG
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr() + 4, 128, 64, 0, None) == dg.ERR_INVALID_ARG
-    assert call(h, X.data_ptr(), W.data_ptr(), X.data_ptr(), 128, 64, 0, None) == dg.ERR_INVALID_ARG
-    assert call(h, X.data_ptr(), W.data_ptr(), W.data_ptr(), 128, 64, 0, None) == dg.ERR_INVALID_ARG
-    assert call(h, None, W.data_ptr(), T.data_ptr(), 128, 64, 0, None) == dg.ERR_INVALID_ARG
-    assert call(None, X.data_ptr(), W.data_ptr(), T.data_ptr(), 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 128, 64, dg.RELU, None) == 0
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 128, 64, 2, None) == dg.ERR_INVALID_ARG
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 48, 64, 0, None) == dg.ERR_UNSUPPORTED
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 128, 48, 0, None) == dg.ERR_UNSUPPORTED
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 288, 64, 0, None) == dg.ERR_UNSUPPORTED
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 256, 256, 0, None) == dg.ERR_UNSUPPORTED
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 256, 224, 0, None) == dg.ERR_UNSUPPORTED
+    assert call(h, X.data_ptr() + 4, W.data_ptr(), T.data_ptr(), None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr() + 4, None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    assert call(h, X.data_ptr(), W.data_ptr(), X.data_ptr(), None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    assert call(h, X.data_ptr(), W.data_ptr(), W.data_ptr(), None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    assert call(h, None, W.data_ptr(), T.data_ptr(), None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    assert call(None, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    H = torch.zeros((g.n, 128), dtype=torch.bfloat16, device=device)
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), H.data_ptr(), 128, 64, 0, None) == 0
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), H.data_ptr() + 2, 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), T.data_ptr(), 128, 64, 0, None) == dg.ERR_INVALID_ARG
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), X.data_ptr(), 128, 64, 0, None) == dg.ERR_INVALID_ARG
     torch.cuda.synchronize()
     with pytest.raises(ValueError):
         dg.spmm_update(plan, X, W[:128])
+    plan.destroy()
+
+
+@pytest.mark.parametrize("force", [1, 2])          # every row sparse / every row dense
+@pytest.mark.parametrize("name", ["gnp257", "hub_star", "c1"])
+def test_fused_with_forced_paths(dg, device, name, force):
+    g = _graph(name)
+    plan = dg.Plan(*to_dev(g, device), seed=3, walks_per_node=8, walk_len=4, force_mode=force)
+    X = dense.features_normal(g.n, 64, seed=9, stream_id=43)
+    W = _weights(64, 96, seed=4)
+    Xd, Wd = torch.from_numpy(X).to(device), torch.from_numpy(W).to(device)
+    side = torch.cuda.Stream(device=device)
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        T = dg.spmm_update(plan, Xd, Wd, relu=True)
+    torch.cuda.current_stream().wait_stream(side)
+    assert torch.equal(T, _two_calls(dg, plan, Xd, Wd, True))
     plan.destroy()
