@@ -123,7 +123,7 @@ struct Args {
     const SplitPart *parts;
     double *partials;
     const float *X;
-    void *Y;                    // float32, or bfloat16 when the kernel's BF is set
+    void *Y;                    // float32, or bfloat16 when the kernel's BF is set (fused: H or null)
     int32_t n, n_sparse, n_tasks, n_parts, n_long;
     int32_t ld;                 // leading dimension of X and Y (= F)
     int32_t f0;                 // first feature of this launch window
