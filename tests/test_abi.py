@@ -165,3 +165,24 @@ def test_binding_rejects_host_tensors(dg):
     r = torch.zeros(5, dtype=torch.int32)
     with pytest.raises(TypeError):
         dg.Plan(r, torch.zeros(0, dtype=torch.int32), torch.zeros(0))
+
+
+def test_plain_c_client(dg, tmp_path):
+    """The header compiles as strict C99 and a C program linked with the library runs."""
+    import os
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    libdir = os.path.join(root, "paper_2609_01983_amd")
+    exe = str(tmp_path / "abi_client")
+    subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror",
+                    "-I", os.path.join(root, "include"),
+                    os.path.join(root, "tests", "c_client", "abi_client.c"),
+                    "-L", libdir, "-ldualgcn", "-Wl,-rpath," + libdir, "-o", exe],
+                   check=True, capture_output=True, text=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, f"check {r.returncode} failed: {r.stdout} {r.stderr}"
+    assert "c client: ok" in r.stdout

@@ -39,6 +39,7 @@ GRAPHS = {
     "rows_dup_empty": TINY["rows_dup_empty"],
     "hub_star": TINY["hub_star"],
     "edgeless7": TINY["edgeless7"],
+    "single": TINY["single"],
     "c1": lambda: configs.load_graph("c1"),
     "c2": lambda: configs.load_graph("c2"),
 }
