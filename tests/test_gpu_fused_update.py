@@ -168,3 +168,17 @@ def test_fused_with_forced_paths(dg, device, name, force):
     torch.cuda.current_stream().wait_stream(side)
     assert torch.equal(T, _two_calls(dg, plan, Xd, Wd, True))
     plan.destroy()
+
+
+@pytest.mark.parametrize("name", ["gnp257", "hub_star", "c2"])
+def test_fused_with_identity_weights_is_the_bf16_spmm(dg, device, name):
+    """W = I: every output is one bf16 value times 1 plus exact zeros, so T holds exactly the
+    bfloat16 aggregation the plain kernel writes (as float32)."""
+    g = _graph(name)
+    plan = dg.Plan(*to_dev(g, device), seed=5, walks_per_node=8, walk_len=4)
+    Xd = torch.from_numpy(dense.features_normal(g.n, 128, seed=2, stream_id=44)).to(device)
+    I = torch.eye(128, dtype=torch.float32, device=device)
+    T = dg.spmm_update(plan, Xd, I, relu=True)
+    H = dg.spmm(plan, Xd, relu=True, out_bf16=True)
+    assert torch.equal(T, H.float())
+    plan.destroy()
