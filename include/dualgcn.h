@@ -16,7 +16,8 @@
  *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
  *     Work is enqueued on that stream.  Only dualgcn_partition,
  *     dualgcn_plan_load, dualgcn_plan_export, dualgcn_plan_save,
- *     dualgcn_aggregator_values and dualgcn_arw_patterns wait for the device.
+ *     dualgcn_aggregator_values and dualgcn_arw_patterns wait for the device
+ *     (dualgcn_partition and dualgcn_plan_load for all but their last kernel).
  *   - Every function returns a dualgcn_status (0 = success).  Arguments are
  *     checked before the device is touched.  Outputs are undefined after an
  *     error.  No C++ exception crosses this interface.
@@ -141,8 +142,12 @@ typedef struct dualgcn_plan dualgcn_plan;
  * sparse and the dense region; inside a region rows go by row-length octave,
  * then node id (balanced work, and the locality of the node numbering).  The
  * call waits for `stream` twice (to read the moment sums and the schedule sizes),
- * and once more with the adaptive weight (to read the moments of S and D).
- * *out is set to NULL on error.
+ * and once more with the adaptive weight (to read the moments of S and D).  It
+ * returns while the last kernel, which writes the sorted copy of the matrix from
+ * the CSR arrays, may still run on `stream`: every call that uses the plan orders
+ * its work after it, on any stream, and dualgcn_plan_destroy waits for it.  The
+ * CSR arrays must stay unchanged until then (they are borrowed for the plan's
+ * lifetime in any case).  *out is set to NULL on error.
  */
 int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,
                       uint32_t walk_len, const dualgcn_thresholds *th, void *stream,

@@ -86,6 +86,8 @@ struct Plan {
     int32_t n_split_parts = 0;
     SplitPart *parts = nullptr;        // [n_split_parts]
     double *partials = nullptr;        // [n_split_parts][kMaxSlice]
+    int32_t *tile_row = nullptr;       // [nnz / 4096 + 2] rows of the sorted copy's tiles
+    hipEvent_t ready = nullptr;        // recorded after the sorted copy was written
 
     uint64_t kstar = 0, kmax = 0;
     u128 s1 = 0, s2 = 0;
@@ -146,8 +148,10 @@ __device__ __forceinline__ unsigned short to_bf16(float f) {
 
 // ---- SpMM (spmm.hip): Y = A X on one plan, optional ReLU on the result; with out_bf16
 // Y holds the bfloat16 rounding (nearest-even) of the float32 results.
-// Host wait for the work queued on a stream, polling instead of blocking (partition.hip).
+// Host waits that poll instead of blocking (partition.hip): for the work queued on a
+// stream so far, or for an event.
 int wait_stream(hipStream_t stream);
+int wait_event(hipEvent_t event);
 
 int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool out_bf16,
                 hipStream_t stream);

@@ -12,12 +12,15 @@
 //   host            K* = least integer >= mu_K + beta sigma_K (exact integers)
 //   radix sort      stable LSD sort of (K_v, v) on 8-bit digits      -> perm
 //   split           n_sparse = lower_bound(sorted K, K*)
-//   sorted copy     the rows of the matrix in processing order (region, row-length
-//                   octave, node id; row pointers by a scan), so that both regions
-//                   are contiguous streams (Sec. 3.2: the sorted nodes are cut into
-//                   contiguous blocks)
+//   row pointers    of the rows in processing order (region, row-length octave,
+//                   node id), by a scan
 //   schedule        sparse tasks (runs of at most kTaskRows short rows) and the
-//                   parts of dense rows longer than one dense chunk   -> host wait 2
+//                   parts of dense rows longer than one dense chunk
+//   sorted copy     the rows of the matrix in processing order, so that both regions
+//                   are contiguous streams (Sec. 3.2: the sorted nodes are cut into
+//                   contiguous blocks); host wait 2 reads the schedule sizes while it
+//                   runs, and the call returns with it queued (plan users wait for
+//                   the plan's ready event)
 //
 // Everything is integer arithmetic, so the plan does not depend on launch order
 // or reduction order: it is the unique sort of (K_v, v) cut at K*.
@@ -683,10 +686,13 @@ struct ScratchBlock {
     void *p = nullptr;
     size_t bytes = 0;
     hipStream_t stream = nullptr;
+    hipEvent_t done = nullptr;     // recorded after its last use, when that is known
     ~ScratchBlock() {
-        if (!p) return;
-        (void)wait_stream(stream);
-        release_block(p, bytes);
+        if (p) {
+            (void)(done ? wait_event(done) : wait_stream(stream));
+            release_block(p, bytes);
+        }
+        if (done) (void)hipEventDestroy(done);
     }
 };
 
@@ -695,25 +701,46 @@ struct ScratchBlock {
 // Waits until the work queued on s so far has finished by polling an event: a wait
 // that blocks in the runtime resumes 50-150 us after the last kernel, which the
 // partition's host waits would otherwise add to every build (the GPU idles meanwhile).
+int wait_event(hipEvent_t e) {
+    for (;;) {
+        const hipError_t q = hipEventQuery(e);
+        if (q == hipSuccess) return DUALGCN_OK;
+        if (q != hipErrorNotReady) return hip_status(q);
+        std::this_thread::yield();
+    }
+}
+
 int wait_stream(hipStream_t s) {
     hipEvent_t e = nullptr;
     int st = hip_status(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     if (st) return st;
     st = hip_status(hipEventRecord(e, s));
-    while (!st) {
-        const hipError_t q = hipEventQuery(e);
-        if (q == hipSuccess) break;
-        if (q != hipErrorNotReady) {
-            st = hip_status(q);
-            break;
-        }
-        std::this_thread::yield();
-    }
+    if (!st) st = wait_event(e);
     (void)hipEventDestroy(e);
     return st;
 }
 
 namespace {
+
+// A small pinned host buffer per host thread for the partition's read-backs: the copies
+// into it are asynchronous, so the host waits only by polling (wait_stream, wait_event).
+// It lives until the process ends (one buffer per thread that builds plans).
+constexpr size_t kReadbackBytes = 256;
+void *readback_buffer() {
+    thread_local void *buf = nullptr;
+    if (!buf && hipHostMalloc(&buf, kReadbackBytes, hipHostMallocPortable) != hipSuccess) buf = nullptr;
+    return buf;
+}
+
+// Copies `bytes` of device memory to *dst through the pinned buffer and waits for them.
+int read_back(void *dst, const void *src, size_t bytes, hipStream_t s) {
+    void *pin = readback_buffer();
+    if (!pin) return DUALGCN_ERR_OOM;
+    int st = hip_status(hipMemcpyAsync(pin, src, bytes, hipMemcpyDeviceToHost, s));
+    if (!st) st = wait_stream(s);
+    if (!st) std::memcpy(dst, pin, bytes);
+    return st;
+}
 
 // Exclusive scan of `count` u32 values in place; `sums` holds one word per tile.
 // Writes the grand total to *grand (device) when grand is not null.
@@ -836,6 +863,7 @@ int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t
 void free_plan(Plan *p) {
     if (!p) return;
     release_block(p->mem, p->mem_bytes);
+    if (p->ready) (void)hipEventDestroy(p->ready);
     delete p;
 }
 
@@ -904,14 +932,14 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_pcol = lp.take(sizeof(int32_t) * unnz), o_pval = lp.take(sizeof(float) * unnz),
                  o_tasks = lp.take(sizeof(int32_t) * (un + 1)),
                  o_parts = lp.take(sizeof(SplitPart) * max_parts),
-                 o_partials = lp.take(sizeof(double) * max_parts * kMaxSlice);
+                 o_partials = lp.take(sizeof(double) * max_parts * kMaxSlice),
+                 o_tiles = lp.take(sizeof(int32_t) * (unnz / kCopyTile + 2));
     const size_t o_flags = ls.take(2 * sizeof(int32_t)), o_mom = ls.take(sizeof(Moments) * nb_keys),
                  o_sum = ls.take(2 * sizeof(Summary)), o_kb0 = ls.take(sizeof(uint64_t) * un),
                  o_kb1 = ls.take(sizeof(uint64_t) * un), o_vb0 = ls.take(sizeof(int32_t) * un),
                  o_scan = ls.take(sizeof(uint32_t) * static_cast<size_t>(scan_tiles)),
                  o_hist = ls.take(sizeof(uint32_t) * kRadix * static_cast<size_t>(nblocks)),
                  o_ssum = ls.take(sizeof(SplitSummary)), o_counts = ls.take(sizeof(uint32_t) * 2 * un),
-                 o_tiles = ls.take(sizeof(int32_t) * (unnz / kCopyTile + 2)),
                  o_info = ls.take(sizeof(int2) * un),
                  o_succ = ls.take(use_succ ? sizeof(int2) * unnz : 0),
                  o_bmax = ls.take(sizeof(int32_t) * kValidateBlocks);
@@ -931,6 +959,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     p->tasks = reinterpret_cast<int32_t *>(pm + o_tasks);
     p->parts = reinterpret_cast<SplitPart *>(pm + o_parts);
     p->partials = reinterpret_cast<double *>(pm + o_partials);
+    p->tile_row = reinterpret_cast<int32_t *>(pm + o_tiles);
     int32_t *bad = reinterpret_cast<int32_t *>(sm + o_flags);
     Moments *moments = reinterpret_cast<Moments *>(sm + o_mom);
     Summary *summary = reinterpret_cast<Summary *>(sm + o_sum);
@@ -981,9 +1010,8 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
         }
         if ((st = hip_status(hipGetLastError()))) return st;
         Summary two[2];
-        if ((st = hip_status(hipMemcpyAsync(two, summary, sizeof(two), hipMemcpyDeviceToHost, s))))
-            return st;
-        if ((st = wait_stream(s))) return st;                           // adaptive alpha only
+        static_assert(sizeof(two) <= kReadbackBytes, "read-back buffer");
+        if ((st = read_back(two, summary, sizeof(two), s))) return st;    // adaptive alpha only
         if (two[0].flag) return DUALGCN_ERR_BAD_CSR;
         if (!square_sum_fits(two[0].m) || !square_sum_fits(two[1].m)) return DUALGCN_ERR_UNSUPPORTED;
         if ((st = adaptive_weight(n, k, th.alpha_den, two[0].m, two[1].m, &pa))) return st;
@@ -997,9 +1025,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                        summary);
     if ((st = hip_status(hipGetLastError()))) return st;
     Summary sum{};
-    if ((st = hip_status(hipMemcpyAsync(&sum, summary, sizeof(sum), hipMemcpyDeviceToHost, s))))
-        return st;
-    if ((st = wait_stream(s))) return st;                               // host wait 1
+    if ((st = read_back(&sum, summary, sizeof(sum), s))) return st;       // host wait 1
     if (sum.flag) return DUALGCN_ERR_BAD_CSR;
 
     p->max_degree = sum.maxdeg;
@@ -1084,14 +1110,6 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     hipLaunchKernelGGL(sorted_degree_kernel, dim3(grid_n1), dim3(kThreads), 0, s, p->order, csr->rowptr,
                        n, pptr_u);
     if ((st = exclusive_scan(pptr_u, static_cast<int64_t>(n) + 1, scan_sums, nullptr, s))) return st;
-    if (nnz > 0) {
-        const unsigned grid_e = static_cast<unsigned>((nnz + kCopyTile - 1) / kCopyTile);
-        int32_t *tile_row = reinterpret_cast<int32_t *>(sm + o_tiles);
-        hipLaunchKernelGGL(tile_row_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, tile_row);
-        hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_e), dim3(kThreads), 0, s, p->order,
-                           csr->rowptr, csr->col, csr->val, p->pptr, tile_row, n, nnz, p->pcol,
-                           p->pval);
-    }
     hipLaunchKernelGGL(task_flag_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt,
                        off);
     if ((st = exclusive_scan(off, n, scan_sums, &dsum->tasks, s))) return st;
@@ -1104,10 +1122,37 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     hipLaunchKernelGGL(split_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, cnt, off, n, p->parts,
                        static_cast<uint32_t>(max_parts));
     if ((st = hip_status(hipGetLastError()))) return st;
-    SplitSummary ss{};
-    if ((st = hip_status(hipMemcpyAsync(&ss, dsum, sizeof(ss), hipMemcpyDeviceToHost, s)))) return st;
+    // the schedule sizes are read back while the sorted copy, the last kernel and the only
+    // one after them, runs: it reads the plan and the caller's matrix, not the scratch block
+    static_assert(sizeof(SplitSummary) <= kReadbackBytes, "read-back buffer");
+    void *pin = readback_buffer();
+    if (!pin) return DUALGCN_ERR_OOM;
+    if ((st = hip_status(hipMemcpyAsync(pin, dsum, sizeof(SplitSummary), hipMemcpyDeviceToHost, s))))
+        return st;
+    {
+        hipEvent_t done = nullptr;    // the scratch block's last use
+        if ((st = hip_status(hipEventCreateWithFlags(&done, hipEventDisableTiming)))) return st;
+        if ((st = hip_status(hipEventRecord(done, s)))) {
+            (void)hipEventDestroy(done);
+            return st;
+        }
+        scratch.done = done;
+    }
+    if (nnz > 0) {
+        const unsigned grid_e = static_cast<unsigned>((nnz + kCopyTile - 1) / kCopyTile);
+        hipLaunchKernelGGL(tile_row_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, p->tile_row);
+        hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_e), dim3(kThreads), 0, s, p->order,
+                           csr->rowptr, csr->col, csr->val, p->pptr, p->tile_row, n, nnz, p->pcol,
+                           p->pval);
+        if ((st = hip_status(hipGetLastError()))) return st;
+    }
+    // every use of the plan's sorted copy waits for this event (its stream, or any other)
+    if ((st = hip_status(hipEventCreateWithFlags(&p->ready, hipEventDisableTiming)))) return st;
+    if ((st = hip_status(hipEventRecord(p->ready, s)))) return st;
     // host wait 2: the region and schedule sizes; the scratch block is released after it
-    if ((st = wait_stream(s))) return st;
+    if ((st = wait_event(scratch.done))) return st;
+    SplitSummary ss{};
+    std::memcpy(&ss, pin, sizeof(ss));
     if (ss.parts > max_parts) return DUALGCN_ERR_HIP;    // impossible: bounded above
     p->n_sparse = ss.n_sparse;
     p->n_tasks = static_cast<int32_t>(ss.tasks);

@@ -693,8 +693,18 @@ size_t spmm_xw_lds_bytes(int32_t F_in, int32_t F_out) {
     return xw_lds_bytes(window_lpr(F_in), F_in, F_out);
 }
 
+namespace {
+
+// Orders work on stream s after the plan's sorted copy (written on the partition's stream).
+int after_plan(const Plan &p, hipStream_t s) {
+    return p.ready ? hip_status(hipStreamWaitEvent(s, p.ready, 0)) : DUALGCN_OK;
+}
+
+}  // namespace
+
 int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, void *H,
                    int32_t F_in, int32_t F_out, bool relu, hipStream_t s) {
+    if (const int st = after_plan(p, s)) return st;
     Args a = plan_args(p, X, H, F_in, relu);
     a.f0 = 0;
     a.fend = F_in;
@@ -710,6 +720,7 @@ int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, void
 
 int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool bf,
                 hipStream_t s) {
+    if (const int st = after_plan(p, s)) return st;
     Args a = plan_args(p, X, Y, F, relu);
 
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&

@@ -393,3 +393,27 @@ def test_gcn_two_layer_c2_graph(dg, device):
     rows = np.random.default_rng(3).choice(g.n, 300, replace=False).astype(np.int32)
     Yr, bound = oracle.gcn_forward_rows(g, X, [W1, W2], rows)
     assert_spmm_close(Y[rows], Yr, bound, tol=GCN_TOL, what="2-layer")
+
+
+def test_plan_used_right_away_on_other_streams(dg, device):
+    """The partition returns with its sorted copy still queued on its stream; SpMMs launched
+    at once on other streams (no synchronisation by the caller) must wait for it."""
+    g = configs.load_graph("c2")
+    rp, c, v = to_dev(g, device)
+    X = torch.from_numpy(dense.features_normal(g.n, 64, seed=3, stream_id=45)).to(device)
+    W = torch.from_numpy(dense.glorot(64, 32, seed=6)).to(device)
+    ref_plan = dg.Plan(rp, c, v, seed=0, walks_per_node=16, walk_len=5)
+    torch.cuda.synchronize()
+    Y_ref = dg.spmm(ref_plan, X)
+    T_ref = dg.spmm_update(ref_plan, X, W, relu=True)
+    torch.cuda.synchronize()
+    build, use = torch.cuda.Stream(device=device), torch.cuda.Stream(device=device)
+    for _ in range(3):
+        plan = dg.Plan(rp, c, v, seed=0, walks_per_node=16, walk_len=5, stream=build)
+        with torch.cuda.stream(use):
+            Y = dg.spmm(plan, X)
+            T = dg.spmm_update(plan, X, W, relu=True)
+        use.synchronize()
+        assert torch.equal(Y, Y_ref) and torch.equal(T, T_ref)
+        plan.destroy()
+    ref_plan.destroy()
