@@ -153,7 +153,8 @@ int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_
                       uint32_t walk_len, const dualgcn_thresholds *th, void *stream,
                       dualgcn_plan **out);
 
-/* Releases a plan and its device memory (waits for the device).  NULL is a no-op. */
+/* Releases a plan and its device memory, after waiting for the plan's own build and for
+ * the work queued by every call that used the plan (on any stream).  NULL is a no-op. */
 void dualgcn_plan_destroy(dualgcn_plan *plan);
 
 /*

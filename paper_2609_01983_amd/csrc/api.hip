@@ -255,8 +255,11 @@ int dualgcn_partition(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_
 
 void dualgcn_plan_destroy(dualgcn_plan *plan) {
     if (!plan) return;
-    (void)hipDeviceSynchronize();
-    dgc::free_plan(reinterpret_cast<Plan *>(plan));
+    Plan *p = reinterpret_cast<Plan *>(plan);
+    // the plan's own build and every launch that used it; on a failed wait (a device
+    // error), wait for the whole device before the memory can be handed out again
+    if (dgc::wait_plan_idle(*p)) (void)hipDeviceSynchronize();
+    dgc::free_plan(p);
 }
 
 int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, void *stream) {

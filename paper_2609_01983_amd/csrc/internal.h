@@ -5,6 +5,9 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <mutex>
+#include <utility>
+#include <vector>
 
 #include "dualgcn.h"
 
@@ -88,6 +91,9 @@ struct Plan {
     double *partials = nullptr;        // [n_split_parts][kMaxSlice]
     int32_t *tile_row = nullptr;       // [nnz / 4096 + 2] rows of the sorted copy's tiles
     hipEvent_t ready = nullptr;        // recorded after the sorted copy was written
+    // the last launch that used the plan on each stream (destroy waits for these)
+    mutable std::mutex use_mu;
+    mutable std::vector<std::pair<hipStream_t, hipEvent_t>> uses;
 
     uint64_t kstar = 0, kmax = 0;
     u128 s1 = 0, s2 = 0;
@@ -152,6 +158,10 @@ __device__ __forceinline__ unsigned short to_bf16(float f) {
 // stream so far, or for an event.
 int wait_stream(hipStream_t stream);
 int wait_event(hipEvent_t event);
+// Records that work using the plan was queued on `stream` (spmm.hip), and waits for every
+// such use and for the plan's own build (partition.hip).
+int note_use(const Plan &p, hipStream_t stream);
+int wait_plan_idle(const Plan &p);
 
 int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool out_bf16,
                 hipStream_t stream);

@@ -864,7 +864,31 @@ void free_plan(Plan *p) {
     if (!p) return;
     release_block(p->mem, p->mem_bytes);
     if (p->ready) (void)hipEventDestroy(p->ready);
+    for (auto &u : p->uses) (void)hipEventDestroy(u.second);
     delete p;
+}
+
+int note_use(const Plan &p, hipStream_t s) {
+    std::lock_guard<std::mutex> lock(p.use_mu);
+    for (auto &u : p.uses)
+        if (u.first == s) return hip_status(hipEventRecord(u.second, s));
+    hipEvent_t e = nullptr;
+    int st = hip_status(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    if (st) return st;
+    if ((st = hip_status(hipEventRecord(e, s)))) {
+        (void)hipEventDestroy(e);
+        return st;
+    }
+    p.uses.emplace_back(s, e);
+    return DUALGCN_OK;
+}
+
+int wait_plan_idle(const Plan &p) {
+    int st = p.ready ? wait_event(p.ready) : DUALGCN_OK;
+    std::lock_guard<std::mutex> lock(p.use_mu);
+    for (auto &u : p.uses)
+        if (!st) st = wait_event(u.second);
+    return st;
 }
 
 int structure_checksum(const int32_t *rowptr, const int32_t *col, int32_t n, int64_t nnz,

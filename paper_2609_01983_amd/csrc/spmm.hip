@@ -711,11 +711,13 @@ int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, void
     a.S = 1;
     const int lpr = window_lpr(F_in);
     a.n_long = p.n_long[long_row_class(lpr)];
-    if (lpr == 8) return launch_xw_window<8>(a, W, T, F_in, F_out, s);
-    if (lpr == 16) return launch_xw_window<16>(a, W, T, F_in, F_out, s);
-    if (lpr == 32) return launch_xw_window<32>(a, W, T, F_in, F_out, s);
-    if (lpr == 64) return launch_xw_window<64>(a, W, T, F_in, F_out, s);
-    return DUALGCN_ERR_UNSUPPORTED;
+    int st = DUALGCN_ERR_UNSUPPORTED;
+    if (lpr == 8) st = launch_xw_window<8>(a, W, T, F_in, F_out, s);
+    else if (lpr == 16) st = launch_xw_window<16>(a, W, T, F_in, F_out, s);
+    else if (lpr == 32) st = launch_xw_window<32>(a, W, T, F_in, F_out, s);
+    else if (lpr == 64) st = launch_xw_window<64>(a, W, T, F_in, F_out, s);
+    if (st) return st;
+    return note_use(p, s);
 }
 
 int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool bf,
@@ -748,7 +750,8 @@ int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bo
             st = launch_window<64, 1>(a, bf, s);
         }
     }
-    return st;
+    if (st) return st;
+    return note_use(p, s);
 }
 
 }  // namespace dgc

@@ -417,3 +417,28 @@ def test_plan_used_right_away_on_other_streams(dg, device):
         assert torch.equal(Y, Y_ref) and torch.equal(T, T_ref)
         plan.destroy()
     ref_plan.destroy()
+
+
+def test_destroy_waits_for_launches_on_other_streams(dg, device):
+    """Destroying a plan while SpMMs that use it are still queued on another stream: the plan's
+    memory is reused only after them (a new plan built at once takes the cached block)."""
+    g = configs.load_graph("c2")
+    rp, c, v = to_dev(g, device)
+    X = torch.from_numpy(dense.features_normal(g.n, 256, seed=8, stream_id=46)).to(device)
+    ref_plan = dg.Plan(rp, c, v, seed=0, walks_per_node=16, walk_len=5)
+    Y_ref = dg.spmm(ref_plan, X)
+    torch.cuda.synchronize()
+    ref_plan.destroy()
+    use = torch.cuda.Stream(device=device)
+    for _ in range(2):
+        plan = dg.Plan(rp, c, v, seed=0, walks_per_node=16, walk_len=5)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(use):
+            Ys = [dg.spmm(plan, X) for _ in range(4)]
+        plan.destroy()                            # must wait for the four launches
+        # same size (the cache hands it the block just released), another processing order
+        other = dg.Plan(rp, c, v, seed=1, walks_per_node=16, walk_len=5, force_mode="dense")
+        use.synchronize()
+        for Y in Ys:
+            assert torch.equal(Y, Y_ref)
+        other.destroy()
