@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstddef>
 #include <cstdint>
 #include <mutex>
@@ -91,6 +92,7 @@ struct Plan {
     double *partials = nullptr;        // [n_split_parts][kMaxSlice]
     int32_t *tile_row = nullptr;       // [nnz / 4096 + 2] rows of the sorted copy's tiles
     hipEvent_t ready = nullptr;        // recorded after the sorted copy was written
+    mutable std::atomic<bool> ready_seen{false};   // `ready` was found complete
     // the last launch that used the plan on each stream (destroy waits for these)
     mutable std::mutex use_mu;
     mutable std::vector<std::pair<hipStream_t, hipEvent_t>> uses;

@@ -695,9 +695,17 @@ size_t spmm_xw_lds_bytes(int32_t F_in, int32_t F_out) {
 
 namespace {
 
-// Orders work on stream s after the plan's sorted copy (written on the partition's stream).
+// Orders work on stream s after the plan's sorted copy (written on the partition's stream);
+// once the copy has been seen complete, launches need no wait (and no barrier packet).
 int after_plan(const Plan &p, hipStream_t s) {
-    return p.ready ? hip_status(hipStreamWaitEvent(s, p.ready, 0)) : DUALGCN_OK;
+    if (!p.ready || p.ready_seen.load(std::memory_order_acquire)) return DUALGCN_OK;
+    const hipError_t q = hipEventQuery(p.ready);
+    if (q == hipSuccess) {
+        p.ready_seen.store(true, std::memory_order_release);
+        return DUALGCN_OK;
+    }
+    if (q != hipErrorNotReady) return hip_status(q);
+    return hip_status(hipStreamWaitEvent(s, p.ready, 0));
 }
 
 }  // namespace
