@@ -1049,7 +1049,32 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                        summary);
     if ((st = hip_status(hipGetLastError()))) return st;
     Summary sum{};
-    if ((st = read_back(&sum, summary, sizeof(sum), s))) return st;       // host wait 1
+    {
+        // host wait 1 reads the sums; the work that needs no threshold is queued behind the
+        // read-back so that it runs while the host wakes up: perm cleared (every entry is a
+        // valid node id even before the sort writes it), and the histogram and scan of the
+        // sort's first digit
+        void *pin = readback_buffer();
+        if (!pin) return DUALGCN_ERR_OOM;
+        if ((st = hip_status(hipMemcpyAsync(pin, summary, sizeof(sum), hipMemcpyDeviceToHost, s))))
+            return st;
+        struct Event {
+            hipEvent_t e = nullptr;
+            ~Event() {
+                if (e) (void)hipEventDestroy(e);
+            }
+        } sums_read;
+        if ((st = hip_status(hipEventCreateWithFlags(&sums_read.e, hipEventDisableTiming)))) return st;
+        if ((st = hip_status(hipEventRecord(sums_read.e, s)))) return st;
+        if ((st = hip_status(hipMemsetAsync(p->perm, 0, sizeof(int32_t) * un, s)))) return st;
+        hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, p->K, n, 0, hist,
+                           nblocks);
+        if ((st = hip_status(hipGetLastError()))) return st;
+        if ((st = exclusive_scan(hist, static_cast<int64_t>(kRadix) * nblocks, scan_sums, nullptr, s)))
+            return st;
+        if ((st = wait_event(sums_read.e))) return st;
+        std::memcpy(&sum, pin, sizeof(sum));
+    }
     if (sum.flag) return DUALGCN_ERR_BAD_CSR;
 
     p->max_degree = sum.maxdeg;
@@ -1060,9 +1085,8 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if ((st = threshold_key(n, p->s1, p->s2, th.beta_num, th.beta_den, &p->kstar))) return st;
 
     phase.next("partition: sort");
-    // stable radix sort of (K, v) on the bits the keys use; every entry of perm is a
-    // valid node id even before the sort writes it
-    if ((st = hip_status(hipMemsetAsync(p->perm, 0, sizeof(int32_t) * un, s)))) return st;
+    // stable radix sort of (K, v) on the bits the keys use (the first digit's histogram and
+    // scan are already queued)
     const int passes = (bit_length(p->kmax) + kRadixBits - 1) / kRadixBits;
     uint64_t *sorted = nullptr;
     if (passes == 0) {
@@ -1089,12 +1113,14 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
             const int shift = pass * kRadixBits;
             uint64_t *kout = kbuf[pass % 2];
             int32_t *vout = vbuf[pass % 2];
-            hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, n,
-                               shift, hist, nblocks);
-            if ((st = hip_status(hipGetLastError()))) return st;
-            if ((st = exclusive_scan(hist, static_cast<int64_t>(kRadix) * nblocks, scan_sums,
-                                     nullptr, s)))
-                return st;
+            if (pass > 0) {
+                hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, n,
+                                   shift, hist, nblocks);
+                if ((st = hip_status(hipGetLastError()))) return st;
+                if ((st = exclusive_scan(hist, static_cast<int64_t>(kRadix) * nblocks, scan_sums,
+                                         nullptr, s)))
+                    return st;
+            }
             hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, vin,
                                n, shift, hist, nblocks, kout, vout);
             if ((st = hip_status(hipGetLastError()))) return st;
