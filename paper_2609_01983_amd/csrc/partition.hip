@@ -281,16 +281,27 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t *t
     return wave_base + inc - x;
 }
 
-// Tile sums of a u32 array (tiles of kTile elements).
+// Tile sums of a u32 array (tiles of kTile elements).  Full tiles of a 16-byte aligned array
+// are read with coalesced 16-byte loads (thread t takes quads t, t + kThreads, ...; the
+// order of a sum of integers does not matter), others element by element.
 __global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const uint32_t *__restrict__ in,
                                                                int64_t count,
                                                                uint32_t *__restrict__ sums) {
     __shared__ uint32_t shw[kThreads / 64];
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile;
     uint32_t s = 0;
-    for (int i = 0; i < kItems; ++i) {
-        const int64_t idx = base + static_cast<int64_t>(threadIdx.x) * kItems + i;
-        if (idx < count) s += in[idx];
+    if (base + kTile <= count && reinterpret_cast<uintptr_t>(in) % 16 == 0) {
+        const uint4 *q = reinterpret_cast<const uint4 *>(in + base);
+#pragma unroll
+        for (int i = 0; i < kItems / 4; ++i) {
+            const uint4 v = q[threadIdx.x + i * kThreads];
+            s += v.x + v.y + v.z + v.w;
+        }
+    } else {
+        for (int i = 0; i < kItems; ++i) {
+            const int64_t idx = base + static_cast<int64_t>(i) * kThreads + threadIdx.x;
+            if (idx < count) s += in[idx];
+        }
     }
     uint32_t total;
     block_exclusive_scan(s, &total, shw);
@@ -314,13 +325,34 @@ __global__ __launch_bounds__(kThreads) void scan_top_kernel(uint32_t *__restrict
     if (threadIdx.x == 0 && grand) *grand = carry;
 }
 
-// Exclusive scan inside each tile plus the tile's offset; out may alias in.
+// Exclusive scan inside each tile plus the tile's offset; out may alias in.  A full tile is
+// taken as kTile / 4 quads in index order, quad c held by thread c % kThreads in round
+// c / kThreads: round by round, a block scan of the quad sums gives each quad its offset,
+// so loads and stores stay coalesced 16-byte accesses (arrays 16-byte aligned).  Other
+// tiles go element by element, each thread scanning kItems consecutive elements.
 __global__ __launch_bounds__(kThreads) void scan_apply_kernel(const uint32_t *in, int64_t count,
                                                               const uint32_t *__restrict__ sums,
                                                               uint32_t *out) {
     __shared__ uint32_t shw[kThreads / 64];
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile +
-                         static_cast<int64_t>(threadIdx.x) * kItems;
+    const int64_t tile = static_cast<int64_t>(blockIdx.x) * kTile;
+    if (tile + kTile <= count && (reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) % 16 == 0) {
+        const uint4 *q = reinterpret_cast<const uint4 *>(in + tile);
+        uint4 v[kItems / 4];
+#pragma unroll
+        for (int i = 0; i < kItems / 4; ++i) v[i] = q[threadIdx.x + i * kThreads];
+        uint32_t carry = sums[blockIdx.x];
+#pragma unroll
+        for (int i = 0; i < kItems / 4; ++i) {
+            const uint32_t qs = v[i].x + v[i].y + v[i].z + v[i].w;
+            uint32_t total;
+            const uint32_t ex = carry + block_exclusive_scan(qs, &total, shw);
+            carry += total;
+            reinterpret_cast<uint4 *>(out + tile)[threadIdx.x + i * kThreads] =
+                make_uint4(ex, ex + v[i].x, ex + v[i].x + v[i].y, ex + v[i].x + v[i].y + v[i].z);
+        }
+        return;
+    }
+    const int64_t base = tile + static_cast<int64_t>(threadIdx.x) * kItems;
     uint32_t v[kItems];
     uint32_t s = 0;
     for (int i = 0; i < kItems; ++i) {
@@ -963,7 +995,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_kb1 = ls.take(sizeof(uint64_t) * un), o_vb0 = ls.take(sizeof(int32_t) * un),
                  o_scan = ls.take(sizeof(uint32_t) * static_cast<size_t>(scan_tiles)),
                  o_hist = ls.take(sizeof(uint32_t) * kRadix * static_cast<size_t>(nblocks)),
-                 o_ssum = ls.take(sizeof(SplitSummary)), o_counts = ls.take(sizeof(uint32_t) * 2 * un),
+                 o_ssum = ls.take(sizeof(SplitSummary)), o_counts = ls.take(sizeof(uint32_t) * 2 * ((un + 3) / 4 * 4)),
                  o_info = ls.take(sizeof(int2) * un),
                  o_succ = ls.take(use_succ ? sizeof(int2) * unnz : 0),
                  o_bmax = ls.take(sizeof(int32_t) * kValidateBlocks);
@@ -994,7 +1026,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     uint32_t *hist = reinterpret_cast<uint32_t *>(sm + o_hist);
     SplitSummary *dsum = reinterpret_cast<SplitSummary *>(sm + o_ssum);
     uint32_t *cnt = reinterpret_cast<uint32_t *>(sm + o_counts);
-    uint32_t *off = cnt + n;
+    uint32_t *off = cnt + (static_cast<int64_t>(n) + 3) / 4 * 4;    // 16-byte aligned
     int2 *nodeinfo = reinterpret_cast<int2 *>(sm + o_info);
     int32_t *blockmax = reinterpret_cast<int32_t *>(sm + o_bmax);
 
