@@ -460,15 +460,35 @@ struct SplitSummary {
     int32_t long_rows[kLongRowClasses];   // dense rows of >= 2^(kLongRowOctave - c) entries
 };
 
-// n_sparse = first position whose key is >= K* (one thread; keys are sorted).
+// First index i of the sorted array a[0, n) with a[i] >= x (n if none), found by one
+// wavefront: each round probes 64 evenly spaced positions strictly inside the candidate
+// range [lo, hi] (a[i] < x below lo, a[i] >= x from hi on) and keeps the gap between the
+// last probe below x and the first one at or above it, until at most 64 candidates are left.
+__device__ int32_t wave_lower_bound(const uint64_t *__restrict__ a, int32_t n, uint64_t x) {
+    const int lane = static_cast<int>(threadIdx.x) & 63;
+    int32_t lo = 0, hi = n;
+    while (hi - lo > 64) {
+        const int64_t span = hi - lo;
+        const int32_t p = lo + static_cast<int32_t>(span * (lane + 1) / 65);
+        const uint64_t m = __ballot(a[p] >= x);
+        if (m == 0) {
+            lo = lo + static_cast<int32_t>(span * 64 / 65) + 1;
+        } else {
+            const int f = __ffsll(static_cast<unsigned long long>(m)) - 1;
+            hi = lo + static_cast<int32_t>(span * (f + 1) / 65);
+            if (f > 0) lo = lo + static_cast<int32_t>(span * f / 65) + 1;
+        }
+    }
+    const int32_t p = lo + lane;
+    const uint64_t m = __ballot(p >= hi || a[p] >= x);
+    return m ? lo + __ffsll(static_cast<unsigned long long>(m)) - 1 : hi;
+}
+
+// n_sparse = first position whose key is >= K* (one wavefront; keys are sorted).
 __global__ void lower_bound_kernel(const uint64_t *__restrict__ sorted, int32_t n, uint64_t kstar,
                                    int32_t force_sparse_count, SplitSummary *__restrict__ out) {
-    int32_t lo = 0, hi = n;
-    while (lo < hi) {
-        const int32_t mid = lo + (hi - lo) / 2;
-        if (sorted[mid] < kstar) lo = mid + 1;
-        else hi = mid;
-    }
+    const int32_t lo = wave_lower_bound(sorted, n, kstar);
+    if (threadIdx.x != 0) return;
     out->n_sparse = force_sparse_count >= 0 ? force_sparse_count : lo;
     out->split_rows = 0;
     out->parts = 0;
@@ -477,20 +497,15 @@ __global__ void lower_bound_kernel(const uint64_t *__restrict__ sorted, int32_t 
 }
 
 // long_rows[c] = rows of the dense region with at least 2^(kLongRowOctave - c) entries: the
-// keys of the processing order are sorted, so they are the rows from the first key >= that
-// class.
-__global__ void long_rows_kernel(const uint64_t *__restrict__ okey, int32_t n,
-                                 SplitSummary *__restrict__ out) {
-    for (int c = 0; c < kLongRowClasses; ++c) {
-        const uint64_t first_long = 32u + kLongRowOctave - c;
-        int32_t lo = 0, hi = n;
-        while (lo < hi) {
-            const int32_t mid = lo + (hi - lo) / 2;
-            if (okey[mid] < first_long) lo = mid + 1;
-            else hi = mid;
-        }
-        out->long_rows[c] = n - lo;
-    }
+// rows whose processing-order key is at least that class's, i.e. n minus the number of
+// smaller keys, which the scanned histogram of the order pass holds (digit-major: entry
+// d * nblocks is the count of keys below d).
+__global__ void long_rows_kernel(const uint32_t *__restrict__ scanned_hist, int32_t nblocks,
+                                 int32_t n, SplitSummary *__restrict__ out) {
+    const int c = static_cast<int>(threadIdx.x);
+    if (c >= kLongRowClasses) return;
+    const uint32_t first_long = 32u + kLongRowOctave - c;
+    out->long_rows[c] = n - static_cast<int32_t>(scanned_hist[static_cast<int64_t>(first_long) * nblocks]);
 }
 
 // Processing order of the SpMM (the row order of the sorted copy): region first (sparse
@@ -1166,7 +1181,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     int32_t forced = -1;
     if (th.force_mode == DUALGCN_FORCE_SPARSE) forced = n;
     if (th.force_mode == DUALGCN_FORCE_DENSE) forced = 0;
-    hipLaunchKernelGGL(lower_bound_kernel, dim3(1), dim3(1), 0, s, sorted, n, p->kstar, forced, dsum);
+    hipLaunchKernelGGL(lower_bound_kernel, dim3(1), dim3(64), 0, s, sorted, n, p->kstar, forced, dsum);
     const unsigned grid_n1 = static_cast<unsigned>((static_cast<int64_t>(n) + 1 + kThreads - 1) / kThreads);
     const unsigned grid_n = static_cast<unsigned>((static_cast<int64_t>(n) + kThreads - 1) / kThreads);
     // processing order: one stable 8-bit pass over the node ids (keys < 64); the buffer of
@@ -1184,7 +1199,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
             return st;
         hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblocks), dim3(kThreads), 0, s, okey, nullptr, n,
                            0, hist, nblocks, okey_out, p->order);
-        hipLaunchKernelGGL(long_rows_kernel, dim3(1), dim3(1), 0, s, okey_out, n, dsum);
+        hipLaunchKernelGGL(long_rows_kernel, dim3(1), dim3(64), 0, s, hist, nblocks, n, dsum);
         if ((st = hip_status(hipGetLastError()))) return st;
     }
     uint32_t *pptr_u = reinterpret_cast<uint32_t *>(p->pptr);
