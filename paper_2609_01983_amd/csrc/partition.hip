@@ -683,11 +683,13 @@ __global__ __launch_bounds__(kThreads) void task_fill_kernel(int32_t n,
     if (i < n && flags[i]) tasks[offsets[i]] = static_cast<int32_t>(i);
 }
 
-// Dense rows of the sorted order longer than one chunk: counts[i] = number of parts.
+// Dense rows of the sorted order longer than one chunk: counts[i] = offsets[i] = number of
+// parts (offsets is scanned afterwards).
 __global__ __launch_bounds__(kThreads) void split_count_kernel(const int32_t *__restrict__ pptr,
                                                                int32_t n,
                                                                SplitSummary *__restrict__ sum,
-                                                               uint32_t *__restrict__ counts) {
+                                                               uint32_t *__restrict__ counts,
+                                                               uint32_t *__restrict__ offsets) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i >= n) return;
     uint32_t c = 0;
@@ -699,6 +701,7 @@ __global__ __launch_bounds__(kThreads) void split_count_kernel(const int32_t *__
         }
     }
     counts[i] = c;
+    offsets[i] = c;        // scanned afterwards
 }
 
 __global__ __launch_bounds__(kThreads) void split_fill_kernel(const uint32_t *__restrict__ counts,
@@ -1212,9 +1215,8 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if ((st = exclusive_scan(off, n, scan_sums, &dsum->tasks, s))) return st;
     hipLaunchKernelGGL(task_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, n, dsum, cnt, off,
                        p->tasks);
-    hipLaunchKernelGGL(split_count_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt);
-    if ((st = hip_status(hipMemcpyAsync(off, cnt, sizeof(uint32_t) * un, hipMemcpyDeviceToDevice, s))))
-        return st;
+    hipLaunchKernelGGL(split_count_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt,
+                       off);
     if ((st = exclusive_scan(off, n, scan_sums, &dsum->parts, s))) return st;
     hipLaunchKernelGGL(split_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, cnt, off, n, p->parts,
                        static_cast<uint32_t>(max_parts));
