@@ -357,6 +357,9 @@ def main():
     ap.add_argument("--mode", choices=["full", "spmm", "train", "planio"], default="full",
                     help="spmm: one partition, then only the dominant SpMM launches (for counter "
                          "runs); train: GCN training steps on one plan (forward, loss, backward, SGD)")
+    ap.add_argument("--cold", action="store_true",
+                    help="--mode spmm: write 512 MiB between launches so that every launch starts "
+                         "with caches that hold none of its data")
     ap.add_argument("--lr", type=float, default=0.5, help="SGD step of --mode train")
     ap.add_argument("--pipeline", action="store_true",
                     help="GCN workloads: build the next step's partition on a second stream while "
@@ -425,8 +428,13 @@ def main():
             Ys = torch.empty((g.n, F_next), dtype=torch.float32, device=dev)
         else:
             Ys = torch.empty(Xs.shape, dtype=torch.bfloat16 if w.is_gcn else torch.float32, device=dev)
+        # --cold: 512 MiB written between launches (outside the timed events), so that
+        # neither the L2s nor the 256 MiB MALL hold anything of the previous launch
+        flush = torch.empty(1 << 27, dtype=torch.float32, device=dev) if args.cold else None
         times = []
         for _ in range(args.spmm_reps):
+            if flush is not None:
+                flush.fill_(float(len(times)))
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
             if fused_w:
@@ -438,7 +446,8 @@ def main():
         torch.cuda.synchronize()
         ms = [a.elapsed_time(b) for a, b in times]
         print(json.dumps({"mode": "spmm", "config": w.name, "F": F_dom, "fused_update": fused_w,
-                          "ms": [round(x, 4) for x in ms],
+                          "caches": "cold" if args.cold else "warm",
+                          "ms": [round(x, 4) for x in ms], "median_ms": round(float(np.median(ms)), 4),
                           "bytes_min": (fused_bytes(g.n, g.nnz, F_dom, F_next) if fused_w else
                                         spmm_bytes(g.n, g.nnz, F_dom, 2 if w.is_gcn else 4))}),
               flush=True)
