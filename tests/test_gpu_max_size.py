@@ -2,10 +2,12 @@
 bound), built on the device as a circulant (row r holds columns r + o mod n for 127
 fixed offsets, value 1/127).  The partition must cover every row exactly once, and the
 SpMM must match the closed form on sampled rows: entry indices near 2^31 exercise every
-32-bit index path of the kernels."""
+32-bit index path of the kernels.  The fused layer junction runs on the same plan."""
 import numpy as np
 import pytest
 import torch
+
+from graphgen import dense
 
 pytestmark = pytest.mark.gpu
 
@@ -61,4 +63,23 @@ def test_max_size_circulant(dg, device):
             want = v32 * xs.sum()
             bound = v32 * np.abs(xs).sum()
             assert abs(Yh[i, f] - want) <= 1e-5 * bound + 1e-30, (r, f, Yh[i, f], want)
+    del X, Y
+    # the fused layer junction at the same size (F_in = F_out = 32, ReLU): bit-identical to
+    # the two calls, and within the update's bound of the closed form on the sampled rows
+    FI = 32
+    X = torch.stack([(((cidx * (f + 1)) % 97).to(torch.float32) / 97.0 - 0.5) for f in range(FI)],
+                    1).contiguous()
+    W = dense.glorot(FI, FI, seed=11)
+    Wd = torch.from_numpy(W).to(device)
+    T = dg.spmm_update(plan, X, Wd, relu=True)
+    assert torch.equal(T, dg.update(dg.spmm(plan, X, relu=True, out_bf16=True), Wd))
+    Th = T[torch.from_numpy(rows).to(device)].cpu().numpy().astype(np.float64)
+    cs = (rows[:, None].astype(np.int64) + offsets[None, :]) % N              # (rows, DEG)
+    xs = np.stack([((cs * (f + 1)) % 97) / 97.0 - 0.5 for f in range(FI)], 2)
+    xs = xs.astype(np.float32).astype(np.float64)                             # X as stored
+    H = np.maximum(v32 * xs.sum(1), 0.0)
+    B = v32 * np.abs(xs).sum(1)
+    W64 = W.astype(np.float64)
+    err = np.abs(Th - H @ W64)
+    assert np.all(err <= 1e-2 * ((np.abs(H) + B) @ np.abs(W64))), float(err.max())
     plan.destroy()
