@@ -130,8 +130,9 @@ typedef struct dualgcn_plan dualgcn_plan;
  * K_v >= K* (Eq. (1), ties dense).  `perm` lists the nodes sorted by (K_v, v)
  * ascending; its first n_sparse entries form the sparse region.
  *
- * Requirements: 1 <= k, 1 <= d <= 255, q k max(d + 1, nnz) < 2^63 and the
- * moment sums must fit 128 bits (else DUALGCN_ERR_UNSUPPORTED).  The CSR is
+ * Requirements: 1 <= k, 1 <= d <= 255, k (d + 1) < 2^32 (S_v is 32-bit),
+ * q k max(d + 1, nnz) < 2^63 and the moment sums must fit 128 bits (else
+ * DUALGCN_ERR_UNSUPPORTED).  The CSR is
  * validated on the device first (DUALGCN_ERR_BAD_CSR).
  *
  * The plan owns one block of device memory of about 9 nnz + 28 n bytes (S, K,
@@ -418,8 +419,8 @@ int dualgcn_plan_export(const dualgcn_plan *plan, int32_t *perm_h, uint32_t *S_h
  * dualgcn_arw_patterns -- the anonymous walks themselves (Sec. 3.2), for tests:
  * out (device, uint8[n][k][d+1]) receives, for walk w of node v, the label of
  * each visited position (1 + order of first occurrence), with the random
- * stream of dualgcn_partition.  Requires n k (d + 1) < 2^40 and d <= 255
- * (else DUALGCN_ERR_UNSUPPORTED).  Waits for `stream`.
+ * stream of dualgcn_partition.  Requires n k (d + 1) < 2^40, k (d + 1) < 2^32
+ * and d <= 255 (else DUALGCN_ERR_UNSUPPORTED).  Waits for `stream`.
  */
 int dualgcn_arw_patterns(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_per_node,
                          uint32_t walk_len, uint8_t *out, void *stream);

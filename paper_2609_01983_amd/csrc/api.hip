@@ -168,6 +168,9 @@ int check_csr(const dualgcn_csr *c) {
 int check_walks(uint32_t k, uint32_t d) {
     if (k < 1 || d < 1) return DUALGCN_ERR_INVALID_ARG;
     if (d > 255) return DUALGCN_ERR_UNSUPPORTED;
+    // S_v <= k (d + 1) is held in 32 bits
+    if (static_cast<uint64_t>(k) * (static_cast<uint64_t>(d) + 1) >= (static_cast<uint64_t>(1) << 32))
+        return DUALGCN_ERR_UNSUPPORTED;
     return DUALGCN_OK;
 }
 

@@ -5,12 +5,12 @@
 // by the order of its first occurrence; the density of node v is the mean
 // number of distinct nodes over its k walks, N_v = S_v / k.
 //
-// One lane runs one (node, walk) pair, or two walks of a node in lockstep (so
-// that both walks' reads are in flight together) when only the sums are needed,
-// d <= 8 and k is a power of two between 2 and 128.  Lanes of a node are
-// adjacent, so for such k the counts are summed with cross-lane shuffles and
-// written with one plain store; otherwise each lane adds its count with an
-// integer atomic (order-independent, hence exact).
+// When only the sums are needed (the partition) and d <= 32, one lane runs two
+// walks of a node in lockstep, so that both walks' reads are in flight together;
+// the lanes of a node are adjacent and their counts are summed across lanes.  For
+// the walk patterns, or longer walks, one lane runs one (node, walk) pair.  Counts
+// that cannot be summed inside one wavefront are added with integer atomics
+// (order-independent, hence exact).
 //
 // Random stream: step s of walk w from v uses the 32-bit half r (low for even s,
 // high for odd s) of 64-bit word floor(s/2) mod 4 of the Philox-4x64-10 block
@@ -101,29 +101,29 @@ __device__ __forceinline__ uint32_t walk_one(const int32_t *__restrict__ rowptr,
     return distinct;
 }
 
-// WPL walks of d steps (d <= MAXD) from node v advanced in lockstep, so that their
-// memory reads are in flight together; u[j] receives the distinct-node count of walk
-// w0 + j.  Same stream and counts as walk_one (no pattern output).  A walk that
+// Walks w0 .. w0 + nw - 1 (nw <= WPL) of d steps (d <= MAXD) from node v advanced in
+// lockstep, so that their memory reads are in flight together; u[j] receives the
+// distinct-node count of walk w0 + j (0 for j >= nw).  Same stream and counts as walk_one (no pattern output).  A walk that
 // steps onto a node whose only entry is a self-loop (or that has no entry) can never
 // leave it nor meet a new node, so it stops reading memory there: its lane is masked
 // off for the remaining steps, which saves L2 requests without changing any count.
 template <int MAXD, int WPL>
 __device__ __forceinline__ void walk_lockstep(const int2 *__restrict__ nodeinfo,
                                               const int32_t *__restrict__ col, uint32_t v,
-                                              uint32_t w0, uint32_t d, uint64_t seed,
+                                              uint32_t w0, uint32_t nw, uint32_t d, uint64_t seed,
                                               uint32_t (&u)[WPL]) {
     int32_t path[WPL][MAXD + 1];
     int32_t cur[WPL];
     bool live[WPL];
     Block4 blk[WPL];
 #pragma unroll
-    for (int j = 0; j < WPL; ++j) {
+    for (int j = 0; j < WPL; ++j) {       // walks w0 + j for j < nw; the others count 0
         path[j][0] = static_cast<int32_t>(v);
         cur[j] = static_cast<int32_t>(v);
-        live[j] = true;
-        u[j] = 1;
+        live[j] = static_cast<uint32_t>(j) < nw;
+        u[j] = live[j] ? 1 : 0;
     }
-#pragma unroll
+#pragma unroll MAXD
     for (int s = 0; s < MAXD; ++s) {
         if (static_cast<uint32_t>(s) >= d) break;
         int2 ni[WPL];             // (first entry, degree) of the current nodes
@@ -148,7 +148,7 @@ __device__ __forceinline__ void walk_lockstep(const int2 *__restrict__ nodeinfo,
         for (int j = 0; j < WPL; ++j) {
             if (live[j]) {
                 bool seen = false;
-#pragma unroll
+#pragma unroll MAXD
                 for (int i = 0; i <= s; ++i) seen |= path[j][i] == nxt[j];
                 if (!seen) ++u[j];
                 live[j] = !(ni[j].y <= 1 && nxt[j] == cur[j]);   // absorbed: stays put for good
@@ -173,8 +173,8 @@ __device__ __forceinline__ int32_t node_key(int2 rec) {
 template <int MAXD, int WPL>
 __device__ __forceinline__ void walk_lockstep_succ(const int2 *__restrict__ nodeinfo,
                                                    const int2 *__restrict__ succ, uint32_t v,
-                                                   uint32_t w0, uint32_t d, uint64_t seed,
-                                                   uint32_t (&u)[WPL]) {
+                                                   uint32_t w0, uint32_t nw, uint32_t d,
+                                                   uint64_t seed, uint32_t (&u)[WPL]) {
     int32_t path[WPL][MAXD + 1];
     int2 cur[WPL];                // (first entry, degree) of the current node
     bool live[WPL];
@@ -184,10 +184,10 @@ __device__ __forceinline__ void walk_lockstep_succ(const int2 *__restrict__ node
     for (int j = 0; j < WPL; ++j) {
         path[j][0] = node_key(start);
         cur[j] = start;
-        live[j] = true;
-        u[j] = 1;
+        live[j] = static_cast<uint32_t>(j) < nw;
+        u[j] = live[j] ? 1 : 0;
     }
-#pragma unroll
+#pragma unroll MAXD
     for (int s = 0; s < MAXD; ++s) {
         if (static_cast<uint32_t>(s) >= d) break;
         int2 nxt[WPL];
@@ -205,7 +205,7 @@ __device__ __forceinline__ void walk_lockstep_succ(const int2 *__restrict__ node
             const int32_t key = node_key(nxt[j]);
             if (live[j]) {
                 bool seen = false;
-#pragma unroll
+#pragma unroll MAXD
                 for (int i = 0; i <= s; ++i) seen |= path[j][i] == key;
                 if (!seen) ++u[j];
                 live[j] = !(cur[j].y <= 1 && key == path[j][s]);   // absorbed: stays put for good
@@ -249,33 +249,55 @@ __global__ __launch_bounds__(256) void arw_kernel(const int32_t *__restrict__ ro
     }
 }
 
-// Density sums only, WPL walks per lane: k = 2^k_log2 with WPL <= k <= 64 WPL, so the
-// k / WPL lanes of a node are adjacent and aligned inside the wavefront.
-template <int MAXD, int WPL>
+// Density sums only, two walks per lane: lane p of node v (L = ceil(k / 2) adjacent
+// lanes per node) runs walks 2p and 2p + 1, or only 2p when that is the node's last
+// walk.  When L is a power of two up to 64 the lanes of a node are aligned inside the
+// wavefront: their counts are summed with shuffles and stored once.  Otherwise the
+// counts are summed per node inside the wavefront (a segmented scan) and the node's
+// last lane in the wavefront adds the sum to S[v], which starts at zero.
+template <int MAXD>
 __global__ __launch_bounds__(256) void arw_sum_kernel(const int2 *__restrict__ nodeinfo,
                                                       const int32_t *__restrict__ col,
                                                       const int2 *__restrict__ succ,
-                                                      int32_t n, uint64_t seed, uint32_t d,
-                                                      int k_log2, uint32_t *__restrict__ S,
+                                                      int32_t n, uint64_t seed, uint32_t k,
+                                                      uint32_t d, uint32_t L, int L_log2,
+                                                      uint32_t *__restrict__ S,
                                                       const int32_t *__restrict__ bad_flag) {
     if (*bad_flag) return;
     const int64_t gid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    const int lanes_log2 = k_log2 - (WPL == 2 ? 1 : (WPL == 4 ? 2 : 0));
-    const bool valid = gid < (static_cast<int64_t>(n) << lanes_log2);
-    const uint32_t v = static_cast<uint32_t>(gid >> lanes_log2);
-    const uint32_t w0 = static_cast<uint32_t>(gid & ((1 << lanes_log2) - 1)) * WPL;
+    const bool valid = gid < static_cast<int64_t>(n) * L;
+    int64_t v64, p;
+    if (L_log2 >= 0) {
+        v64 = gid >> L_log2;
+        p = gid & ((static_cast<int64_t>(1) << L_log2) - 1);
+    } else {
+        v64 = gid / L;
+        p = gid - v64 * L;
+    }
+    const uint32_t v = static_cast<uint32_t>(v64);
+    const uint32_t w0 = static_cast<uint32_t>(p) * 2;
     uint32_t u = 0;
     if (valid) {
-        uint32_t uj[WPL];
+        const uint32_t nw = k - w0 >= 2 ? 2 : 1;
+        uint32_t uj[2];
         if (succ)
-            walk_lockstep_succ<MAXD, WPL>(nodeinfo, succ, v, w0, d, seed, uj);
+            walk_lockstep_succ<MAXD, 2>(nodeinfo, succ, v, w0, nw, d, seed, uj);
         else
-            walk_lockstep<MAXD, WPL>(nodeinfo, col, v, w0, d, seed, uj);
-#pragma unroll
-        for (int j = 0; j < WPL; ++j) u += uj[j];
+            walk_lockstep<MAXD, 2>(nodeinfo, col, v, w0, nw, d, seed, uj);
+        u = uj[0] + uj[1];
     }
-    for (int off = 1; off < (1 << lanes_log2); off <<= 1) u += __shfl_xor(u, off, 64);
-    if (valid && w0 == 0) S[v] = u;
+    if (L_log2 >= 0 && L_log2 <= 6) {
+        for (int off = 1; off < (1 << L_log2); off <<= 1) u += __shfl_xor(u, off, 64);
+        if (valid && p == 0) S[v] = u;
+        return;
+    }
+    const int lane = static_cast<int>(threadIdx.x) & 63;
+    const int first = lane - static_cast<int>(p < lane ? p : lane);   // node's first lane here
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t t = __shfl_up(u, off, 64);
+        if (lane - off >= first) u += t;
+    }
+    if (valid && (p == static_cast<int64_t>(L) - 1 || lane == 63)) atomicAdd(&S[v], u);
 }
 
 }  // namespace
@@ -283,16 +305,26 @@ __global__ __launch_bounds__(256) void arw_sum_kernel(const int2 *__restrict__ n
 int launch_density(const int2 *nodeinfo, const int32_t *col, const int2 *succ, int32_t n,
                    uint64_t seed, uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
                    hipStream_t stream) {
-    int k_log2 = -1;
-    if ((k & (k - 1)) == 0) {
-        k_log2 = 0;
-        while ((1u << k_log2) < k) ++k_log2;
+    if (d > 32 || k < 1) return DUALGCN_ERR_UNSUPPORTED;
+    const uint32_t L = k / 2 + (k & 1);                 // lanes per node, two walks each
+    int L_log2 = -1;
+    if ((L & (L - 1)) == 0) {
+        L_log2 = 0;
+        while ((1u << L_log2) < L) ++L_log2;
     }
-    if (d > 8 || k_log2 < 1 || k_log2 > 7) return DUALGCN_ERR_UNSUPPORTED;
-    const int64_t blocks = (static_cast<int64_t>(n) * k / 2 + 255) / 256;   // two walks per lane
+    const int64_t blocks = (static_cast<int64_t>(n) * L + 255) / 256;
     if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL((arw_sum_kernel<8, 2>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                       stream, nodeinfo, col, succ, n, seed, d, k_log2, S, bad_flag);
+    if (L_log2 < 0 || L_log2 > 6) {                     // summed with atomics
+        const int st = hip_status(hipMemsetAsync(S, 0, sizeof(uint32_t) * static_cast<size_t>(n), stream));
+        if (st) return st;
+    }
+    const dim3 grid(static_cast<unsigned>(blocks)), block(256);
+    if (d <= 8)
+        hipLaunchKernelGGL((arw_sum_kernel<8>), grid, block, 0, stream, nodeinfo, col, succ, n, seed,
+                           k, d, L, L_log2, S, bad_flag);
+    else
+        hipLaunchKernelGGL((arw_sum_kernel<32>), grid, block, 0, stream, nodeinfo, col, succ, n,
+                           seed, k, d, L, L_log2, S, bad_flag);
     return hip_status(hipGetLastError());
 }
 

@@ -121,10 +121,9 @@ int launch_arw(const int32_t *rowptr, const int32_t *col, int32_t n, uint64_t se
                uint32_t d, uint32_t *S, uint8_t *patterns, const int32_t *bad_flag,
                hipStream_t stream);
 // The same sums from nodeinfo (every node's (first entry, degree), as validate_csr writes
-// it), two walks per lane advanced in lockstep.  With succ (succ[e] = (col[e], first entry
-// and degree of that node)) each step reads one record instead of a node's bounds and then
-// a column.  DUALGCN_ERR_UNSUPPORTED (nothing launched) unless d <= 8 and k is a power of
-// two in [2, 128].
+// it), two walks per lane advanced in lockstep.  With succ (succ[e] = (first entry, degree)
+// of the node in column e) each step reads one record instead of a node's bounds and then
+// a column.  DUALGCN_ERR_UNSUPPORTED (nothing launched) when d > 32.
 int launch_density(const int2 *nodeinfo, const int32_t *col, const int2 *succ, int32_t n,
                    uint64_t seed, uint32_t k, uint32_t d, uint32_t *S, const int32_t *bad_flag,
                    hipStream_t stream);

@@ -50,6 +50,10 @@ def test_partition_argument_checks(dg):
     assert L.dualgcn_partition(ctypes.byref(c), 0, 0, 4, None, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
     assert L.dualgcn_partition(ctypes.byref(c), 0, 4, 0, None, None, ctypes.byref(out)) == dg.ERR_INVALID_ARG
     assert L.dualgcn_partition(ctypes.byref(c), 0, 4, 256, None, None, ctypes.byref(out)) == dg.ERR_UNSUPPORTED
+    # S_v <= k (d + 1) must fit 32 bits
+    assert L.dualgcn_partition(ctypes.byref(c), 0, 1 << 28, 15, None, None, ctypes.byref(out)) == dg.ERR_UNSUPPORTED
+    assert L.dualgcn_partition(ctypes.byref(c), 0, (1 << 28) - 1, 15, None, None,
+                               ctypes.byref(out)) == dg.ERR_NO_DEVICE
     big = _csr(dg, nnz=1 << 31)
     assert L.dualgcn_partition(ctypes.byref(big), 0, 4, 4, None, None, ctypes.byref(out)) == dg.ERR_UNSUPPORTED
     for bad in [_csr(dg, n=0), _csr(dg, nnz=-1), _csr(dg, rowptr=0), _csr(dg, col=0)]:

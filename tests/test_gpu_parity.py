@@ -253,6 +253,20 @@ def test_paper_walk_parameters_c1(dg, device, k, d):
     assert_plan_matches(dg, plan, g, 3, k, d)
 
 
+@pytest.mark.parametrize("k,d", [(1, 1), (3, 8), (2, 9), (128, 3), (129, 2), (256, 2), (300, 9),
+                                 (7, 32), (5, 33)])
+def test_walk_sum_lane_layouts_c1(dg, device, k, d):
+    """Every lane layout of the partition's walk sums, bit-exact: one lane per node, a node's
+    last lane with one walk (k odd), up to 64 lanes summed inside a wavefront, nodes whose
+    lanes span wavefronts (k = 129, 256, 300), walks of up to 32 steps in lockstep, and the
+    one-walk-per-lane kernel beyond; on c1 both with and without successor records
+    (k d below and above twice the entries per node)."""
+    g = configs.load_graph("c1")
+    plan = dg.Plan(*to_dev(g, device), seed=5, walks_per_node=k, walk_len=d)
+    assert_plan_matches(dg, plan, g, 5, k, d)
+    plan.destroy()
+
+
 def _sample_rows(g, plan_info_perm, n_sparse, count, seed):
     """Random rows plus the heaviest dense rows and the rows around the region boundary."""
     gen = np.random.default_rng(seed)
