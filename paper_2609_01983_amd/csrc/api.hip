@@ -1,5 +1,6 @@
 // C ABI of libdualgcn: argument checks, status codes and dispatch to the kernels.
 // Every check that needs no device runs before the device is touched.
+#include <atomic>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -31,6 +32,23 @@ int device_status() {
         return DUALGCN_ERR_NO_DEVICE;
     }
     return DUALGCN_OK;
+}
+
+int device_cus() {
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cached[kMaxDevices];    // zero-initialised: not queried yet
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    const bool slot = dev >= 0 && dev < kMaxDevices;
+    if (slot) {
+        const int c = cached[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    if (slot) cached[dev].store(cus, std::memory_order_relaxed);
+    return cus;
 }
 
 // Allocation-failure injection for tests: while DUALGCN_TEST_FAIL_ALLOC holds N > 0 (any

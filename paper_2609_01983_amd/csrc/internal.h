@@ -115,6 +115,9 @@ int alloc_block(void **p, size_t *capacity, size_t bytes);
 // Returns a block to the cache (or to HIP); the device must no longer use it.
 void release_block(void *p, size_t capacity);
 
+// Compute units of the current device, queried once per device (256 if the query fails).
+int device_cus();
+
 // ---- anonymous walks (arw.hip)
 // S[v] = sum over k walks of distinct-node counts; patterns (may be null) receives labels.
 int launch_arw(const int32_t *rowptr, const int32_t *col, int32_t n, uint64_t seed, uint32_t k,

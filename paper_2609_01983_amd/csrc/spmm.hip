@@ -592,18 +592,6 @@ int64_t schedule_blocks(Args &a) {
     return static_cast<int64_t>(a.nb_parts) + a.nb_dense + nb_sparse;
 }
 
-int device_cus() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
-            cus = 256;
-    }
-    return cus;
-}
-
 template <int LPR>
 int launch_xw_window(Args a, const float *W, float *T, int32_t K, int32_t N, hipStream_t s) {
     const int64_t blocks = schedule_blocks<LPR>(a);

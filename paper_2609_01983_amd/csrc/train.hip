@@ -384,18 +384,6 @@ int wgrad_max_blocks(int32_t n) {
     return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(chunks, kMaxPartials)));
 }
 
-int device_cus() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
-            cus = 256;
-    }
-    return cus;
-}
-
 size_t wgrad_lds_bytes(int IB, int JB) {
     return static_cast<size_t>(IB + JB) * kLdsRow * sizeof(unsigned short);
 }

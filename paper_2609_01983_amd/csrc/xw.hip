@@ -226,18 +226,6 @@ __global__ __launch_bounds__(kThreads) void xw_mfma_kernel(const void *__restric
     }
 }
 
-int num_cus() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
-            cus = 256;
-    }
-    return cus;
-}
-
 // Dynamic LDS above 64 KiB must be requested per kernel.
 int allow_lds(const void *kernel, size_t bytes) {
     if (bytes <= 64 * 1024) return DUALGCN_OK;
@@ -254,7 +242,7 @@ int launch_tiles(const void *X, const float *W, const void *M, float *T, int32_t
     // workgroups per CU allowed by the LDS of one CU (160 KiB) and by 2048 threads per CU
     const int per_cu = std::max<int>(1, std::min<int>(2048 / kThreads, static_cast<int>((160 * 1024) / lds)));
     const int64_t tiles = (static_cast<int64_t>(n) + kRowsPerBlock - 1) / kRowsPerBlock;
-    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(tiles, static_cast<int64_t>(num_cus()) * per_cu));
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(tiles, static_cast<int64_t>(device_cus()) * per_cu));
     hipLaunchKernelGGL((xw_mfma_kernel<NT, XBF, MASK>), dim3(static_cast<unsigned>(grid)),
                        dim3(kThreads), lds, s, X, W, M, T, n, K, N, sk, sn, c0, ntiles);
     return hip_status(hipGetLastError());
