@@ -21,6 +21,8 @@
  *   - Every function returns a dualgcn_status (0 = success).  Arguments are
  *     checked before the device is touched.  Outputs are undefined after an
  *     error.  No C++ exception crosses this interface.
+ *   - Entry points may be called from several host threads at once (the
+ *     library's shared state is locked; the last HIP error is per thread).
  *   - A plan may be used by one stream at a time.  Results do not depend on
  *     the launch order of the kernels: every output element is written by
  *     exactly one workgroup, in a fixed summation order (bit-reproducible).
