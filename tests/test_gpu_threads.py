@@ -59,7 +59,7 @@ def test_threads_share_the_library(dg, device):
         except Exception as e:                               # reported by the main thread
             errors.append((name, repr(e)))
 
-    threads = [threading.Thread(target=worker, args=(name,)) for name in inputs]
+    threads = [threading.Thread(target=worker, args=(name,), daemon=True) for name in inputs]
     for t in threads:
         t.start()
     for t in threads:
