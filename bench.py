@@ -634,6 +634,11 @@ def main():
             "gather_bytes_per_launch": 4 * (g.n + 1) + 8 * g.nnz + 4 * g.nnz * F_dom
                                        + out_bytes + 4 * g.n,
             "spmm_ge_s": round(g.nnz * F_dom / (spmm_ms * 1e-3) / 1e9, 2)}
+    if traffic is not None:
+        # the counted fabric bytes over the same launch time: how close the kernel runs to the
+        # memory system's rate, where B_min counts every X row once
+        roof["traffic_GBps"] = round(traffic / (spmm_ms * 1e-3) / 1e9, 1)
+        roof["traffic_frac"] = round(traffic / (spmm_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
     out = {
         "metric": METRIC,
         "value": round(value, 3),
