@@ -366,6 +366,31 @@ int dualgcn_weight_grad(const void *X, const void *G, float *dW, int32_t n, int3
                         int32_t F_out, uint32_t flags, float lr, float *W, void *workspace,
                         size_t workspace_bytes, void *stream);
 
+/* Size of the library's static device array that dualgcn_weight_grad_noalloc keeps its
+ * partial dW matrices in (64 MiB, held on every device the library runs on). */
+#define DUALGCN_WGRAD_NOALLOC_BYTES (64u << 20)
+
+/*
+ * dualgcn_weight_grad_noalloc -- dualgcn_weight_grad without a workspace and without any
+ * device allocation, for callers that cannot allocate (code under HIP graph capture, tight
+ * serving or training loops, harnesses that forbid hipMalloc).  The per-workgroup partial
+ * dW matrices go to a static device array of DUALGCN_WGRAD_NOALLOC_BYTES bytes that the
+ * library holds on each device; the kernels, their workgroup count and the fixed
+ * summation order are those of dualgcn_weight_grad, so dW (and W after the SGD step) are
+ * bit-identical to what dualgcn_weight_grad writes on the same device.
+ *
+ * Arguments, flags and shape limits as for dualgcn_weight_grad.  The partials need
+ * (workgroups) x F_in x F_out x 4 bytes, the workgroups being as many as the device holds
+ * at once (one per compute unit on MI355X), at most one per 64 rows: shapes whose partials
+ * exceed the array return DUALGCN_ERR_UNSUPPORTED before any work is queued (F_in x F_out
+ * up to 256 x 128 fits on MI355X for any n).  Every call on a device shares that device's
+ * array: two calls that overlap in time on one device (other streams, other host threads)
+ * race and give undefined results; calls on one stream are ordered.  Asynchronous.
+ */
+int dualgcn_weight_grad_noalloc(const void *X, const void *G, float *dW, int32_t n,
+                                int32_t F_in, int32_t F_out, uint32_t flags, float lr, float *W,
+                                void *stream);
+
 /*
  * dualgcn_backward_data -- dX = (G W^T) * [M > 0], the gradient that flows from a
  * layer's update phase to its input, masked by the ReLU that produced that input.

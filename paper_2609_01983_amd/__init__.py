@@ -89,6 +89,8 @@ def _load():
         "dualgcn_weight_grad_workspace": ([I32, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "dualgcn_weight_grad": ([P, P, P, I32, I32, I32, U32, ctypes.c_float, P, P, SZ, P],
                                 ctypes.c_int),
+        "dualgcn_weight_grad_noalloc": ([P, P, P, I32, I32, I32, U32, ctypes.c_float, P, P],
+                                        ctypes.c_int),
         "dualgcn_backward_data": ([P, P, P, P, I32, I32, I32, U32, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
@@ -415,6 +417,32 @@ def weight_grad(X, G, dW=None, lr=0.0, W=None, workspace=None, stream=None):
     return dW
 
 
+def weight_grad_noalloc(X, G, dW, lr=0.0, W=None, stream=None):
+    """dualgcn_weight_grad_noalloc: weight_grad with the partial products in the library's
+    static device array (no workspace, nothing allocated by the library).  dW [F_in, F_out]
+    float32 is the caller's."""
+    _float_or_bf16(X, "X")
+    _float_or_bf16(G, "G")
+    n, F_in = X.shape
+    if G.shape[0] != n:
+        raise ValueError("X and G must have the same rows")
+    F_out = G.shape[1]
+    _dev(dW, torch.float32, "dW")
+    if dW.shape != (F_in, F_out):
+        raise ValueError("dW must be [F_in, F_out]")
+    if W is not None:
+        _dev(W, torch.float32, "W")
+        if W.shape != (F_in, F_out):
+            raise ValueError("W must be [F_in, F_out]")
+    flags = (IN_BF16 if X.dtype == torch.bfloat16 else 0) | \
+            (GRAD_BF16 if G.dtype == torch.bfloat16 else 0)
+    _check(_lib.dualgcn_weight_grad_noalloc(X.data_ptr(), G.data_ptr(), dW.data_ptr(), n, F_in,
+                                            F_out, flags, float(lr),
+                                            W.data_ptr() if W is not None else None,
+                                            _stream(stream)), "dualgcn_weight_grad_noalloc")
+    return dW
+
+
 def backward_data(G, W, M=None, dX=None, stream=None):
     """dX = (G W^T) * [M > 0] on the bf16 matrix cores (no mask without M).
     G: [n, F_out] float32 or bfloat16, W: [F_in, F_out] float32, M: [n, F_in]."""
@@ -454,6 +482,6 @@ def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
 __all__ = ["Plan", "spmm", "spmm_update", "update", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
            "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
            "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16",
-           "ALPHA_ADAPTIVE", "GRAD_BF16", "LOSS_SLOTS", "softmax_xent", "weight_grad",
+           "ALPHA_ADAPTIVE", "GRAD_BF16", "LOSS_SLOTS", "softmax_xent", "weight_grad", "weight_grad_noalloc",
            "weight_grad_workspace_bytes", "backward_data", "aggregator_values", "AGG_GCN",
            "AGG_MEAN", "AGG_SUM"]

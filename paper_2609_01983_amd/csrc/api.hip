@@ -432,6 +432,26 @@ int dualgcn_weight_grad(const void *X, const void *G, float *dW, int32_t n, int3
                                    static_cast<hipStream_t>(stream));
 }
 
+int dualgcn_weight_grad_noalloc(const void *X, const void *G, float *dW, int32_t n, int32_t F_in,
+                                int32_t F_out, uint32_t flags, float lr, float *W, void *stream) {
+    dgc::TraceRange trace("dualgcn_weight_grad_noalloc");
+    if (!G || !dW || n < 1) return DUALGCN_ERR_INVALID_ARG;
+    int st = check_update(X, W ? W : dW, dW, F_in, F_out);
+    if (st) return st;
+    if (flags & ~(DUALGCN_IN_BF16 | DUALGCN_GRAD_BF16)) return DUALGCN_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(G) % 16) return DUALGCN_ERR_INVALID_ARG;
+    const bool xbf = (flags & DUALGCN_IN_BF16) != 0, gbf = (flags & DUALGCN_GRAD_BF16) != 0;
+    const size_t un = static_cast<size_t>(n);
+    const size_t xb = un * F_in * (xbf ? 2 : 4), gb = un * F_out * (gbf ? 2 : 4);
+    const size_t wb = static_cast<size_t>(F_in) * F_out * sizeof(float);
+    if (overlaps(dW, wb, X, xb) || overlaps(dW, wb, G, gb)) return DUALGCN_ERR_INVALID_ARG;
+    if (W && (overlaps(W, wb, X, xb) || overlaps(W, wb, G, gb) || overlaps(W, wb, dW, wb)))
+        return DUALGCN_ERR_INVALID_ARG;
+    if ((st = dgc::device_status())) return st;
+    return dgc::launch_weight_grad_noalloc(X, xbf, G, gbf, dW, n, F_in, F_out, lr, W,
+                                           static_cast<hipStream_t>(stream));
+}
+
 int dualgcn_backward_data(const void *G, const float *W, const void *M, float *dX, int32_t n,
                           int32_t F_in, int32_t F_out, uint32_t flags, void *stream) {
     dgc::TraceRange trace("dualgcn_backward_data");

@@ -209,5 +209,14 @@ size_t wgrad_workspace_bytes(int32_t n, int32_t F_in, int32_t F_out);
 int launch_weight_grad(const void *X, bool x_bf16, const void *G, bool g_bf16, float *dW,
                        int32_t n, int32_t F_in, int32_t F_out, float lr, float *W, void *workspace,
                        hipStream_t stream);
+// The same with the partials in the library's static device array (no workspace, no
+// allocation): DUALGCN_ERR_UNSUPPORTED when they need more than its
+// DUALGCN_WGRAD_NOALLOC_BYTES.  wgrad_noalloc_bytes gives what they need on the current
+// device.
+int wgrad_noalloc_bytes(bool x_bf16, bool g_bf16, int32_t n, int32_t F_in, int32_t F_out,
+                        size_t *bytes);
+int launch_weight_grad_noalloc(const void *X, bool x_bf16, const void *G, bool g_bf16, float *dW,
+                               int32_t n, int32_t F_in, int32_t F_out, float lr, float *W,
+                               hipStream_t stream);
 
 }  // namespace dgc

@@ -463,20 +463,28 @@ size_t wgrad_workspace_bytes(int32_t n, int32_t F_in, int32_t F_out) {
     return static_cast<size_t>(wgrad_max_blocks(n)) * F_in * F_out * sizeof(float);
 }
 
+// Workgroups (partial dW matrices) of one weight-gradient product on the current device: as
+// many as the CUs hold at once for the widest pass, at most one per chunk and kMaxPartials.
+// Every pass uses the same count, fixed for a device, so the reduction order is fixed too.
+int wgrad_blocks(bool x_bf16, bool g_bf16, int32_t n, int32_t F_in, int32_t F_out, int *blocks) {
+    int resident = 1;
+    const int st = launch_wgrad_any(x_bf16, g_bf16, nullptr, nullptr, nullptr, 0, &resident, n, F_in,
+                                    F_out, 0, std::min<int>(F_in, kMaxIB), 0,
+                                    std::min<int>(F_out, kMaxJB), nullptr);
+    if (st) return st;
+    *blocks = std::min(wgrad_max_blocks(n), device_cus() * resident);
+    return DUALGCN_OK;
+}
+
 int launch_weight_grad(const void *X, bool x_bf16, const void *G, bool g_bf16, float *dW,
                        int32_t n, int32_t F_in, int32_t F_out, float lr, float *W, void *workspace,
                        hipStream_t s) {
     float *partial = static_cast<float *>(workspace);
     const int JB = std::min<int>(F_out, kMaxJB);
     const int IB = std::min<int>(F_in, kMaxIB);
-    // workgroups: as many as the CUs hold at once for the widest pass, at most one per
-    // chunk and kMaxPartials; every pass uses the same count, fixed for a device, so the
-    // reduction order is fixed too
-    int resident = 1;
-    const int st0 = launch_wgrad_any(x_bf16, g_bf16, X, G, partial, 0, &resident, n, F_in, F_out,
-                                     0, IB, 0, JB, s);
+    int blocks = 0;
+    const int st0 = wgrad_blocks(x_bf16, g_bf16, n, F_in, F_out, &blocks);
     if (st0) return st0;
-    const int blocks = std::min(wgrad_max_blocks(n), device_cus() * resident);
     for (int j0 = 0; j0 < F_out; j0 += JB) {
         for (int i0 = 0; i0 < F_in; i0 += IB) {
             const int ib = std::min(IB, F_in - i0), jb = std::min(JB, F_out - j0);
@@ -492,4 +500,62 @@ int launch_weight_grad(const void *X, bool x_bf16, const void *G, bool g_bf16, f
     return hip_status(hipGetLastError());
 }
 
+// ------------------------------------------------------------------ without allocation
+//
+// The partial dW matrices of launch_weight_grad in a static device array instead of a
+// caller's workspace, for callers that cannot allocate.  Each device holds its own copy
+// of the array (for the life of the process); host code must not pass the array's name to
+// a kernel (in host code it is only a stand-in for the symbol), so its address on each
+// device is looked up once, with that device current, and kept.  Every partial a product
+// uses is written in full before it is read, so the array needs no clearing; two calls that
+// overlap on one device share it and race.
+namespace {
+
+__device__ __align__(256) float scratch[DUALGCN_WGRAD_NOALLOC_BYTES / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_ptr[kMaxDevices] = {};
+
+// The scratch array's address on the current device (looked up on first use there).
+int scratch_address(void **out) {
+    int dev = 0;
+    int st = hip_status(hipGetDevice(&dev));
+    if (st) return st;
+    if (dev < 0 || dev >= kMaxDevices) return DUALGCN_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_ptr[dev]) {
+        void *p = nullptr;
+        if ((st = hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))))) return st;
+        if (!p) return DUALGCN_ERR_HIP;
+        scratch_ptr[dev] = p;
+    }
+    *out = scratch_ptr[dev];
+    return DUALGCN_OK;
+}
+
+}  // namespace
+
+int wgrad_noalloc_bytes(bool x_bf16, bool g_bf16, int32_t n, int32_t F_in, int32_t F_out,
+                        size_t *bytes) {
+    int blocks = 0;
+    const int st = wgrad_blocks(x_bf16, g_bf16, n, F_in, F_out, &blocks);
+    if (st) return st;
+    *bytes = static_cast<size_t>(blocks) * F_in * F_out * sizeof(float);
+    return DUALGCN_OK;
+}
+
+int launch_weight_grad_noalloc(const void *X, bool x_bf16, const void *G, bool g_bf16, float *dW,
+                               int32_t n, int32_t F_in, int32_t F_out, float lr, float *W,
+                               hipStream_t s) {
+    size_t need = 0;
+    int st = wgrad_noalloc_bytes(x_bf16, g_bf16, n, F_in, F_out, &need);
+    if (st) return st;
+    if (need > DUALGCN_WGRAD_NOALLOC_BYTES) return DUALGCN_ERR_UNSUPPORTED;
+    void *partial = nullptr;
+    if ((st = scratch_address(&partial))) return st;
+    return launch_weight_grad(X, x_bf16, G, g_bf16, dW, n, F_in, F_out, lr, W, partial, s);
+}
+
 }  // namespace dgc
+

@@ -144,6 +144,15 @@ def test_training_entry_points_check_arguments(dg):
     assert L.dualgcn_weight_grad(X, G, dW, 100, 32, 32, 0, 0.0, None, ws, 16, None) == dg.ERR_INVALID_ARG
     assert L.dualgcn_weight_grad(X, G, X, 100, 32, 32, 0, 0.0, None, ws, big, None) == dg.ERR_INVALID_ARG
     assert L.dualgcn_weight_grad(X, G, dW, 100, 32, 32, 0, 0.1, dW, ws, big, None) == dg.ERR_INVALID_ARG
+    # weight gradient without allocation: the same checks, no workspace
+    assert L.dualgcn_weight_grad_noalloc(None, G, dW, 100, 32, 32, 0, 0.0, None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad_noalloc(X, G, None, 100, 32, 32, 0, 0.0, None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad_noalloc(X, G, dW, 0, 32, 32, 0, 0.0, None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad_noalloc(X, G, dW, 100, 48, 32, 0, 0.0, None, None) == dg.ERR_UNSUPPORTED
+    assert L.dualgcn_weight_grad_noalloc(X, G, dW, 100, 32, 32, 1, 0.0, None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad_noalloc(X, G + 8, dW, 100, 32, 32, 0, 0.0, None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad_noalloc(X, G, X, 100, 32, 32, 0, 0.0, None, None) == dg.ERR_INVALID_ARG
+    assert L.dualgcn_weight_grad_noalloc(X, G, dW, 100, 32, 32, 0, 0.1, dW, None) == dg.ERR_INVALID_ARG
     # backward data
     M, dX = 1 << 34, 1 << 35
     assert L.dualgcn_backward_data(None, 16, M, dX, 10, 32, 32, 0, None) == dg.ERR_INVALID_ARG
@@ -162,6 +171,8 @@ def test_valid_arguments_without_device_report_no_device(dg):
     assert out.value is None
     assert L.dualgcn_arw_patterns(ctypes.byref(c), 0, 4, 4, 1, None) == dg.ERR_NO_DEVICE
     assert L.dualgcn_aggregator_values(ctypes.byref(c), 0, 0.0, 1 << 30, None) == dg.ERR_NO_DEVICE
+    assert L.dualgcn_weight_grad_noalloc(1 << 30, 1 << 31, 1 << 32, 100, 32, 32, 0, 0.0, None,
+                                          None) == dg.ERR_NO_DEVICE
 
 
 def test_binding_rejects_host_tensors(dg):
