@@ -19,10 +19,17 @@ The JSON line also carries
                 bfloat16) + 4 n (order)
                 per launch over its mean duration, timed with HIP events on its
                 stream around every launch of it inside the timed steps;
-                `traffic` is the HBM bytes per launch from the rocprofv3 FETCH_SIZE /
-                WRITE_SIZE summary under profiles/ (null when the kernel source has
-                changed since those counters were taken);
-  cpu_baseline  the CPU oracle timed on a bounded sample of the same workload;
+                `traffic` is the bytes per launch from the rocprofv3 FETCH_SIZE /
+                WRITE_SIZE summary under profiles/, copy-calibrated.  These counters see
+                the memory side of the L2s (Infinity Cache hits included), so they are
+                fabric bytes, an upper bound on HBM bytes; null when the kernel or plan
+                sources, the workload or its graph differ from those of the counters;
+  bandwidth     copy and read rates of a plain streaming kernel measured in the same run
+                (what the memory system delivers, next to the nominal 8 TB/s);
+  cpu_baseline  the CPU oracle, single-threaded, timed on a bounded sample of the same
+                workload (each part's sample fraction stated), with the same oracle on
+                all host cores as context;
+  paper_context the paper's own speedups (RTX 3090), context only;
   phases_ms     mean milliseconds of each phase inside the timed steps.
 """
 import argparse
@@ -39,8 +46,18 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 METRIC = "SpMM GE/s (nnz·F/s) and achieved HBM GB/s vs peak, 1×MI355X"
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "spmm_c5_hbm_counters.md")
+# the counted bytes of the SpMM depend on its kernels and on the plan the partition builds
+# (processing order, tasks, split rows)
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_01983_amd", "csrc", f)
-                  for f in ("spmm.hip", "internal.h")]
+                  for f in ("spmm.hip", "partition.hip", "arw.hip", "internal.h")]
+# The paper's own results (abstract, Sec. 4.1-4.2): average SpMM kernel speedups over
+# three baselines on its 12 datasets.  Other hardware and workloads: context only.
+PAPER_CONTEXT = {"speedup_vs_cusparse": 2.53, "speedup_vs_gnnadvisor": 3.8,
+                 "speedup_vs_accel": 2.13, "range_full_dualgcn": [1.48, 6.4],
+                 "hardware": "NVIDIA RTX 3090, Ubuntu 20.04, CUDA/NVCC 12.0",
+                 "timing": "kernel time only (transfers and CPU preprocessing excluded)",
+                 "workloads": "12 real graphs, F = 16..128 (not available here)",
+                 "note": "context only: relative speedups on other hardware, not a target"}
 
 
 def spmm_bytes(n, nnz, F, ybytes=4):
@@ -62,11 +79,14 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def counter_traffic(workload, kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary, if still valid."""
-    if not os.path.exists(COUNTER_SUMMARY):
+def counter_traffic(workload, kernel, run=None, path=None):
+    """Bytes per launch of `kernel` from the committed counter summary, if it was taken on
+    the same sources, workload and graph.  `run` holds the run's graph_sha256, F_in, F_out,
+    walks_per_node and walk_len; every one must match the summary's line of that name."""
+    path = path or COUNTER_SUMMARY
+    if not os.path.exists(path):
         return None, "no counter summary"
-    text = open(COUNTER_SUMMARY).read()
+    text = open(path).read()
     m_w = re.search(r"^workload: (\S+)", text, re.M)
     m_k = re.search(r"^kernel: (.+)$", text, re.M)
     m_t = re.search(r"^traffic_bytes_per_launch: (\d+)", text, re.M)
@@ -76,8 +96,14 @@ def counter_traffic(workload, kernel):
     if not m_k or m_k.group(1).strip() != kernel:
         return None, "no counters for this kernel"
     if m_h.group(1) != kernel_source_hash():
-        return None, "kernel changed since the counters were taken"
-    return int(m_t.group(1)), "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
+        return None, "kernel or plan sources changed since the counters were taken"
+    for key, want in (run or {}).items():
+        m = re.search(rf"^{key}: (\S+)", text, re.M)
+        if not m or m.group(1) != str(want):
+            return None, f"counters taken with another {key}"
+    return int(m_t.group(1)), ("rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated: memory-side "
+                               "fabric bytes (Infinity Cache hits included), an upper bound on "
+                               "HBM bytes")
 
 
 def _grow(fn, total, first, budget_s):
@@ -93,28 +119,60 @@ def _grow(fn, total, first, budget_s):
         size = min(total, max(size * 2, int(size * budget_s / max(dt, 1e-3) * 1.2)))
 
 
+def host_cores():
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def _on_threads(fn, items, threads):
+    """fn over chunks of `items` on `threads` worker threads (the oracle's C calls release the
+    interpreter lock); returns the wall time."""
+    import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
+    chunks = [c for c in np.array_split(items, threads * 4) if c.size]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(fn, chunks))
+    return time.perf_counter() - t0
+
+
 def cpu_baseline(w, g, X, weights, part_budget_s=2.5):
-    """Times the oracle on bounded random samples of each part of one step and scales
-    every part to the whole workload."""
+    """Times the oracle on bounded random samples of each part of one step and scales every
+    part to the whole workload by its sample fraction (stated per part).  The same samples
+    are also run on all host cores (the single-threaded oracle on chunks from worker
+    threads), as context."""
     import numpy as np
     import oracle
     gen = np.random.default_rng(7)
-    t_total = 0.0
+    threads = max(1, min(16, host_cores()))
     parts = []
+
+    def part(name, unit, size, total, dt, dt_mt):
+        parts.append({"part": name, "sample": int(size), "total": int(total), "unit": unit,
+                      "fraction": round(size / total, 6), "seconds": round(dt, 4),
+                      "seconds_all_cores": round(dt_mt, 4),
+                      "est_seconds": round(dt * total / size, 4),
+                      "est_seconds_all_cores": round(dt_mt * total / size, 4)})
+
     if w.name != "c1":
         order = gen.permutation(g.n).astype(np.int32)
         dt, ns = _grow(lambda s: oracle.density_sums(g, 0, w.walks, w.steps, order[:s]),
                        g.n, 2000, part_budget_s)
-        t_total += dt * g.n / ns
-        parts.append(f"walks of {ns} nodes")
+        dt_mt = _on_threads(lambda c: oracle.density_sums(g, 0, w.walks, w.steps, c),
+                            order[:ns], threads)
+        part("walks (density sums)", "nodes", ns, g.n, dt, dt_mt)
+        # keys, threshold and sort of every node: plain numpy and Python integers, whole
+        # (sums of the right size stand in for the walks' S)
         S = gen.integers(w.walks, w.walks * (w.steps + 1) + 1, g.n).astype(np.uint32)
         t0 = time.perf_counter()
         K = oracle.hybrid_keys(S, oracle.degrees(g), w.walks)
         S1, S2 = oracle.moments(K)
         oracle.threshold_key(g.n, S1, S2)
         np.lexsort((np.arange(g.n), K))
-        t_total += time.perf_counter() - t0
-        parts.append("keys, threshold and sort of all nodes")
+        dt = time.perf_counter() - t0
+        part("keys, threshold and sort (stand-in S)", "nodes", g.n, g.n, dt, dt)
     rp = np.asarray(g.rowptr, dtype=np.int64)
     layers = w.layers if w.is_gcn else ((None, w.F),)
     for li, (fin, fout) in enumerate(layers):
@@ -125,9 +183,9 @@ def cpu_baseline(w, g, X, weights, part_budget_s=2.5):
             Xin = X if fin == X.shape[1] else np.ascontiguousarray(X[:, :fin])
             dt, nr = _grow(lambda s: oracle.xw(Xin, Wl, rows_all[:s]), g.n, 500,
                            part_budget_s / 2)
+            dt_mt = _on_threads(lambda c: oracle.xw(Xin, Wl, c), rows_all[:nr], threads)
             del Xin
-            t_total += dt * g.n / nr
-            parts.append(f"layer {li + 1}: X W of {nr} rows")
+            part(f"layer {li + 1}: X W (stand-in input)", "rows", nr, g.n, dt, dt_mt)
             T = np.ascontiguousarray(X[:, :fout])   # a stand-in of the layer's SpMM input shape
         else:
             T = X
@@ -139,15 +197,51 @@ def cpu_baseline(w, g, X, weights, part_budget_s=2.5):
             oracle.spmm(g, T, rows)
 
         dt, nr = _grow(run_spmm, g.n, 500, part_budget_s / 2)
-        t_total += dt * g.nnz / max(nnz_of[nr], 1)
-        parts.append(f"layer {li + 1}: SpMM of {nr} rows ({nnz_of[nr]} entries)"
-                     if w.is_gcn else f"SpMM of {nr} rows ({nnz_of[nr]} entries)")
+        dt_mt = _on_threads(lambda c: oracle.spmm(g, T, c), rows_all[:nr], threads)
+        part(f"layer {li + 1}: SpMM" if w.is_gcn else "SpMM", "entries", nnz_of[nr], g.nnz,
+             dt, dt_mt)
         del T
     ge = g.nnz * sum(fo for _, fo in layers)
-    return {"value": ge / t_total / 1e9, "unit": "GE/s", "cores": 1, "kind": "oracle",
-            "sample": "single-threaded C oracle on random samples of the same workload: "
-                      + "; ".join(parts) + "; each part scaled to the whole workload",
-            "est_step_s": round(t_total, 3)}
+    est = sum(p["est_seconds"] for p in parts)
+    est_mt = sum(p["est_seconds_all_cores"] for p in parts)
+    measured = sum(p["seconds"] for p in parts)
+    desc = "; ".join(f"{p['part']}: {p['sample']} of {p['total']} {p['unit']} "
+                     f"({100 * p['fraction']:.2f}%)" for p in parts)
+    return {"value": ge / est / 1e9, "unit": "GE/s", "cores": 1, "kind": "oracle",
+            "sample": "single-threaded C oracle on random samples of the same workload, each part "
+                      "scaled to the whole by its sample fraction: " + desc,
+            "measured_cpu_seconds": round(measured, 3), "est_step_s": round(est, 3),
+            "parts": parts,
+            "all_cores": {"value": ge / est_mt / 1e9, "unit": "GE/s", "cores": threads,
+                          "est_step_s": round(est_mt, 3),
+                          "how": f"the same oracle on {threads} threads over node and row chunks "
+                                 "of the same samples (context)"}}
+
+
+def bandwidth(dg, torch, dev, stream, gib=2, reps=5):
+    """Copy and read rates of dualgcn_bandwidth_probe over `gib` GiB (median of reps)."""
+    import numpy as np
+    src = torch.ones((gib << 28,), dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    out = {}
+    for name, kind, moved in (("copy", dg.PROBE_COPY, 2), ("read", dg.PROBE_READ, 1)):
+        ms = []
+        for _ in range(reps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            dg.bandwidth_probe(kind, src, dst)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ms.append(a.elapsed_time(b))
+        t = float(np.median(ms[1:]))
+        out[f"{name}_GBps"] = round(moved * src.numel() * 4 / (t * 1e-3) / 1e9, 1)
+    del src, dst
+    out["bytes"] = gib << 30
+    out["how"] = ("dualgcn_bandwidth_probe: copy counts bytes read + written, read the bytes "
+                  "read; median of %d" % reps)
+    out["frac_of_peak"] = {"copy": round(out["copy_GBps"] / PEAK_HBM_GBS, 4),
+                           "read": round(out["read_GBps"] / PEAK_HBM_GBS, 4)}
+    return out
 
 
 # Partition variants of the ablation: the paper's dual metric, its degree-only analogue
@@ -624,21 +718,26 @@ def main():
         kname = f"spmm_dual_kernel<{lpr}, 4, {'true' if w.is_gcn else 'false'}>"
         kdesc = f"{kname} (F={F_dom}{', ReLU, bfloat16 output' if w.is_gcn else ''})"
     achieved = bmin / (spmm_ms * 1e-3) / 1e9
-    traffic, traffic_src = counter_traffic(w.name, kname)
+    run_keys = {"graph_sha256": g.sha256()[:16], "F_in": F_dom,
+                "F_out": w.layers[1][1] if fused else F_dom,
+                "walks_per_node": w.walks, "walk_len": w.steps}
+    traffic, traffic_src = counter_traffic(w.name, kname, run_keys)
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
             "kernel": kdesc,
             "bytes_per_launch": bmin, "ms_per_launch": round(spmm_ms, 4),
             "launches_timed": len(phases[dom_key]),
-            "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
+            "traffic_unit": "bytes per launch", "traffic_source": traffic_src,
             "gather_bytes_per_launch": 4 * (g.n + 1) + 8 * g.nnz + 4 * g.nnz * F_dom
                                        + out_bytes + 4 * g.n,
             "spmm_ge_s": round(g.nnz * F_dom / (spmm_ms * 1e-3) / 1e9, 2)}
     if traffic is not None:
-        # the counted fabric bytes over the same launch time: how close the kernel runs to the
-        # memory system's rate, where B_min counts every X row once
-        roof["traffic_GBps"] = round(traffic / (spmm_ms * 1e-3) / 1e9, 1)
-        roof["traffic_frac"] = round(traffic / (spmm_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
+        # the counted bytes over the same launch time: the rate at which the kernel moves data
+        # through the memory side of the L2s (Infinity Cache hits included), where B_min counts
+        # every X row once.  Not a roofline fraction: it counts bytes the kernel need not move.
+        roof["fabric_GBps"] = round(traffic / (spmm_ms * 1e-3) / 1e9, 1)
+        roof["fabric_unit"] = ("memory-side fabric bytes per second (FETCH_SIZE + WRITE_SIZE, "
+                               "Infinity Cache hits included, copy-calibrated)")
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -661,12 +760,21 @@ def main():
                    "steps_overlap": ("partition of the next step beside this step's updates and SpMMs"
                                      if pipelined else "layer-1 update beside the partition")},
         "roofline": roof,
+        "bandwidth": None,
+        "host_cores": host_cores(),
+        "paper_context": PAPER_CONTEXT,
         "phases_ms": {k: round(float(np.mean(v)), 4) for k, v in phases.items()},
         "plan": {"n_sparse": info["n_sparse"], "n_dense": info["n_dense"],
                  "kstar": info["kstar"], "n_tasks": info["n_tasks"],
                  "n_split_rows": info["n_split_rows"], "n_split_parts": info["n_split_parts"]},
     }
+    if w.name == "c4":
+        # the workload names a hub degree above 10^5; the seeded R-MAT draw reaches a little less
+        out["config"]["max_degree_stated"] = "> 1e5"
+        out["config"]["max_degree_note"] = (f"the generated graph's largest row has {g.max_degree()} "
+                                            "entries, below the stated > 1e5")
     holder["plan"].destroy()
+    out["bandwidth"] = bandwidth(dg, torch, dev, stream)
     if not args.no_cpu_baseline:
         t0 = time.time()
         out["cpu_baseline"] = cpu_baseline(w, g, X, weights)

@@ -407,6 +407,27 @@ int dualgcn_weight_grad_noalloc(const void *X, const void *G, float *dW, int32_t
 int dualgcn_backward_data(const void *G, const float *W, const void *M, float *dX, int32_t n,
                           int32_t F_in, int32_t F_out, uint32_t flags, void *stream);
 
+/* ------------------------------------------------------------------ measurement */
+
+enum { DUALGCN_PROBE_COPY = 0, DUALGCN_PROBE_READ = 1 };
+
+/*
+ * dualgcn_bandwidth_probe -- a plain streaming kernel that shows the memory bandwidth the
+ * device delivers, the yardstick next to which the SpMM's rates are read (the paper reports
+ * kernel times only, Sec. 4.1; this library reports each kernel's bytes against the
+ * memory system).
+ *   DUALGCN_PROBE_COPY  dst = src over `bytes` (read once, written once with
+ *                       non-temporal stores); src and dst must not overlap.
+ *   DUALGCN_PROBE_READ  every byte of src read once and summed; dst receives one float per
+ *                       workgroup, at most dualgcn_bandwidth_probe_out_floats() of them.
+ * src and dst are device memory, 16-byte aligned; `bytes` a positive multiple of 16
+ * (else DUALGCN_ERR_INVALID_ARG).  Time it with events on `stream`.  Asynchronous.
+ */
+int dualgcn_bandwidth_probe(int32_t kind, const void *src, void *dst, size_t bytes, void *stream);
+
+/* Floats the read probe writes at most (host-only). */
+int32_t dualgcn_bandwidth_probe_out_floats(void);
+
 /* ------------------------------------------------------------------ introspection */
 
 typedef struct dualgcn_plan_info {

@@ -92,6 +92,8 @@ def _load():
         "dualgcn_weight_grad_noalloc": ([P, P, P, I32, I32, I32, U32, ctypes.c_float, P, P],
                                         ctypes.c_int),
         "dualgcn_backward_data": ([P, P, P, P, I32, I32, I32, U32, P], ctypes.c_int),
+        "dualgcn_bandwidth_probe": ([I32, P, P, SZ, P], ctypes.c_int),
+        "dualgcn_bandwidth_probe_out_floats": ([], I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -469,6 +471,25 @@ def backward_data(G, W, M=None, dX=None, stream=None):
     return dX
 
 
+PROBE_COPY, PROBE_READ = 0, 1
+
+
+def bandwidth_probe(kind, src, dst, stream=None):
+    """dualgcn_bandwidth_probe: kind PROBE_COPY (dst = src) or PROBE_READ (src read once;
+    dst receives per-workgroup sums, at least bandwidth_probe_out_floats() floats)."""
+    nbytes = src.numel() * src.element_size()
+    if kind == PROBE_COPY and dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst smaller than src")
+    if kind == PROBE_READ and dst.numel() * dst.element_size() < 4 * _lib.dualgcn_bandwidth_probe_out_floats():
+        raise ValueError("dst too small for the read probe's sums")
+    _check(_lib.dualgcn_bandwidth_probe(kind, src.data_ptr(), dst.data_ptr(), nbytes, _stream(stream)),
+           "dualgcn_bandwidth_probe")
+
+
+def bandwidth_probe_out_floats():
+    return int(_lib.dualgcn_bandwidth_probe_out_floats())
+
+
 def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
     """uint8 [n, k, d+1] anonymous walks (labels) of every node, on the device."""
     csr = make_csr(rowptr, col, val)
@@ -484,4 +505,5 @@ __all__ = ["Plan", "spmm", "spmm_update", "update", "gcn_layer", "gcn_layer_work
            "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16",
            "ALPHA_ADAPTIVE", "GRAD_BF16", "LOSS_SLOTS", "softmax_xent", "weight_grad", "weight_grad_noalloc",
            "weight_grad_workspace_bytes", "backward_data", "aggregator_values", "AGG_GCN",
-           "AGG_MEAN", "AGG_SUM"]
+           "AGG_MEAN", "AGG_SUM", "bandwidth_probe", "bandwidth_probe_out_floats",
+           "PROBE_COPY", "PROBE_READ"]

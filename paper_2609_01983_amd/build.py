@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdualgcn.so")
-SOURCES = ["aggregate.hip", "api.hip", "arw.hip", "partition.hip", "spmm.hip", "train.hip", "xw.hip"]
+SOURCES = ["aggregate.hip", "api.hip", "arw.hip", "partition.hip", "probe.hip", "spmm.hip", "train.hip", "xw.hip"]
 ARCH = os.environ.get("DUALGCN_ARCH", "gfx950")
 
 

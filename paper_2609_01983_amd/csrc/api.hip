@@ -661,3 +661,17 @@ int dualgcn_aggregator_values(const dualgcn_csr *csr, int32_t kind, float eps, f
 }
 
 }  // extern "C"
+
+int dualgcn_bandwidth_probe(int32_t kind, const void *src, void *dst, size_t bytes, void *stream) {
+    dgc::TraceRange trace("dualgcn_bandwidth_probe");
+    if (!src || !dst || bytes == 0 || bytes % 16 || reinterpret_cast<uintptr_t>(src) % 16 ||
+        reinterpret_cast<uintptr_t>(dst) % 16)
+        return DUALGCN_ERR_INVALID_ARG;
+    if (kind != DUALGCN_PROBE_COPY && kind != DUALGCN_PROBE_READ) return DUALGCN_ERR_INVALID_ARG;
+    if (kind == DUALGCN_PROBE_COPY && overlaps(src, bytes, dst, bytes)) return DUALGCN_ERR_INVALID_ARG;
+    const int st = dgc::device_status();
+    if (st) return st;
+    return dgc::launch_bandwidth_probe(kind, src, dst, bytes, static_cast<hipStream_t>(stream));
+}
+
+int32_t dualgcn_bandwidth_probe_out_floats(void) { return dgc::kMaxProbeGrid; }

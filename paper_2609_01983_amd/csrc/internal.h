@@ -219,4 +219,10 @@ int launch_weight_grad_noalloc(const void *X, bool x_bf16, const void *G, bool g
                                int32_t n, int32_t F_in, int32_t F_out, float lr, float *W,
                                hipStream_t stream);
 
+// ---- attainable bandwidth (probe.hip): kind DUALGCN_PROBE_COPY or DUALGCN_PROBE_READ; the
+// read probe writes one float per workgroup (probe_grid() <= kMaxProbeGrid) to dst.
+constexpr int kMaxProbeGrid = 16384;
+int probe_grid();
+int launch_bandwidth_probe(int kind, const void *src, void *dst, size_t bytes, hipStream_t stream);
+
 }  // namespace dgc

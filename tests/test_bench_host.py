@@ -24,10 +24,15 @@ def test_byte_model_at_full_sizes():
     assert bench.fused_bytes(n5, nnz5, 128, 128) == bench.spmm_bytes(n5, nnz5, 128)
 
 
-def _summary(tmp_path, workload="c5", kernel="spmm_xw_kernel<32>", digest=None):
+RUN = {"graph_sha256": "8f58468c61854d5c", "F_in": 128, "F_out": 64, "walks_per_node": 16,
+       "walk_len": 5}
+
+
+def _summary(tmp_path, workload="c5", kernel="spmm_xw_kernel<32>", digest=None, run=RUN):
     p = tmp_path / "summary.md"
     p.write_text("# counters\n\nworkload: %s\nkernel: %s\ntraffic_bytes_per_launch: 123456\n"
-                 "kernel_source_sha256: %s\n" % (workload, kernel, digest or bench.kernel_source_hash()))
+                 "kernel_source_sha256: %s\n" % (workload, kernel, digest or bench.kernel_source_hash())
+                 + "".join(f"{k}: {v}\n" for k, v in run.items()))
     return str(p)
 
 
@@ -41,6 +46,38 @@ def test_counter_summary_is_reported_only_when_it_matches(tmp_path, monkeypatch)
     assert value is None and "changed" in why
     monkeypatch.setattr(bench, "COUNTER_SUMMARY", str(tmp_path / "missing.md"))
     assert bench.counter_traffic("c5", "spmm_xw_kernel<32>")[0] is None
+
+
+def test_counter_summary_must_match_the_run(tmp_path, monkeypatch):
+    """Counters taken on another graph, feature widths or walk parameters are not reported,
+    and the plan's sources (partition, walks) are part of the source hash."""
+    monkeypatch.setattr(bench, "COUNTER_SUMMARY", _summary(tmp_path))
+    assert bench.counter_traffic("c5", "spmm_xw_kernel<32>", RUN)[0] == 123456
+    for key, other in (("graph_sha256", "0123456789abcdef"), ("F_in", 256), ("F_out", 128),
+                       ("walks_per_node", 50), ("walk_len", 30)):
+        value, why = bench.counter_traffic("c5", "spmm_xw_kernel<32>", dict(RUN, **{key: other}))
+        assert value is None and key in why
+    # a summary without the run's lines is not reported either
+    monkeypatch.setattr(bench, "COUNTER_SUMMARY", _summary(tmp_path, run={}))
+    assert bench.counter_traffic("c5", "spmm_xw_kernel<32>", RUN)[0] is None
+    names = [os.path.basename(p) for p in bench.KERNEL_SOURCES]
+    assert "partition.hip" in names and "spmm.hip" in names and "arw.hip" in names
+
+
+def test_cpu_baseline_states_each_part_fraction():
+    """On c1 (no walks: one SpMM), the baseline names its sample as a fraction of the whole,
+    and the same samples on all host cores give a context figure with the thread count."""
+    import numpy as np
+    from graphgen import configs
+    w = configs.WORKLOADS["c1"]
+    g = configs.load_graph("c1")
+    X = configs.load_features("c1")
+    out = bench.cpu_baseline(w, g, X, [], part_budget_s=0.05)
+    assert out["cores"] == 1 and out["kind"] == "oracle" and out["value"] > 0
+    assert out["parts"] and all(0 < p["fraction"] <= 1 for p in out["parts"])
+    assert "%" in out["sample"] and out["all_cores"]["cores"] >= 1
+    est = sum(p["seconds"] / p["fraction"] for p in out["parts"])
+    assert abs(est - out["est_step_s"]) <= 1e-3 * est + 1e-3
 
 
 def test_committed_counter_summary_names_the_default_kernel():

@@ -230,7 +230,7 @@ def test_transposed_aggregation_on_plan_of_transpose(dg, device):
 
 R_MFMA = 1e-2       # one bf16 matrix-core product (two roundings and float32 sums)
 R_SPMM = 1e-5       # one float32 aggregation
-R_STORE = 2.0 ** -8  # one bfloat16 store (nearest-even: at most 2^-9 relative)
+R_STORE = 2.0 ** -8  # one bfloat16 store (nearest-even: unit roundoff 2^-8, 8 significand bits)
 
 
 def test_two_layer_training_step_c2(dg, device):
