@@ -246,9 +246,11 @@ def bandwidth(dg, torch, dev, stream, gib=2, reps=5):
 
 # Partition variants of the ablation: the paper's dual metric, its degree-only analogue
 # (the baseline partitioning of the paper's DualGCN_0 experiment), density only, and a
-# single path for every row, and the adaptive weight (each metric's share of the spread).
+# single path for every row, the adaptive weight (each metric's share of the spread) and
+# the balanced weight (both terms of H spread alike, so that density can move the split).
 ABLATION = [("dual-metric alpha=1/2", (1, 2), "auto"),
             ("dual-metric adaptive alpha", (0xFFFFFFFF, 1024), "auto"),
+            ("dual-metric balanced alpha", (0xFFFFFFFE, 1024), "auto"),
             ("degree only alpha=0", (0, 1), "auto"),
             ("density only alpha=1", (1, 1), "auto"),
             ("all rows sparse path", (1, 2), "sparse"),
@@ -259,9 +261,11 @@ def block_stats(g, perm, K, np, blocks=1024):
     """Partition-quality statistics of the paper's objective (Sec. 3.2): cut the sorted order
     into `blocks` contiguous blocks and report the work imbalance max/avg of the blocks'
     entries (Theorem 2's measure) and the sum of the within-block variances of H (in
-    key units), next to the same for blocks of consecutive node ids."""
+    key units, and as a share of blocks x the variance of all keys), next to the same for
+    blocks of consecutive node ids."""
     deg = np.diff(g.rowptr.astype(np.int64))
     Kf = K.astype(np.float64)
+    total_var = float(Kf.var())
     out = {}
     for name, order in (("sorted", perm.astype(np.int64)), ("node_id", np.arange(g.n))):
         edges = np.linspace(0, g.n, blocks + 1).astype(np.int64)
@@ -271,8 +275,13 @@ def block_stats(g, perm, K, np, blocks=1024):
         s2 = np.add.reduceat(kk * kk, edges[:-1])
         cnt = np.diff(edges)
         var = s2 / cnt - (s1 / cnt) ** 2
+        within = float(np.maximum(var, 0).sum())
         out[name] = {"imbalance_max_over_avg": round(float(work.max() / work.mean()), 2),
-                     "sum_block_var_K": float(np.maximum(var, 0).sum())}
+                     "sum_block_var_K": within,
+                     # unit-free: the share of the key's variance left inside the blocks
+                     # (comparable across weights alpha, whose keys have other units)
+                     "within_block_var_share": round(within / (blocks * total_var), 6)
+                                               if total_var > 0 else 0.0}
     out["blocks"] = blocks
     return out
 

@@ -82,8 +82,9 @@ typedef struct dualgcn_csr {
 
 enum { DUALGCN_FORCE_AUTO = 0, DUALGCN_FORCE_SPARSE = 1, DUALGCN_FORCE_DENSE = 2 };
 
-/* alpha_num that selects the adaptive weight (see dualgcn_thresholds). */
+/* alpha_num values that select an adaptive weight (see dualgcn_thresholds). */
 #define DUALGCN_ALPHA_ADAPTIVE 0xFFFFFFFFu
+#define DUALGCN_ALPHA_BALANCED 0xFFFFFFFEu
 
 /*
  * Partition parameters, as exact rationals.
@@ -96,8 +97,14 @@ enum { DUALGCN_FORCE_AUTO = 0, DUALGCN_FORCE_SPARSE = 1, DUALGCN_FORCE_DENSE = 2
  *           the total spread, alpha = Var(N) / (Var(N) + Var(D)) (population
  *           variances over all nodes), rounded down to a multiple of
  *           1 / alpha_den, and 1/2 (alpha_num = floor(alpha_den / 2)) when
- *           neither metric varies.  The weight chosen is reported by
- *           dualgcn_plan_query.
+ *           neither metric varies.  alpha_num = DUALGCN_ALPHA_BALANCED reads the
+ *           variance analysis as balancing the two terms instead: alpha such that
+ *           alpha sigma_N = (1 - alpha) sigma_D, i.e. alpha = sigma_D / (sigma_N +
+ *           sigma_D) (population standard deviations), rounded down to a multiple
+ *           of 1 / alpha_den; then both terms of H spread alike and equal spreads
+ *           give the paper's default 1/2.  A metric that does not vary gets no
+ *           weight (alpha = 0 when N is constant, 1 when D is), and 1/2 when
+ *           neither varies.  The weight chosen is reported by dualgcn_plan_query.
  *   beta  = beta_num / beta_den, the threshold tau = mu_H + beta sigma_H of
  *           Eq. (1) (Sec. 3.3); the paper uses 1/2.  Requires den > 0.
  *   force_mode  DUALGCN_FORCE_AUTO applies Eq. (1); FORCE_SPARSE / FORCE_DENSE

@@ -12,7 +12,8 @@ Pieces and the passages they follow (DualGCN paper):
 * hybrid metric -- Sec. 3.2: H_v = alpha N_v + (1 - alpha) D_v.  With
   alpha = p/q this is kept as the exact integer K_v = q k H_v = p S_v + (q-p) k D_v.
   The adaptive alpha (Sec. 3.2, "Time Complexity") is Var(N) / (Var(N) + Var(D)),
-  rounded down to a multiple of 1/q.
+  rounded down to a multiple of 1/q; the balanced alpha sigma_D / (sigma_N + sigma_D)
+  gives both terms of H the same spread.
 * threshold and mode -- Sec. 3.3 Eq. (1): dense iff H_v >= tau with
   tau = mu_H + 0.5 sigma_H (population statistics over all nodes).  Evaluated
   exactly with Python integers: H >= mu + (b/c) sigma  <=>  c (n K - S1) >= b sqrt(V)
@@ -159,6 +160,46 @@ def adaptive_alpha(S, D, k, q):
     return q // 2 if den == 0 else q * VS // den
 
 
+ALPHA_BALANCED = 0xFFFFFFFE   # alpha numerator that asks for the balanced weight
+
+
+def balanced_alpha(S, D, k, q):
+    """Balanced alpha = p/q: the variance analysis of Sec. 3.2 ("Time Complexity and Overhead
+    Analysis"; alpha defaults to 1/2, no formula given) read as balancing the two terms of
+    H = alpha N + (1 - alpha) D, so that alpha sigma_N = (1 - alpha) sigma_D, i.e.
+    alpha = sigma_D / (sigma_N + sigma_D) with N_v = S_v / k and population standard
+    deviations, rounded down to a multiple of 1/q.  A metric that does not vary carries no
+    information and gets no weight (alpha = 0 when N is constant, 1 when D is); 1/2 when
+    neither varies.
+
+    Taken step by step with exact fractions: the variances as Fractions, then the largest p
+    (scanning down from q) with p sigma_N <= (q - p) sigma_D, compared through squares (both
+    sides are non-negative)."""
+    from fractions import Fraction
+    S = np.asarray(S, dtype=np.int64).ravel()
+    D = np.asarray(D, dtype=np.int64).ravel()
+    n = int(S.size)
+
+    def variance(values, scale):
+        # population variance of values / scale: E[x^2] - E[x]^2 from exact integer sums
+        s1 = int(values.sum())
+        s2 = int((values * values).sum())
+        return Fraction(s2, n * scale * scale) - Fraction(s1, n * scale) ** 2
+
+    var_n = variance(S, k)
+    var_d = variance(D, 1)
+    if var_n == 0 and var_d == 0:
+        return q // 2
+    if var_n == 0:
+        return 0
+    if var_d == 0:
+        return q
+    for p in range(q, -1, -1):
+        if p * p * var_n <= (q - p) * (q - p) * var_d:
+            return p
+    return 0
+
+
 def moments(K):
     """(S1, S2) = (sum K, sum K^2) as exact Python integers."""
     values, counts = np.unique(np.asarray(K, dtype=np.uint64), return_counts=True)
@@ -193,13 +234,15 @@ def threshold_key(n, S1, S2, beta=(1, 2)):
 def partition(g, seed, k, steps, alpha=(1, 2), beta=(1, 2), force=FORCE_AUTO, S=None):
     """The whole plan: S, K, K*, dense flags, perm (sorted by (K, v)) and n_sparse.
 
-    alpha = (ALPHA_ADAPTIVE, q) takes the adaptive weight p/q; the alpha used is
-    returned under "alpha"."""
+    alpha = (ALPHA_ADAPTIVE, q) takes the adaptive weight p/q, (ALPHA_BALANCED, q) the
+    balanced one; the alpha used is returned under "alpha"."""
     if S is None:
         S = density_sums(g, seed, k, steps)
     D = degrees(g)
     if alpha[0] == ALPHA_ADAPTIVE:
         alpha = (adaptive_alpha(S, D, k, alpha[1]), alpha[1])
+    elif alpha[0] == ALPHA_BALANCED:
+        alpha = (balanced_alpha(S, D, k, alpha[1]), alpha[1])
     K = hybrid_keys(S, D, k, alpha)
     n = g.n
     S1, S2 = moments(K)

@@ -24,6 +24,7 @@ FORCE_AUTO, FORCE_SPARSE, FORCE_DENSE = 0, 1, 2
 RELU, OUT_BF16, IN_BF16, GRAD_BF16 = 1, 2, 4, 8
 LOSS_SLOTS = 1025                # float64 entries of the loss buffer of softmax_xent
 ALPHA_ADAPTIVE = 0xFFFFFFFF      # alpha = (ALPHA_ADAPTIVE, q): adaptive weight in steps of 1/q
+ALPHA_BALANCED = 0xFFFFFFFE      # alpha = (ALPHA_BALANCED, q): weight balancing the spreads of N and D
 
 _FORCE = {"auto": FORCE_AUTO, "sparse": FORCE_SPARSE, "dense": FORCE_DENSE,
           FORCE_AUTO: FORCE_AUTO, FORCE_SPARSE: FORCE_SPARSE, FORCE_DENSE: FORCE_DENSE}
@@ -503,7 +504,7 @@ def arw_patterns(rowptr, col, val, seed, walks_per_node, walk_len, stream=None):
 __all__ = ["Plan", "spmm", "spmm_update", "update", "gcn_layer", "gcn_layer_workspace_bytes", "arw_patterns",
            "DualGCNError", "lib", "status_str", "make_csr", "Csr", "Thresholds", "PlanInfo",
            "FORCE_AUTO", "FORCE_SPARSE", "FORCE_DENSE", "RELU", "OUT_BF16", "IN_BF16",
-           "ALPHA_ADAPTIVE", "GRAD_BF16", "LOSS_SLOTS", "softmax_xent", "weight_grad", "weight_grad_noalloc",
+           "ALPHA_ADAPTIVE", "ALPHA_BALANCED", "GRAD_BF16", "LOSS_SLOTS", "softmax_xent", "weight_grad", "weight_grad_noalloc",
            "weight_grad_workspace_bytes", "backward_data", "aggregator_values", "AGG_GCN",
            "AGG_MEAN", "AGG_SUM", "bandwidth_probe", "bandwidth_probe_out_floats",
            "PROBE_COPY", "PROBE_READ"]

@@ -200,10 +200,11 @@ bool keys_fit(uint32_t q, uint32_t k, uint32_t d, int64_t nnz) {
 }
 
 // Thresholds of a partition: rationals below 2^16 with non-zero denominators, alpha <= 1
-// (or the adaptive marker when `adaptive_ok`), a known force mode.
+// (or an adaptive marker when `adaptive_ok`), a known force mode.
 int check_thresholds(const dualgcn_thresholds &t, bool adaptive_ok) {
     if (t.alpha_den == 0 || t.beta_den == 0) return DUALGCN_ERR_INVALID_ARG;
-    if (t.alpha_num > t.alpha_den && !(adaptive_ok && t.alpha_num == DUALGCN_ALPHA_ADAPTIVE))
+    if (t.alpha_num > t.alpha_den &&
+        !(adaptive_ok && (t.alpha_num == DUALGCN_ALPHA_ADAPTIVE || t.alpha_num == DUALGCN_ALPHA_BALANCED)))
         return DUALGCN_ERR_INVALID_ARG;
     if (t.alpha_den >= kMaxRational || t.beta_den >= kMaxRational || t.beta_num >= kMaxRational)
         return DUALGCN_ERR_INVALID_ARG;

@@ -1,11 +1,11 @@
 // Dual-metric partition on gfx950 (DualGCN Sec. 3.2 and Sec. 3.3 Eq. (1)).
 //
-// Pipeline (one stream, two host waits; three with the adaptive alpha):
+// Pipeline (one stream, two host waits; three with an adaptive or balanced alpha):
 //   validate        rowptr / col checks, the largest degree, node records -> flag
 //   successors      (when walks outnumber entries twice) one record per entry:
 //                   the first entry and degree of the node in that column
 //   walks           S_v (arw.hip), or S from a saved plan
-//   adaptive alpha  (optional) moments of S and D            -> extra host wait
+//   adaptive alpha  (optional; also the balanced one) moments of S and D -> extra host wait
 //   keys            K_v = p S_v + (q - p) k D_v, D_v from the row pointers, and the
 //                   exact 128-bit sums of K and K^2 per workgroup, then one
 //                   workgroup folds them                              -> host wait 1
@@ -894,6 +894,39 @@ int adaptive_weight(int32_t n, uint32_t k, uint32_t q, const Moments &ms, const 
     return DUALGCN_OK;
 }
 
+// Balanced weight p/q: the largest multiple of 1/q with alpha sigma_N <= (1 - alpha) sigma_D
+// (N = S / k), i.e. alpha = sigma_D / (sigma_N + sigma_D) rounded down, so that the two terms
+// of H spread alike.  Squared and scaled by n^2 k^2 q^2:  p^2 V_S <= (q - p)^2 k^2 V_D, which
+// is monotone in p (left side grows, right side shrinks): a binary search over [0, q].
+// A metric that does not vary carries no information and gets no weight (p = 0 when S is
+// constant, p = q when D is), and p = q / 2 when neither varies.
+int balanced_weight(int32_t n, uint32_t k, uint32_t q, const Moments &ms, const Moments &md,
+                    uint64_t *p) {
+    u128 vs, vd, kvd;
+    int st;
+    if ((st = scaled_variance(n, join(ms.s1_lo, ms.s1_hi), join(ms.s2_lo, ms.s2_hi), &vs)))
+        return st;
+    if ((st = scaled_variance(n, join(md.s1_lo, md.s1_hi), join(md.s2_lo, md.s2_hi), &vd)))
+        return st;
+    if (vs == 0 || vd == 0) {
+        *p = vs == 0 && vd == 0 ? q / 2 : (vs == 0 ? 0 : q);
+        return DUALGCN_OK;
+    }
+    if (mul_overflows(static_cast<u128>(k) * k, vd, &kvd)) return DUALGCN_ERR_UNSUPPORTED;
+    uint64_t lo = 0, hi = q;          // p = lo satisfies the inequality, p = q does not
+    while (hi - lo > 1) {
+        const uint64_t mid = lo + (hi - lo) / 2;
+        u128 left, right;
+        if (mul_overflows(static_cast<u128>(mid) * mid, vs, &left) ||
+            mul_overflows(static_cast<u128>(q - mid) * (q - mid), kvd, &right))
+            return DUALGCN_ERR_UNSUPPORTED;
+        if (left <= right) lo = mid;
+        else hi = mid;
+    }
+    *p = lo;
+    return DUALGCN_OK;
+}
+
 // s2 = sum K^2 is accumulated modulo 2^128; it cannot have wrapped when
 // kmax * s1 (an upper bound of it) fits.
 bool square_sum_fits(const Moments &m) {
@@ -1070,11 +1103,11 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
             st = launch_arw(csr->rowptr, csr->col, n, seed, k, d, p->S, nullptr, bad, s);
         if (st) return st;
     }
-    // adaptive alpha: moments of S and of D (two passes of the key kernel with the
-    // weights (1, 0) and (0, 1)), one more host wait, the weight chosen on the host
+    // adaptive or balanced alpha: moments of S and of D (two passes of the key kernel with
+    // the weights (1, 0) and (0, 1)), one more host wait, the weight chosen on the host
     uint64_t pa = th.alpha_num;
     const uint64_t qa = th.alpha_den;
-    if (th.alpha_num == DUALGCN_ALPHA_ADAPTIVE) {
+    if (th.alpha_num == DUALGCN_ALPHA_ADAPTIVE || th.alpha_num == DUALGCN_ALPHA_BALANCED) {
         const uint64_t weights[2][2] = {{1, 0}, {0, 1}};
         for (int m = 0; m < 2; ++m) {
             hipLaunchKernelGGL(keys_kernel, dim3(nb_keys), dim3(kThreads), 0, s, csr->rowptr, p->S,
@@ -1085,10 +1118,13 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
         if ((st = hip_status(hipGetLastError()))) return st;
         Summary two[2];
         static_assert(sizeof(two) <= kReadbackBytes, "read-back buffer");
-        if ((st = read_back(two, summary, sizeof(two), s))) return st;    // adaptive alpha only
+        if ((st = read_back(two, summary, sizeof(two), s))) return st;    // adaptive alphas only
         if (two[0].flag) return DUALGCN_ERR_BAD_CSR;
         if (!square_sum_fits(two[0].m) || !square_sum_fits(two[1].m)) return DUALGCN_ERR_UNSUPPORTED;
-        if ((st = adaptive_weight(n, k, th.alpha_den, two[0].m, two[1].m, &pa))) return st;
+        st = th.alpha_num == DUALGCN_ALPHA_ADAPTIVE
+                 ? adaptive_weight(n, k, th.alpha_den, two[0].m, two[1].m, &pa)
+                 : balanced_weight(n, k, th.alpha_den, two[0].m, two[1].m, &pa);
+        if (st) return st;
         p->th.alpha_num = static_cast<uint32_t>(pa);
     }
     phase.next("partition: keys + threshold");

@@ -125,11 +125,25 @@ def test_adaptive_alpha_bitexact_tiny(dg, device, name, q):
         assert ref["alpha"][0] == 4 * q // 5
 
 
+@pytest.mark.parametrize("name", sorted(TINY) + sorted(ADAPTIVE_TINY))
+@pytest.mark.parametrize("q", [1024, 7, 65535])
+def test_balanced_alpha_bitexact_tiny(dg, device, name, q):
+    g = (TINY.get(name) or ADAPTIVE_TINY[name])()
+    alpha = (dg.ALPHA_BALANCED, q)
+    plan = dg.Plan(*to_dev(g, device), seed=7, walks_per_node=8, walk_len=4, alpha=alpha)
+    ref = assert_plan_matches(dg, plan, g, 7, 8, 4, alpha)
+    if name == "pairs":
+        assert ref["alpha"][0] == q // 2
+    elif name == "triangles":
+        assert ref["alpha"][0] == q // 3
+
+
 @pytest.mark.parametrize("cfg", ["c1", "c2"])
-def test_adaptive_alpha_bitexact_configs(dg, device, cfg):
+@pytest.mark.parametrize("marker", [0xFFFFFFFF, 0xFFFFFFFE])
+def test_adaptive_alpha_bitexact_configs(dg, device, cfg, marker):
     w = configs.WORKLOADS[cfg]
     g = configs.load_graph(cfg)
-    alpha = (dg.ALPHA_ADAPTIVE, 1024)
+    alpha = (marker, 1024)
     plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps,
                    alpha=alpha)
     assert_plan_matches(dg, plan, g, 0, w.walks, w.steps, alpha)
@@ -226,7 +240,7 @@ def test_spmm_configs_full(dg, device, cfg):
 
 @pytest.mark.parametrize("alpha,force", [((1, 2), "auto"), ((0, 1), "auto"), ((1, 1), "auto"),
                                          ((1, 2), "sparse"), ((1, 2), "dense"),
-                                         ((0xFFFFFFFF, 1024), "auto")])
+                                         ((0xFFFFFFFF, 1024), "auto"), ((0xFFFFFFFE, 1024), "auto")])
 def test_ablation_variants_c2(dg, device, alpha, force):
     """Every partition variant of the ablation: its plan matches the oracle and its SpMM
     (with the variant's schedule) matches the plan-independent oracle product."""

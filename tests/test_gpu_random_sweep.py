@@ -50,7 +50,8 @@ def _case(i):
     k = int(gen.choice([1, 2, 3, 4, 8, 9, 16]))
     d = int(gen.integers(1, 10))
     if gen.random() < 0.2:
-        alpha = (oracle.ALPHA_ADAPTIVE, int(gen.choice([4, 16, 1024])))
+        marker = oracle.ALPHA_ADAPTIVE if i % 2 else oracle.ALPHA_BALANCED
+        alpha = (marker, int(gen.choice([4, 16, 1024])))
     else:
         q = int(gen.integers(1, 8))
         alpha = (int(gen.integers(0, q + 1)), q)

@@ -183,6 +183,78 @@ def test_adaptive_alpha_degenerate_cases():
     assert oracle.adaptive_alpha(S, oracle.degrees(g), 4, 1024) == 0
 
 
+# ---------------------------------------------------------------- balanced alpha
+# The balanced weight gives both terms of H the same spread: alpha sigma_N = (1 - alpha)
+# sigma_D, alpha = sigma_D / (sigma_N + sigma_D).  Pinned by closed forms on the same
+# deterministic-walk graphs, by 60-digit square roots, and by its degenerate cases.
+
+@pytest.mark.parametrize("k,q", [(4, 1024), (7, 1000), (1, 2), (16, 65535)])
+def test_balanced_alpha_equal_spreads_is_half(k, q):
+    g = _pairs_and_empties(5, 13)
+    S = oracle.density_sums(g, 9, k, 3)
+    assert oracle.balanced_alpha(S, oracle.degrees(g), k, q) == q // 2
+
+
+@pytest.mark.parametrize("k", [3, 8])
+def test_balanced_alpha_triangles_closed_form(k):
+    # N is 3 or 1, D is 1 or 0 on the same rows: sigma_N = 2 sigma_D, alpha = 1/3 (where
+    # the variance rule gives 4/5: the two readings weigh the metrics oppositely)
+    g = _triangles_and_empties(4, 9)
+    S = oracle.density_sums(g, 2, k, 4)
+    D = oracle.degrees(g)
+    for q in (3, 5, 1000, 1024, 65535):
+        assert oracle.balanced_alpha(S, D, k, q) == q // 3
+    assert oracle.adaptive_alpha(S, D, k, 1000) == 800
+
+
+def test_balanced_alpha_degenerate_cases():
+    g = small.edgeless(12, self_loops=False, normalise=False)          # nothing varies
+    S = oracle.density_sums(g, 0, 4, 3)
+    assert oracle.balanced_alpha(S, oracle.degrees(g), 4, 1024) == 512
+    g = small.cycle(20, self_loops=True, normalise=True)               # constant degree
+    S = oracle.density_sums(g, 1, 6, 4)
+    assert len(set(S.tolist())) > 1
+    assert oracle.balanced_alpha(S, oracle.degrees(g), 6, 1024) == 1024
+    g = small.from_rows([[0] * 3, [1], [2] * 5, [3] * 2])               # constant density
+    S = oracle.density_sums(g, 0, 4, 3)
+    assert set(S.tolist()) == {4}
+    assert oracle.balanced_alpha(S, oracle.degrees(g), 4, 1024) == 0
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_balanced_alpha_against_60_digit_square_roots(seed):
+    """floor(q sigma_D / (sigma_N + sigma_D)) with the standard deviations as 60-digit square
+    roots of the exact variances, against the oracle's exact search."""
+    gen = np.random.default_rng(seed)
+    g = small.random_graph(int(gen.integers(20, 300)), float(gen.uniform(0.01, 0.2)), seed=seed)
+    k = int(gen.choice([2, 8, 16]))
+    S = oracle.density_sums(g, seed, k, 4)
+    D = oracle.degrees(g)
+    getcontext().prec = 60
+    n = len(S)
+    vn = Fraction(sum(int(x) ** 2 for x in S), n * k * k) - Fraction(int(S.sum()), n * k) ** 2
+    vd = Fraction(sum(int(x) ** 2 for x in D), n) - Fraction(int(D.sum()), n) ** 2
+    sn = (Decimal(vn.numerator) / Decimal(vn.denominator)).sqrt()
+    sd = (Decimal(vd.numerator) / Decimal(vd.denominator)).sqrt()
+    for q in (7, 1024, 65535):
+        want = int((Decimal(q) * sd / (sn + sd)).to_integral_value(rounding="ROUND_FLOOR"))
+        assert oracle.balanced_alpha(S, D, k, q) == want
+
+
+def test_balanced_partition_uses_the_chosen_alpha():
+    g = small.random_graph(80, 0.07, seed=11)
+    P = oracle.partition(g, 5, 8, 4, alpha=(oracle.ALPHA_BALANCED, 1024))
+    p = P["alpha"][0]
+    assert P["alpha"][1] == 1024 and 0 < p < 1024
+    fixed = oracle.partition(g, 5, 8, 4, alpha=(p, 1024))
+    assert np.array_equal(P["perm"], fixed["perm"]) and P["kstar"] == fixed["kstar"]
+    N = P["S"] / 8.0
+    D = P["D"].astype(np.float64)
+    a = D.std() / (N.std() + D.std())
+    assert p <= a * 1024 < p + 1 + 1e-9
+    _check_plan(P, g.n)
+
+
 def test_adaptive_partition_uses_the_chosen_alpha():
     g = small.random_graph(80, 0.07, seed=11)
     P = oracle.partition(g, 5, 8, 4, alpha=(oracle.ALPHA_ADAPTIVE, 1024))
