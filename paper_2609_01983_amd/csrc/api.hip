@@ -537,7 +537,7 @@ int dualgcn_arw_patterns(const dualgcn_csr *csr, uint64_t seed, uint32_t walks_p
     uint32_t *S = static_cast<uint32_t *>(scratch);
     int32_t *flags = reinterpret_cast<int32_t *>(S + csr->n);
     st = dgc::hip_status(hipMemsetAsync(flags, 0, 2 * sizeof(int32_t), s));
-    if (!st) st = dgc::validate_csr(csr, flags, nullptr, nullptr, s);
+    if (!st) st = dgc::validate_csr(csr, flags, nullptr, nullptr, nullptr, s);
     if (!st)
         st = dgc::launch_arw(csr->rowptr, csr->col, csr->n, seed, walks_per_node, walk_len, S, out,
                              flags, s);
@@ -651,7 +651,7 @@ int dualgcn_aggregator_values(const dualgcn_csr *csr, int32_t kind, float eps, f
     if ((st = dgc::alloc_bytes(&scratch, 2 * sizeof(int32_t)))) return st;
     int32_t *flags = static_cast<int32_t *>(scratch);
     st = dgc::hip_status(hipMemsetAsync(flags, 0, 2 * sizeof(int32_t), s));
-    if (!st) st = dgc::validate_csr(csr, flags, nullptr, nullptr, s);
+    if (!st) st = dgc::validate_csr(csr, flags, nullptr, nullptr, nullptr, s);
     if (!st) st = dgc::launch_aggregator_values(csr, kind, eps, val, s);
     int32_t bad = 0;
     if (!st) st = dgc::hip_status(hipMemcpyAsync(&bad, flags, sizeof(bad), hipMemcpyDeviceToHost, s));

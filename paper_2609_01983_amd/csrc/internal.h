@@ -49,6 +49,25 @@ constexpr int kLongRowClasses = 4;
 constexpr int kTaskRows = 8;
 constexpr int kTaskEntries = 32;
 
+// Gather heat of a node: how often the SpMM reads its feature row, on a log scale with
+// eight steps per octave (8 floor(log2 d) + the three bits below the leading one of d,
+// 0 for d = 0).  d is the node's row length, which for the symmetric aggregation matrix
+// is also the number of entries in its column, i.e. the number of times its row of X is
+// gathered.  It only steers cache policies of the gathers, never a result.
+constexpr int kHeatLevels = 256;
+// Gathers use cache classes only on operands larger than the memory-side cache (256 MiB);
+// a launch reads rows of at most kMaxSlice floats, so smaller plans mark no columns.
+constexpr uint64_t kGatherClassMinBytes = 256ull << 20;
+// Rows of X whose gathers keep the default cache policy: the hottest kHotRows columns
+// (32 MiB of 128-float rows, the L2s' share of the hottest rows).
+constexpr uint32_t kHotRows = 65536;
+__host__ __device__ inline uint32_t heat_of(uint32_t d) {
+    if (d == 0) return 0;
+    const uint32_t o = 31u - static_cast<uint32_t>(__builtin_clz(d));
+    const uint32_t frac = o >= 3 ? (d >> (o - 3)) & 7u : (d << (3 - o)) & 7u;
+    return 8u * o + frac;
+}
+
 // One part of a split dense row: position of the row in the sorted order, part index,
 // number of parts, index of the row's first part.
 struct SplitPart {
@@ -81,6 +100,8 @@ struct Plan {
     int32_t *pcol = nullptr;           // [nnz]
     float *pval = nullptr;             // [nnz]
     int32_t *tasks = nullptr;          // [n_tasks + 1] first sorted row of each sparse task
+    bool cold_marked = false;          // bit 31 of pcol marks columns outside the hottest
+                                       // kHotRows (plans on which gathers may use classes)
 
     int32_t n_sparse = 0;
     int32_t n_tasks = 0;
@@ -135,10 +156,11 @@ int launch_density(const int2 *nodeinfo, const int32_t *col, const int2 *succ, i
 // Checks the CSR on the device: flags[0] |= 1 (row pointers) | 2 (columns); flags must
 // start at zero.  nodeinfo (may be null, n entries) receives (rowptr[v], rowptr[v+1] -
 // rowptr[v]); blockmax (may be null, kValidateBlocks entries) each workgroup's largest
-// row length.
+// row length; heat_hist (may be null, kHeatLevels counters that start at zero) the number
+// of nodes per heat_of(row length).
 constexpr int kValidateBlocks = 2048;
 int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t *blockmax,
-                 hipStream_t stream);
+                 uint32_t *heat_hist, hipStream_t stream);
 // S_host (host, n sums), when given, replaces the walks: the density sums of a saved plan.
 int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                const dualgcn_thresholds &th, const uint32_t *S_host, hipStream_t stream,

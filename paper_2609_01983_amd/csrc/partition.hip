@@ -41,23 +41,37 @@ constexpr int kRadix = 1 << kRadixBits;
 
 // ------------------------------------------------------------------ validation
 
-// Checks the row pointers and columns, records the largest degree, and writes every
-// node's (first entry, degree) record for the walks (one 8-byte read per step).
+// Checks the row pointers and columns, records the largest degree, writes every node's
+// (first entry, degree) record for the walks (one 8-byte read per step) and counts the
+// nodes per gather heat (per workgroup in LDS, then one atomic per non-empty value and
+// workgroup).
 __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__restrict__ rowptr,
                                                             const int32_t *__restrict__ col,
                                                             int32_t n, int64_t nnz,
                                                             int32_t *__restrict__ flag,
                                                             int2 *__restrict__ nodeinfo,
-                                                            int32_t *__restrict__ blockmax) {
+                                                            int32_t *__restrict__ blockmax,
+                                                            uint32_t *__restrict__ heat_hist) {
     __shared__ int32_t sh_bad[kThreads / 64], sh_max[kThreads / 64];
+    __shared__ uint32_t sh_hist[kHeatLevels];
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
     const int64_t t0 = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (heat_hist) {
+        for (int h = static_cast<int>(threadIdx.x); h < kHeatLevels; h += kThreads) sh_hist[h] = 0;
+        __syncthreads();
+    }
     int32_t bad = 0, dmax = 0;
     for (int64_t i = t0; i < n; i += stride) {
         const int32_t a = rowptr[i], b = rowptr[i + 1];
         if (b < a) bad |= 1;
         dmax = max(dmax, b - a);
         if (nodeinfo) nodeinfo[i] = make_int2(a, b - a);
+        if (heat_hist) atomicAdd(&sh_hist[heat_of(b > a ? static_cast<uint32_t>(b - a) : 0u)], 1u);
+    }
+    if (heat_hist) {
+        __syncthreads();
+        for (int h = static_cast<int>(threadIdx.x); h < kHeatLevels; h += kThreads)
+            if (sh_hist[h]) atomicAdd(&heat_hist[h], sh_hist[h]);
     }
     if (t0 == 0) {
         if (rowptr[0] != 0) bad |= 1;
@@ -103,18 +117,43 @@ __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__res
 }
 
 // Successor records of the walks: succ[e] = (first entry of c, degree of c) for
-// c = col[e], the node record validate_kernel wrote.  A column out of range (the
-// validation flags it, and nothing walks then) gets a record without reading them.
+// c = col[e], the node record validate_kernel wrote.  With marked, also the column with
+// bit 31 set when c is outside the hottest columns (heat below *hot_heat), in the
+// matrix's entry order: the sorted copy then reads it in place of the column, and the
+// mark costs it nothing.  A column out of range (the validation flags it, and nothing
+// walks or copies then) gets a record without reading them.
 __global__ __launch_bounds__(kThreads) void successor_kernel(const int2 *__restrict__ nodeinfo,
                                                              const int32_t *__restrict__ col,
                                                              int32_t n, int64_t nnz,
-                                                             int2 *__restrict__ succ) {
+                                                             int2 *__restrict__ succ,
+                                                             const uint32_t *__restrict__ hot_heat,
+                                                             int32_t *__restrict__ marked) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    const uint32_t hot = marked ? *hot_heat : 0u;
     for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < nnz;
          e += stride) {
         const int32_t c = col[e];
-        succ[e] = c >= 0 && c < n ? nodeinfo[c] : make_int2(0, 0);
+        const int2 r = c >= 0 && c < n ? nodeinfo[c] : make_int2(0, 0);
+        if (succ) succ[e] = r;
+        if (marked) {
+            const bool cold = heat_of(static_cast<uint32_t>(r.y)) < hot;
+            marked[e] = static_cast<int32_t>(static_cast<uint32_t>(c) | (cold ? 0x80000000u : 0u));
+        }
     }
+}
+
+// *hot_heat = the smallest heat h whose nodes of heat >= h number at most hot_rows (one
+// thread; hist counts the nodes per heat value).
+__global__ void hot_heat_kernel(const uint32_t *__restrict__ hist, uint32_t hot_rows,
+                                uint32_t *__restrict__ hot_heat) {
+    if (threadIdx.x != 0) return;
+    uint32_t hot = kHeatLevels;
+    uint64_t above = 0;
+    for (int h = kHeatLevels - 1; h >= 0 && above + hist[h] <= hot_rows; --h) {
+        above += hist[h];
+        hot = static_cast<uint32_t>(h);
+    }
+    *hot_heat = hot;
 }
 
 // ------------------------------------------------------------------ structure checksum
@@ -937,9 +976,9 @@ bool square_sum_fits(const Moments &m) {
 }  // namespace
 
 int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t *blockmax,
-                 hipStream_t s) {
+                 uint32_t *heat_hist, hipStream_t s) {
     hipLaunchKernelGGL(validate_kernel, dim3(kValidateBlocks), dim3(kThreads), 0, s, csr->rowptr,
-                       csr->col, csr->n, csr->nnz, flags, nodeinfo, blockmax);
+                       csr->col, csr->n, csr->nnz, flags, nodeinfo, blockmax, heat_hist);
     return hip_status(hipGetLastError());
 }
 
@@ -1028,6 +1067,11 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     // costs one random read per entry and saves one dependent random read per step.
     const bool use_succ = S_host == nullptr &&
                           static_cast<u128>(n) * k * d >= 2 * static_cast<u128>(unnz);
+    // columns outside the hottest kHotRows are marked (bit 31 of the sorted copy's columns)
+    // for the cache classes of the gathers, only when a launch on the plan can use them
+    // (an operand of rows up to kMaxSlice floats larger than kGatherClassMinBytes): the
+    // successor pass writes the marked columns and the sorted copy reads them
+    const bool mark = nnz > 0 && static_cast<uint64_t>(n) * kMaxSlice * sizeof(float) > kGatherClassMinBytes;
     const int32_t nb_keys = static_cast<int32_t>(std::min<int64_t>((n + kThreads - 1) / kThreads, 1024));
     const int32_t nblocks = static_cast<int32_t>((static_cast<int64_t>(n) + kTile - 1) / kTile);
     const int64_t scan_tiles = std::max((static_cast<int64_t>(kRadix) * nblocks + kTile - 1) / kTile,
@@ -1041,7 +1085,10 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_parts = lp.take(sizeof(SplitPart) * max_parts),
                  o_partials = lp.take(sizeof(double) * max_parts * kMaxSlice),
                  o_tiles = lp.take(sizeof(int32_t) * (unnz / kCopyTile + 2));
-    const size_t o_flags = ls.take(2 * sizeof(int32_t)), o_mom = ls.take(sizeof(Moments) * nb_keys),
+    // the validation flags and the heat histogram are cleared by one fill; the hot heat
+    // value follows them
+    constexpr size_t kFlagBytes = 2 * sizeof(int32_t), kHistBytes = sizeof(uint32_t) * kHeatLevels;
+    const size_t o_flags = ls.take(kFlagBytes + kHistBytes + sizeof(uint32_t)), o_mom = ls.take(sizeof(Moments) * nb_keys),
                  o_sum = ls.take(2 * sizeof(Summary)), o_kb0 = ls.take(sizeof(uint64_t) * un),
                  o_kb1 = ls.take(sizeof(uint64_t) * un), o_vb0 = ls.take(sizeof(int32_t) * un),
                  o_scan = ls.take(sizeof(uint32_t) * static_cast<size_t>(scan_tiles)),
@@ -1049,6 +1096,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                  o_ssum = ls.take(sizeof(SplitSummary)), o_counts = ls.take(sizeof(uint32_t) * 2 * ((un + 3) / 4 * 4)),
                  o_info = ls.take(sizeof(int2) * un),
                  o_succ = ls.take(use_succ ? sizeof(int2) * unnz : 0),
+                 o_marked = ls.take(mark ? sizeof(int32_t) * unnz : 0),
                  o_bmax = ls.take(sizeof(int32_t) * kValidateBlocks);
     if ((st = alloc_block(&p->mem, &p->mem_bytes, lp.bytes))) return st;
     ScratchBlock scratch;
@@ -1067,7 +1115,11 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     p->parts = reinterpret_cast<SplitPart *>(pm + o_parts);
     p->partials = reinterpret_cast<double *>(pm + o_partials);
     p->tile_row = reinterpret_cast<int32_t *>(pm + o_tiles);
+    p->cold_marked = mark;
+    int32_t *marked = mark ? reinterpret_cast<int32_t *>(sm + o_marked) : nullptr;
     int32_t *bad = reinterpret_cast<int32_t *>(sm + o_flags);
+    uint32_t *heat_hist = reinterpret_cast<uint32_t *>(sm + o_flags + kFlagBytes);
+    uint32_t *hot_heat = heat_hist + kHeatLevels;
     Moments *moments = reinterpret_cast<Moments *>(sm + o_mom);
     Summary *summary = reinterpret_cast<Summary *>(sm + o_sum);
     uint64_t *kb0 = reinterpret_cast<uint64_t *>(sm + o_kb0);
@@ -1082,14 +1134,15 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     int32_t *blockmax = reinterpret_cast<int32_t *>(sm + o_bmax);
 
     TraceRange phase("partition: validate + walks");
-    if ((st = hip_status(hipMemsetAsync(bad, 0, 2 * sizeof(int32_t), s)))) return st;
-    if ((st = validate_csr(csr, bad, nodeinfo, blockmax, s))) return st;
+    if ((st = hip_status(hipMemsetAsync(bad, 0, kFlagBytes + kHistBytes, s)))) return st;
+    if ((st = validate_csr(csr, bad, nodeinfo, blockmax, mark ? heat_hist : nullptr, s))) return st;
+    if (mark) hipLaunchKernelGGL(hot_heat_kernel, dim3(1), dim3(64), 0, s, heat_hist, kHotRows, hot_heat);
     int2 *succ = nullptr;
-    if (use_succ && nnz > 0) {
-        succ = reinterpret_cast<int2 *>(sm + o_succ);
+    if ((use_succ || mark) && nnz > 0) {
+        if (use_succ) succ = reinterpret_cast<int2 *>(sm + o_succ);
         const int64_t sblocks = std::min<int64_t>((nnz + kThreads - 1) / kThreads, 65536);
         hipLaunchKernelGGL(successor_kernel, dim3(static_cast<unsigned>(sblocks)), dim3(kThreads), 0,
-                           s, nodeinfo, csr->col, n, nnz, succ);
+                           s, nodeinfo, csr->col, n, nnz, succ, hot_heat, marked);
     }
     if (S_host) {
         // the density sums of a saved plan of this matrix: no walks
@@ -1264,23 +1317,30 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if (!pin) return DUALGCN_ERR_OOM;
     if ((st = hip_status(hipMemcpyAsync(pin, dsum, sizeof(SplitSummary), hipMemcpyDeviceToHost, s))))
         return st;
-    {
-        hipEvent_t done = nullptr;    // the scratch block's last use
-        if ((st = hip_status(hipEventCreateWithFlags(&done, hipEventDisableTiming)))) return st;
-        if ((st = hip_status(hipEventRecord(done, s)))) {
+    // the scratch block's last use: before the sorted copy, unless the copy reads the
+    // marked columns from it (then host wait 2 also waits for the copy); until it is
+    // recorded, an early return waits for the whole stream before releasing the block
+    auto record_done = [&]() -> int {
+        hipEvent_t done = nullptr;
+        int rs = hip_status(hipEventCreateWithFlags(&done, hipEventDisableTiming));
+        if (rs) return rs;
+        if ((rs = hip_status(hipEventRecord(done, s)))) {
             (void)hipEventDestroy(done);
-            return st;
+            return rs;
         }
         scratch.done = done;
-    }
+        return DUALGCN_OK;
+    };
+    if (!marked && (st = record_done())) return st;
     if (nnz > 0) {
         const unsigned grid_e = static_cast<unsigned>((nnz + kCopyTile - 1) / kCopyTile);
         hipLaunchKernelGGL(tile_row_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, p->tile_row);
         hipLaunchKernelGGL(sorted_copy_kernel, dim3(grid_e), dim3(kThreads), 0, s, p->order,
-                           csr->rowptr, csr->col, csr->val, p->pptr, p->tile_row, n, nnz, p->pcol,
-                           p->pval);
+                           csr->rowptr, marked ? marked : csr->col, csr->val, p->pptr, p->tile_row,
+                           n, nnz, p->pcol, p->pval);
         if ((st = hip_status(hipGetLastError()))) return st;
     }
+    if (marked && (st = record_done())) return st;
     // every use of the plan's sorted copy waits for this event (its stream, or any other)
     if ((st = hip_status(hipEventCreateWithFlags(&p->ready, hipEventDisableTiming)))) return st;
     if ((st = hip_status(hipEventRecord(p->ready, s)))) return st;

@@ -124,6 +124,7 @@ struct Args {
     double *partials;
     const float *X;
     void *Y;                    // float32, or bfloat16 when the kernel's BF is set (fused: H or null)
+    uint32_t x_bytes;           // bytes of X that gathers may read (cache-class loads)
     int32_t n, n_sparse, n_tasks, n_parts, n_long;
     int32_t ld;                 // leading dimension of X and Y (= F)
     int32_t f0;                 // first feature of this launch window
@@ -189,9 +190,18 @@ struct StageRows {
     }
 };
 
+// Cache classes of the gathers (kernels instantiated with CP): a gathered row is read
+// with the default policy when its column is among the hottest (rows the L2s keep), and
+// non-temporal otherwise, so that rows read a few times per launch do not push the hot
+// rows out of the L2.  The plan marks the other columns with bit 31 of the sorted copy's
+// column (a column is below 2^31 - 1, so a marked one never reads as the invalid -1);
+// every kernel masks it off, and it never changes which row is read.
+constexpr int kCpolNt = 2;                    // the nt field of a gfx950 buffer load
+constexpr uint32_t kRowMask = 0x7FFFFFFFu;
+
 // Entries [e, min(e + kRound, e_end)) of the sorted copy, as seen by lane li of a
 // group whose first lane is gbase: lane li loads entries e + li + k LPR; entry u is
-// then held by lane u % LPR in register u / LPR.
+// then held by lane u % LPR in register u / LPR.  An invalid entry holds column -1.
 template <int LPR>
 struct Round {
     static constexpr int EPL = (kRound + LPR - 1) / LPR;   // entries per lane
@@ -210,28 +220,61 @@ struct Round {
     }
 };
 
+template <int POLICY>
+__device__ __forceinline__ void load_x_cp(__amdgpu_buffer_rsrc_t rx, uint32_t off, float (&x)[4]) {
+    const f32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, POLICY);
+    x[0] = v[0];
+    x[1] = v[1];
+    x[2] = v[2];
+    x[3] = v[3];
+}
+
 // Requests the kRound neighbour slices of a round (invalid entries read nothing and
 // get weight zero).
-template <int LPR, int VEC>
+// The broadcasts read lane gbase + u % LPR with ds_bpermute: the group's base byte
+// address is hidden from the optimiser, so that the constant u % LPR lanes go into the
+// instruction's offset field instead of one precomputed address register per u
+// (sixteen registers held through the whole kernel otherwise).
+template <int LPR, int VEC, bool CP>
 __device__ __forceinline__ void gather(const Args &a, const Round<LPR> &r, int gbase, int f,
                                        bool fin, float (&as)[kRound], float (&xs)[kRound][VEC]) {
+    static_assert(!CP || VEC == 4, "cache classes need 16-byte loads");
+    int base4 = gbase * 4;
+    asm volatile("" : "+v"(base4));
 #pragma unroll
     for (int u = 0; u < kRound; ++u) {
-        const int32_t cc = __shfl(r.c[u / LPR], gbase + u % LPR, 64);
-        as[u] = __shfl(r.v[u / LPR], gbase + u % LPR, 64);
-        if (cc >= 0 && fin) {
-            load_x<VEC>(a.X + static_cast<int64_t>(cc) * a.ld + f, xs[u]);
-        } else {
-            as[u] = 0.f;
+        const int src = base4 + (u % LPR) * 4;
+        const int32_t cc = __builtin_amdgcn_ds_bpermute(src, r.c[u / LPR]);
+        as[u] = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(r.v[u / LPR])));
+        if constexpr (CP) {
+            if (cc != -1 && fin) {
+                // the host checked that n ld 4 bytes fit the 32-bit range of the buffer
+                const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<float *>(a.X), 0, static_cast<int>(a.x_bytes), 0x00020000);
+                const uint32_t row = static_cast<uint32_t>(cc) & kRowMask;
+                const uint32_t off = (row * static_cast<uint32_t>(a.ld) + static_cast<uint32_t>(f)) * 4u;
+                if (cc >= 0) load_x_cp<0>(rx, off, xs[u]);
+                else load_x_cp<kCpolNt>(rx, off, xs[u]);      // a marked (cold) column
+            } else {
+                as[u] = 0.f;
 #pragma unroll
-            for (int j = 0; j < VEC; ++j) xs[u][j] = 0.f;
+                for (int j = 0; j < VEC; ++j) xs[u][j] = 0.f;
+            }
+        } else {
+            if (cc != -1 && fin) {
+                load_x<VEC>(a.X + static_cast<int64_t>(static_cast<uint32_t>(cc) & kRowMask) * a.ld + f, xs[u]);
+            } else {
+                as[u] = 0.f;
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) xs[u][j] = 0.f;
+            }
         }
     }
 }
 
 // Dense path: one wavefront accumulates entries [e0, e1) of one row; on return every
 // lane holds the row's sums for its features (groups reduced by a butterfly).
-template <int LPR, int VEC>
+template <int LPR, int VEC, bool CP>
 __device__ __forceinline__ void dense_row(const Args &a, int32_t e0, int32_t e1, int li, int gw,
                                           int gbase, int f, bool fin, double (&tot)[VEC]) {
     constexpr int GPW = 64 / LPR;
@@ -241,7 +284,7 @@ __device__ __forceinline__ void dense_row(const Args &a, int32_t e0, int32_t e1,
         Round<LPR> r;
         r.load(a, e, e1, li);
         float as[kRound], xs[kRound][VEC];
-        gather<LPR, VEC>(a, r, gbase, f, fin, as, xs);
+        gather<LPR, VEC, CP>(a, r, gbase, f, fin, as, xs);
         float acc[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
@@ -270,7 +313,7 @@ __device__ __forceinline__ int32_t task_meta(const int32_t (&m)[N], int j, int g
 
 // The work of logical workgroup lb (feature slice `slice`) for wavefront `wave` of a
 // workgroup of WAVES wavefronts; finished rows go to `emit`.
-template <int LPR, int VEC, int WAVES, class Emit>
+template <int LPR, int VEC, int WAVES, bool CP, class Emit>
 __device__ __forceinline__ void spmm_block(const Args &a, int lb, int slice, int wave,
                                            const Emit &emit) {
     constexpr int GPW = 64 / LPR;                 // lane groups per wavefront
@@ -297,7 +340,7 @@ __device__ __forceinline__ void spmm_block(const Args &a, int lb, int slice, int
             Round<LPR> r;
             r.load(a, e, e1, li);
             float as[kRound], xs[kRound][VEC];
-            gather<LPR, VEC>(a, r, gbase, f, fin, as, xs);
+            gather<LPR, VEC, CP>(a, r, gbase, f, fin, as, xs);
             float acc[VEC];
 #pragma unroll
             for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
@@ -332,7 +375,7 @@ __device__ __forceinline__ void spmm_block(const Args &a, int lb, int slice, int
             if (e1 - e0 > kDenseChunk) return;     // covered by its parts
         }
         double tot[VEC];
-        dense_row<LPR, VEC>(a, e0, e1, li, gw, gbase, f, fin, tot);
+        dense_row<LPR, VEC, CP>(a, e0, e1, li, gw, gbase, f, fin, tot);
         if (part < 0) {
             if (gw == 0) emit.row(a.perm[i], 0, tot, f, fin);
             return;
@@ -381,7 +424,7 @@ __device__ __forceinline__ void spmm_block(const Args &a, int lb, int slice, int
         Round<LPR> r;
         r.load(a, e, e_end, li);
         float as[kRound], xs[kRound][VEC];
-        gather<LPR, VEC>(a, r, gbase, f, fin, as, xs);
+        gather<LPR, VEC, CP>(a, r, gbase, f, fin, as, xs);
 #pragma unroll
         for (int u = 0; u < kRound; ++u) {
 #pragma unroll
@@ -409,10 +452,10 @@ __device__ __forceinline__ void spmm_block(const Args &a, int lb, int slice, int
     }
 }
 
-template <int LPR, int VEC, bool BF>
+template <int LPR, int VEC, bool BF, bool CP>
 __global__ __launch_bounds__(kThreads) void spmm_dual_kernel(const Args a) {
     const StoreRows<VEC, BF> emit{a.Y, a.ld, a.relu != 0};
-    spmm_block<LPR, VEC, kWaves>(a, static_cast<int>(blockIdx.x) / a.S,
+    spmm_block<LPR, VEC, kWaves, CP>(a, static_cast<int>(blockIdx.x) / a.S,
                                  static_cast<int>(blockIdx.x) % a.S,
                                  static_cast<int>(threadIdx.x) >> 6, emit);
 }
@@ -450,6 +493,13 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Args a) {
 //
 // MFMA 16x16x32 operands (l = lane): A row l % 16 and B column l % 16, eight
 // consecutive k of group l / 16; D rows 4 (l / 16) + j, j < 4, column l % 16.
+//
+// Occupancy.  A wavefront loads its A fragments of a 16-row tile into registers before
+// the tile's products, so the tile's LDS rows are free while its results are staged:
+// when a 16-row tile of bfloat16 rows is at least as large as the output staging
+// (K >= 128), the staging lives in the tile.  At K = 128, N = 64 that takes a workgroup
+// from 51 to 35 KiB of LDS, and the kernel is compiled for 4 wavefronts per SIMD
+// (at most 128 registers), so four workgroups share a CU instead of three.
 constexpr int kXwPad = 8;                     // bfloat16 padding per LDS row
 constexpr int kXwBlocksPerGroup = 8;          // logical workgroups per launched workgroup
 constexpr int kXwStageLd = 68;                // floats per staged output row (64 + padding)
@@ -461,16 +511,23 @@ struct XwTile {
     static constexpr int kRows = kSlots < 16 ? 16 : kSlots; // rows of its LDS tile
 };
 
+// Does a 16-row tile of bfloat16 rows K + kXwPad apart hold a wavefront's output staging?
+__host__ __device__ constexpr bool xw_stage_in_tile(int K) {
+    return (K + kXwPad) * 2 >= kXwStageLd * 4;
+}
+
 size_t xw_lds_bytes(int lpr, int K, int N) {
     const int slots = (64 / lpr) * kTaskRows;
     const size_t rows = slots < 16 ? 16 : slots;
     const size_t ld = static_cast<size_t>(K) + kXwPad;
     return (static_cast<size_t>(N) + kWaves * rows) * ld * sizeof(unsigned short) +
-           kWaves * rows * sizeof(int32_t) + static_cast<size_t>(kWaves) * kXwStageWords * sizeof(float);
+           kWaves * rows * sizeof(int32_t) +
+           (xw_stage_in_tile(K) ? 0 : static_cast<size_t>(kWaves) * kXwStageWords * sizeof(float));
 }
 
-template <int LPR>
-__global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const float *__restrict__ W,
+template <int LPR, bool CP>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void spmm_xw_kernel(const Args a, const float *__restrict__ W,
                                                            float *__restrict__ T, int32_t K,
                                                            int32_t N, int32_t nblocks) {
     constexpr int ROWS = XwTile<LPR>::kRows;
@@ -482,8 +539,9 @@ __global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const f
     unsigned short *wt = xw_lds;                                   // [N][ld]: W^T in bfloat16
     unsigned short *h = xw_lds + (N + wave * ROWS) * ld;           // this wavefront's rows
     int32_t *outs = reinterpret_cast<int32_t *>(xw_lds + (N + kWaves * ROWS) * ld) + wave * ROWS;
-    float *stage = reinterpret_cast<float *>(reinterpret_cast<int32_t *>(xw_lds + (N + kWaves * ROWS) * ld) +
-                                             kWaves * ROWS) + wave * kXwStageWords;
+    const bool stage_in_tile = xw_stage_in_tile(K);
+    float *stage_own = reinterpret_cast<float *>(reinterpret_cast<int32_t *>(xw_lds + (N + kWaves * ROWS) * ld) +
+                                                 kWaves * ROWS) + wave * kXwStageWords;
     for (int idx = static_cast<int>(threadIdx.x); idx < K * N; idx += kThreads) {
         const int c = idx / N, j = idx % N;   // consecutive threads read consecutive columns
         wt[j * ld + c] = to_bf16(W[idx]);
@@ -492,11 +550,16 @@ __global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const f
     __syncthreads();
 
     const StageRows emit{h, outs, ld, a.relu != 0, lane % LPR == 0, static_cast<unsigned short *>(a.Y), a.ld};
-    const int lrow = lane & 15, kgrp = lane >> 4;
-    const int sr = lane >> 4, sc = (lane & 15) * 4;        // first staged row and the columns a lane stores
+    constexpr int KF = LPR / 8;               // A fragments of a row: K <= 4 LPR, 32 k each
     for (int lb = static_cast<int>(blockIdx.x); lb < nblocks; lb += static_cast<int>(gridDim.x)) {
-        spmm_block<LPR, 4, kWaves>(a, lb, 0, wave, emit);
+        spmm_block<LPR, 4, kWaves, CP>(a, lb, 0, wave, emit);
         __syncwarp();
+        // the lane's MFMA coordinates, recomputed here (hidden from the optimiser) rather
+        // than held in registers through the aggregation
+        int ln = static_cast<int>(threadIdx.x) & 63;
+        asm volatile("" : "+v"(ln));
+        const int lrow = ln & 15, kgrp = ln >> 4;
+        const int sr = ln >> 4, sc = (ln & 15) * 4;        // first staged row and the columns a lane stores
 #pragma unroll
         for (int rt = 0; rt < ROWS / 16; ++rt) {
             if (__ballot(outs[rt * 16 + lrow] >= 0) == 0) continue;   // no row in this tile
@@ -504,16 +567,23 @@ __global__ __launch_bounds__(kThreads) void spmm_xw_kernel(const Args a, const f
 #pragma unroll
             for (int q = 0; q < 4; ++q) orow[q] = outs[rt * 16 + sr + 4 * q];
             const unsigned short *hrow = h + (rt * 16 + lrow) * ld + kgrp * 8;
+            u16x8 afrag[KF];
+#pragma unroll
+            for (int q = 0; q < KF; ++q)
+                afrag[q] = q * 32 < K ? *reinterpret_cast<const u16x8 *>(hrow + q * 32) : u16x8{};
+            __syncwarp();
+            float *stage = stage_in_tile ? reinterpret_cast<float *>(h + rt * 16 * ld) : stage_own;
             // one 16-column tile of T at a time (the k order of each tile is the update's),
             // staged in LDS and stored 64 columns at a time: each store instruction writes
             // four whole 256-byte row pieces (16 lanes x 16 bytes each)
             for (int t = 0; t < ntiles; ++t) {
                 const unsigned short *wrow = wt + (t * 16 + lrow) * ld + kgrp * 8;
                 f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-                for (int kk = 0; kk < K; kk += 32) {
-                    const u16x8 a16 = *reinterpret_cast<const u16x8 *>(hrow + kk);
-                    const u16x8 b16 = *reinterpret_cast<const u16x8 *>(wrow + kk);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a16),
+#pragma unroll
+                for (int q = 0; q < KF; ++q) {
+                    if (q * 32 >= K) break;
+                    const u16x8 b16 = *reinterpret_cast<const u16x8 *>(wrow + q * 32);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, afrag[q]),
                                                                   __builtin_bit_cast(bf16x8, b16), acc,
                                                                   0, 0, 0);
                 }
@@ -592,13 +662,13 @@ int64_t schedule_blocks(Args &a) {
     return static_cast<int64_t>(a.nb_parts) + a.nb_dense + nb_sparse;
 }
 
-template <int LPR>
+template <int LPR, bool CP>
 int launch_xw_window(Args a, const float *W, float *T, int32_t K, int32_t N, hipStream_t s) {
     const int64_t blocks = schedule_blocks<LPR>(a);
     if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
     if (blocks > 0) {
         const size_t lds = xw_lds_bytes(LPR, K, N);
-        const void *kern = reinterpret_cast<const void *>(&spmm_xw_kernel<LPR>);
+        const void *kern = reinterpret_cast<const void *>(&spmm_xw_kernel<LPR, CP>);
         if (lds > 64 * 1024) {
             const int st = hip_status(hipFuncSetAttribute(
                 kern, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
@@ -611,7 +681,7 @@ int launch_xw_window(Args a, const float *W, float *T, int32_t K, int32_t N, hip
         const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(2048 / kThreads, (160 * 1024) / lds));
         const int64_t grid = std::min<int64_t>(
             blocks, std::max<int64_t>(per_cu * device_cus(), (blocks + kXwBlocksPerGroup - 1) / kXwBlocksPerGroup));
-        hipLaunchKernelGGL((spmm_xw_kernel<LPR>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
+        hipLaunchKernelGGL((spmm_xw_kernel<LPR, CP>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
                            lds, s, a, W, T, K, N, static_cast<int32_t>(blocks));
     }
     if (a.n_parts > 0)
@@ -620,16 +690,16 @@ int launch_xw_window(Args a, const float *W, float *T, int32_t K, int32_t N, hip
     return hip_status(hipGetLastError());
 }
 
-template <int LPR, int VEC>
+template <int LPR, int VEC, bool CP = false>
 int launch_window(Args a, bool bf, hipStream_t s) {
     const int64_t blocks = schedule_blocks<LPR>(a) * a.S;
     if (blocks == 0) return DUALGCN_OK;
     if (blocks > 0x7FFFFFFF) return DUALGCN_ERR_UNSUPPORTED;
     if (bf)
-        hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC, true>), dim3(static_cast<unsigned>(blocks)),
+        hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC, true, CP>), dim3(static_cast<unsigned>(blocks)),
                            dim3(kThreads), 0, s, a);
     else
-        hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC, false>), dim3(static_cast<unsigned>(blocks)),
+        hipLaunchKernelGGL((spmm_dual_kernel<LPR, VEC, false, CP>), dim3(static_cast<unsigned>(blocks)),
                            dim3(kThreads), 0, s, a);
     if (a.n_parts > 0) {
         if (bf)
@@ -675,6 +745,28 @@ int long_row_class(int lpr) {
     return cls;
 }
 
+// Cache classes of a launch's gathers (the plan marks every column outside the hottest
+// kHotRows; classes apply from operands larger than the 256 MiB memory-side cache, below
+// which non-temporal loads would only lose rows that cache holds).  Measured on R-MAT
+// graphs with shuffled ids (c5: n = 2^22, 67M entries; c4: n = 2^21, 63M entries),
+// F = 128: the layer-1 aggregation fused with the next update 4.27 -> 4.03 ms (c5) and
+// 3.72 -> 3.45 ms (c4), the plain SpMM 4.46 -> 4.24 and 3.70 -> 3.47 ms; the L2 hit rate of
+// the fused kernel rose from 22.5% to 27.5% and its fetched bytes fell by 6%.  Hot sets of
+// 16 MiB or less, or a third class loading warm rows with sc0, were slower.
+
+// Sets the class fields of `a` for gathers of w features of rows ld apart and returns
+// true when the launch should use them: the plan marked its cold columns, rows are read
+// whole with 16-byte loads, the operand fits the 32-bit offsets of a buffer load, and it
+// is larger than the memory-side cache.
+bool gather_classes(const Plan &p, int32_t ld, int32_t w, bool vec, Args &a) {
+    if (!vec || !p.cold_marked) return false;
+    const uint64_t bytes = static_cast<uint64_t>(p.n) * static_cast<uint64_t>(ld) * sizeof(float);
+    const uint64_t row_bytes = static_cast<uint64_t>(w) * sizeof(float);
+    if (bytes > 0xFFFFFFFFull || static_cast<uint64_t>(p.n) * row_bytes <= kGatherClassMinBytes) return false;
+    a.x_bytes = static_cast<uint32_t>(bytes);
+    return true;
+}
+
 }  // namespace
 
 size_t spmm_xw_lds_bytes(int32_t F_in, int32_t F_out) {
@@ -707,11 +799,16 @@ int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, void
     a.S = 1;
     const int lpr = window_lpr(F_in);
     a.n_long = p.n_long[long_row_class(lpr)];
+    const bool cp = gather_classes(p, F_in, F_in, true, a);
     int st = DUALGCN_ERR_UNSUPPORTED;
-    if (lpr == 8) st = launch_xw_window<8>(a, W, T, F_in, F_out, s);
-    else if (lpr == 16) st = launch_xw_window<16>(a, W, T, F_in, F_out, s);
-    else if (lpr == 32) st = launch_xw_window<32>(a, W, T, F_in, F_out, s);
-    else if (lpr == 64) st = launch_xw_window<64>(a, W, T, F_in, F_out, s);
+    if (lpr == 8) st = cp ? launch_xw_window<8, true>(a, W, T, F_in, F_out, s)
+                          : launch_xw_window<8, false>(a, W, T, F_in, F_out, s);
+    else if (lpr == 16) st = cp ? launch_xw_window<16, true>(a, W, T, F_in, F_out, s)
+                                : launch_xw_window<16, false>(a, W, T, F_in, F_out, s);
+    else if (lpr == 32) st = cp ? launch_xw_window<32, true>(a, W, T, F_in, F_out, s)
+                                : launch_xw_window<32, false>(a, W, T, F_in, F_out, s);
+    else if (lpr == 64) st = cp ? launch_xw_window<64, true>(a, W, T, F_in, F_out, s)
+                                : launch_xw_window<64, false>(a, W, T, F_in, F_out, s);
     if (st) return st;
     return note_use(p, s);
 }
@@ -733,13 +830,15 @@ int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bo
             // groups under 32 lanes hand rows from a lower length bound to wavefronts
             a.S = 1;
             a.n_long = p.n_long[long_row_class(window_lpr(w))];
+            // cache classes for the widths whose rows fill whole 128-byte lines
+            const bool cp = w > 16 && gather_classes(p, F, w, true, a);
             if (w <= 4) st = launch_window<1, 4>(a, bf, s);
             else if (w <= 8) st = launch_window<2, 4>(a, bf, s);
             else if (w <= 16) st = launch_window<4, 4>(a, bf, s);
-            else if (w <= 32) st = launch_window<8, 4>(a, bf, s);
-            else if (w <= 64) st = launch_window<16, 4>(a, bf, s);
-            else if (w <= 128) st = launch_window<32, 4>(a, bf, s);
-            else st = launch_window<64, 4>(a, bf, s);
+            else if (w <= 32) st = cp ? launch_window<8, 4, true>(a, bf, s) : launch_window<8, 4>(a, bf, s);
+            else if (w <= 64) st = cp ? launch_window<16, 4, true>(a, bf, s) : launch_window<16, 4>(a, bf, s);
+            else if (w <= 128) st = cp ? launch_window<32, 4, true>(a, bf, s) : launch_window<32, 4>(a, bf, s);
+            else st = cp ? launch_window<64, 4, true>(a, bf, s) : launch_window<64, 4>(a, bf, s);
         } else {
             // any other width or alignment: one feature per lane, 64-feature slices
             a.S = (w + 63) / 64;

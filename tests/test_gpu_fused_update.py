@@ -65,7 +65,7 @@ def _two_calls(dg, plan, Xd, Wd, relu):
 @pytest.mark.parametrize("name", sorted(GRAPHS))
 @pytest.mark.parametrize("F_in,F_out,relu", [(128, 64, True), (64, 32, False), (32, 32, True),
                                              (256, 64, True), (96, 160, False), (128, 256, True),
-                                             (256, 192, False)])
+                                             (256, 192, False), (256, 224, True)])
 def test_fused_equals_two_calls_and_oracle(dg, device, name, F_in, F_out, relu):
     g = _graph(name)
     plan = dg.Plan(*to_dev(g, device), seed=3, walks_per_node=8, walk_len=4)
@@ -135,7 +135,8 @@ def test_fused_argument_checks(dg, device):
     assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 128, 48, 0, None) == dg.ERR_UNSUPPORTED
     assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 288, 64, 0, None) == dg.ERR_UNSUPPORTED
     assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 256, 256, 0, None) == dg.ERR_UNSUPPORTED
-    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 256, 224, 0, None) == dg.ERR_UNSUPPORTED
+    # W^T (224 x 264 bfloat16) and the row tiles fit, with the output staging inside the tile
+    assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr(), None, 256, 224, 0, None) == 0
     assert call(h, X.data_ptr() + 4, W.data_ptr(), T.data_ptr(), None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
     assert call(h, X.data_ptr(), W.data_ptr(), T.data_ptr() + 4, None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
     assert call(h, X.data_ptr(), W.data_ptr(), X.data_ptr(), None, 128, 64, 0, None) == dg.ERR_INVALID_ARG
