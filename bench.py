@@ -71,6 +71,13 @@ def fused_bytes(n, nnz, F_in, F_out):
     return 4 * (n + 1) + 8 * nnz + 4 * n * F_in + 4 * n * F_out + 4 * n
 
 
+def gather_classes(info, n, F):
+    """Does an SpMM of F-wide rows on this plan read cold rows non-temporally?  The
+    library's rule: the plan marked its cold columns, the rows fill whole lines (F > 16),
+    and the operand is larger than the 256 MiB memory-side cache and below 4 GiB."""
+    return bool(info.get("cold_marked")) and F > 16 and 4 * n * F <= 0xFFFFFFFF and 4 * n * F > (256 << 20)
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
@@ -713,18 +720,19 @@ def main():
     ge_per_step = g.nnz * (sum(fo for _, fo in w.layers) if w.is_gcn else w.F)
     value = ge_per_step / (ms_per_step * 1e-3) / 1e9
     lpr = min(64, max(1, 1 << max(0, (F_dom - 1).bit_length() - 2)))
+    cp = "true" if gather_classes(info, g.n, F_dom) else "false"
     if fused:
         # the dominant kernel is layer 1's aggregation with layer 2's update fused in: it
         # writes T (float32, F_next wide) instead of the layer's output
         F_next = w.layers[1][1]
         out_bytes = 4 * g.n * F_next
         bmin = fused_bytes(g.n, g.nnz, F_dom, F_next)
-        kname = f"spmm_xw_kernel<{lpr}>"
+        kname = f"spmm_xw_kernel<{lpr}, {cp}>"
         kdesc = f"{kname} (F={F_dom} -> {F_next}, ReLU, fused update)"
     else:
         out_bytes = (2 if w.is_gcn else 4) * g.n * F_dom   # every layer but the last: bfloat16
         bmin = spmm_bytes(g.n, g.nnz, F_dom, 2 if w.is_gcn else 4)
-        kname = f"spmm_dual_kernel<{lpr}, 4, {'true' if w.is_gcn else 'false'}>"
+        kname = f"spmm_dual_kernel<{lpr}, 4, {'true' if w.is_gcn else 'false'}, {cp}>"
         kdesc = f"{kname} (F={F_dom}{', ReLU, bfloat16 output' if w.is_gcn else ''})"
     achieved = bmin / (spmm_ms * 1e-3) / 1e9
     run_keys = {"graph_sha256": g.sha256()[:16], "F_in": F_dom,

@@ -256,6 +256,13 @@ int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F
  * matrix cores in the update's order --, without reading H back: with H = NULL the
  * n x F_in intermediate never goes through device memory at all.
  *
+ * Route (Sec. 3.3: the execution path follows the data).  The fused kernel pays where
+ * the aggregation is bound by the memory fabric; where the operand fits the memory-side
+ * cache, or the kernel's LDS leaves fewer than three workgroups per CU, the two calls are
+ * faster.  dualgcn_spmm_update_route tells which; when H is given (16-byte aligned) this
+ * call takes the faster route itself, with H as the intermediate.  With H = NULL it
+ * always runs the fused kernel.  Either route writes the same T (and H).
+ *
  * X is float32 n x F_in row-major (16-byte aligned), W float32 F_in x F_out row-major
  * (rounded to bfloat16 as in dualgcn_update), T float32 n x F_out row-major (16-byte
  * aligned), overlapping neither X nor W.  H is NULL, or bfloat16 n x F_in row-major
@@ -268,6 +275,13 @@ int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F
  */
 int dualgcn_spmm_update(const dualgcn_plan *plan, const float *X, const float *W, float *T,
                         void *H, int32_t F_in, int32_t F_out, uint32_t flags, void *stream);
+
+/* Host-only: *fused = 1 when the fused kernel of dualgcn_spmm_update is the faster route
+ * for this plan and shape (the operand n x F_in float32 exceeds the 256 MiB memory-side
+ * cache and at least three workgroups fit a CU), 0 when the two calls are.  Shape limits
+ * and status as for dualgcn_spmm_update; *fused is left unchanged on error. */
+int dualgcn_spmm_update_route(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,
+                              int32_t *fused);
 
 /* Bytes of device workspace dualgcn_gcn_layer needs (host-only, no device use):
  * room for the float32 n x F_out product T. */
@@ -458,6 +472,10 @@ typedef struct dualgcn_plan_info {
     int32_t n_long_rows;     /* dense rows of >= 512 entries (a wavefront each; the
                                 shorter dense rows get a lane group each; for F <= 64
                                 the bound is 256, for F <= 32 128, for F <= 16 64) */
+    int32_t cold_marked;     /* 1 when the plan marks the columns outside the hottest
+                                65,536 (plans of more than 2^18 nodes): an SpMM whose
+                                operand is larger than 256 MiB and smaller than 4 GiB then
+                                gathers their rows with non-temporal loads (same results) */
 } dualgcn_plan_info;
 
 /* Fills *out from host-side copies kept in the plan (no device use). */

@@ -59,7 +59,8 @@ class PlanInfo(ctypes.Structure):
                 ("walks_per_node", ctypes.c_uint32), ("walk_len", ctypes.c_uint32),
                 ("max_degree", ctypes.c_int32), ("dense_chunk", ctypes.c_int32),
                 ("n_split_rows", ctypes.c_int32), ("n_split_parts", ctypes.c_int32),
-                ("n_tasks", ctypes.c_int32), ("n_long_rows", ctypes.c_int32)]
+                ("n_tasks", ctypes.c_int32), ("n_long_rows", ctypes.c_int32),
+                ("cold_marked", ctypes.c_int32)]
 
 
 def _load():
@@ -77,6 +78,7 @@ def _load():
         "dualgcn_spmm": ([P, P, P, I32, P], ctypes.c_int),
         "dualgcn_spmm_act": ([P, P, P, I32, U32, P], ctypes.c_int),
         "dualgcn_spmm_update": ([P, P, P, P, P, I32, I32, U32, P], ctypes.c_int),
+        "dualgcn_spmm_update_route": ([P, I32, I32, P], ctypes.c_int),
         "dualgcn_update": ([P, P, P, I32, I32, I32, U32, P], ctypes.c_int),
         "dualgcn_gcn_layer_workspace": ([P, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "dualgcn_gcn_layer": ([P, P, P, P, I32, I32, U32, P, SZ, P], ctypes.c_int),
@@ -264,11 +266,20 @@ def update(X, W, T=None, stream=None):
     return T
 
 
+def spmm_update_route(plan, F_in, F_out):
+    """True when the fused kernel is the faster route of spmm_update on this plan and shape."""
+    fused = ctypes.c_int32()
+    _check(_lib.dualgcn_spmm_update_route(plan.handle, F_in, F_out, ctypes.byref(fused)),
+           "dualgcn_spmm_update_route")
+    return bool(fused.value)
+
+
 def spmm_update(plan, X, W, T=None, relu=False, H=None, stream=None):
     """T = bf16(act(A X)) bf16(W) (float32 accumulation): the aggregation of one layer fused
     with the next layer's update.  X: float32 [n, F_in], W: float32 [F_in, F_out],
-    T: float32 [n, F_out].  H: None (act(A X) is not stored), or a bfloat16 [n, F_in]
-    tensor that receives bf16(act(A X))."""
+    T: float32 [n, F_out].  H: None (act(A X) is not kept), or a bfloat16 [n, F_in]
+    tensor that receives bf16(act(A X)).  Where the library's two-call route is the faster
+    one and no H is given, a temporary H is allocated for it (the same T either way)."""
     _dev(X, torch.float32, "X")
     _dev(W, torch.float32, "W")
     if X.dim() != 2 or X.shape[0] != plan.n:
@@ -287,6 +298,8 @@ def spmm_update(plan, X, W, T=None, relu=False, H=None, stream=None):
         if H.shape != (plan.n, F_in):
             raise ValueError("H must be [n, F_in]")
         hp = H.data_ptr()
+    elif not spmm_update_route(plan, F_in, F_out):
+        hp = torch.empty((plan.n, F_in), dtype=torch.bfloat16, device=X.device).data_ptr()
     _check(_lib.dualgcn_spmm_update(plan.handle, X.data_ptr(), W.data_ptr(), T.data_ptr(), hp,
                                     F_in, F_out, RELU if relu else 0, _stream(stream)),
            "dualgcn_spmm_update")

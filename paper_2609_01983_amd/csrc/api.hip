@@ -330,8 +330,26 @@ int dualgcn_spmm_update(const dualgcn_plan *plan, const float *X, const float *W
             return DUALGCN_ERR_INVALID_ARG;
     }
     if ((st = dgc::device_status())) return st;
-    return dgc::launch_spmm_xw(*p, X, W, T, H, F_in, F_out, (flags & DUALGCN_RELU) != 0,
-                               static_cast<hipStream_t>(stream));
+    const bool relu = (flags & DUALGCN_RELU) != 0;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (H && reinterpret_cast<uintptr_t>(H) % 16 == 0 && !dgc::fused_junction_pays(*p, F_in, F_out)) {
+        // the two calls are faster here, and H holds their intermediate: the same bits
+        if ((st = dgc::launch_spmm(*p, X, H, F_in, relu, true, s))) return st;
+        return dgc::launch_xw(H, true, W, T, p->n, F_in, F_out, s);
+    }
+    return dgc::launch_spmm_xw(*p, X, W, T, H, F_in, F_out, relu, s);
+}
+
+int dualgcn_spmm_update_route(const dualgcn_plan *plan, int32_t F_in, int32_t F_out,
+                              int32_t *fused) {
+    int st = check_plan(plan);
+    if (st) return st;
+    if (!fused || F_in < 1 || F_out < 1) return DUALGCN_ERR_INVALID_ARG;
+    if (F_in % 32 || F_out % 32 || F_in > 256 || F_out > 256 ||
+        dgc::spmm_xw_lds_bytes(F_in, F_out) > 160 * 1024)
+        return DUALGCN_ERR_UNSUPPORTED;
+    *fused = dgc::fused_junction_pays(*as_plan(plan), F_in, F_out) ? 1 : 0;
+    return DUALGCN_OK;
 }
 
 int dualgcn_update(const void *X, const float *W, float *T, int32_t n, int32_t F_in,
@@ -502,6 +520,7 @@ int dualgcn_plan_query(const dualgcn_plan *plan, dualgcn_plan_info *out) {
     i.n_split_parts = p->n_split_parts;
     i.n_tasks = p->n_tasks;
     i.n_long_rows = p->n_long[0];
+    i.cold_marked = p->cold_marked ? 1 : 0;
     *out = i;
     return DUALGCN_OK;
 }

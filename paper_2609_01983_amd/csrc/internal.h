@@ -198,6 +198,9 @@ int launch_spmm_xw(const Plan &p, const float *X, const float *W, float *T, void
                    int32_t F_in, int32_t F_out, bool relu, hipStream_t stream);
 // LDS bytes a workgroup of launch_spmm_xw takes (at most 160 KiB are supported).
 size_t spmm_xw_lds_bytes(int32_t F_in, int32_t F_out);
+// Is launch_spmm_xw faster than launch_spmm (bfloat16 output) followed by launch_xw on this
+// plan and shape?  (A cost rule from measurements; both routes give the same bits.)
+bool fused_junction_pays(const Plan &p, int32_t F_in, int32_t F_out);
 
 // ---- update phase (xw.hip)
 // Bytes of the float32 T = X W buffer a layer keeps in its workspace (256-byte multiple).

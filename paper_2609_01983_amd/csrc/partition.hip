@@ -26,6 +26,8 @@
 // or reduction order: it is the unique sort of (K_v, v) cut at K*.
 #include "internal.h"
 
+#include <chrono>
+
 #include <algorithm>
 #include <cstring>
 #include <thread>
@@ -142,18 +144,28 @@ __global__ __launch_bounds__(kThreads) void successor_kernel(const int2 *__restr
     }
 }
 
-// *hot_heat = the smallest heat h whose nodes of heat >= h number at most hot_rows (one
-// thread; hist counts the nodes per heat value).
-__global__ void hot_heat_kernel(const uint32_t *__restrict__ hist, uint32_t hot_rows,
-                                uint32_t *__restrict__ hot_heat) {
-    if (threadIdx.x != 0) return;
-    uint32_t hot = kHeatLevels;
-    uint64_t above = 0;
-    for (int h = kHeatLevels - 1; h >= 0 && above + hist[h] <= hot_rows; --h) {
-        above += hist[h];
-        hot = static_cast<uint32_t>(h);
+// *hot_heat = the smallest heat h whose nodes of heat >= h number at most hot_rows
+// (kHeatLevels if even the hottest value has more); hist counts the nodes per heat value.
+// One workgroup of kHeatLevels threads: a suffix sum in LDS, then the smallest qualifying
+// value by an LDS minimum.
+__global__ __launch_bounds__(kHeatLevels) void hot_heat_kernel(const uint32_t *__restrict__ hist,
+                                                               uint32_t hot_rows,
+                                                               uint32_t *__restrict__ hot_heat) {
+    __shared__ uint64_t above[kHeatLevels];
+    __shared__ uint32_t best;
+    const int h = static_cast<int>(threadIdx.x);
+    above[h] = hist[h];
+    if (h == 0) best = kHeatLevels;
+    __syncthreads();
+    for (int d = 1; d < kHeatLevels; d <<= 1) {      // above[h] = sum of hist[h..]
+        const uint64_t add = h + d < kHeatLevels ? above[h + d] : 0;
+        __syncthreads();
+        above[h] += add;
+        __syncthreads();
     }
-    *hot_heat = hot;
+    if (above[h] <= hot_rows) atomicMin(&best, static_cast<uint32_t>(h));
+    __syncthreads();
+    if (h == 0) *hot_heat = best;
 }
 
 // ------------------------------------------------------------------ structure checksum
@@ -787,14 +799,19 @@ struct ScratchBlock {
 
 }  // namespace
 
-// Waits until the work queued on s so far has finished by polling an event: a wait
-// that blocks in the runtime resumes 50-150 us after the last kernel, which the
-// partition's host waits would otherwise add to every build (the GPU idles meanwhile).
+// Waits until an event has completed by polling it: a wait that blocks in the runtime
+// resumes 50-150 us after the last kernel, which the partition's host waits would
+// otherwise add to every build (the GPU idles meanwhile).  Polling stops after
+// kPollLimit (the waits of a build take a few milliseconds at the sizes measured here);
+// a longer wait blocks in the runtime instead of keeping a host core busy.
+constexpr auto kPollLimit = std::chrono::milliseconds(20);
 int wait_event(hipEvent_t e) {
+    const auto t0 = std::chrono::steady_clock::now();
     for (;;) {
         const hipError_t q = hipEventQuery(e);
         if (q == hipSuccess) return DUALGCN_OK;
         if (q != hipErrorNotReady) return hip_status(q);
+        if (std::chrono::steady_clock::now() - t0 > kPollLimit) return hip_status(hipEventSynchronize(e));
         std::this_thread::yield();
     }
 }
@@ -1136,7 +1153,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     TraceRange phase("partition: validate + walks");
     if ((st = hip_status(hipMemsetAsync(bad, 0, kFlagBytes + kHistBytes, s)))) return st;
     if ((st = validate_csr(csr, bad, nodeinfo, blockmax, mark ? heat_hist : nullptr, s))) return st;
-    if (mark) hipLaunchKernelGGL(hot_heat_kernel, dim3(1), dim3(64), 0, s, heat_hist, kHotRows, hot_heat);
+    if (mark) hipLaunchKernelGGL(hot_heat_kernel, dim3(1), dim3(kHeatLevels), 0, s, heat_hist, kHotRows, hot_heat);
     int2 *succ = nullptr;
     if ((use_succ || mark) && nnz > 0) {
         if (use_succ) succ = reinterpret_cast<int2 *>(sm + o_succ);

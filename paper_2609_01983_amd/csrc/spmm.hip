@@ -773,6 +773,21 @@ size_t spmm_xw_lds_bytes(int32_t F_in, int32_t F_out) {
     return xw_lds_bytes(window_lpr(F_in), F_in, F_out);
 }
 
+// The fused junction pays where the aggregation is bound by the memory fabric: the
+// operand is larger than the memory-side cache (then the n x F_in intermediate it never
+// writes or reads back is traffic saved), and the kernel's LDS still lets at least
+// kFusedMinGroups workgroups share a CU.  Measured (F_in -> F_out): R-MAT c4 (n = 2^21)
+// 128 -> 64 fused 3.42 ms against 3.66 ms for the two calls, 64 -> 32 1.76 against 1.85;
+// the SBM c3 (n = 2^18, 128 MiB operand) 0.76 against 0.62 and R-MAT c2 (n = 2^17) 0.33
+// against 0.29; 256 -> 128, where one workgroup fills a CU's LDS, 16.0 against 7.85 ms (c4).
+constexpr int kFusedMinGroups = 3;
+
+bool fused_junction_pays(const Plan &p, int32_t F_in, int32_t F_out) {
+    const size_t lds = xw_lds_bytes(window_lpr(F_in), F_in, F_out);
+    const uint64_t groups = (160 * 1024) / lds;
+    return static_cast<uint64_t>(p.n) * F_in * sizeof(float) > kGatherClassMinBytes && groups >= kFusedMinGroups;
+}
+
 namespace {
 
 // Orders work on stream s after the plan's sorted copy (written on the partition's stream);

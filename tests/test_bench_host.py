@@ -81,8 +81,12 @@ def test_cpu_baseline_states_each_part_fraction():
 
 
 def test_committed_counter_summary_names_the_default_kernel():
+    """The committed summary is for the kernel the default run times: c5's layer-1
+    aggregation fused with layer 2's update, with cache classes (the plan marks cold
+    columns and the 2 GiB operand is within the classes' range)."""
     text = open(bench.COUNTER_SUMMARY).read()
-    assert "workload: c5" in text and "kernel: spmm_xw_kernel<32>" in text
+    cp = bench.gather_classes({"cold_marked": 1}, 1 << 22, 128)
+    assert "workload: c5" in text and f"kernel: spmm_xw_kernel<32, {'true' if cp else 'false'}>" in text
 
 
 @pytest.mark.parametrize("gpus", ["2", "8"])
@@ -92,3 +96,18 @@ def test_more_than_one_gpu_is_refused(gpus):
     assert r.returncode == 2
     line = json.loads(r.stdout.strip().splitlines()[-1])
     assert "one GPU" in line["error"] and line["n_gpus"] == int(gpus)
+
+
+def test_gather_class_rule_names_the_kernel_that_runs():
+    """The bench names the instantiation the library launches: cache classes only on plans
+    that marked their cold columns, for rows of more than 16 floats, with the operand above
+    the 256 MiB memory-side cache and within the 4 GiB a buffer load addresses."""
+    marked, unmarked = {"cold_marked": 1}, {"cold_marked": 0}
+    n5 = 1 << 22
+    assert bench.gather_classes(marked, n5, 128)          # c5 layer 1: 2 GiB
+    assert bench.gather_classes(marked, n5, 64)           # c5 layer 2: 1 GiB
+    assert not bench.gather_classes(marked, n5, 256)      # 4 GiB: beyond 32-bit offsets
+    assert not bench.gather_classes(unmarked, n5, 128)
+    assert not bench.gather_classes(marked, n5, 16)       # rows of a quarter line
+    assert not bench.gather_classes(marked, 1 << 17, 64)  # 32 MiB: fits the memory-side cache
+    assert not bench.gather_classes(marked, 1 << 18, 256) # exactly 256 MiB

@@ -120,6 +120,30 @@ def test_fused_on_a_shifted_plan_matches_after_rebuild(dg, device):
         plan.destroy()
 
 
+def test_route_choice(dg, device):
+    """Small operands (they fit the memory-side cache) take the two calls when H is given;
+    an H that is only 8-byte aligned keeps the fused kernel; both give the same bits."""
+    g = _graph("gnp257")
+    plan = dg.Plan(*to_dev(g, device), seed=1, walks_per_node=4, walk_len=3)
+    assert not dg.spmm_update_route(plan, 128, 64)
+    with pytest.raises(dg.DualGCNError):
+        dg.spmm_update_route(plan, 48, 64)
+    X = torch.from_numpy(dense.features_normal(g.n, 128, seed=5, stream_id=44)).to(device)
+    W = torch.from_numpy(_weights(128, 64, seed=6)).to(device)
+    T_fused = dg.spmm_update(plan, X, W, relu=True)               # no H: the fused kernel
+    H16 = torch.full((g.n, 128), float("nan"), dtype=torch.bfloat16, device=device)
+    T_two = dg.spmm_update(plan, X, W, relu=True, H=H16)          # H given: the two calls
+    buf = torch.full((g.n * 128 + 4,), float("nan"), dtype=torch.bfloat16, device=device)
+    H8 = buf[4:].view(g.n, 128)                                   # 8-byte aligned only
+    assert H8.data_ptr() % 16 == 8
+    T_h8 = dg.spmm_update(plan, X, W, relu=True, H=H8)
+    assert torch.equal(T_two, T_fused) and torch.equal(T_h8, T_fused)
+    H_ref = dg.spmm(plan, X, relu=True, out_bf16=True)
+    assert torch.equal(H16.view(torch.int16), H_ref.view(torch.int16))
+    assert torch.equal(H8.view(torch.int16), H_ref.view(torch.int16))
+    plan.destroy()
+
+
 def test_fused_argument_checks(dg, device):
     g = _graph("gnp257")
     plan = dg.Plan(*to_dev(g, device), seed=1, walks_per_node=4, walk_len=3)

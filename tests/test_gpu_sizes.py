@@ -101,6 +101,10 @@ def test_c5_fused_junction_sampled(dg, device):
     Xd = torch.from_numpy(X).to(device)
     T1 = dg.update(Xd, torch.from_numpy(W1).to(device))
     del Xd
+    # the library's route: the fused kernel at the benchmark's shape (2 GiB operand, four
+    # workgroups per CU); the two calls where one workgroup fills a CU's LDS
+    assert dg.spmm_update_route(plan, 128, 64)
+    assert not dg.spmm_update_route(plan, 256, 128)
     T2 = dg.spmm_update(plan, T1, W2d, relu=True)
     T2_two = dg.update(dg.spmm(plan, T1, relu=True, out_bf16=True), W2d)
     assert torch.equal(T2, T2_two), "fused and two-call results differ at full size"

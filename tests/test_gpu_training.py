@@ -15,6 +15,7 @@ import pytest
 import torch
 
 import oracle
+import trainbound
 from graphgen import configs, dense, small
 from graphgen.csr import transposed
 
@@ -59,14 +60,6 @@ def _labels(n, C, seed):
     return y
 
 
-def _loss_bound(Y, labels, scale):
-    Y = np.asarray(Y, dtype=np.float64)
-    C = Y.shape[1]
-    on = np.flatnonzero((labels >= 0) & (labels < C))
-    m = np.abs(Y).max(axis=1)
-    return scale * float((np.abs(Y[on, labels[on]]) + m[on] + np.log(C) + 1.0).sum())
-
-
 @pytest.mark.parametrize("n,C", [(1, 1), (300, 3), (1000, 16), (777, 17), (4096, 64), (513, 100)])
 def test_softmax_xent(dg, device, n, C):
     Y = dense.features_normal(n, C, seed=n + C) * np.float32(3.0)
@@ -76,7 +69,7 @@ def test_softmax_xent(dg, device, n, C):
                               scale)
     ref_loss, ref_G = oracle.softmax_xent(Y, labels, scale)
     _within(G.cpu().numpy(), ref_G, np.full(ref_G.shape, scale), 1e-5, "G")
-    assert abs(loss[0].item() - ref_loss) <= 1e-5 * _loss_bound(Y, labels, scale)
+    assert abs(loss[0].item() - ref_loss) <= 1e-5 * trainbound.loss_bound(Y, labels, scale)
     # unlabeled rows get exactly zero gradient
     off = (labels < 0) | (labels >= C)
     assert np.all(G.cpu().numpy()[off] == 0.0)
@@ -102,7 +95,7 @@ def test_softmax_xent_c5_shape(dg, device):
     total = 0.0
     for lo in range(0, n, 1 << 20):
         total += oracle.softmax_xent(Y[lo:lo + (1 << 20)], labels[lo:lo + (1 << 20)], scale)[0]
-    assert abs(loss[0].item() - total) <= 1e-5 * _loss_bound(Y, labels, scale)
+    assert abs(loss[0].item() - total) <= 1e-5 * trainbound.loss_bound(Y, labels, scale)
 
 
 # ---------------------------------------------------------------- weight gradient
@@ -228,9 +221,6 @@ def test_transposed_aggregation_on_plan_of_transpose(dg, device):
 
 # ---------------------------------------------------------------- whole training step
 
-R_MFMA = 1e-2       # one bf16 matrix-core product (two roundings and float32 sums)
-R_SPMM = 1e-5       # one float32 aggregation
-R_STORE = 2.0 ** -8  # one bfloat16 store (nearest-even: unit roundoff 2^-8, 8 significand bits)
 
 
 def test_two_layer_training_step_c2(dg, device):
@@ -262,36 +252,9 @@ def test_two_layer_training_step_c2(dg, device):
 
     ref = oracle.gcn_train_grads(g, X, [W1, W2], labels, scale)
     # error budgets propagated through the chain (float64, with |A| for every aggregation)
-    ga = type(g)(n=g.n, rowptr=g.rowptr, col=g.col, val=np.abs(g.val))
-    agg = lambda M: oracle.spmm_f64(ga, M)            # |A| M (= |A|^T M: symmetric)
-    aX, aW1, aW2 = np.abs(X.astype(np.float64)), np.abs(W1.astype(np.float64)), np.abs(W2.astype(np.float64))
-    E_T1 = R_MFMA * aX @ aW1
-    E_P1 = agg(E_T1) + R_SPMM * agg(aX @ aW1)
-    H1r = ref["H"][0]
-    E_H1 = E_P1 + R_STORE * (np.abs(H1r) + E_P1)
-    aH1 = np.abs(H1r) + E_H1
-    E_T2 = E_H1 @ aW2 + R_MFMA * aH1 @ aW2
-    E_Y2 = agg(E_T2) + R_SPMM * agg(aH1 @ aW2)
-    on = (labels >= 0) & (labels < C)
-    rowE = E_Y2.max(axis=1)
-    E_G2 = np.where(on[:, None], scale * (0.5 * rowE[:, None] + 1e-6), 0.0)
-    E_loss = scale * float((2 * rowE[on]).sum()) + 1e-5 * _loss_bound(ref["H"][1], labels, scale)
+    E_loss, (E_dW1, E_dW2) = trainbound.two_layer_bounds(g, X, [W1, W2], labels, scale, ref)
     assert abs(loss[0].item() - ref["loss"]) <= E_loss
-    G2r = ref["G"][1]
-    dT2r = ref["GT"][1]
-    E_dT2 = agg(E_G2) + R_SPMM * agg(np.abs(G2r)) + R_STORE * (np.abs(dT2r) + agg(E_G2))
-    adT2 = np.abs(dT2r) + E_dT2
-    E_dW2 = E_H1.T @ adT2 + np.abs(H1r).T @ E_dT2 + R_MFMA * aH1.T @ adT2
     _within(dW2, ref["dW"][1], E_dW2, 1.0, "dW2")
-    P1r = ref["P"][0]
-    ambiguous = np.abs(P1r) <= E_P1
-    keep = (P1r > 0) & ~ambiguous
-    full = adT2 @ aW2.T
-    E_dH1 = np.where(keep, E_dT2 @ aW2.T + R_MFMA * full, 0.0) + np.where(ambiguous, full * (1 + R_MFMA), 0.0)
-    dT1r = ref["GT"][0]
-    dH1r = ref["GP"][0]
-    E_dT1 = agg(E_dH1) + R_SPMM * agg(np.abs(dH1r)) + R_STORE * (np.abs(dT1r) + agg(E_dH1))
-    E_dW1 = aX.T @ E_dT1 + R_MFMA * aX.T @ (np.abs(dT1r) + E_dT1)
     _within(dW1, ref["dW"][0], E_dW1, 1.0, "dW1")
     # Those bounds hold whatever the signs, so over the n-row sums of dW they are loose.
     # Tight: the same chain with the declared bfloat16 roundings (operands of every dense
