@@ -117,6 +117,10 @@ struct Plan {
     // the last launch that used the plan on each stream (destroy waits for these)
     mutable std::mutex use_mu;
     mutable std::vector<std::pair<hipStream_t, hipEvent_t>> uses;
+    // the build's scratch block while the sorted copy may still read it (plans that mark
+    // cold columns): released once `ready` has been seen complete, or with the plan
+    mutable void *pending = nullptr;
+    mutable size_t pending_bytes = 0;
 
     uint64_t kstar = 0, kmax = 0;
     u128 s1 = 0, s2 = 0;
@@ -188,6 +192,8 @@ int wait_event(hipEvent_t event);
 // such use and for the plan's own build (partition.hip).
 int note_use(const Plan &p, hipStream_t stream);
 int wait_plan_idle(const Plan &p);
+// Returns the plan's pending scratch block to the block cache; only once `ready` has completed.
+void release_pending(const Plan &p);
 
 int launch_spmm(const Plan &p, const float *X, void *Y, int32_t F, bool relu, bool out_bf16,
                 hipStream_t stream);

@@ -1001,6 +1001,7 @@ int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t
 
 void free_plan(Plan *p) {
     if (!p) return;
+    if (p->pending) release_block(p->pending, p->pending_bytes);
     release_block(p->mem, p->mem_bytes);
     if (p->ready) (void)hipEventDestroy(p->ready);
     for (auto &u : p->uses) (void)hipEventDestroy(u.second);
@@ -1022,8 +1023,17 @@ int note_use(const Plan &p, hipStream_t s) {
     return DUALGCN_OK;
 }
 
+void release_pending(const Plan &p) {
+    std::lock_guard<std::mutex> lock(p.use_mu);
+    if (!p.pending) return;
+    release_block(p.pending, p.pending_bytes);
+    p.pending = nullptr;
+    p.pending_bytes = 0;
+}
+
 int wait_plan_idle(const Plan &p) {
     int st = p.ready ? wait_event(p.ready) : DUALGCN_OK;
+    if (!st) release_pending(p);
     std::lock_guard<std::mutex> lock(p.use_mu);
     for (auto &u : p.uses)
         if (!st) st = wait_event(u.second);
@@ -1334,21 +1344,25 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if (!pin) return DUALGCN_ERR_OOM;
     if ((st = hip_status(hipMemcpyAsync(pin, dsum, sizeof(SplitSummary), hipMemcpyDeviceToHost, s))))
         return st;
-    // the scratch block's last use: before the sorted copy, unless the copy reads the
-    // marked columns from it (then host wait 2 also waits for the copy); until it is
-    // recorded, an early return waits for the whole stream before releasing the block
-    auto record_done = [&]() -> int {
+    {
+        // host wait 2 reads the sizes at this point; the scratch block's last use is here
+        // too, unless the sorted copy reads the marked columns from it: then the plan keeps
+        // the block until its `ready` event (after the copy) is seen complete, so that the
+        // host does not wait for the copy (an early return from here on synchronises the
+        // stream before the plan and the block are released)
         hipEvent_t done = nullptr;
-        int rs = hip_status(hipEventCreateWithFlags(&done, hipEventDisableTiming));
-        if (rs) return rs;
-        if ((rs = hip_status(hipEventRecord(done, s)))) {
+        if ((st = hip_status(hipEventCreateWithFlags(&done, hipEventDisableTiming)))) return st;
+        if ((st = hip_status(hipEventRecord(done, s)))) {
             (void)hipEventDestroy(done);
-            return rs;
+            return st;
         }
         scratch.done = done;
-        return DUALGCN_OK;
-    };
-    if (!marked && (st = record_done())) return st;
+        if (marked) {
+            p->pending = scratch.p;
+            p->pending_bytes = scratch.bytes;
+            scratch.p = nullptr;
+        }
+    }
     if (nnz > 0) {
         const unsigned grid_e = static_cast<unsigned>((nnz + kCopyTile - 1) / kCopyTile);
         hipLaunchKernelGGL(tile_row_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, p->tile_row);
@@ -1357,7 +1371,6 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                            n, nnz, p->pcol, p->pval);
         if ((st = hip_status(hipGetLastError()))) return st;
     }
-    if (marked && (st = record_done())) return st;
     // every use of the plan's sorted copy waits for this event (its stream, or any other)
     if ((st = hip_status(hipEventCreateWithFlags(&p->ready, hipEventDisableTiming)))) return st;
     if ((st = hip_status(hipEventRecord(p->ready, s)))) return st;

@@ -797,6 +797,7 @@ int after_plan(const Plan &p, hipStream_t s) {
     const hipError_t q = hipEventQuery(p.ready);
     if (q == hipSuccess) {
         p.ready_seen.store(true, std::memory_order_release);
+        release_pending(p);
         return DUALGCN_OK;
     }
     if (q != hipErrorNotReady) return hip_status(q);
