@@ -86,3 +86,30 @@ def test_fused_junction_on_the_class_path(dg, device, hub):
     assert torch.equal(T, T_two)
     assert not dg.spmm_update_route(plan, 256, 64)        # two workgroups per CU: the two calls
     assert torch.equal(dg.spmm_update(plan, X, W, relu=True), T_two)
+
+
+def test_narrow_features_on_the_class_path(dg, device):
+    """F = 32 (8-lane groups): an operand of 2^21 + 3 rows is 256 MiB + 384 bytes, so the plain
+    SpMM and the fused junction (32 -> 32, fused route) read marked rows non-temporally."""
+    n = (1 << 21) + 3
+    gen = np.random.Generator(np.random.Philox(key=np.array([32, 1], dtype=np.uint64)))
+    a, b = gen.integers(0, n, 2 * n), gen.integers(0, n, 2 * n)
+    keep = a != b
+    a, b = a[keep], b[keep]
+    rows = np.concatenate([a, b, np.arange(n)])
+    cols = np.concatenate([b, a, np.arange(n)])
+    rowptr, col = csr_from_pairs(n, rows, cols)
+    g = Graph(n=n, rowptr=rowptr, col=col, val=normalised_values(rowptr, col), meta={"kind": "sparse"})
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=4, walk_len=3)
+    assert plan.info()["cold_marked"] == 1
+    X = dense.features_normal(n, 32, seed=8, stream_id=63)
+    Xd = torch.from_numpy(X).to(device)
+    Y = torch.full((n, 32), float("nan"), dtype=torch.float32, device=device)
+    dg.spmm(plan, Xd, Y)
+    Yr, B = oracle.spmm(g, X)
+    assert_spmm_close(Y.cpu().numpy(), Yr, B, what="F=32 class path")
+    W = torch.from_numpy(dense.glorot(32, 32, seed=9)).to(device)
+    assert dg.spmm_update_route(plan, 32, 32)
+    T = dg.spmm_update(plan, Xd, W, relu=True)
+    assert torch.equal(T, dg.update(dg.spmm(plan, Xd, relu=True, out_bf16=True), W))
+    plan.destroy()
