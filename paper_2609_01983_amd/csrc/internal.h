@@ -161,10 +161,11 @@ int launch_density(const int2 *nodeinfo, const int32_t *col, const int2 *succ, i
 // start at zero.  nodeinfo (may be null, n entries) receives (rowptr[v], rowptr[v+1] -
 // rowptr[v]); blockmax (may be null, kValidateBlocks entries) each workgroup's largest
 // row length; heat_hist (may be null, kHeatLevels counters that start at zero) the number
-// of nodes per heat_of(row length).
+// of nodes per heat_of(row length).  check_cols = false leaves the columns to a later pass
+// over them (the partition's successor pass, which sets bit 2 the same way).
 constexpr int kValidateBlocks = 2048;
 int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t *blockmax,
-                 uint32_t *heat_hist, hipStream_t stream);
+                 uint32_t *heat_hist, hipStream_t stream, bool check_cols = true);
 // S_host (host, n sums), when given, replaces the walks: the density sums of a saved plan.
 int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
                const dualgcn_thresholds &th, const uint32_t *S_host, hipStream_t stream,

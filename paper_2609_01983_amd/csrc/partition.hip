@@ -43,17 +43,18 @@ constexpr int kRadix = 1 << kRadixBits;
 
 // ------------------------------------------------------------------ validation
 
-// Checks the row pointers and columns, records the largest degree, writes every node's
-// (first entry, degree) record for the walks (one 8-byte read per step) and counts the
-// nodes per gather heat (per workgroup in LDS, then one atomic per non-empty value and
-// workgroup).
+// Checks the row pointers and (with check_cols; otherwise the successor pass checks them)
+// the columns, records the largest degree, writes every node's (first entry, degree)
+// record for the walks (one 8-byte read per step) and counts the nodes per gather heat
+// (per workgroup in LDS, then one atomic per non-empty value and workgroup).
 __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__restrict__ rowptr,
                                                             const int32_t *__restrict__ col,
                                                             int32_t n, int64_t nnz,
                                                             int32_t *__restrict__ flag,
                                                             int2 *__restrict__ nodeinfo,
                                                             int32_t *__restrict__ blockmax,
-                                                            uint32_t *__restrict__ heat_hist) {
+                                                            uint32_t *__restrict__ heat_hist,
+                                                            int32_t check_cols) {
     __shared__ int32_t sh_bad[kThreads / 64], sh_max[kThreads / 64];
     __shared__ uint32_t sh_hist[kHeatLevels];
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
@@ -80,6 +81,7 @@ __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__res
         if (static_cast<int64_t>(rowptr[n]) != nnz) bad |= 1;
     }
     // columns: scalar head up to a 16-byte boundary, 16-byte loads, scalar tail
+    if (!check_cols) nnz = 0;
     const int64_t head = std::min<int64_t>(nnz, ((16 - (reinterpret_cast<uintptr_t>(col) & 15)) & 15) / 4);
     const int64_t body = (nnz - head) / 4;
     const int4 *__restrict__ c4 = reinterpret_cast<const int4 *>(col + head);
@@ -122,20 +124,24 @@ __global__ __launch_bounds__(kThreads) void validate_kernel(const int32_t *__res
 // c = col[e], the node record validate_kernel wrote.  With marked, also the column with
 // bit 31 set when c is outside the hottest columns (heat below *hot_heat), in the
 // matrix's entry order: the sorted copy then reads it in place of the column, and the
-// mark costs it nothing.  A column out of range (the validation flags it, and nothing
-// walks or copies then) gets a record without reading them.
+// mark costs it nothing.  This pass reads every column, so it also checks them (the
+// validation then checks only the row pointers): a column out of range sets bit 2 of
+// the flag (nothing walks or copies then) and gets a record without reading them.
 __global__ __launch_bounds__(kThreads) void successor_kernel(const int2 *__restrict__ nodeinfo,
                                                              const int32_t *__restrict__ col,
                                                              int32_t n, int64_t nnz,
                                                              int2 *__restrict__ succ,
                                                              const uint32_t *__restrict__ hot_heat,
-                                                             int32_t *__restrict__ marked) {
+                                                             int32_t *__restrict__ marked,
+                                                             int32_t *__restrict__ flag) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
     const uint32_t hot = marked ? *hot_heat : 0u;
     for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < nnz;
          e += stride) {
         const int32_t c = col[e];
-        const int2 r = c >= 0 && c < n ? nodeinfo[c] : make_int2(0, 0);
+        const bool in = c >= 0 && c < n;
+        if (!in) atomicOr(flag, 2);
+        const int2 r = in ? nodeinfo[c] : make_int2(0, 0);
         if (succ) succ[e] = r;
         if (marked) {
             const bool cold = heat_of(static_cast<uint32_t>(r.y)) < hot;
@@ -993,9 +999,10 @@ bool square_sum_fits(const Moments &m) {
 }  // namespace
 
 int validate_csr(const dualgcn_csr *csr, int32_t *flags, int2 *nodeinfo, int32_t *blockmax,
-                 uint32_t *heat_hist, hipStream_t s) {
+                 uint32_t *heat_hist, hipStream_t s, bool check_cols) {
     hipLaunchKernelGGL(validate_kernel, dim3(kValidateBlocks), dim3(kThreads), 0, s, csr->rowptr,
-                       csr->col, csr->n, csr->nnz, flags, nodeinfo, blockmax, heat_hist);
+                       csr->col, csr->n, csr->nnz, flags, nodeinfo, blockmax, heat_hist,
+                       check_cols ? 1 : 0);
     return hip_status(hipGetLastError());
 }
 
@@ -1162,14 +1169,18 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
 
     TraceRange phase("partition: validate + walks");
     if ((st = hip_status(hipMemsetAsync(bad, 0, kFlagBytes + kHistBytes, s)))) return st;
-    if ((st = validate_csr(csr, bad, nodeinfo, blockmax, mark ? heat_hist : nullptr, s))) return st;
+    // the successor pass reads every column: where it runs, it checks them in place of the
+    // validation (which then reads only the row pointers)
+    const bool succ_pass = (use_succ || mark) && nnz > 0;
+    if ((st = validate_csr(csr, bad, nodeinfo, blockmax, mark ? heat_hist : nullptr, s, !succ_pass)))
+        return st;
     if (mark) hipLaunchKernelGGL(hot_heat_kernel, dim3(1), dim3(kHeatLevels), 0, s, heat_hist, kHotRows, hot_heat);
     int2 *succ = nullptr;
-    if ((use_succ || mark) && nnz > 0) {
+    if (succ_pass) {
         if (use_succ) succ = reinterpret_cast<int2 *>(sm + o_succ);
         const int64_t sblocks = std::min<int64_t>((nnz + kThreads - 1) / kThreads, 65536);
         hipLaunchKernelGGL(successor_kernel, dim3(static_cast<unsigned>(sblocks)), dim3(kThreads), 0,
-                           s, nodeinfo, csr->col, n, nnz, succ, hot_heat, marked);
+                           s, nodeinfo, csr->col, n, nnz, succ, hot_heat, marked, bad);
     }
     if (S_host) {
         // the density sums of a saved plan of this matrix: no walks

@@ -158,18 +158,23 @@ def test_partition_bitexact_configs(dg, device, cfg):
     assert 0 < ref["n_sparse"] < g.n
 
 
-def test_bad_csr_rejected(dg, device):
+@pytest.mark.parametrize("k,d", [(4, 3), (1, 1)])
+def test_bad_csr_rejected(dg, device, k, d):
+    """Columns are checked by the successor pass where it runs (walks of k d >= 2 nnz / n steps
+    per node: 4 x 3 here) and by the validation otherwise (1 x 1)."""
     g = small.random_graph(20, 0.2, seed=3)
+    assert (20 * k * d >= 2 * g.nnz) == (k * d == 12)
     rp, c, v = to_dev(g, device)
-    c_bad = c.clone()
-    c_bad[3] = 20                                    # column out of range
-    with pytest.raises(dg.DualGCNError) as e:
-        dg.Plan(rp, c_bad, v, walks_per_node=4, walk_len=3)
-    assert e.value.status == dg.ERR_BAD_CSR
+    for bad in (20, -1, 1 << 30):                    # columns out of range
+        c_bad = c.clone()
+        c_bad[3] = bad
+        with pytest.raises(dg.DualGCNError) as e:
+            dg.Plan(rp, c_bad, v, walks_per_node=k, walk_len=d)
+        assert e.value.status == dg.ERR_BAD_CSR
     rp_bad = rp.clone()
     rp_bad[5] = rp_bad[6] + 1                        # not monotone
     with pytest.raises(dg.DualGCNError) as e:
-        dg.Plan(rp_bad, c, v, walks_per_node=4, walk_len=3)
+        dg.Plan(rp_bad, c, v, walks_per_node=k, walk_len=d)
     assert e.value.status == dg.ERR_BAD_CSR
 
 
