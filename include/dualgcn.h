@@ -201,8 +201,11 @@ int dualgcn_plan_load(const dualgcn_csr *csr, const void *buf, size_t bytes, voi
  * Every row of Y is written, rows without entries with zeros.  Products are
  * float32; sums are formed in float32 over at most 16 terms and then in
  * float64, and each output is rounded once to float32, so results do not
- * depend on timing (bit-reproducible for a given plan and F).
- * 1 <= F < 2^20.  Asynchronous.
+ * depend on timing (bit-reproducible for a given plan and F).  On plans that mark
+ * cold columns (dualgcn_plan_info.cold_marked) and X larger than 256 MiB and
+ * smaller than 4 GiB, rows of X outside the hottest 65,536 are read with
+ * non-temporal loads, which keeps the hottest rows in the L2; the results are the
+ * same.  1 <= F < 2^20.  Asynchronous.
  */
 int dualgcn_spmm(const dualgcn_plan *plan, const float *X, float *Y, int32_t F, void *stream);
 

@@ -31,7 +31,9 @@
 // each lane loads kRound / LPR (column, value) pairs with coalesced loads, the
 // pairs are broadcast inside the group with shuffles, and all kRound neighbour
 // slices are requested before the first product, so every group keeps kRound
-// loads in flight (the ILP of the paper's dense path, Alg. 1, deepened).
+// loads in flight (the ILP of the paper's dense path, Alg. 1, deepened).  On large
+// operands the rows of cold columns (marked by the plan) are read non-temporally
+// (the cache classes below).
 //
 // Dense path (paper: one row per block, 4-way ILP and a shared reduction): a long
 // row gets a wavefront whose groups take rounds of the row in turn and are summed
