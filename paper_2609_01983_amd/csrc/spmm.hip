@@ -753,13 +753,13 @@ int long_row_class(int lpr) {
 // graphs with shuffled ids (c5: n = 2^22, 67M entries; c4: n = 2^21, 63M entries),
 // F = 128: the layer-1 aggregation fused with the next update 4.27 -> 4.03 ms (c5) and
 // 3.72 -> 3.45 ms (c4), the plain SpMM 4.46 -> 4.24 and 3.70 -> 3.47 ms; the L2 hit rate of
-// the fused kernel rose from 22.5% to 27.5% and its fetched bytes fell by 6%.  Hot sets of
-// 16 MiB or less, or a third class loading warm rows with sc0, were slower.
-
-// Sets the class fields of `a` for gathers of w features of rows ld apart and returns
-// true when the launch should use them: the plan marked its cold columns, rows are read
-// whole with 16-byte loads, the operand fits the 32-bit offsets of a buffer load, and it
-// is larger than the memory-side cache.
+// the fused kernel rose from 22.5% to 26.8% and its fetched bytes fell from 28.6 to 27.0 GB.
+// Hot sets of 16 MiB or less, or a third class loading warm rows with sc0, were slower.
+//
+// gather_classes sets the class fields of `a` for gathers of w features of rows ld apart
+// and returns true when the launch should use them: the plan marked its cold columns, rows
+// are read whole with 16-byte loads, the operand fits the 32-bit offsets of a buffer load,
+// and it is larger than the memory-side cache.
 bool gather_classes(const Plan &p, int32_t ld, int32_t w, bool vec, Args &a) {
     if (!vec || !p.cold_marked) return false;
     const uint64_t bytes = static_cast<uint64_t>(p.n) * static_cast<uint64_t>(ld) * sizeof(float);
