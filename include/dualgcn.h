@@ -381,7 +381,9 @@ int dualgcn_weight_grad_workspace(int32_t n, int32_t F_in, int32_t F_out, size_t
  * and multiplied on the matrix cores with float32 accumulation over chunks of
  * rows; the per-workgroup partial matrices (in `workspace`, device, 256-byte
  * aligned, at least dualgcn_weight_grad_workspace bytes) are summed in a fixed
- * order in float64, so results do not depend on timing.  If W (device, float32
+ * order in float64, so results do not depend on timing, nor on which operands come
+ * in bfloat16 (an operand passed as its bfloat16 rounding gives the same bits as the
+ * float32 original; with both in bfloat16 half the bytes are read).  If W (device, float32
  * F_in x F_out) is not NULL, the same call applies the SGD step W -= lr dW.
  * Shapes: F_in and F_out multiples of 32, F_in <= 1024, F_out <= 256 (else
  * DUALGCN_ERR_UNSUPPORTED); X and G 16-byte aligned.  Asynchronous.

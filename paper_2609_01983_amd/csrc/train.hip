@@ -218,26 +218,26 @@ struct Stage {
         return qb < width / 32;
     }
 
+    // Every lane issues every load, without branches: a row past the end reads row n - 1
+    // (n >= 1) and an item outside `width` reads its row's first quad.  With no load under
+    // a condition, the compiler counts the loads in flight exactly and waits only for the
+    // chunk being stored while the next chunk's loads are still on their way.  store()
+    // writes zeros for rows past the end.
     __device__ __forceinline__ void load(const void *src, int64_t ld, int64_t n, int64_t r0,
                                          int col0, int width) {
 #pragma unroll
         for (int it = 0; it < ITEMS; ++it) {
             int rp, cq;
             const bool ok = item(it, width, rp, cq);
+            const int64_t c = col0 + (ok ? 4 * cq : 0);
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int64_t r = r0 + 2 * rp + h;
-                if constexpr (BF) {
-                    v[it][h] = make_uint2(0u, 0u);
-                    if (ok && r < n)
-                        v[it][h] = *reinterpret_cast<const uint2 *>(static_cast<const unsigned short *>(src) +
-                                                                    r * ld + col0 + 4 * cq);
-                } else {
-                    v[it][h] = f32x4{0.f, 0.f, 0.f, 0.f};
-                    if (ok && r < n)
-                        v[it][h] = *reinterpret_cast<const f32x4 *>(static_cast<const float *>(src) +
-                                                                    r * ld + col0 + 4 * cq);
-                }
+                const int64_t at = (r < n ? r : n - 1) * ld + c;
+                if constexpr (BF)
+                    v[it][h] = *reinterpret_cast<const uint2 *>(static_cast<const unsigned short *>(src) + at);
+                else
+                    v[it][h] = *reinterpret_cast<const f32x4 *>(static_cast<const float *>(src) + at);
             }
         }
     }
@@ -251,14 +251,17 @@ struct Stage {
         }
     }
 
-    __device__ __forceinline__ void store(uint32_t *t, int width) const {
+    // The chunk of rows from r0 into t[col][row] (bfloat16 pairs), zeros past row n.
+    __device__ __forceinline__ void store(uint32_t *t, int width, int64_t r0, int64_t n) const {
 #pragma unroll
         for (int it = 0; it < ITEMS; ++it) {
             int rp, cq;
             if (item(it, width, rp, cq)) {
+                const bool in0 = r0 + 2 * rp < n, in1 = r0 + 2 * rp + 1 < n;
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
-                    t[(4 * cq + c) * kLdsRow2 + rp] = bits(v[it][0], c) | (bits(v[it][1], c) << 16);
+                    t[(4 * cq + c) * kLdsRow2 + rp] = (in0 ? bits(v[it][0], c) : 0u) |
+                                                      ((in1 ? bits(v[it][1], c) : 0u) << 16);
             }
         }
     }
@@ -273,9 +276,10 @@ __device__ __forceinline__ bf16x8 fragment(const uint32_t *t, int row, int kk) {
 }
 
 // partial[blockIdx.x] (F_in x F_out, only the block [i0, i0 + IB) x [j0, j0 + JB)) =
-// sum over this workgroup's chunks of bf16(X)^T bf16(G).  Tiles of 16 x 16 go to the
-// wavefronts in row-major order, NT per wavefront.  The loads of chunk c + gridDim.x are
-// in flight while chunk c is stored to LDS and multiplied.
+// sum over this workgroup's chunks c = blockIdx.x, + gridDim.x, + 2 gridDim.x, ... of
+// bf16(X)^T bf16(G), accumulated in that order (two k-steps of 32 rows per chunk).  Tiles
+// of 16 x 16 go to the wavefronts in row-major order, NT per wavefront.  The loads of
+// chunk c + gridDim.x are in flight while chunk c is stored to LDS and multiplied.
 template <int NT, bool XBF, bool GBF>
 __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restrict__ X,
                                                            const void *__restrict__ G,
@@ -300,20 +304,16 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restric
     Stage<XBF, kXItems> xs, xn;
     Stage<GBF, kGItems> gs, gn;
     const int64_t chunks = (static_cast<int64_t>(n) + kChunk - 1) / kChunk;
-    int64_t c = blockIdx.x;
-    if (c < chunks) {
-        xs.load(X, F_in, n, c * kChunk, i0, IB);
-        gs.load(G, F_out, n, c * kChunk, j0, JB);
-    }
+    int64_t c = blockIdx.x;                  // the launch has at most one workgroup per chunk
+    xs.load(X, F_in, n, c * kChunk, i0, IB);
+    gs.load(G, F_out, n, c * kChunk, j0, JB);
     for (; c < chunks; c += gridDim.x) {
-        const int64_t next = c + gridDim.x;
-        if (next < chunks) {
-            xn.load(X, F_in, n, next * kChunk, i0, IB);
-            gn.load(G, F_out, n, next * kChunk, j0, JB);
-        }
+        const int64_t next = c + gridDim.x;  // past the last chunk: rows n - 1, never stored
+        xn.load(X, F_in, n, next * kChunk, i0, IB);
+        gn.load(G, F_out, n, next * kChunk, j0, JB);
         __syncthreads();                     // the previous chunk's MFMAs are done with LDS
-        xs.store(xt, IB);
-        gs.store(gt, JB);
+        xs.store(xt, IB, c * kChunk, n);
+        gs.store(gt, JB, c * kChunk, n);
         __syncthreads();
 #pragma unroll
         for (int ks = 0; ks < kChunk / 32; ++ks) {
@@ -342,6 +342,154 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_kernel(const void *__restric
                 out[static_cast<int64_t>(i0 + it * 16 + kgrp * 4 + r) * F_out + j0 + jt * 16 + lrow] = acc[u][r];
         }
     }
+}
+
+// ------------------------------------------------ both operands bfloat16: transposing reads
+//
+// The same product (same chunks, k-steps and order of accumulation, hence the same bits)
+// when X and G are both stored in bfloat16.  A chunk is copied to LDS row-major, 16 bytes
+// per lane, and the matrix-core operands, which need eight consecutive rows of one column
+// per lane, come from gfx950's transposing LDS read (ds_read_b64_tr_b16): within each group
+// of 16 lanes, lane i receives element i % 4 of the 4-element pieces that lanes
+// i / 4, 4 + i / 4, 8 + i / 4 and 12 + i / 4 point at.  So lane 4t + u of a group points at
+// row t of its four, columns 4u .. 4u + 3 of the 16-column tile, and receives one column
+// over four consecutive rows.
+//
+// 512 threads: eight wavefronts as 4 x 2 over the dW block, each with up to 4 x 4 tiles of
+// 16 x 16 (tile rows wm, wm + 4, ..; tile columns wn, wn + 2, ..), so that a k-step reads
+// 4 + 4 fragments per wavefront for 16 products (the row-per-wavefront split of
+// wgrad_kernel reads 9 for 8).  LDS rows are kMaxIB (X) and kMaxJB (G) elements long; the
+// 16-element blocks of row r are XOR-permuted by (r % 4) + 4 ((r / 8) % 2), which puts the
+// 16 rows one transposing read touches on eight different 32-byte bank groups, two each.
+constexpr int kTrThreads = 512;
+constexpr int kTrTiles = 4;                       // tile rows and tile columns per wavefront
+constexpr int kTrXItems = kChunk * kMaxIB / 8 / kTrThreads;   // 16-byte pieces per thread: 4
+constexpr int kTrGItems = kChunk * kMaxJB / 8 / kTrThreads;   // 2
+constexpr int kTrBufElems = kChunk * (kMaxIB + kMaxJB);       // one chunk of X and G in LDS
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ int tr_swizzle(int r) {
+    return (r & 3) | ((r >> 1) & 4);
+}
+
+// `width` columns (from col0) of a 64-row chunk of a bfloat16 matrix, 16 bytes per item.
+// Loads are unconditional (rows past the end read row n - 1, items past the chunk read its
+// first piece), so the compiler waits only for the chunk it stores; rows past the end are
+// stored as zeros.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int ITEMS>
+struct RowStage {
+    u32x4 v[ITEMS];
+
+    __device__ __forceinline__ void load(const unsigned short *src, int64_t ld, int64_t n,
+                                         int64_t r0, int col0, int width) {
+        const int per_row = width / 8, total = kChunk * per_row;
+#pragma unroll
+        for (int it = 0; it < ITEMS; ++it) {
+            int p = static_cast<int>(threadIdx.x) + it * kTrThreads;
+            p = p < total ? p : 0;
+            const int64_t r = r0 + p / per_row;
+            v[it] = *reinterpret_cast<const u32x4 *>(src + (r < n ? r : n - 1) * ld + col0 + (p % per_row) * 8);
+        }
+    }
+
+    // t: [kChunk][pitch] bfloat16, blocks of 16 elements permuted per row
+    __device__ __forceinline__ void store(unsigned short *t, int pitch, int64_t r0, int64_t n,
+                                          int width) const {
+        const int per_row = width / 8, total = kChunk * per_row;
+#pragma unroll
+        for (int it = 0; it < ITEMS; ++it) {
+            const int p = static_cast<int>(threadIdx.x) + it * kTrThreads;
+            if (p < total) {                                  // uniform over a wavefront
+                const int row = p / per_row, c8 = p % per_row;
+                const uint32_t keep = r0 + row < n ? ~0u : 0u;
+                *reinterpret_cast<u32x4 *>(t + row * pitch + (((c8 >> 1) ^ tr_swizzle(row)) << 4) + (c8 & 1) * 8) =
+                    v[it] & keep;
+            }
+        }
+    }
+};
+
+// The 16 x 32 operand of tile columns [c0, c0 + 16) over rows [kb, kb + 32) of t: lane
+// (16 g + s) gets column c0 + s at rows kb + 8 g .. kb + 8 g + 7.
+__device__ __forceinline__ bf16x8 tr_fragment(const unsigned short *t, int pitch, int kb, int c0,
+                                              int lane) {
+    const int s = lane & 15, g = lane >> 4;
+    const int r = kb + 8 * g + (s >> 2);
+    const int col = (((c0 >> 4) ^ tr_swizzle(r)) << 4) + 4 * (s & 3);   // rows r and r + 4 share the permutation
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(t + r * pitch + col));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(t + (r + 4) * pitch + col));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+__global__ __launch_bounds__(kTrThreads) void wgrad_tr_kernel(const unsigned short *__restrict__ X,
+                                                              const unsigned short *__restrict__ G,
+                                                              float *__restrict__ partial, int32_t n,
+                                                              int32_t F_in, int32_t F_out, int32_t i0,
+                                                              int32_t IB, int32_t j0, int32_t JB) {
+    extern __shared__ uint4 lds4[];
+    unsigned short *xt = reinterpret_cast<unsigned short *>(lds4);   // [kChunk][kMaxIB]
+    unsigned short *gt = xt + kChunk * kMaxIB;                         // [kChunk][kMaxJB]
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int it_count = IB / 16, jt_count = JB / 16;
+
+    f32x4 acc[kTrTiles][kTrTiles];
+#pragma unroll
+    for (int a = 0; a < kTrTiles; ++a)
+#pragma unroll
+        for (int b = 0; b < kTrTiles; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    RowStage<kTrXItems> xs, xn;
+    RowStage<kTrGItems> gs, gn;
+    const int64_t chunks = (static_cast<int64_t>(n) + kChunk - 1) / kChunk;
+    int64_t c = blockIdx.x;                  // the launch has at most one workgroup per chunk
+    xs.load(X, F_in, n, c * kChunk, i0, IB);
+    gs.load(G, F_out, n, c * kChunk, j0, JB);
+    for (; c < chunks; c += gridDim.x) {
+        const int64_t next = c + gridDim.x;  // past the last chunk: rows n - 1, never stored
+        xn.load(X, F_in, n, next * kChunk, i0, IB);
+        gn.load(G, F_out, n, next * kChunk, j0, JB);
+        __syncthreads();                     // the previous chunk's products are done with LDS
+        xs.store(xt, kMaxIB, c * kChunk, n, IB);
+        gs.store(gt, kMaxJB, c * kChunk, n, JB);
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < kChunk / 32; ++ks) {
+            bf16x8 af[kTrTiles], bf[kTrTiles];
+#pragma unroll
+            for (int a = 0; a < kTrTiles; ++a)
+                if (wm + 4 * a < it_count) af[a] = tr_fragment(xt, kMaxIB, ks * 32, (wm + 4 * a) * 16, lane);
+#pragma unroll
+            for (int b = 0; b < kTrTiles; ++b)
+                if (wn + 2 * b < jt_count) bf[b] = tr_fragment(gt, kMaxJB, ks * 32, (wn + 2 * b) * 16, lane);
+#pragma unroll
+            for (int a = 0; a < kTrTiles; ++a)
+#pragma unroll
+                for (int b = 0; b < kTrTiles; ++b)
+                    if (wm + 4 * a < it_count && wn + 2 * b < jt_count)
+                        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bf[b], acc[a][b], 0, 0, 0);
+        }
+        xs = xn;
+        gs = gn;
+    }
+    float *out = partial + static_cast<int64_t>(blockIdx.x) * F_in * F_out;
+    const int s = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int a = 0; a < kTrTiles; ++a)
+#pragma unroll
+        for (int b = 0; b < kTrTiles; ++b) {
+            const int it = wm + 4 * a, jt = wn + 2 * b;
+            if (it < it_count && jt < jt_count) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    out[static_cast<int64_t>(i0 + it * 16 + g * 4 + r) * F_out + j0 + jt * 16 + s] = acc[a][b][r];
+            }
+        }
 }
 
 // dW[e] = sum over workgroups b of partial[b][e] in float64: eight threads sum consecutive
@@ -387,54 +535,43 @@ int wgrad_max_blocks(int32_t n) {
 size_t wgrad_lds_bytes(int IB, int JB) {
     return static_cast<size_t>(IB + JB) * kLdsRow * sizeof(unsigned short);
 }
+static_assert((kMaxIB + kMaxJB) * kLdsRow * sizeof(unsigned short) <= 64 * 1024 &&
+                  kTrBufElems * sizeof(unsigned short) <= 64 * 1024,
+              "weight-gradient LDS within the default dynamic limit");
 
-// One pass over the rows for the dW block [i0, i0 + IB) x [j0, j0 + JB).  With `blocks`
-// == 0 nothing is launched: *resident receives how many workgroups of this kernel a CU
-// holds at once (registers, LDS and threads).
+// One pass over the rows for the dW block [i0, i0 + IB) x [j0, j0 + JB).
 template <int NT, bool XBF, bool GBF>
-int launch_wgrad_pass(const void *X, const void *G, float *partial, int blocks, int *resident,
-                      int32_t n, int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB,
-                      hipStream_t s) {
-    const size_t lds = wgrad_lds_bytes(IB, JB);
-    if (lds > 64 * 1024) {                   // dynamic LDS above 64 KiB is requested per kernel
-        const int st = hip_status(hipFuncSetAttribute(
-            reinterpret_cast<const void *>(&wgrad_kernel<NT, XBF, GBF>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
-        if (st) return st;
-    }
-    if (blocks == 0) {
-        int per_cu = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wgrad_kernel<NT, XBF, GBF>,
-                                                         kWgThreads, lds) != hipSuccess || per_cu < 1)
-            per_cu = 1;
-        *resident = per_cu;
-        return DUALGCN_OK;
-    }
-    hipLaunchKernelGGL((wgrad_kernel<NT, XBF, GBF>), dim3(blocks), dim3(kWgThreads), lds, s, X, G,
-                       partial, n, F_in, F_out, i0, IB, j0, JB);
+int launch_wgrad_pass(const void *X, const void *G, float *partial, int blocks, int32_t n,
+                      int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB, hipStream_t s) {
+    hipLaunchKernelGGL((wgrad_kernel<NT, XBF, GBF>), dim3(blocks), dim3(kWgThreads),
+                       wgrad_lds_bytes(IB, JB), s, X, G, partial, n, F_in, F_out, i0, IB, j0, JB);
     return hip_status(hipGetLastError());
 }
 
 template <bool XBF, bool GBF>
-int launch_wgrad_nt(const void *X, const void *G, float *partial, int blocks, int *resident,
-                    int32_t n, int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB,
-                    hipStream_t s) {
+int launch_wgrad_nt(const void *X, const void *G, float *partial, int blocks, int32_t n,
+                    int32_t F_in, int32_t F_out, int i0, int IB, int j0, int JB, hipStream_t s) {
     const int per_wave = ((IB / 16) * (JB / 16) + kWgWaves - 1) / kWgWaves;
     if (per_wave <= 2)
-        return launch_wgrad_pass<2, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
+        return launch_wgrad_pass<2, XBF, GBF>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s);
     if (per_wave <= 4)
-        return launch_wgrad_pass<4, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
-    return launch_wgrad_pass<8, XBF, GBF>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
+        return launch_wgrad_pass<4, XBF, GBF>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s);
+    return launch_wgrad_pass<8, XBF, GBF>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s);
 }
 
 int launch_wgrad_any(bool x_bf16, bool g_bf16, const void *X, const void *G, float *partial,
-                     int blocks, int *resident, int32_t n, int32_t F_in, int32_t F_out, int i0,
-                     int IB, int j0, int JB, hipStream_t s) {
+                     int blocks, int32_t n, int32_t F_in, int32_t F_out, int i0, int IB, int j0,
+                     int JB, hipStream_t s) {
+    if (x_bf16 && g_bf16) {
+        hipLaunchKernelGGL(wgrad_tr_kernel, dim3(blocks), dim3(kTrThreads),
+                           kTrBufElems * sizeof(unsigned short), s, static_cast<const unsigned short *>(X),
+                           static_cast<const unsigned short *>(G), partial, n, F_in, F_out, i0, IB, j0, JB);
+        return hip_status(hipGetLastError());
+    }
     if (x_bf16)
-        return g_bf16 ? launch_wgrad_nt<true, true>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s)
-                      : launch_wgrad_nt<true, false>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
-    return g_bf16 ? launch_wgrad_nt<false, true>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s)
-                  : launch_wgrad_nt<false, false>(X, G, partial, blocks, resident, n, F_in, F_out, i0, IB, j0, JB, s);
+        return launch_wgrad_nt<true, false>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s);
+    return g_bf16 ? launch_wgrad_nt<false, true>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s)
+                  : launch_wgrad_nt<false, false>(X, G, partial, blocks, n, F_in, F_out, i0, IB, j0, JB, s);
 }
 
 }  // namespace
@@ -463,17 +600,13 @@ size_t wgrad_workspace_bytes(int32_t n, int32_t F_in, int32_t F_out) {
     return static_cast<size_t>(wgrad_max_blocks(n)) * F_in * F_out * sizeof(float);
 }
 
-// Workgroups (partial dW matrices) of one weight-gradient product on the current device: as
-// many as the CUs hold at once for the widest pass, at most one per chunk and kMaxPartials.
-// Every pass uses the same count, fixed for a device, so the reduction order is fixed too.
-int wgrad_blocks(bool x_bf16, bool g_bf16, int32_t n, int32_t F_in, int32_t F_out, int *blocks) {
-    int resident = 1;
-    const int st = launch_wgrad_any(x_bf16, g_bf16, nullptr, nullptr, nullptr, 0, &resident, n, F_in,
-                                    F_out, 0, std::min<int>(F_in, kMaxIB), 0,
-                                    std::min<int>(F_out, kMaxJB), nullptr);
-    if (st) return st;
-    *blocks = std::min(wgrad_max_blocks(n), device_cus() * resident);
-    return DUALGCN_OK;
+// Workgroups (partial dW matrices) of one weight-gradient product on the current device:
+// one per CU (each kernel's workgroup fills a CU's registers: 16 wavefronts of up to 128
+// VGPRs, or 8 of up to 256), at most one per chunk and kMaxPartials.  The count depends
+// only on the device and n, never on the operand types, so every kernel sums the same
+// chunks into the same partials in the same order.
+int wgrad_blocks(int32_t n) {
+    return std::max(1, std::min(wgrad_max_blocks(n), device_cus()));
 }
 
 int launch_weight_grad(const void *X, bool x_bf16, const void *G, bool g_bf16, float *dW,
@@ -482,14 +615,12 @@ int launch_weight_grad(const void *X, bool x_bf16, const void *G, bool g_bf16, f
     float *partial = static_cast<float *>(workspace);
     const int JB = std::min<int>(F_out, kMaxJB);
     const int IB = std::min<int>(F_in, kMaxIB);
-    int blocks = 0;
-    const int st0 = wgrad_blocks(x_bf16, g_bf16, n, F_in, F_out, &blocks);
-    if (st0) return st0;
+    const int blocks = wgrad_blocks(n);
     for (int j0 = 0; j0 < F_out; j0 += JB) {
         for (int i0 = 0; i0 < F_in; i0 += IB) {
             const int ib = std::min(IB, F_in - i0), jb = std::min(JB, F_out - j0);
-            const int st = launch_wgrad_any(x_bf16, g_bf16, X, G, partial, blocks, nullptr, n, F_in,
-                                            F_out, i0, ib, j0, jb, s);
+            const int st = launch_wgrad_any(x_bf16, g_bf16, X, G, partial, blocks, n, F_in, F_out,
+                                            i0, ib, j0, jb, s);
             if (st) return st;
         }
     }
@@ -538,10 +669,7 @@ int scratch_address(void **out) {
 
 int wgrad_noalloc_bytes(bool x_bf16, bool g_bf16, int32_t n, int32_t F_in, int32_t F_out,
                         size_t *bytes) {
-    int blocks = 0;
-    const int st = wgrad_blocks(x_bf16, g_bf16, n, F_in, F_out, &blocks);
-    if (st) return st;
-    *bytes = static_cast<size_t>(blocks) * F_in * F_out * sizeof(float);
+    *bytes = static_cast<size_t>(wgrad_blocks(n)) * F_in * F_out * sizeof(float);
     return DUALGCN_OK;
 }
 

@@ -167,6 +167,27 @@ def test_weight_grad_c5_layer1_shape(dg, device):
     _within(dW, ref, B, BF16_TOL, "dW c5 layer 1")
     _within(dW, refr, Br, 1e-4, "dW c5 layer 1 vs bf16 operands")
     assert np.linalg.norm(dW - refr) <= 1e-4 * np.linalg.norm(refr)
+    # the bfloat16 copy of X (both operands bfloat16: the transposing-read kernel) gives
+    # the same bits
+    dWb = dg.weight_grad(torch.from_numpy(X).to(device).to(torch.bfloat16),
+                         torch.from_numpy(G).to(device).to(torch.bfloat16)).cpu().numpy()
+    assert np.array_equal(dWb, dW)
+
+
+@pytest.mark.parametrize("n,fin,fout", [(1, 32, 32), (64, 32, 32), (4133, 256, 128), (777, 128, 64),
+                                        (2050, 1024, 256), (300, 96, 160), (129, 512, 32),
+                                        (70001, 224, 96)])
+def test_weight_grad_operand_types_give_the_same_bits(dg, device, n, fin, fout):
+    """Every operand is rounded to bfloat16 before the matrix cores, and every kernel takes
+    the same chunks, k-steps and order of accumulation: passing X or G already rounded to
+    bfloat16 (the kernel for two bfloat16 operands reads LDS with transposing reads) gives
+    the same bits as passing them in float32."""
+    X = torch.from_numpy(dense.features_normal(n, fin, seed=fin + 3 * n)).to(device)
+    G = torch.from_numpy(dense.features_normal(n, fout, seed=fout + 5, stream_id=7)).to(device)
+    want = dg.weight_grad(X, G)
+    for xa, ga in ((X.to(torch.bfloat16), G), (X, G.to(torch.bfloat16)),
+                   (X.to(torch.bfloat16), G.to(torch.bfloat16))):
+        assert torch.equal(dg.weight_grad(xa, ga), want), (xa.dtype, ga.dtype)
 
 
 # ---------------------------------------------------------------- backward data
