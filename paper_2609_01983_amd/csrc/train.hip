@@ -59,6 +59,10 @@ __global__ __launch_bounds__(kThreads) void softmax_xent_kernel(
         float *gr = G + row * C;
         const int32_t lab = labels[row];
         const bool labeled = lab >= 0 && lab < C;
+        if (!labeled) {                     // zero gradient, whatever the logits: Y is not read
+            for (int j = l; j < C; j += kGroup) gr[j] = 0.f;
+            continue;
+        }
         float m = -INFINITY;
         for (int j = l; j < C; j += kGroup) m = fmaxf(m, y[j]);
         m = group_max(m);
@@ -68,9 +72,9 @@ __global__ __launch_bounds__(kThreads) void softmax_xent_kernel(
         const float inv = 1.f / s;
         for (int j = l; j < C; j += kGroup) {
             const float p = expf(y[j] - m) * inv;
-            gr[j] = labeled ? scale * (p - (j == lab ? 1.f : 0.f)) : 0.f;
+            gr[j] = scale * (p - (j == lab ? 1.f : 0.f));
         }
-        if (labeled && l == 0) acc += static_cast<double>(logf(s) + m - y[lab]);
+        if (l == 0) acc += static_cast<double>(logf(s) + m - y[lab]);
     }
     const int t = threadIdx.x;
     sh[t] = acc;
@@ -83,8 +87,8 @@ __global__ __launch_bounds__(kThreads) void softmax_xent_kernel(
 }
 
 // The same for C % 4 == 0, C <= 64 QPL, 16-byte aligned rows: every lane keeps QPL float4 of
-// each of RPG rows in registers (one read of Y, one write of G), and a group has the loads
-// of all RPG rows in flight before it reduces any of them.
+// each of RPG rows in registers (one read of Y on labeled rows, one write of G), and a group
+// has the loads of all RPG rows in flight before it reduces any of them.
 template <int QPL, int RPG>
 __global__ __launch_bounds__(kThreads) void softmax_xent_vec_kernel(
     const float *__restrict__ Y, const int32_t *__restrict__ labels, int32_t n, int32_t C,
@@ -102,11 +106,17 @@ __global__ __launch_bounds__(kThreads) void softmax_xent_vec_kernel(
         for (int r = 0; r < RPG; ++r) {
             const int64_t row = base + r * kRowsPerBlock + g;
             lab[r] = row < n ? labels[row] : -1;
+        }
+        // an unlabeled row's gradient is zero whatever its logits: Y is read on labeled rows only
+#pragma unroll
+        for (int r = 0; r < RPG; ++r) {
+            const int64_t row = base + r * kRowsPerBlock + g;
+            const bool want = lab[r] >= 0 && lab[r] < C;
 #pragma unroll
             for (int q = 0; q < QPL; ++q) {
                 const int j = l + q * kGroup;
                 v[r][q] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-                if (row < n && j < quads) v[r][q] = *reinterpret_cast<const f32x4 *>(Y + row * C + 4 * j);
+                if (want && j < quads) v[r][q] = *reinterpret_cast<const f32x4 *>(Y + row * C + 4 * j);
             }
         }
 #pragma unroll

@@ -79,6 +79,25 @@ def test_softmax_xent(dg, device, n, C):
     assert torch.equal(G, G2) and loss[0].item() == loss2[0].item()
 
 
+@pytest.mark.parametrize("n,C", [(1000, 16), (777, 17), (4096, 64), (513, 100)])
+def test_softmax_xent_unlabeled_logits_do_not_matter(dg, device, n, C):
+    """The loss and its gradient depend on labeled rows only: logits of unlabeled rows
+    replaced by NaN and infinities give the same G and loss bits (the vectorised and the
+    scalar kernel do not read them)."""
+    Y = dense.features_normal(n, C, seed=n + 2 * C) * np.float32(3.0)
+    labels = _labels(n, C, seed=C + 1)
+    scale = 1.0 / max(1, int(((labels >= 0) & (labels < C)).sum()))
+    off = (labels < 0) | (labels >= C)
+    Yb = Y.copy()
+    Yb[off] = np.float32(np.nan)
+    Yb[off, ::3] = np.float32(np.inf)
+    Yb[off, 1::3] = np.float32(-np.inf)
+    lab = torch.from_numpy(labels).to(device)
+    G, loss = dg.softmax_xent(torch.from_numpy(Y).to(device), lab, scale)
+    Gb, lossb = dg.softmax_xent(torch.from_numpy(Yb).to(device), lab, scale)
+    assert torch.equal(G, Gb) and loss[0].item() == lossb[0].item()
+
+
 def test_softmax_xent_c5_shape(dg, device):
     """The last layer of c5: n = 2^22 rows of 64 classes; every G row sampled, the loss whole."""
     n, C = 1 << 22, 64
