@@ -470,7 +470,9 @@ typedef struct dualgcn_plan_info {
     uint64_t seed;
     uint32_t walks_per_node, walk_len;
     int32_t max_degree;
-    int32_t dense_chunk;     /* entries per dense-region wavefront */
+    int32_t dense_chunk;     /* entries per dense-region wavefront: 4096 below 2^20
+                                entries, else the largest power of two from 512 to 4096
+                                not above nnz / 2048 */
     int32_t n_split_rows;    /* dense rows longer than dense_chunk */
     int32_t n_split_parts;   /* wavefronts those rows are split over */
     int32_t n_tasks;         /* sparse-region tasks (runs of at most 8 short rows) */

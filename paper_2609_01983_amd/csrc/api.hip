@@ -515,7 +515,7 @@ int dualgcn_plan_query(const dualgcn_plan *plan, dualgcn_plan_info *out) {
     i.walks_per_node = p->k;
     i.walk_len = p->d;
     i.max_degree = p->max_degree;
-    i.dense_chunk = dgc::kDenseChunk;
+    i.dense_chunk = p->dense_chunk;
     i.n_split_rows = p->n_split_rows;
     i.n_split_parts = p->n_split_parts;
     i.n_tasks = p->n_tasks;

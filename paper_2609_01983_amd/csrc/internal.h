@@ -32,9 +32,24 @@ class TraceRange {
 
 using u128 = unsigned __int128;
 
-// Entries of one dense row handled by one wavefront; longer rows are split into
-// parts of this many entries and combined in a fixed order.
-constexpr int kDenseChunk = 4096;
+// Entries of one dense row handled by one wavefront (a plan's dense chunk); longer rows are
+// split into parts of this many entries and combined in a fixed order.  A wavefront takes a
+// part in C / 64 rounds of dependent loads (F = 128), while the whole matrix spread over the
+// ~4096 wavefronts the chip holds needs about nnz / 2^18 rounds: the chunk is the largest
+// power of two up to kMaxDenseChunk with C <= nnz / 2048, so that no part takes more than
+// about twice the launch's rounds, and at least kMinDenseChunk (the long-row bound, below
+// which a dense row is a lane group's).  Matrices of fewer than kSplitMinEntries entries keep
+// the largest chunk: their launches last a few microseconds, less than splitting would add
+// (the kernel that combines the parts).
+constexpr int kMaxDenseChunk = 4096;
+constexpr int kMinDenseChunk = 512;
+constexpr int64_t kSplitMinEntries = int64_t{1} << 20;
+inline int32_t dense_chunk_for(int64_t nnz) {
+    int32_t c = kMaxDenseChunk;
+    if (nnz < kSplitMinEntries) return c;
+    while (c > kMinDenseChunk && static_cast<int64_t>(c) * 2048 > nnz) c >>= 1;
+    return c;
+}
 // Widest feature window one SpMM launch covers; wider F is processed in windows.
 constexpr int kMaxSlice = 256;
 // Dense rows of at least 2^kLongRowOctave entries get a wavefront each; shorter dense
@@ -107,6 +122,7 @@ struct Plan {
     int32_t n_tasks = 0;
     int32_t n_long[kLongRowClasses] = {};   // dense rows of >= 2^(kLongRowOctave - c) entries
                                             // (the last ones of the order)
+    int32_t dense_chunk = kMaxDenseChunk;   // entries per part of a split dense row
     int32_t n_split_rows = 0;
     int32_t n_split_parts = 0;
     SplitPart *parts = nullptr;        // [n_split_parts]

@@ -743,7 +743,7 @@ __global__ __launch_bounds__(kThreads) void task_fill_kernel(int32_t n,
 // Dense rows of the sorted order longer than one chunk: counts[i] = offsets[i] = number of
 // parts (offsets is scanned afterwards).
 __global__ __launch_bounds__(kThreads) void split_count_kernel(const int32_t *__restrict__ pptr,
-                                                               int32_t n,
+                                                               int32_t n, int32_t chunk,
                                                                SplitSummary *__restrict__ sum,
                                                                uint32_t *__restrict__ counts,
                                                                uint32_t *__restrict__ offsets) {
@@ -752,8 +752,8 @@ __global__ __launch_bounds__(kThreads) void split_count_kernel(const int32_t *__
     uint32_t c = 0;
     if (i >= sum->n_sparse) {
         const int32_t deg = pptr[i + 1] - pptr[i];
-        if (deg > kDenseChunk) {
-            c = static_cast<uint32_t>((deg + kDenseChunk - 1) / kDenseChunk);
+        if (deg > chunk) {
+            c = static_cast<uint32_t>((deg + chunk - 1) / chunk);
             atomicAdd(&sum->split_rows, 1);
         }
     }
@@ -1095,7 +1095,8 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     // Every array of the plan lives in one device block, every scratch array of the
     // build in another: two allocations per plan.  Split parts are bounded by
     // sum over rows longer than C of ceil(deg / C) < 2 nnz / C + 1.
-    const size_t max_parts = unnz / kDenseChunk * 2 + 1;
+    p->dense_chunk = dense_chunk_for(nnz);
+    const size_t max_parts = unnz / static_cast<size_t>(p->dense_chunk) * 2 + 1;
     // The lockstep walker reads successor records (8 bytes per entry, scratch) when the
     // walks take at least twice as many steps as the matrix has entries: building them
     // costs one random read per entry and saves one dependent random read per step.
@@ -1342,8 +1343,8 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     if ((st = exclusive_scan(off, n, scan_sums, &dsum->tasks, s))) return st;
     hipLaunchKernelGGL(task_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, n, dsum, cnt, off,
                        p->tasks);
-    hipLaunchKernelGGL(split_count_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n, dsum, cnt,
-                       off);
+    hipLaunchKernelGGL(split_count_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->pptr, n,
+                       p->dense_chunk, dsum, cnt, off);
     if ((st = exclusive_scan(off, n, scan_sums, &dsum->parts, s))) return st;
     hipLaunchKernelGGL(split_fill_kernel, dim3(grid_n), dim3(kThreads), 0, s, cnt, off, n, p->parts,
                        static_cast<uint32_t>(max_parts));

@@ -8,7 +8,8 @@
 // covers both paths; every workgroup picks its path from its index:
 //
 //   parts      rows of the dense region longer than one chunk, split into parts
-//              of kDenseChunk entries (heaviest row first), one wavefront per part
+//              of the plan's dense chunk (512 to 4096 entries, by the matrix's size;
+//              heaviest row first), one wavefront per part
 //   long       the other dense rows of at least 2^kLongRowOctave entries (one to
 //              three octaves fewer for groups narrower than 32 lanes), one
 //              wavefront per row, heaviest first
@@ -128,6 +129,7 @@ struct Args {
     void *Y;                    // float32, or bfloat16 when the kernel's BF is set (fused: H or null)
     uint32_t x_bytes;           // bytes of X that gathers may read (cache-class loads)
     int32_t n, n_sparse, n_tasks, n_parts, n_long;
+    int32_t dense_chunk;        // entries per part of a split dense row (the plan's)
     int32_t ld;                 // leading dimension of X and Y (= F)
     int32_t f0;                 // first feature of this launch window
     int32_t fend;               // end of the valid features of the window
@@ -367,14 +369,14 @@ __device__ __forceinline__ void spmm_block(const Args &a, int lb, int slice, int
             i = sp.row;
             part = sp.part;
             first = sp.first;
-            e0 = a.pptr[i] + part * kDenseChunk;
-            e1 = min(e0 + kDenseChunk, a.pptr[i + 1]);
+            e0 = a.pptr[i] + part * a.dense_chunk;
+            e1 = min(e0 + a.dense_chunk, a.pptr[i + 1]);
         } else {
             i = a.n - 1 - (w - a.nb_parts * WAVES);
             if (i < a.n - a.n_long) return;
             e0 = a.pptr[i];
             e1 = a.pptr[i + 1];
-            if (e1 - e0 > kDenseChunk) return;     // covered by its parts
+            if (e1 - e0 > a.dense_chunk) return;   // covered by its parts
         }
         double tot[VEC];
         dense_row<LPR, VEC, CP>(a, e0, e1, li, gw, gbase, f, fin, tot);
@@ -729,6 +731,7 @@ Args plan_args(const Plan &p, const float *X, void *Y, int32_t F, bool relu) {
     a.n_sparse = p.n_sparse;
     a.n_tasks = p.n_tasks;
     a.n_parts = p.n_split_parts;
+    a.dense_chunk = p.dense_chunk;
     a.n_long = p.n_long[0];
     a.ld = F;
     a.relu = relu ? 1 : 0;

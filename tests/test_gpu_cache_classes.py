@@ -1,8 +1,9 @@
 """Cache classes of the gathers: a plan of more than 2^18 nodes marks the columns outside the
 hottest 65,536 (bit 31 of its sorted copy's columns), and an SpMM whose operand exceeds the
 256 MiB memory-side cache reads the marked rows with non-temporal loads.  Results must not
-depend on either.  A sparse graph of 2^18 + 7 nodes with 64 hub rows (8 of them longer than one
-4096-entry part) keeps the oracle fast
+depend on either.  A sparse graph of 2^18 + 7 nodes with 64 hub rows (56 of about 800 entries,
+one wavefront each, and 8 of about 12,000 split into parts of the plan's 1024-entry chunk) keeps
+the oracle fast
 while an F = 256 operand (256 MiB + 7 KiB) takes the class path of the plain SpMM
 (spmm_dual_kernel<64, 4, *, true>) and of the fused junction (spmm_xw_kernel<64, true>).
 The aggregation is the one of Sec. 1 and Sec. 2.1; every row is checked against the oracle
@@ -32,7 +33,7 @@ def _hub_graph():
     gen = np.random.Generator(np.random.Philox(key=np.array([31, 7], dtype=np.uint64)))
     a, b = gen.integers(0, n, 3 * n), gen.integers(0, n, 3 * n)
     hubs = gen.choice(n, 64, replace=False)
-    ha = np.repeat(hubs, [2000] * 56 + [5000] * 8)      # long rows, and rows split into parts
+    ha = np.repeat(hubs, [800] * 56 + [12000] * 8)      # long rows, and rows split into parts
     hb = gen.integers(0, n, ha.size)
     src, dst = np.concatenate([a, ha]), np.concatenate([b, hb])
     keep = src != dst
@@ -53,7 +54,10 @@ def hub(dg, device):
 
 def test_large_plan_marks_cold_columns(dg, device, hub):
     g, plan = hub
-    assert plan.info()["cold_marked"] == 1
+    info = plan.info()
+    assert info["cold_marked"] == 1
+    # 2.1M entries: parts of 1024 entries; the 8 longest rows are split, the other hubs not
+    assert info["dense_chunk"] == 1024 and info["n_split_rows"] == 8
     small = dg.Plan(*to_dev(g.__class__(n=4096, rowptr=np.arange(4097, dtype=np.int32),
                                         col=np.arange(4096, dtype=np.int32),
                                         val=np.ones(4096, dtype=np.float32)), device),

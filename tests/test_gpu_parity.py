@@ -223,7 +223,10 @@ def test_spmm_split_rows_repeat_calls(dg, device):
     g = small.star(20000, self_loops=True, normalise=True)
     plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=4, walk_len=3)
     info = plan.info()
-    assert info["n_split_rows"] == 1 and info["n_split_parts"] == 5
+    # a matrix of about 60,000 entries keeps the largest chunk, 4096 entries
+    hub = int(np.diff(g.rowptr).max())                  # 20,001 entries: 5 parts
+    assert info["dense_chunk"] == 4096
+    assert info["n_split_rows"] == 1 and info["n_split_parts"] == -(-hub // 4096) == 5
     Yr = None
     for F in (128, 64, 128, 17):
         X = dense.features_normal(g.n, F, seed=F, stream_id=23)
@@ -238,6 +241,10 @@ def test_spmm_configs_full(dg, device, cfg):
     g = configs.load_graph(cfg)
     X = configs.load_features(cfg)
     plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=w.walks, walk_len=w.steps)
+    # c1 (69,632 entries) keeps 4096-entry parts (no row is split); c2 (1,310,720 entries)
+    # splits its 154 rows of 512 entries or more into 512-entry parts
+    info = plan.info()
+    assert (info["dense_chunk"], info["n_split_rows"]) == {"c1": (4096, 0), "c2": (512, 154)}[cfg]
     Y = dg.spmm(plan, torch.from_numpy(X).to(device)).cpu().numpy()
     Yr, B = oracle.spmm(g, X)
     assert_spmm_close(Y, Yr, B, what=cfg)

@@ -44,6 +44,9 @@ def test_full_partition_and_sampled_spmm(dg, device, cfg):
     _log(f"{cfg}: partition bit-exact (oracle {time.time() - t0:.1f}s), "
          f"n_sparse={ref['n_sparse']} K*={ref['kstar']}")
     assert 0 < ref["n_sparse"] < g.n
+    # 63-67M entries: dense rows are split into parts of the largest chunk, 4096 entries
+    info = plan.info()
+    assert info["dense_chunk"] == 4096
     rows = _sample_rows(g, ref["perm"], ref["n_sparse"], 4000, seed=11)
     for F in ([w.F] if cfg == "c4" else [128, 64]):
         if cfg == "c4":
