@@ -426,6 +426,13 @@ __global__ __launch_bounds__(kThreads) void scan_apply_kernel(const uint32_t *in
 
 // ------------------------------------------------------------------ radix sort of (K, v)
 
+// Sort tiles hold kThreads * ITEMS keys: 16 per thread on large inputs, 4 below
+// kSortSmallKeys keys, where 4096-key tiles would leave most CUs idle and make every
+// wavefront walk 16 rounds in a row (c2, 2^17 keys: 32 workgroups).
+constexpr int kSortItemsSmall = 4;
+constexpr int64_t kSortSmallKeys = int64_t{1} << 20;
+
+template <int ITEMS>
 __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint64_t *__restrict__ keys,
                                                               int32_t n, int shift,
                                                               uint32_t *__restrict__ hist,
@@ -433,8 +440,8 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint64_t *__
     __shared__ uint32_t h[kRadix];
     h[threadIdx.x] = 0;
     __syncthreads();
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile;
-    for (int i = 0; i < kItems; ++i) {
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kThreads * ITEMS;
+    for (int i = 0; i < ITEMS; ++i) {
         const int64_t idx = base + static_cast<int64_t>(i) * kThreads + threadIdx.x;
         if (idx < n) atomicAdd(&h[(keys[idx] >> shift) & (kRadix - 1)], 1u);
     }
@@ -442,10 +449,11 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint64_t *__
     hist[static_cast<int64_t>(threadIdx.x) * nblocks + blockIdx.x] = h[threadIdx.x];
 }
 
-// Stable scatter of one 8-bit digit.  Wave w owns items [base + 1024 w, base + 1024 (w+1)),
-// taken in rounds of 64 consecutive items; lanes with equal digits find each other with
-// eight ballots, so an item's rank is (earlier items of its digit in this wave) +
+// Stable scatter of one 8-bit digit.  Wave w owns items [base + 64 ITEMS w, base + 64 ITEMS
+// (w+1)), taken in rounds of 64 consecutive items; lanes with equal digits find each other
+// with eight ballots, so an item's rank is (earlier items of its digit in this wave) +
 // (earlier lanes of its digit in this round).  Tile order = index order, hence stable.
+template <int ITEMS>
 __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     const uint64_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in, int32_t n,
     int shift, const uint32_t *__restrict__ offsets, int32_t nblocks,
@@ -458,10 +466,10 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     __syncthreads();
 
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile +
-                         static_cast<int64_t>(wave) * (kItems * 64);
-    uint32_t rank[kItems];
-    for (int j = 0; j < kItems; ++j) {
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kThreads * ITEMS +
+                         static_cast<int64_t>(wave) * (ITEMS * 64);
+    uint32_t rank[ITEMS];
+    for (int j = 0; j < ITEMS; ++j) {
         const int64_t idx = base + static_cast<int64_t>(j) * 64 + lane;
         const bool valid = idx < n;
         const uint32_t dg = valid ? static_cast<uint32_t>((keys_in[idx] >> shift) & (kRadix - 1)) : 0;
@@ -488,7 +496,7 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
         }
     }
     __syncthreads();
-    for (int j = 0; j < kItems; ++j) {
+    for (int j = 0; j < ITEMS; ++j) {
         const int64_t idx = base + static_cast<int64_t>(j) * 64 + lane;
         if (idx < n) {
             const uint64_t key = keys_in[idx];
@@ -1108,7 +1116,9 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     // successor pass writes the marked columns and the sorted copy reads them
     const bool mark = nnz > 0 && static_cast<uint64_t>(n) * kMaxSlice * sizeof(float) > kGatherClassMinBytes;
     const int32_t nb_keys = static_cast<int32_t>(std::min<int64_t>((n + kThreads - 1) / kThreads, 1024));
-    const int32_t nblocks = static_cast<int32_t>((static_cast<int64_t>(n) + kTile - 1) / kTile);
+    const int sort_items = n < kSortSmallKeys ? kSortItemsSmall : kItems;
+    const int64_t sort_tile = static_cast<int64_t>(kThreads) * sort_items;
+    const int32_t nblocks = static_cast<int32_t>((static_cast<int64_t>(n) + sort_tile - 1) / sort_tile);
     const int64_t scan_tiles = std::max((static_cast<int64_t>(kRadix) * nblocks + kTile - 1) / kTile,
                                         (static_cast<int64_t>(n) + 1 + kTile - 1) / kTile) + 1;
     Layout lp, ls;
@@ -1162,6 +1172,24 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
     int32_t *vb0 = reinterpret_cast<int32_t *>(sm + o_vb0);
     uint32_t *scan_sums = reinterpret_cast<uint32_t *>(sm + o_scan);
     uint32_t *hist = reinterpret_cast<uint32_t *>(sm + o_hist);
+    // one pass of the radix sort: the digit histogram of `keys` at `shift`, or the scatter
+    auto radix_hist = [&](const uint64_t *keys, int shift) {
+        if (sort_items == kItems)
+            hipLaunchKernelGGL(radix_hist_kernel<kItems>, dim3(nblocks), dim3(kThreads), 0, s, keys, n,
+                               shift, hist, nblocks);
+        else
+            hipLaunchKernelGGL(radix_hist_kernel<kSortItemsSmall>, dim3(nblocks), dim3(kThreads), 0, s,
+                               keys, n, shift, hist, nblocks);
+    };
+    auto radix_scatter = [&](const uint64_t *kin, const int32_t *vin, int shift, uint64_t *kout,
+                             int32_t *vout) {
+        if (sort_items == kItems)
+            hipLaunchKernelGGL(radix_scatter_kernel<kItems>, dim3(nblocks), dim3(kThreads), 0, s, kin,
+                               vin, n, shift, hist, nblocks, kout, vout);
+        else
+            hipLaunchKernelGGL(radix_scatter_kernel<kSortItemsSmall>, dim3(nblocks), dim3(kThreads), 0,
+                               s, kin, vin, n, shift, hist, nblocks, kout, vout);
+    };
     SplitSummary *dsum = reinterpret_cast<SplitSummary *>(sm + o_ssum);
     uint32_t *cnt = reinterpret_cast<uint32_t *>(sm + o_counts);
     uint32_t *off = cnt + (static_cast<int64_t>(n) + 3) / 4 * 4;    // 16-byte aligned
@@ -1245,8 +1273,7 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
         if ((st = hip_status(hipEventCreateWithFlags(&sums_read.e, hipEventDisableTiming)))) return st;
         if ((st = hip_status(hipEventRecord(sums_read.e, s)))) return st;
         if ((st = hip_status(hipMemsetAsync(p->perm, 0, sizeof(int32_t) * un, s)))) return st;
-        hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, p->K, n, 0, hist,
-                           nblocks);
+        radix_hist(p->K, 0);
         if ((st = hip_status(hipGetLastError()))) return st;
         if ((st = exclusive_scan(hist, static_cast<int64_t>(kRadix) * nblocks, scan_sums, nullptr, s)))
             return st;
@@ -1292,15 +1319,13 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
             uint64_t *kout = kbuf[pass % 2];
             int32_t *vout = vbuf[pass % 2];
             if (pass > 0) {
-                hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, n,
-                                   shift, hist, nblocks);
+                radix_hist(kin, shift);
                 if ((st = hip_status(hipGetLastError()))) return st;
                 if ((st = exclusive_scan(hist, static_cast<int64_t>(kRadix) * nblocks, scan_sums,
                                          nullptr, s)))
                     return st;
             }
-            hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblocks), dim3(kThreads), 0, s, kin, vin,
-                               n, shift, hist, nblocks, kout, vout);
+            radix_scatter(kin, vin, shift, kout, vout);
             if ((st = hip_status(hipGetLastError()))) return st;
             kin = kout;
             vin = vout;
@@ -1324,12 +1349,10 @@ int build_plan(const dualgcn_csr *csr, uint64_t seed, uint32_t k, uint32_t d,
         uint64_t *okey_out = sorted == kb0 ? kb0 : kb1;
         hipLaunchKernelGGL(order_key_kernel, dim3(grid_n), dim3(kThreads), 0, s, p->K, p->kstar,
                            region, csr->rowptr, n, okey);
-        hipLaunchKernelGGL(radix_hist_kernel, dim3(nblocks), dim3(kThreads), 0, s, okey, n, 0, hist,
-                           nblocks);
+        radix_hist(okey, 0);
         if ((st = exclusive_scan(hist, static_cast<int64_t>(kRadix) * nblocks, scan_sums, nullptr, s)))
             return st;
-        hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblocks), dim3(kThreads), 0, s, okey, nullptr, n,
-                           0, hist, nblocks, okey_out, p->order);
+        radix_scatter(okey, nullptr, 0, okey_out, p->order);
         hipLaunchKernelGGL(long_rows_kernel, dim3(1), dim3(64), 0, s, hist, nblocks, n, dsum);
         if ((st = hip_status(hipGetLastError()))) return st;
     }
