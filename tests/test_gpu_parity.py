@@ -235,6 +235,35 @@ def test_spmm_split_rows_repeat_calls(dg, device):
         assert_spmm_close(Y, Yr, B, what=f"star F={F}")
 
 
+def test_spmm_dense_chunk_2048(dg, device):
+    """A matrix of 4-8M entries splits its dense rows into 2048-entry parts: 2^19 + 5 nodes of
+    about 9 entries each plus 24 hub rows, 12 of about 1,500 entries (one wavefront each) and
+    12 of 3,000-9,000 (2 to 5 parts); every row against the oracle, F = 64 and a ragged
+    F = 37."""
+    from graphgen.csr import Graph, csr_from_pairs, normalised_values
+    n = (1 << 19) + 5
+    gen = np.random.Generator(np.random.Philox(key=np.array([41, 3], dtype=np.uint64)))
+    a, b = gen.integers(0, n, 4 * n), gen.integers(0, n, 4 * n)
+    hubs = gen.choice(n, 24, replace=False)
+    ha = np.repeat(hubs, [1500] * 12 + [3000, 5000, 8000, 9000] * 3)
+    src, dst = np.concatenate([a, ha]), np.concatenate([b, gen.integers(0, n, ha.size)])
+    keep = src != dst
+    src, dst = src[keep], dst[keep]
+    rowptr, col = csr_from_pairs(n, np.concatenate([src, dst, np.arange(n)]),
+                                 np.concatenate([dst, src, np.arange(n)]))
+    g = Graph(n=n, rowptr=rowptr, col=col, val=normalised_values(rowptr, col), meta={"kind": "hubs"})
+    plan = dg.Plan(*to_dev(g, device), seed=0, walks_per_node=4, walk_len=3)
+    info = plan.info()
+    assert (1 << 22) <= g.nnz < (1 << 23) and info["dense_chunk"] == 2048
+    assert info["n_split_rows"] == 12
+    for F in (64, 37):
+        X = dense.features_normal(n, F, seed=F, stream_id=29)
+        Y = dg.spmm(plan, torch.from_numpy(X).to(device)).cpu().numpy()
+        Yr, B = oracle.spmm(g, X)
+        assert_spmm_close(Y, Yr, B, what=f"chunk 2048 F={F}")
+    plan.destroy()
+
+
 @pytest.mark.parametrize("cfg", ["c1", "c2"])
 def test_spmm_configs_full(dg, device, cfg):
     w = configs.WORKLOADS[cfg]
