@@ -703,12 +703,18 @@ __global__ __launch_bounds__(kThreads) void sorted_copy_kernel(
 constexpr int32_t kTaskProbe = 64;
 
 // Does row i of the sorted order start a sparse-region task?  A task is a run of at most
-// kTaskRows consecutive rows whose first entries lie in one window of kTaskEntries entries;
-// an empty row forms a task of its own.
+// kTaskRows consecutive rows whose first entries lie in one window of kTaskEntries entries,
+// or a run of at most kTaskRows consecutive empty rows: a run of empty rows (they share
+// their first entry) is cut into tasks of kTaskRows from its first row, and the row after
+// an empty row starts a task.
 __device__ __forceinline__ bool starts_task(const int32_t *__restrict__ pptr, int32_t i) {
     const int32_t b = pptr[i];
-    if (i == 0 || pptr[i + 1] == b || pptr[i - 1] == b) return true;
-    const int32_t w0 = (b / kTaskEntries) * kTaskEntries;
+    if (i == 0) return true;
+    const bool empty = pptr[i + 1] == b;
+    if (!empty && pptr[i - 1] == b) return true;      // the first row after empty rows
+    // window start: empty rows count from the first row starting at b (the first of their
+    // run: an earlier row ending at b is not empty, so it starts before b)
+    const int32_t w0 = empty ? b : (b / kTaskEntries) * kTaskEntries;
     // first row whose first entry is >= w0: it lies within the last kTaskProbe rows unless
     // the window holds that many empty rows, so probe there before searching all of [0, i]
     int32_t lo = 0, hi = i;

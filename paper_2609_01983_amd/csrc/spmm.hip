@@ -407,11 +407,11 @@ __device__ __forceinline__ void spmm_block(const Args &a, int lb, int slice, int
     }
     const int32_t e_begin = a.pptr[r0];
     const int32_t e_end = task_meta<LPR>(rend, m - 1, gbase);
-    if (e_begin == e_end) {                   // an empty row is a task of its own
-        double z[VEC];
+    if (e_begin == e_end) {                   // a task of empty rows (a run of them is cut
+        double z[VEC];                        // into tasks of at most kTaskRows)
 #pragma unroll
         for (int j = 0; j < VEC; ++j) z[j] = 0.0;
-        emit.row(task_meta<LPR>(rout, 0, gbase), gw * kTaskRows, z, f, fin);
+        for (int j = 0; j < m; ++j) emit.row(task_meta<LPR>(rout, j, gbase), gw * kTaskRows + j, z, f, fin);
         return;
     }
     int cur = 0;                              // every row of a task with entries is non-empty

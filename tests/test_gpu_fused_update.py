@@ -34,7 +34,19 @@ def dg(device):
     return dg
 
 
+def _empty_runs():
+    """3,001 rows, 40% of them empty (one run of about 1,200 empty rows in the processing
+    order, cut into tasks of 8), the others 1-19 random columns with values in (0, 1]."""
+    gen = np.random.default_rng(17)
+    n = 3001
+    g = small.from_rows([[] if gen.random() < 0.4 else gen.integers(0, n, gen.integers(1, 20)).tolist()
+                         for _ in range(n)])
+    g.val[:] = gen.random(g.val.size).astype(np.float32) + np.float32(1e-3)
+    return g
+
+
 GRAPHS = {
+    "empty_runs": _empty_runs,
     "gnp257": TINY["gnp257"],
     "rows_dup_empty": TINY["rows_dup_empty"],
     "hub_star": TINY["hub_star"],
