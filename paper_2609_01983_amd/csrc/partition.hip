@@ -12,8 +12,9 @@
 //   host            K* = least integer >= mu_K + beta sigma_K (exact integers)
 //   radix sort      stable LSD sort of (K_v, v) on 8-bit digits      -> perm
 //   split           n_sparse = lower_bound(sorted K, K*)
-//   row pointers    of the rows in processing order (region, row-length octave,
-//                   node id), by a scan
+//   processing order  (region, row-length octave, node id): one stable radix pass
+//                   over the node ids on a key of (region, octave) below 64
+//   row pointers    of the rows in processing order, by a scan
 //   schedule        sparse tasks (runs of at most kTaskRows short rows) and the
 //                   parts of dense rows longer than one dense chunk
 //   sorted copy     the rows of the matrix in processing order, so that both regions
