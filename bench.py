@@ -30,7 +30,9 @@ The JSON line also carries
                 workload (each part's sample fraction stated), with the same oracle on
                 all host cores as context;
   paper_context the paper's own speedups (RTX 3090), context only;
-  phases_ms     mean milliseconds of each phase inside the timed steps.
+  phases_ms     mean milliseconds of each phase inside the timed steps;
+  partition_alone_ms  (GCN workloads) median of three partitions built alone after the
+                timed steps: inside a step the partition runs beside layer 1's update.
 """
 import argparse
 import hashlib
@@ -800,6 +802,19 @@ def main():
         out["config"]["max_degree_note"] = (f"the generated graph's largest row has {g.max_degree()} "
                                             "entries, below the stated > 1e5")
     holder["plan"].destroy()
+    if w.is_gcn and not pipelined:
+        # inside the step the partition shares the memory fabric with layer 1's update;
+        # built alone (after the timed steps, outside them) it shows its own cost
+        alone = []
+        for _ in range(3):
+            a, b = ev(), ev()
+            a.record(stream)
+            pl = dg.Plan(rowptr, col, val, seed=0, walks_per_node=w.walks, walk_len=w.steps)
+            b.record(stream)
+            torch.cuda.synchronize()
+            alone.append(a.elapsed_time(b))
+            pl.destroy()
+        out["partition_alone_ms"] = round(float(np.median(alone)), 4)
     out["bandwidth"] = bandwidth(dg, torch, dev, stream)
     if not args.no_cpu_baseline:
         t0 = time.time()
